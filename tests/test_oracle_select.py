@@ -1,0 +1,158 @@
+"""Pins of the oracle's latency model, weight normalisation, TPT, model-mode DP
+and stage 2 (no GPU)."""
+import math
+import os
+
+import numpy as np
+import pytest
+
+import workloads as W
+from oracle import latency as LAT
+from oracle import model as M
+from oracle import select as SEL
+from oracle import generate as GEN
+
+GOLD = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def test_latency_fit_recovers_coefficients():
+    c = (0.41, 3.3e-5, 0.12)
+    n = np.array([1024, 4096, 16384, 65536, 131072], dtype=float)
+    t_a = c[1] * n + c[2]
+    t_m = np.full(5, c[0])
+    c1, c2, c3 = LAT.fit_latency(n, t_a, t_m)
+    assert c1 == pytest.approx(c[0], rel=1e-14)
+    assert c2 == pytest.approx(c[1], rel=1e-10)
+    assert c3 == pytest.approx(c[2], rel=1e-10)
+
+
+def test_quantize_appendix_c_worked_example():
+    rows = [l.split() for l in open(os.path.join(GOLD, "quantize_appc.txt"))
+            if l.strip() and not l.startswith("#")]
+    assert len(rows) == 3
+    for r in rows:
+        c1, c2, c3 = float(r[0]), float(r[1]), float(r[2])
+        L, n = int(r[3]), int(r[4])
+        ta, tm, delta = float(r[5]), float(r[6]), float(r[7])
+        wa, wm, K = int(r[8]), int(r[9]), int(r[10])
+        assert LAT.latencies((c1, c2, c3), n) == pytest.approx((ta, tm), rel=1e-12)
+        q = LAT.quantize((c1, c2, c3), n, L, "paper_min")
+        assert q.delta == pytest.approx(delta, rel=1e-12)
+        assert (q.w_attn, q.w_mlp, q.C) == (wa, wm, K)
+
+
+def test_quantize_bins_tiny():
+    # t_A = 0.01*140 + 0.2 = 1.6, t_M = 1.0, Delta = 4*2.6/64 = 0.1625
+    q = LAT.quantize(W.TINY_LATENCY, 140, 4, "bins", 64)
+    assert q.delta == pytest.approx(0.1625, rel=1e-15)
+    assert (q.w_attn, q.w_mlp, q.C) == (10, 6, 64)
+    with pytest.raises(ValueError):
+        LAT.quantize((1.0, -1.0, 0.0), 10, 4, "paper_min")
+
+
+def test_tpt_full_model_is_one_over_capacity():
+    for C in (8, 64, 128):
+        for g in range(1, 11):
+            assert SEL.tpt(1.0, g, C, C) == pytest.approx(1.0 / C, rel=1e-15)
+
+
+def test_tpt_reduces_to_tpl_when_latencies_equal():
+    """Eq. TPL: TPL(l, gamma) = (1 - a^(g+1))/(1 - a) / (gamma*l + L).  With equal
+    sublayer latencies t an early exit at layer l costs 2*l sublayers, so
+    TPT = TPL / (2t) and both metrics order candidates identically."""
+    L = 16
+    rng = np.random.default_rng(5)
+    for _ in range(50):
+        a = rng.uniform(0.05, 0.98)
+        ell = int(rng.integers(1, L))
+        g = int(rng.integers(1, 11))
+        tpl = (1 - a ** (g + 1)) / (1 - a) / (g * ell + L)
+        # weights 1 per sublayer, executed weight 2*ell, capacity 2L
+        v = SEL.tpt(a, g, 2 * ell, 2 * L)
+        assert v == pytest.approx(tpl / 2, rel=1e-12)
+
+
+def test_stage2_grid_toy():
+    """Three candidates enumerated by hand (C = 10, D = 3):
+    j=0 alpha=1: TPT = 1/10 for all gamma.
+    j=4 alpha=0.9, executed 6: gamma=1 1.9/16=.11875, gamma=2 2.71/22=.123181..,
+        gamma=3 3.439/28=.122821..
+    j=5 alpha=0.5, executed 5: gamma=1 1.5/15=.1, 2 1.75/20, 3 1.875/25.
+    The maximum is (j=4, gamma=2)."""
+    best = (0, None)
+    for j, a in ((0, 1.0), (4, 0.9), (5, 0.5)):
+        for g in (1, 2, 3):
+            v = SEL.tpt(a, g, 10 - j, 10)
+            if v > best[0]:
+                best = (v, (j, g))
+    assert best[1] == (4, 2)
+    assert best[0] == pytest.approx(2.71 / 22, rel=1e-14)
+
+
+@pytest.fixture(scope="module")
+def tiny_hist():
+    cfg = W.config("tiny")
+    model = M.Model(cfg, W.generate_weights(cfg, seed=0))
+    st = M.prefill(model, W.prompt_ids(cfg.vocab, 48, 1), 128, 10)
+    pos, X = M.history(st)
+    return model, st, pos, X
+
+
+def test_dp_reachable_cells_are_subset_sums(tiny_hist):
+    model, st, pos, X = tiny_hist
+    wa, wm, C = 3, 2, 20
+    dp = SEL.dp_select(model, st.cache, pos, X, wa, wm, C, tau=-math.inf)
+    sums = {0}
+    for i in range(1, 9):
+        w = SEL.item_weight(i, wa, wm)
+        sums = sums | {s + w for s in sums}
+        want = np.array([j in sums for j in range(dp.J + 1)])
+        np.testing.assert_array_equal(dp.reach_rows[i], want)
+
+
+def test_dp_terminal_states_match_backtracked_masks(tiny_hist):
+    model, st, pos, X = tiny_hist
+    wa, wm, C = 10, 6, 64
+    dp = SEL.dp_select(model, st.cache, pos, X, wa, wm, C, tau=0.5)
+    assert dp.reach[0]
+    np.testing.assert_array_equal(dp.states[0], X[-1])
+    brute = SEL.brute_force_cos(model, st.cache, pos, X, wa, wm, dp.J)
+    n_opt = 0
+    for j in range(dp.J + 1):
+        if not dp.reach[j]:
+            continue
+        ex = SEL.backtrack(dp.bits, j, wa, wm)
+        skipped = sum(SEL.item_weight(i + 1, wa, wm) for i in range(8) if not ex[i])
+        assert skipped == j
+        re = SEL.apply_mask(model, st.cache, pos, X[0], ex)
+        np.testing.assert_allclose(dp.states[j], re, rtol=1e-12, atol=1e-12)
+        c = SEL.cos_matrix(dp.states[j], X[-1])
+        assert c <= brute[j][0] + 1e-12
+        n_opt += abs(c - brute[j][0]) < 1e-12
+    assert n_opt >= 1
+
+
+def test_stage2_fallback_and_alpha(tiny_hist):
+    model, st, pos, X = tiny_hist
+    dp = SEL.dp_select(model, st.cache, pos, X, 10, 6, 64, tau=0.5)
+    sel = SEL.stage2(model, dp, X[-1], 10, 6, 64, D=10)
+    assert sel.alphas[0] == 1.0
+    assert sel.tpt_star >= 1.0 / 64
+    skipped = sum(SEL.item_weight(i + 1, 10, 6) for i in range(8) if not sel.exec_mask[i])
+    assert skipped == sel.j_star
+    # tau above every candidate's cosine leaves only the full model
+    dp2 = SEL.dp_select(model, st.cache, pos, X, 10, 6, 64, tau=1.0 + 1e-9)
+    assert np.flatnonzero(dp2.reach).tolist() == [0]
+    sel2 = SEL.stage2(model, dp2, X[-1], 10, 6, 64)
+    assert sel2.j_star == 0 and sel2.exec_mask.all() and sel2.gamma_star == 1
+
+
+def test_generate_equals_ar_tiny():
+    cfg = W.config("tiny")
+    model = M.Model(cfg, W.generate_weights(cfg, seed=0))
+    prompt = W.prompt_ids(cfg.vocab, 64, 1)
+    out, log = GEN.generate(model, prompt, 20, gamma=4, T=8, lat=W.TINY_LATENCY,
+                            quant_mode="bins", bins=64)
+    ref = M.generate_ar(model, prompt, 20, 128)
+    assert out == ref
+    assert len(log.selections) >= 2
