@@ -1,0 +1,332 @@
+/*
+ * knapspec.h - C ABI of the MI355X self-speculative decode step of KnapSpec
+ * (Cha, Kim, Han, Yang, Han: "KnapSpec: Self-Speculative Decoding via Adaptive
+ * Layer Selection as a Knapsack Problem", arXiv 2602.20217).
+ *
+ * One library, libknapspec.so, built for gfx950.  Every entry point takes plain
+ * host or device pointers and sizes.  The caller owns every buffer (model
+ * weights, KV cache, workspace); the library never allocates device memory
+ * and never frees caller memory.  The only object the library allocates is the
+ * host-side ks_ctx.
+ *
+ * Conventions
+ *  - Errors: every call validates its arguments before it launches anything and
+ *    returns a negative ks_status on failure, leaving outputs and the context
+ *    state unchanged; ks_last_error() then describes the failure (thread-local
+ *    string).  No C++ exception crosses this interface.
+ *  - Streams: "stream" arguments are hipStream_t values passed as void*.  Calls
+ *    that return host values synchronise that stream; calls on raw device
+ *    pointers (ks_hidden_cos, ks_knapsack_*) are asynchronous on the stream.
+ *  - A ks_ctx is bound to one stream and is not thread-safe.
+ *  - Precision: the residual stream, selection history and DP states are float32;
+ *    weights and KV cache are float32 (KS_F32) or bf16 (KS_BF16).
+ *  - Sublayer numbering follows Section 2 of the paper: sublayer i in 1..2L,
+ *    odd i = attention of layer (i+1)/2, even i = MLP of layer i/2.  Masks are
+ *    arrays of 2L bytes, byte i-1 nonzero = sublayer i executed.
+ */
+#ifndef KNAPSPEC_H
+#define KNAPSPEC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  KS_OK = 0,
+  KS_EINVAL = -1,     /* bad argument (null pointer, size out of range, ...) */
+  KS_ENOMEM = -2,     /* caller-provided buffer smaller than required */
+  KS_ECAPACITY = -3,  /* context length would exceed the KV cache capacity */
+  KS_ESTATE = -4,     /* call order violated (e.g. verify before prefill) */
+  KS_EHIP = -5        /* a HIP runtime call failed */
+} ks_status;
+
+enum { KS_F32 = 0, KS_BF16 = 1 };
+enum { KS_QUANT_PAPER_MIN = 0, KS_QUANT_BINS = 1 };
+enum { KS_MAX_SUBLAYERS = 256 };
+
+/* Decoder description (Llama / Qwen3 style). */
+typedef struct ks_model_desc {
+  int L;          /* layers; 2L sublayers */
+  int d;          /* model width (multiple of 32) */
+  int hq, hkv;    /* query / key-value heads, hq % hkv == 0 */
+  int hd;         /* head dim: 64 or 128 */
+  int ffn;        /* MLP width (multiple of 32) */
+  int vocab;      /* vocabulary (multiple of 16) */
+  int n_max;      /* KV cache capacity in positions */
+  int qk_norm;    /* 1: per-head RMSNorm of q and k before RoPE (Qwen3) */
+  int dtype;      /* KS_F32 or KS_BF16: weights and KV cache */
+  float eps;      /* RMSNorm epsilon */
+  double rope_theta;
+} ks_model_desc;
+
+/* Size limits fixed at creation; they set the workspace size. */
+typedef struct ks_limits {
+  int gamma_max;      /* longest draft; verify runs gamma+1 rows (<= 15) */
+  int m_rounds;       /* history keeps the last m rounds (paper: 5) */
+  int cap_max;        /* largest knapsack capacity C accepted by the selection */
+  int prefill_chunk;  /* rows per prefill pass (multiple of 16) */
+} ks_limits;
+
+/*
+ * Model weights: device pointers, caller-owned, valid for the context lifetime.
+ * Per-layer entries are host arrays of L device pointers.
+ *
+ * Matrix layouts.  Every matrix is logically W[N][K] (out x in), y = W x.
+ *  - KS_F32: plain row-major float32.
+ *  - KS_BF16: the MFMA tile layout written by ks_pack_matrix (see there).
+ *  wqkv     [ (hq + 2 hkv) hd ][ d ]  rows: q heads, then k heads, then v heads
+ *  wo       [ d ][ hq hd ]
+ *  w_gate_up: written by ks_pack_gate_up from separate gate and up [ffn][d]
+ *  w_down   [ d ][ ffn ]
+ *  lm_head  [ vocab ][ d ]
+ *  embed    [ vocab ][ d ] plain row-major in the model dtype (not packed)
+ *  norm gains: float32 vectors (attn_norm, mlp_norm, final_norm: d; q_norm,
+ *  k_norm: hd, only read when qk_norm = 1, may be NULL otherwise).
+ */
+typedef struct ks_weights {
+  const void* embed;
+  const void* lm_head;
+  const float* final_norm;
+  const float* const* attn_norm;
+  const void* const* wqkv;
+  const void* const* wo;
+  const float* const* q_norm;
+  const float* const* k_norm;
+  const float* const* mlp_norm;
+  const void* const* w_gate_up;
+  const void* const* w_down;
+} ks_weights;
+
+/* Selection parameters (Section 3.4 and Appendix C of the paper). */
+typedef struct ks_select_params {
+  double c1, c2, c3;  /* latency model: t_MLP = c1, t_Attn(n) = c2 n + c3 */
+  int quant_mode;     /* KS_QUANT_PAPER_MIN: Delta = min(t_Attn, t_MLP);
+                         KS_QUANT_BINS: Delta = L (t_Attn + t_MLP) / bins */
+  int bins;
+  float tau;          /* cosine pruning threshold (paper: 0.5); -inf disables */
+  int prune_half;     /* 1: skipped weight <= C/2 (paper's second pruning rule) */
+  int D;              /* largest draft length in the TPT grid (paper: 10) */
+} ks_select_params;
+
+/* Result of one selection. */
+typedef struct ks_selection {
+  uint8_t exec[KS_MAX_SUBLAYERS]; /* chosen draft mask S* (byte i-1: sublayer i) */
+  int j_star;        /* skipped weight of S* */
+  int gamma_star;    /* gamma of the best (S, gamma) pair (reported only) */
+  int C;             /* capacity L (w_attn + w_mlp) */
+  int w_attn, w_mlp; /* integer sublayer weights */
+  int n_rows;        /* history rows r used */
+  int n_cells;       /* reachable terminal budgets */
+  double tpt_star;   /* TPT of (S*, gamma*) in tokens per Delta */
+  double alpha_hat;  /* estimated acceptance of S* (Eq. acceptance) */
+  double delta;      /* latency unit Delta */
+} ks_selection;
+
+/* Optional per-decision record of a selection (host arrays the caller sizes;
+ * J = C/2 with prune_half, else C; rows indexed i = 0..2L). */
+typedef struct ks_selection_debug {
+  int J_cap;          /* in: entries per row available in the arrays below */
+  uint8_t* bits;      /* [(2L+1)][J_cap]  1 = skip candidate chosen */
+  uint8_t* reach;     /* [(2L+1)][J_cap]  cell reachable after sublayer i */
+  double* sig_e;      /* [(2L+1)][J_cap]  cos of execute candidate (NaN if none) */
+  double* sig_s;      /* [(2L+1)][J_cap]  cos of skip candidate (NaN if none) */
+  int* n_match;       /* [J_cap]  argmax agreements of terminal cells (-1 if none) */
+} ks_selection_debug;
+
+typedef struct ks_gen_stats {
+  int n_rounds;        /* speculative rounds (verify passes) */
+  int n_selections;    /* knapsack selections run */
+  int n_drafted;       /* draft tokens proposed */
+  int n_accepted;      /* draft tokens accepted */
+  double ms_total;     /* wall time of the generation loop (after prefill) */
+  double ms_select;    /* part of ms_total spent in selections */
+  double ms_prefill;   /* prefill wall time (outside ms_total) */
+} ks_gen_stats;
+
+typedef struct ks_ctx ks_ctx;
+
+const char* ks_last_error(void);
+
+/* ---- sizing ------------------------------------------------------------- */
+size_t ks_kv_cache_bytes(const ks_model_desc* desc);
+size_t ks_workspace_bytes(const ks_model_desc* desc, const ks_limits* lim);
+
+/* ---- weight layout ------------------------------------------------------ */
+/*
+ * ks_pack_matrix: converts row-major W[N][K] (src, device) into the layout the
+ * kernels read (dst, device, same byte size).  KS_F32: plain copy.  KS_BF16:
+ * N % 16 == 0, K % 32 == 0; dst is a sequence of 1 KiB tiles, tile (nt, kt)
+ * at element offset (nt * K/32 + kt) * 512, covering rows 16 nt..16 nt+15 and
+ * columns 32 kt..32 kt+31; inside a tile, lane l = (n % 16) + 16 ((k % 32) / 8)
+ * holds elements k % 8 = 0..7 at offset 8 l.  This is the B-operand register
+ * layout of the gfx950 16x16x32 bf16 matrix instruction, so one 64-lane load
+ * reads one contiguous KiB.  src and dst must not overlap.
+ */
+ks_status ks_pack_matrix(const void* src, void* dst, int N, int K, int dtype, void* stream);
+/*
+ * ks_pack_gate_up: gate and up projections, each row-major [ffn][d] (device).
+ * KS_F32: dst = [gate rows; up rows] row-major [2 ffn][d].  KS_BF16: packed as
+ * a [2 ffn][d] matrix whose 16-row tiles alternate gate tile t, up tile t.
+ */
+ks_status ks_pack_gate_up(const void* gate, const void* up, void* dst, int ffn, int d,
+                          int dtype, void* stream);
+
+/* ---- context ------------------------------------------------------------ */
+/*
+ * ks_create: kv_cache is a device buffer of ks_kv_cache_bytes(desc) bytes, laid
+ * out [L][2 (K, V)][hkv][n_max][hd] in the model dtype; workspace is a device
+ * buffer of ks_workspace_bytes(desc, lim) bytes.  Both stay caller-owned.
+ * Fills the rotary table (float64 angles rounded to float32) on the stream.
+ */
+ks_status ks_create(const ks_model_desc* desc, const ks_limits* lim, const ks_weights* w,
+                    void* kv_cache, size_t kv_bytes, void* workspace, size_t ws_bytes,
+                    void* stream, ks_ctx** out);
+ks_status ks_destroy(ks_ctx* ctx);
+
+/*
+ * ks_prefill (Section 2; setup step): runs the prompt tokens (host int32[n],
+ * 1 <= n < n_max) through the full model, fills the KV cache for positions
+ * 0..n-1 and commits the target's greedy token s at position n (no keys/values
+ * yet).  The last min(n, m_rounds (gamma_max+1)) rows of every sublayer output
+ * X^(0..2L) become the first history block.  Resets all decode state.
+ */
+ks_status ks_prefill(ks_ctx* ctx, const int32_t* tokens, int n, int32_t* out_first_token);
+
+/*
+ * ks_set_context: declares that the caller has filled the KV cache for
+ * positions 0..n_cached-1 itself and that last_token is the committed token at
+ * position n_cached.  Clears the history and the pending draft.
+ */
+ks_status ks_set_context(ks_ctx* ctx, int n_cached, int32_t last_token);
+
+/*
+ * ks_draft_step (Section 2.1, draft model f^(S)): one greedy draft token.  The
+ * k-th call since the last verify (k = 0, 1, ...) processes, at position P+k,
+ * the committed token s (k = 0) or the previous draft token; executed attention
+ * sublayers store their keys/values at P+k.  exec: host uint8[2L] mask S.
+ * Returns the token and its top-1 probability.  k must stay below gamma_max.
+ */
+ks_status ks_draft_step(ks_ctx* ctx, const uint8_t* exec, int32_t* out_token,
+                        float* out_top1_prob);
+
+/*
+ * ks_verify (Section 2.1, greedy verification): runs the full model on tokens
+ * (host int32[gamma+1] = s, d_1..d_gamma; tokens[0] must be the committed s) at
+ * positions P..P+gamma, overwriting their keys/values, and accepts the longest
+ * prefix with d_i equal to the target's argmax y_{i-1}.  Commits d_1..d_a and
+ * y_a (a+1 tokens); the new s is y_a at position P+a+1.  The rows 0..a of every
+ * sublayer output become a history block (the last m_rounds blocks are kept).
+ * out_pred: host int32[gamma+1] target argmaxes; out_n_accepted: a.
+ */
+ks_status ks_verify(ks_ctx* ctx, const int32_t* tokens, int gamma, int32_t* out_pred,
+                    int* out_n_accepted);
+
+/*
+ * ks_hidden_cos (Section 2): out[g] = (1/r) sum_t cos(X[g][t], Y[t]) for
+ * g < groups; X device float32 [groups][r][d], Y device float32 [r][d], out
+ * device float32 [groups].  A row with zero norm contributes 0.  Row sums are
+ * accumulated in float64.  Asynchronous on stream.
+ */
+ks_status ks_hidden_cos(const float* X, const float* Y, int groups, int r, int d, float* out,
+                        void* stream);
+
+/*
+ * ks_knapsack_select (Section 3.3-3.5, Algorithms 1 and 2 of Appendix D): on
+ * the current history (r rows at positions n-r..n-1) computes integer weights
+ * from the latency model at the committed length n, runs the model-mode DP over
+ * budgets j = 0..J (J = C/2 with prune_half): cell (i, j) takes the execute
+ * candidate f^(i)(g[i-1, j]) unless the skip candidate g[i-1, j - w_i] has a
+ * strictly higher cosine with X^(i); candidates with cosine <= tau are dropped;
+ * g[i, 0] = X^(i).  Attention of a candidate row at position p reads the target
+ * cache below p and the row's own key/value at p.  Stage 2 backtracks every
+ * reachable terminal cell, estimates alpha by argmax agreement with X^(2L)
+ * (Eq. acceptance) and maximises Eq. TPT over gamma = 1..D (first strict max).
+ * dbg may be NULL.
+ */
+ks_status ks_knapsack_select(ks_ctx* ctx, const ks_select_params* p, ks_selection* out,
+                             ks_selection_debug* dbg);
+
+/*
+ * ks_generate: greedy self-speculative generation (Sections 2.1 and 3): prefill,
+ * a first selection, then rounds of gamma draft steps with the selected mask
+ * and one verify, re-selecting at the first round boundary after the number of
+ * generated tokens crosses a multiple of reselect_every.  gamma = 0 runs plain
+ * greedy autoregressive decoding on the same kernels (p may then be NULL).
+ * out_tokens: host int32[n_new] (the first is the prefill's token).
+ * sel_log: optional host array of max_sel_log selections (may be NULL).
+ */
+ks_status ks_generate(ks_ctx* ctx, const int32_t* prompt, int n_prompt, int n_new, int gamma,
+                      int reselect_every, const ks_select_params* p, int32_t* out_tokens,
+                      ks_gen_stats* stats, ks_selection* sel_log, int max_sel_log);
+
+/* ---- lower-level calls (per-sublayer parity and latency profiling) ------- */
+/*
+ * ks_sublayer_apply: applies sublayer i (1..2L) to R rows of the residual
+ * stream x_in (device float32 [R][d]) at positions pos (host int32[R]), writing
+ * x_out (device float32 [R][d], may equal x_in).  mode 0: rows store their
+ * keys/values at their positions, then row t attends cache positions
+ * 0..pos[t] (decode / verify semantics).  mode 1: nothing is stored; row t
+ * attends cache positions 0..pos[t]-1 plus its own key/value (selection-DP
+ * semantics).  R <= 16 uses the decode kernels, larger R the batched ones.
+ */
+ks_status ks_sublayer_apply(ks_ctx* ctx, int i, const float* x_in, float* x_out,
+                            const int32_t* pos, int R, int mode);
+/*
+ * ks_head_rows: final RMSNorm + LM head + greedy argmax over R rows of x
+ * (device float32 [R][d]).  logits (device float32 [R][vocab]) may be NULL
+ * (then a workspace buffer is used); argmax (device int32[R]) and top1 (device
+ * float32[R], probability of the argmax token) must be valid.  Lowest index
+ * wins ties.
+ */
+ks_status ks_head_rows(ks_ctx* ctx, const float* x, int R, float* logits, int32_t* argmax,
+                       float* top1);
+
+/* ---- isolated integer knapsack (batched) -------------------------------- */
+/*
+ * ks_knapsack_quantize (host): per instance b, Delta_b = sum_i t[b][i] / bins,
+ * w[b][i] = max(1, floor(t[b][i]/Delta_b + 1/2)) (Section 3.4, BINS mode) and the
+ * integer loss q[b][i] = floor(-ln(s[b][i]) 2^24 + 1/2) of skipping item i, whose
+ * similarity score is s in (0, 1].  All arrays host, [B][n] row-major.
+ */
+ks_status ks_knapsack_quantize(const double* t, const double* s, int B, int n, int bins,
+                               int32_t* w, int32_t* q);
+/*
+ * ks_knapsack_batch (Eq. objective_knapsack in isolation, parallel over the
+ * capacity axis): for every instance b (device arrays w, q int32 [B][n]) and
+ * budget j = 0..C, best[b][j] = minimum total loss of a skip set whose weights
+ * sum to exactly j (INT32_MAX if none or j > max_skip).  Recurrence over items
+ * i = 0..n-1: skip item i at budget j iff j >= w_i and
+ * best_{i-1}[j - w_i] + q_i < best_{i-1}[j] (strict; ties keep the item).
+ * bits[b][i][j/64] bit j%64 records that decision (uint64 words, C/64 + 1 per
+ * item).  Requires C <= 16383, n <= 4096, total loss < 2^31.  Asynchronous.
+ */
+ks_status ks_knapsack_batch(const int32_t* w, const int32_t* q, int B, int n, int C,
+                            int max_skip, int32_t* best, uint64_t* bits, void* stream);
+/*
+ * ks_knapsack_backtrack: skip[b][i] (device uint8 [B][n]) of budget j[b]
+ * (device int32 [B]) from the decision bits, following items n-1 down to 0.
+ * Writes err[b] = 0, or 1 if the walk does not end at budget 0 or j[b] is out
+ * of range (device int32 [B]).  Asynchronous.
+ */
+ks_status ks_knapsack_backtrack(const uint64_t* bits, const int32_t* w, int B, int n, int C,
+                                const int32_t* j, uint8_t* skip, int32_t* err, void* stream);
+/*
+ * ks_knapsack_batch_select (stage 2 with the surrogate acceptance
+ * alpha_j = prod_{i skipped} s_i, float64, ascending i): for every instance,
+ * every reachable budget j and gamma = 1..D, TPT = (sum_{k<=gamma} alpha^k) /
+ * (gamma (W - j) + W) with W = sum_i w_i; j ascending, gamma ascending, first
+ * strict maximum wins.  Outputs j_star, gamma_star (int32 [B]), tpt (double
+ * [B]) and skip (uint8 [B][n]); s is device double [B][n].  Asynchronous.
+ */
+ks_status ks_knapsack_batch_select(const int32_t* best, const uint64_t* bits, const int32_t* w,
+                                   const double* s, int B, int n, int C, int D,
+                                   int32_t* j_star, int32_t* gamma_star, double* tpt,
+                                   uint8_t* skip, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* KNAPSPEC_H */

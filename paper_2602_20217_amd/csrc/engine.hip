@@ -1,0 +1,957 @@
+// libknapspec engine: context, workspace layout, the forward passes of the
+// self-speculative decode step, the knapsack selection and the C ABI.
+//
+//  decode / draft (1 row) and verify (gamma+1 rows): skinny MFMA products,
+//      128-position attention splits; identical per-row arithmetic, so greedy
+//      speculative output equals greedy AR output bit for bit.
+//  prefill (chunks) and selection DP (cells x history rows): tiled MFMA
+//      products, 1024-position attention splits.
+//  selection (Sections 3.3-3.5): the DP runs on the GPU one sublayer at a
+//      time over the reachable budgets only; per-cell cosines come back to the
+//      host, which applies Eq. dp_main with the tau / C/2 pruning, records the
+//      decision bits and launches one gather of the surviving states.  Stage 2
+//      (backtrack, alpha-hat, TPT grid) runs on the host from the bits and the
+//      GPU's argmax rows.
+#include "ks_internal.h"
+
+#include <algorithm>
+#include <chrono>
+#include <cmath>
+#include <limits>
+
+namespace ks {
+static thread_local std::string g_err;
+void set_error(const std::string& m) { g_err = m; }
+}  // namespace ks
+
+using namespace ks;
+
+#define REQ(cond, msg)        \
+  do {                        \
+    if (!(cond)) {            \
+      set_error(msg);         \
+      return KS_EINVAL;       \
+    }                         \
+  } while (0)
+#define HIPCHK(x)                                                          \
+  do {                                                                     \
+    hipError_t e_ = (x);                                                   \
+    if (e_ != hipSuccess) {                                                \
+      set_error(std::string(#x) + ": " + hipGetErrorString(e_));           \
+      return KS_EHIP;                                                      \
+    }                                                                      \
+  } while (0)
+
+namespace {
+
+constexpr int PB = 512;        // rows per batched attention / head pass
+constexpr int DEC_TILES = 1;   // decode/verify: 128 positions per split
+constexpr int BAT_TILES = 8;   // prefill/DP: 1024 positions per split
+
+size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
+
+struct Layout {
+  size_t rope, x, a1hi, a1lo, a2hi, a2lo, qkv, q, kvself, part, logits, am, top1;
+  size_t tok, pos, len, stage, hist, xh, g0, g1, ge, dpos, dlen, sig, ptrs, total;
+  int FR, RING, cells, DR, XR, LR, nqkv, a2w, part_rows;
+  size_t part_elems;
+};
+
+Layout make_layout(const ks_model_desc& d, const ks_limits& lim) {
+  Layout y{};
+  const int gam1 = lim.gamma_max + 1;
+  y.FR = std::max(std::max(lim.prefill_chunk, gam1), 16);
+  y.RING = (2 * lim.m_rounds - 1) * gam1;
+  y.cells = lim.cap_max + 1;
+  y.DR = y.cells * y.RING;
+  y.XR = std::max(y.FR, y.DR);
+  y.LR = std::max(gam1, PB);
+  y.nqkv = (d.hq + 2 * d.hkv) * d.hd;
+  y.a2w = std::max(d.hq * d.hd, d.ffn);
+  const int ns_dec = attn_nsplit(d.n_max, DEC_TILES);
+  const int ns_bat = attn_nsplit(d.n_max, BAT_TILES);
+  y.part_rows = PB;
+  y.part_elems = std::max((size_t)16 * d.hq * ns_dec, (size_t)PB * d.hq * ns_bat) * (d.hd + 2);
+  const size_t es = d.dtype == KS_BF16 ? 2 : 4;
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    size_t r = o;
+    o = align_up(o + bytes);
+    return r;
+  };
+  y.rope = take((size_t)d.n_max * (d.hd / 2) * 2 * 4);
+  y.x = take((size_t)y.XR * d.d * 4);
+  y.a1hi = take((size_t)y.XR * d.d * (es == 4 ? 4 : 2));
+  y.a1lo = take((size_t)y.XR * d.d * 2);
+  y.a2hi = take((size_t)y.XR * y.a2w * (es == 4 ? 4 : 2));
+  y.a2lo = take((size_t)y.XR * y.a2w * 2);
+  y.qkv = take((size_t)y.XR * y.nqkv * 4);
+  y.q = take((size_t)y.XR * d.hq * d.hd * 4);
+  y.kvself = take((size_t)y.XR * 2 * d.hkv * d.hd * 4);
+  y.part = take(y.part_elems * 4);
+  y.logits = take((size_t)y.LR * d.vocab * 4);
+  y.am = take((size_t)(y.XR + y.RING + 64) * 4);
+  y.top1 = take((size_t)(y.XR + 64) * 4);
+  y.tok = take((size_t)(y.FR + 64) * 4);
+  y.pos = take((size_t)y.XR * 4);
+  y.len = take((size_t)y.XR * 4);
+  y.stage = take((size_t)(2 * d.L + 1) * gam1 * d.d * 4);
+  y.hist = take((size_t)(2 * d.L + 1) * y.RING * d.d * 4);
+  y.xh = take((size_t)(2 * d.L + 1) * y.RING * d.d * 4);
+  y.g0 = take((size_t)y.DR * d.d * 4);
+  y.g1 = take((size_t)y.DR * d.d * 4);
+  y.ge = take((size_t)y.DR * d.d * 4);
+  y.dpos = take((size_t)y.DR * 4);
+  y.dlen = take((size_t)y.DR * 4);
+  y.sig = take((size_t)2 * y.cells * 8);
+  y.ptrs = take((size_t)4 * (y.cells + 2 * d.L + 2) * 8);
+  y.total = o;
+  return y;
+}
+
+}  // namespace
+
+struct ks_ctx {
+  ks_model_desc md;
+  ks_limits lim;
+  hipStream_t st;
+  const void* embed;
+  const void* lm_head;
+  const float* final_norm;
+  std::vector<const void*> wqkv, wo, wgu, wdown;
+  std::vector<const float*> attn_norm, mlp_norm, q_norm, k_norm;
+  char* kv;
+  char* ws;
+  Layout y;
+  int32_t* pin = nullptr;  // pinned host staging: [0,16) draft tokens, [16,32) verify argmax
+  // decode state
+  bool ready = false;
+  int P = 0;
+  int32_t s = 0;
+  int k_draft = 0;
+  std::deque<std::pair<int, int>> blocks;  // (first position, rows)
+
+  template <typename T>
+  T* at(size_t off) const { return (T*)(ws + off); }
+  bool bf() const { return md.dtype == KS_BF16; }
+  size_t es() const { return bf() ? 2 : 4; }
+  void* kc(int l) const {
+    return kv + (size_t)l * 2 * md.hkv * md.n_max * md.hd * es();
+  }
+  void* vc(int l) const {
+    return kv + ((size_t)l * 2 + 1) * md.hkv * md.n_max * md.hd * es();
+  }
+  Act act1() const { return Act{ws + y.a1hi, ws + y.a1lo, md.d}; }
+  Act act2() const { return Act{ws + y.a2hi, ws + y.a2lo, y.a2w}; }
+  float* hist_row(int i, int slot) const {
+    return at<float>(y.hist) + ((size_t)i * y.RING + slot) * md.d;
+  }
+  float* stage_row(int i, int k) const {
+    return at<float>(y.stage) + ((size_t)i * (lim.gamma_max + 1) + k) * md.d;
+  }
+};
+
+namespace {
+
+// ---------------------------------------------------------- forward pieces
+void gemm(ks_ctx* c, int M, int N, int K, Act A, const void* W, int epi, float* out, int ldo,
+          const float* res, int ldres, Act aout, bool batched) {
+  GemmArgs g{M, N, K, A, W, epi, out, ldo, res, ldres, aout};
+  if (!c->bf()) gemm_f32(g, c->st);
+  else if (!batched && M <= 16) gemm_bf16_skinny(g, c->st);
+  else gemm_bf16_tiled(g, c->st);
+}
+
+// Attention sublayer of layer l on R rows: x_out = x_in + Wo attn(...).
+// mode 0: keys/values stored at pos; mode 1: own key/value (selection DP).
+void attn_rows(ks_ctx* c, int l, const float* xin, float* xout, int R, const int32_t* pos,
+               const int32_t* len, int max_len, int mode, bool batched) {
+  const ks_model_desc& d = c->md;
+  const Act a1 = c->act1(), a2 = c->act2();
+  float* qkv = c->at<float>(c->y.qkv);
+  float* q = c->at<float>(c->y.q);
+  float* kvs = c->at<float>(c->y.kvself);
+  norm_act(xin, d.d, c->attn_norm[l], d.eps, R, d.d, d.dtype, a1, c->st);
+  gemm(c, R, c->y.nqkv, d.d, a1, c->wqkv[l], EPI_STORE, qkv, c->y.nqkv, nullptr, 0, Act{}, batched);
+  QkvPostArgs qp{R, d.hq, d.hkv, d.hd, d.n_max, d.dtype, d.qk_norm, d.eps, qkv,
+                 c->at<float>(c->y.rope), c->q_norm[l], c->k_norm[l], pos, q,
+                 c->kc(l), c->vc(l), kvs, mode};
+  qkv_post(qp, c->st);
+  const int tiles = batched ? BAT_TILES : DEC_TILES;
+  const int ns = attn_nsplit(d.n_max, tiles);
+  const int step = batched ? PB : 16;
+  for (int r0 = 0; r0 < R; r0 += step) {
+    const int rr = std::min(step, R - r0);
+    AttnArgs aa{rr, d.hq, d.hkv, d.hd, d.n_max, d.dtype,
+                q + (size_t)r0 * d.hq * d.hd, c->kc(l), c->vc(l), len + r0, max_len, tiles,
+                64 / (d.hq / d.hkv) < 16 ? 64 / (d.hq / d.hkv) : 16, c->at<float>(c->y.part), ns};
+    attn_split(aa, c->st);
+    Act out2 = a2;
+    const size_t off = (size_t)r0 * a2.ld * (c->bf() ? 2 : 4);
+    out2.hi = (char*)a2.hi + off;
+    out2.lo = c->bf() ? (char*)a2.lo + (size_t)r0 * a2.ld * 2 : nullptr;
+    attn_combine(aa, mode == 1 ? kvs + (size_t)r0 * 2 * d.hkv * d.hd : nullptr, out2, c->st);
+  }
+  gemm(c, R, d.d, d.hq * d.hd, a2, c->wo[l], EPI_RESID, xout, d.d, xin, d.d, Act{}, batched);
+}
+
+void mlp_rows(ks_ctx* c, int l, const float* xin, float* xout, int R, bool batched) {
+  const ks_model_desc& d = c->md;
+  const Act a1 = c->act1(), a2 = c->act2();
+  norm_act(xin, d.d, c->mlp_norm[l], d.eps, R, d.d, d.dtype, a1, c->st);
+  gemm(c, R, 2 * d.ffn, d.d, a1, c->wgu[l], EPI_SWIGLU, nullptr, 0, nullptr, 0, a2, batched);
+  gemm(c, R, d.d, d.ffn, a2, c->wdown[l], EPI_RESID, xout, d.d, xin, d.d, Act{}, batched);
+}
+
+void sublayer_rows(ks_ctx* c, int i, const float* xin, float* xout, int R, const int32_t* pos,
+                   const int32_t* len, int max_len, int mode, bool batched) {
+  const int l = (i - 1) / 2;
+  if (i % 2 == 1) attn_rows(c, l, xin, xout, R, pos, len, max_len, mode, batched);
+  else mlp_rows(c, l, xin, xout, R, batched);
+}
+
+// final norm + LM head + argmax for R rows (chunked by the logits buffer)
+void head_rows(ks_ctx* c, const float* x, int R, float* logits_out, int32_t* am, float* top1,
+               bool batched) {
+  const ks_model_desc& d = c->md;
+  const Act a1 = c->act1();
+  const int step = logits_out ? R : c->y.LR;
+  for (int r0 = 0; r0 < R; r0 += step) {
+    const int rr = std::min(step, R - r0);
+    float* lg = logits_out ? logits_out : c->at<float>(c->y.logits);
+    norm_act(x + (size_t)r0 * d.d, d.d, c->final_norm, d.eps, rr, d.d, d.dtype, a1, c->st);
+    gemm(c, rr, d.vocab, d.d, a1, c->lm_head, EPI_STORE, lg, d.vocab, nullptr, 0, Act{},
+         batched || rr > 16);
+    argmax_rows(lg, rr, d.vocab, am + r0, top1 ? top1 + r0 : nullptr, c->st);
+  }
+}
+
+// one decode row at position p from token tok_dev[0]; writes argmax to am_out
+void decode_row(ks_ctx* c, const int32_t* tok_dev, int p, const uint8_t* exec, int32_t* am_out,
+                float* top1_out) {
+  const ks_model_desc& d = c->md;
+  float* x = c->at<float>(c->y.x);
+  int32_t* pos = c->at<int32_t>(c->y.pos);
+  int32_t* len = c->at<int32_t>(c->y.len);
+  fill_pos(pos, len, p, 1, 1, 1, c->st);
+  embed_rows(c->embed, d.dtype, tok_dev, 1, d.d, x, d.d, c->st);
+  for (int i = 1; i <= 2 * d.L; ++i)
+    if (!exec || exec[i - 1]) sublayer_rows(c, i, x, x, 1, pos, len, p + 1, 0, false);
+  head_rows(c, x, 1, nullptr, am_out, top1_out, false);
+}
+
+// verify rows of tokens tok_dev[0..R) at positions P..P+R-1, snapshots into stage
+void verify_rows(ks_ctx* c, const int32_t* tok_dev, int R, int32_t* am_out) {
+  const ks_model_desc& d = c->md;
+  int32_t* pos = c->at<int32_t>(c->y.pos);
+  int32_t* len = c->at<int32_t>(c->y.len);
+  fill_pos(pos, len, c->P, R, R, 1, c->st);
+  embed_rows(c->embed, d.dtype, tok_dev, R, d.d, c->stage_row(0, 0), d.d, c->st);
+  for (int i = 1; i <= 2 * d.L; ++i)
+    sublayer_rows(c, i, c->stage_row(i - 1, 0), c->stage_row(i, 0), R, pos, len, c->P + R, 0,
+                  false);
+  head_rows(c, c->stage_row(2 * d.L, 0), R, nullptr, am_out, nullptr, false);
+}
+
+// copy rows [0, n) of plane set src (row stride ld_src rows per plane) into the
+// history ring at positions p0..p0+n-1 for every sublayer output
+hipError_t stash_history(ks_ctx* c, const float* src0, size_t plane_stride_rows, int n, int p0) {
+  const ks_model_desc& d = c->md;
+  const size_t row_bytes = (size_t)d.d * 4;
+  int done = 0;
+  while (done < n) {
+    const int slot = (p0 + done) % c->y.RING;
+    const int run = std::min(n - done, c->y.RING - slot);
+    for (int i = 0; i <= 2 * d.L; ++i) {
+      hipError_t e = hipMemcpyAsync(c->hist_row(i, slot),
+                                    src0 + ((size_t)i * plane_stride_rows + done) * d.d,
+                                    run * row_bytes, hipMemcpyDeviceToDevice, c->st);
+      if (e != hipSuccess) return e;
+    }
+    done += run;
+  }
+  return hipSuccess;
+}
+
+int hist_rows(const ks_ctx* c) {
+  int r = 0;
+  for (auto& b : c->blocks) r += b.second;
+  return r;
+}
+
+}  // namespace
+
+// =============================================================== C ABI
+extern "C" {
+
+const char* ks_last_error(void) { return g_err.c_str(); }
+
+static ks_status check_desc(const ks_model_desc* d) {
+  REQ(d, "desc is null");
+  REQ(d->L >= 1 && 2 * d->L <= KS_MAX_SUBLAYERS, "L out of range");
+  REQ(d->hq >= 1 && d->hkv >= 1 && d->hq % d->hkv == 0, "hq must be a multiple of hkv");
+  REQ(d->hq / d->hkv <= 64, "query heads per kv head must be <= 64");
+  REQ(d->dtype == KS_F32 || d->dtype == KS_BF16, "dtype must be KS_F32 or KS_BF16");
+  REQ((d->dtype == KS_BF16 && d->hd == 128) || (d->dtype == KS_F32 && d->hd == 64),
+      "supported head dims: 128 for bf16 models, 64 for float32 models");
+  REQ(d->d >= 32 && d->d % 32 == 0, "d must be a positive multiple of 32");
+  REQ(d->ffn >= 32 && d->ffn % 32 == 0, "ffn must be a positive multiple of 32");
+  REQ((d->hq * d->hd) % 32 == 0, "hq*hd must be a multiple of 32");
+  REQ(d->vocab >= 16 && d->vocab % 16 == 0, "vocab must be a positive multiple of 16");
+  REQ(d->n_max >= 2, "n_max must be >= 2");
+  REQ(d->eps >= 0.f, "eps must be >= 0");
+  REQ(d->rope_theta > 0.0, "rope_theta must be > 0");
+  return KS_OK;
+}
+
+static ks_status check_lim(const ks_limits* l) {
+  REQ(l, "limits is null");
+  REQ(l->gamma_max >= 0 && l->gamma_max <= 15, "gamma_max must be in [0, 15]");
+  REQ(l->m_rounds >= 1 && l->m_rounds <= 64, "m_rounds must be in [1, 64]");
+  REQ(l->cap_max >= 1 && l->cap_max <= 8192, "cap_max must be in [1, 8192]");
+  REQ(l->prefill_chunk >= 16 && l->prefill_chunk <= 4096 && l->prefill_chunk % 16 == 0,
+      "prefill_chunk must be a multiple of 16 in [16, 4096]");
+  return KS_OK;
+}
+
+size_t ks_kv_cache_bytes(const ks_model_desc* d) {
+  if (check_desc(d) != KS_OK) return 0;
+  return (size_t)d->L * 2 * d->hkv * d->n_max * d->hd * (d->dtype == KS_BF16 ? 2 : 4);
+}
+
+size_t ks_workspace_bytes(const ks_model_desc* d, const ks_limits* l) {
+  if (check_desc(d) != KS_OK || check_lim(l) != KS_OK) return 0;
+  return make_layout(*d, *l).total;
+}
+
+ks_status ks_pack_matrix(const void* src, void* dst, int N, int K, int dtype, void* stream) {
+  REQ(src && dst, "null pointer");
+  REQ(N > 0 && K > 0, "N and K must be positive");
+  REQ(dtype == KS_F32 || dtype == KS_BF16, "bad dtype");
+  hipStream_t st = (hipStream_t)stream;
+  if (dtype == KS_F32) {
+    HIPCHK(hipMemcpyAsync(dst, src, (size_t)N * K * 4, hipMemcpyDeviceToDevice, st));
+    return KS_OK;
+  }
+  REQ(N % 16 == 0 && K % 32 == 0, "bf16 packing needs N % 16 == 0 and K % 32 == 0");
+  pack_matrix_bf16((const bf16_t*)src, (bf16_t*)dst, N, K, st);
+  HIPCHK(hipGetLastError());
+  return KS_OK;
+}
+
+ks_status ks_pack_gate_up(const void* gate, const void* up, void* dst, int ffn, int d, int dtype,
+                          void* stream) {
+  REQ(gate && up && dst, "null pointer");
+  REQ(ffn > 0 && d > 0, "sizes must be positive");
+  REQ(dtype == KS_F32 || dtype == KS_BF16, "bad dtype");
+  hipStream_t st = (hipStream_t)stream;
+  if (dtype == KS_F32) {
+    const size_t b = (size_t)ffn * d * 4;
+    HIPCHK(hipMemcpyAsync(dst, gate, b, hipMemcpyDeviceToDevice, st));
+    HIPCHK(hipMemcpyAsync((char*)dst + b, up, b, hipMemcpyDeviceToDevice, st));
+    return KS_OK;
+  }
+  REQ(ffn % 16 == 0 && d % 32 == 0, "bf16 packing needs ffn % 16 == 0 and d % 32 == 0");
+  pack_gate_up_bf16((const bf16_t*)gate, (const bf16_t*)up, (bf16_t*)dst, ffn, d, st);
+  HIPCHK(hipGetLastError());
+  return KS_OK;
+}
+
+ks_status ks_create(const ks_model_desc* desc, const ks_limits* lim, const ks_weights* w,
+                    void* kv_cache, size_t kv_bytes, void* workspace, size_t ws_bytes,
+                    void* stream, ks_ctx** out) {
+  ks_status s = check_desc(desc);
+  if (s != KS_OK) return s;
+  s = check_lim(lim);
+  if (s != KS_OK) return s;
+  REQ(w && out && kv_cache && workspace, "null pointer");
+  REQ(w->embed && w->lm_head && w->final_norm && w->attn_norm && w->wqkv && w->wo &&
+          w->mlp_norm && w->w_gate_up && w->w_down,
+      "null weight pointer");
+  for (int l = 0; l < desc->L; ++l) {
+    REQ(w->attn_norm[l] && w->wqkv[l] && w->wo[l] && w->mlp_norm[l] && w->w_gate_up[l] &&
+            w->w_down[l],
+        "null per-layer weight pointer");
+    if (desc->qk_norm) REQ(w->q_norm && w->k_norm && w->q_norm[l] && w->k_norm[l], "qk_norm gains missing");
+  }
+  const Layout y = make_layout(*desc, *lim);
+  if (kv_bytes < ks_kv_cache_bytes(desc)) {
+    set_error("kv cache smaller than ks_kv_cache_bytes");
+    return KS_ENOMEM;
+  }
+  if (ws_bytes < y.total) {
+    set_error("workspace smaller than ks_workspace_bytes");
+    return KS_ENOMEM;
+  }
+  ks_ctx* c = new ks_ctx();
+  c->md = *desc;
+  c->lim = *lim;
+  c->st = (hipStream_t)stream;
+  c->embed = w->embed;
+  c->lm_head = w->lm_head;
+  c->final_norm = w->final_norm;
+  for (int l = 0; l < desc->L; ++l) {
+    c->wqkv.push_back(w->wqkv[l]);
+    c->wo.push_back(w->wo[l]);
+    c->wgu.push_back(w->w_gate_up[l]);
+    c->wdown.push_back(w->w_down[l]);
+    c->attn_norm.push_back(w->attn_norm[l]);
+    c->mlp_norm.push_back(w->mlp_norm[l]);
+    c->q_norm.push_back(desc->qk_norm ? w->q_norm[l] : nullptr);
+    c->k_norm.push_back(desc->qk_norm ? w->k_norm[l] : nullptr);
+  }
+  c->kv = (char*)kv_cache;
+  c->ws = (char*)workspace;
+  c->y = y;
+  hipError_t he = hipHostMalloc((void**)&c->pin, 4096, hipHostMallocDefault);
+  if (he != hipSuccess) {
+    set_error(std::string("pinned staging: ") + hipGetErrorString(he));
+    delete c;
+    return KS_EHIP;
+  }
+  rope_table(c->at<float>(y.rope), desc->n_max, desc->hd, desc->rope_theta, c->st);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) {
+    set_error(std::string("rope table: ") + hipGetErrorString(e));
+    (void)hipHostFree(c->pin);
+    delete c;
+    return KS_EHIP;
+  }
+  *out = c;
+  return KS_OK;
+}
+
+ks_status ks_destroy(ks_ctx* c) {
+  REQ(c, "ctx is null");
+  if (c->pin) (void)hipHostFree(c->pin);
+  delete c;
+  return KS_OK;
+}
+
+ks_status ks_prefill(ks_ctx* c, const int32_t* tokens, int n, int32_t* out_first) {
+  REQ(c && tokens, "null pointer");
+  const ks_model_desc& d = c->md;
+  REQ(n >= 1, "prompt must have at least one token");
+  if (n >= d.n_max) {
+    set_error("prompt does not fit the KV cache");
+    return KS_ECAPACITY;
+  }
+  for (int t = 0; t < n; ++t) REQ(tokens[t] >= 0 && tokens[t] < d.vocab, "token id out of range");
+  const int FR = c->lim.prefill_chunk;
+  const int r0 = std::min(n, c->lim.m_rounds * (c->lim.gamma_max + 1));
+  float* x = c->at<float>(c->y.x);
+  int32_t* tok = c->at<int32_t>(c->y.tok);
+  int32_t* pos = c->at<int32_t>(c->y.pos);
+  int32_t* len = c->at<int32_t>(c->y.len);
+  int32_t* am = c->at<int32_t>(c->y.am);
+  for (int c0 = 0; c0 < n; c0 += FR) {
+    const int R = std::min(FR, n - c0);
+    HIPCHK(hipMemcpyAsync(tok, tokens + c0, R * 4, hipMemcpyHostToDevice, c->st));
+    fill_pos(pos, len, c0, R, R, 1, c->st);
+    embed_rows(c->embed, d.dtype, tok, R, d.d, x, d.d, c->st);
+    const int h0 = std::max(c0, n - r0);  // first history row in this chunk
+    for (int i = 0; i <= 2 * d.L; ++i) {
+      if (i > 0) sublayer_rows(c, i, x, x, R, pos, len, c0 + R, 0, true);
+      for (int p = h0; p < c0 + R;) {
+        const int slot = p % c->y.RING;
+        const int run = std::min(c0 + R - p, c->y.RING - slot);
+        HIPCHK(hipMemcpyAsync(c->hist_row(i, slot), x + (size_t)(p - c0) * d.d,
+                              (size_t)run * d.d * 4, hipMemcpyDeviceToDevice, c->st));
+        p += run;
+      }
+    }
+    if (c0 + R == n) head_rows(c, x + (size_t)(R - 1) * d.d, 1, nullptr, am, nullptr, false);
+  }
+  HIPCHK(hipGetLastError());
+  int32_t first = 0;
+  HIPCHK(hipMemcpyAsync(&first, am, 4, hipMemcpyDeviceToHost, c->st));
+  HIPCHK(hipStreamSynchronize(c->st));
+  c->P = n;
+  c->s = first;
+  c->k_draft = 0;
+  c->blocks.clear();
+  c->blocks.push_back({n - r0, r0});
+  c->ready = true;
+  if (out_first) *out_first = first;
+  return KS_OK;
+}
+
+ks_status ks_set_context(ks_ctx* c, int n_cached, int32_t last_token) {
+  REQ(c, "ctx is null");
+  REQ(n_cached >= 0, "n_cached must be >= 0");
+  if (n_cached >= c->md.n_max) {
+    set_error("n_cached exceeds the KV cache");
+    return KS_ECAPACITY;
+  }
+  REQ(last_token >= 0 && last_token < c->md.vocab, "token id out of range");
+  c->P = n_cached;
+  c->s = last_token;
+  c->k_draft = 0;
+  c->blocks.clear();
+  c->ready = true;
+  return KS_OK;
+}
+
+static ks_status draft_internal(ks_ctx* c, const uint8_t* exec) {
+  int32_t* dt = c->at<int32_t>(c->y.tok);
+  if (c->k_draft == 0) set_i32(dt, c->s, c->st);
+  decode_row(c, dt + c->k_draft, c->P + c->k_draft, exec, dt + c->k_draft + 1,
+             c->at<float>(c->y.top1) + c->k_draft);
+  c->k_draft++;
+  return KS_OK;
+}
+
+ks_status ks_draft_step(ks_ctx* c, const uint8_t* exec, int32_t* out_token, float* out_top1) {
+  REQ(c && exec, "null pointer");
+  if (!c->ready) {
+    set_error("ks_draft_step before ks_prefill / ks_set_context");
+    return KS_ESTATE;
+  }
+  REQ(c->k_draft < c->lim.gamma_max, "draft longer than gamma_max");
+  if (c->P + c->k_draft + 1 >= c->md.n_max) {
+    set_error("draft position exceeds the KV cache");
+    return KS_ECAPACITY;
+  }
+  draft_internal(c, exec);
+  HIPCHK(hipGetLastError());
+  int32_t t = 0;
+  float p = 0.f;
+  HIPCHK(hipMemcpyAsync(&t, c->at<int32_t>(c->y.tok) + c->k_draft, 4, hipMemcpyDeviceToHost, c->st));
+  HIPCHK(hipMemcpyAsync(&p, c->at<float>(c->y.top1) + c->k_draft - 1, 4, hipMemcpyDeviceToHost, c->st));
+  HIPCHK(hipStreamSynchronize(c->st));
+  if (out_token) *out_token = t;
+  if (out_top1) *out_top1 = p;
+  return KS_OK;
+}
+
+// verify the gamma+1 tokens already in the device token buffer; host copies of
+// the drafts in toks (toks[0] = s)
+static ks_status verify_internal(ks_ctx* c, const int32_t* toks, int gamma, int32_t* out_pred,
+                                 int* out_a) {
+  const int R = gamma + 1;
+  int32_t* am = c->at<int32_t>(c->y.am);
+  verify_rows(c, c->at<int32_t>(c->y.tok), R, am);
+  HIPCHK(hipGetLastError());
+  int32_t* y = c->pin + 16;
+  HIPCHK(hipMemcpyAsync(y, am, R * 4, hipMemcpyDeviceToHost, c->st));
+  HIPCHK(hipStreamSynchronize(c->st));
+  int a = 0;
+  while (a < gamma && toks[a + 1] == y[a]) ++a;
+  HIPCHK(stash_history(c, c->stage_row(0, 0), c->lim.gamma_max + 1, a + 1, c->P));
+  c->blocks.push_back({c->P, a + 1});
+  while ((int)c->blocks.size() > c->lim.m_rounds) c->blocks.pop_front();
+  c->P += a + 1;
+  c->s = y[a];
+  c->k_draft = 0;
+  if (out_pred) std::copy(y, y + R, out_pred);
+  if (out_a) *out_a = a;
+  return KS_OK;
+}
+
+ks_status ks_verify(ks_ctx* c, const int32_t* tokens, int gamma, int32_t* out_pred, int* out_a) {
+  REQ(c && tokens, "null pointer");
+  if (!c->ready) {
+    set_error("ks_verify before ks_prefill / ks_set_context");
+    return KS_ESTATE;
+  }
+  REQ(gamma >= 0 && gamma <= c->lim.gamma_max, "gamma out of range");
+  REQ(tokens[0] == c->s, "tokens[0] must be the committed token");
+  for (int t = 0; t <= gamma; ++t) REQ(tokens[t] >= 0 && tokens[t] < c->md.vocab, "token id out of range");
+  if (c->P + gamma + 1 >= c->md.n_max) {
+    set_error("verify positions exceed the KV cache");
+    return KS_ECAPACITY;
+  }
+  HIPCHK(hipMemcpyAsync(c->at<int32_t>(c->y.tok), tokens, (gamma + 1) * 4, hipMemcpyHostToDevice,
+                        c->st));
+  return verify_internal(c, tokens, gamma, out_pred, out_a);
+}
+
+ks_status ks_hidden_cos(const float* X, const float* Y, int groups, int r, int d, float* out,
+                        void* stream) {
+  REQ(X && Y && out, "null pointer");
+  REQ(groups >= 0 && r >= 1 && r <= 8192 && d >= 1, "sizes out of range (1 <= r <= 8192)");
+  cos_groups(X, Y, groups, r, d, out, (hipStream_t)stream);
+  HIPCHK(hipGetLastError());
+  return KS_OK;
+}
+
+// ------------------------------------------------------------- selection
+static ks_status select_internal(ks_ctx* c, const ks_select_params* p, ks_selection* out,
+                                 ks_selection_debug* dbg) {
+  const ks_model_desc& d = c->md;
+  const int L2 = 2 * d.L;
+  const int r = hist_rows(c);
+  const int n = c->P;
+  // latency weights (Section 3.4, Appendix C)
+  const double ta = p->c2 * n + p->c3, tm = p->c1;
+  REQ(ta > 0 && tm > 0, "latency model gives a non-positive latency");
+  double delta;
+  if (p->quant_mode == KS_QUANT_PAPER_MIN) {
+    delta = std::min(ta, tm);
+  } else {
+    REQ(p->bins >= 1, "bins must be >= 1");
+    delta = d.L * (ta + tm) / p->bins;
+  }
+  const int wa = std::max(1, (int)std::floor(ta / delta + 0.5));
+  const int wm = std::max(1, (int)std::floor(tm / delta + 0.5));
+  const int C = d.L * (wa + wm);
+  if (C > c->lim.cap_max) {
+    set_error("knapsack capacity exceeds cap_max");
+    return KS_ENOMEM;
+  }
+  const int J = p->prune_half ? C / 2 : C;
+  if (dbg) REQ(dbg->J_cap >= J + 1, "debug arrays too small");
+  const int base = n - r;
+  float* Xh = c->at<float>(c->y.xh);  // [2L+1][r][d]
+  // gather history rows into contiguous planes
+  for (int i = 0; i <= L2; ++i) {
+    int done = 0;
+    while (done < r) {
+      const int slot = (base + done) % c->y.RING;
+      const int run = std::min(r - done, c->y.RING - slot);
+      HIPCHK(hipMemcpyAsync(Xh + ((size_t)i * r + done) * d.d, c->hist_row(i, slot),
+                            (size_t)run * d.d * 4, hipMemcpyDeviceToDevice, c->st));
+      done += run;
+    }
+  }
+  auto X = [&](int i) { return Xh + (size_t)i * r * d.d; };
+  int32_t* dpos = c->at<int32_t>(c->y.dpos);
+  int32_t* dlen = c->at<int32_t>(c->y.dlen);
+  fill_pos(dpos, dlen, base, r, c->y.cells * r, 0, c->st);
+  float* gprev = c->at<float>(c->y.g0);
+  float* gnext = c->at<float>(c->y.g1);
+  float* E = c->at<float>(c->y.ge);
+  double* sig = c->at<double>(c->y.sig);
+  const float** ptr_src = c->at<const float*>(c->y.ptrs);
+  float** ptr_dst = (float**)(ptr_src + c->y.cells + 2);
+  const size_t cell = (size_t)r * d.d;
+  HIPCHK(hipMemcpyAsync(gprev, X(0), cell * 4, hipMemcpyDeviceToDevice, c->st));
+  std::vector<int> cells = {0};       // reachable budgets, ascending
+  std::vector<int> idx(J + 1, -1);    // budget -> compact index
+  std::vector<uint8_t> bits((size_t)(L2 + 1) * (J + 1), 0);
+  std::vector<double> se(J + 1), ss(J + 1);
+  std::vector<const float*> hs;
+  std::vector<float*> hd;
+  if (dbg) {
+    for (int j = 0; j < dbg->J_cap; ++j) dbg->n_match[j] = -1;
+    for (int i = 0; i <= L2; ++i)
+      for (int j = 0; j < dbg->J_cap; ++j) {
+        const size_t o = (size_t)i * dbg->J_cap + j;
+        dbg->bits[o] = 0;
+        dbg->reach[o] = (i == 0 && j == 0);
+        dbg->sig_e[o] = std::numeric_limits<double>::quiet_NaN();
+        dbg->sig_s[o] = std::numeric_limits<double>::quiet_NaN();
+      }
+  }
+  for (int i = 1; i <= L2; ++i) {
+    const int w = (i % 2 == 1) ? wa : wm;
+    const int nc = (int)cells.size();
+    const int M = nc * r;
+    // execute candidates for every reachable budget
+    sublayer_rows(c, i, gprev, E, M, dpos, dlen, n, 1, true);
+    cos_groups_f64(E, X(i), nc, r, d.d, sig, c->st);
+    cos_groups_f64(gprev, X(i), nc, r, d.d, sig + c->y.cells, c->st);
+    HIPCHK(hipGetLastError());
+    std::vector<double> hsig(2 * (size_t)c->y.cells);
+    HIPCHK(hipMemcpyAsync(hsig.data(), sig, 2 * c->y.cells * 8, hipMemcpyDeviceToHost, c->st));
+    HIPCHK(hipStreamSynchronize(c->st));
+    std::fill(idx.begin(), idx.end(), -1);
+    for (int k = 0; k < nc; ++k) idx[cells[k]] = k;
+    std::vector<int> ncells;
+    hs.clear();
+    hd.clear();
+    for (int j = 0; j <= J; ++j) {
+      const int ie = idx[j];
+      const int is = j >= w ? idx[j - w] : -1;
+      const double sge = ie >= 0 ? hsig[ie] : std::numeric_limits<double>::quiet_NaN();
+      const double sgs = is >= 0 ? hsig[c->y.cells + is] : std::numeric_limits<double>::quiet_NaN();
+      const bool e_ok = ie >= 0 && sge > (double)p->tau;
+      const bool s_ok = is >= 0 && sgs > (double)p->tau;
+      const float* src = nullptr;
+      uint8_t bit = 0;
+      if (j == 0) {
+        src = X(i);  // g[i, 0] = X^(i)
+      } else if (e_ok && (!s_ok || sge >= sgs)) {
+        src = E + (size_t)ie * cell;
+      } else if (s_ok) {
+        src = gprev + (size_t)is * cell;
+        bit = 1;
+      }
+      if (dbg) {
+        const size_t o = (size_t)i * dbg->J_cap + j;
+        dbg->sig_e[o] = sge;
+        dbg->sig_s[o] = sgs;
+        dbg->bits[o] = bit;
+        dbg->reach[o] = src != nullptr;
+      }
+      bits[(size_t)i * (J + 1) + j] = bit;
+      if (src) {
+        hd.push_back(gnext + (size_t)ncells.size() * cell);
+        hs.push_back(src);
+        ncells.push_back(j);
+      }
+    }
+    HIPCHK(hipMemcpyAsync(ptr_src, hs.data(), hs.size() * 8, hipMemcpyHostToDevice, c->st));
+    HIPCHK(hipMemcpyAsync(ptr_dst, hd.data(), hd.size() * 8, hipMemcpyHostToDevice, c->st));
+    copy_rows(ptr_src, ptr_dst, (int)hs.size(), (int)cell, c->st);
+    std::swap(gprev, gnext);
+    cells.swap(ncells);
+  }
+  // stage 2: argmax rows of terminal states and of X^(2L)
+  const int nc = (int)cells.size();
+  int32_t* am = c->at<int32_t>(c->y.am);
+  head_rows(c, gprev, nc * r, nullptr, am, nullptr, true);
+  head_rows(c, X(L2), r, nullptr, am + (size_t)nc * r, nullptr, true);
+  HIPCHK(hipGetLastError());
+  std::vector<int32_t> ham((size_t)(nc + 1) * r);
+  HIPCHK(hipMemcpyAsync(ham.data(), am, ham.size() * 4, hipMemcpyDeviceToHost, c->st));
+  HIPCHK(hipStreamSynchronize(c->st));
+  const int32_t* yref = ham.data() + (size_t)nc * r;
+  double best = 0.0;
+  int bj = 0, bg = 1, bm = r;
+  std::vector<uint8_t> bex(L2, 1);
+  for (int k = 0; k < nc; ++k) {
+    const int j = cells[k];
+    int nm = 0;
+    for (int t = 0; t < r; ++t) nm += ham[(size_t)k * r + t] == yref[t];
+    if (dbg) dbg->n_match[j] = nm;
+    const double a = (double)nm / r;
+    for (int g = 1; g <= p->D; ++g) {
+      double e = 0.0, pw = 1.0;
+      for (int q = 0; q <= g; ++q) {
+        e += pw;
+        pw *= a;
+      }
+      const double v = e / (double)((long long)g * (C - j) + C);
+      if (v > best) {
+        best = v;
+        bj = j;
+        bg = g;
+        bm = nm;
+      }
+    }
+  }
+  // backtrack the winner from sublayer 2L down to 1
+  std::vector<uint8_t> ex(L2, 1);
+  int jj = bj;
+  for (int i = L2; i >= 1; --i) {
+    if (bits[(size_t)i * (J + 1) + jj]) {
+      ex[i - 1] = 0;
+      jj -= (i % 2 == 1) ? wa : wm;
+    }
+  }
+  if (jj != 0) {
+    set_error("internal error: backtrack did not end at budget 0");
+    return KS_ESTATE;
+  }
+  std::memset(out->exec, 0, sizeof(out->exec));
+  std::copy(ex.begin(), ex.end(), out->exec);
+  out->j_star = bj;
+  out->gamma_star = bg;
+  out->C = C;
+  out->w_attn = wa;
+  out->w_mlp = wm;
+  out->n_rows = r;
+  out->n_cells = nc;
+  out->tpt_star = best;
+  out->alpha_hat = (double)bm / r;
+  out->delta = delta;
+  return KS_OK;
+}
+
+ks_status ks_knapsack_select(ks_ctx* c, const ks_select_params* p, ks_selection* out,
+                             ks_selection_debug* dbg) {
+  REQ(c && p && out, "null pointer");
+  if (!c->ready || c->blocks.empty()) {
+    set_error("ks_knapsack_select needs a history (run ks_prefill first)");
+    return KS_ESTATE;
+  }
+  REQ(p->D >= 1 && p->D <= 64, "D must be in [1, 64]");
+  REQ(p->quant_mode == KS_QUANT_PAPER_MIN || p->quant_mode == KS_QUANT_BINS, "bad quant_mode");
+  REQ(!std::isnan(p->tau), "tau is NaN");
+  if (dbg) REQ(dbg->bits && dbg->reach && dbg->sig_e && dbg->sig_s && dbg->n_match, "null debug array");
+  return select_internal(c, p, out, dbg);
+}
+
+ks_status ks_sublayer_apply(ks_ctx* c, int i, const float* x_in, float* x_out, const int32_t* pos,
+                            int R, int mode) {
+  REQ(c && x_in && x_out && pos, "null pointer");
+  const ks_model_desc& d = c->md;
+  REQ(i >= 1 && i <= 2 * d.L, "sublayer index out of range");
+  REQ(R >= 1 && R <= c->y.XR, "R out of range");
+  REQ(mode == 0 || mode == 1, "mode must be 0 or 1");
+  int mx = 0;
+  std::vector<int32_t> hl(R);
+  for (int t = 0; t < R; ++t) {
+    REQ(pos[t] >= 0, "negative position");
+    if (pos[t] + 1 >= d.n_max) {
+      set_error("position exceeds the KV cache");
+      return KS_ECAPACITY;
+    }
+    hl[t] = pos[t] + (mode == 0 ? 1 : 0);
+    mx = std::max(mx, hl[t]);
+  }
+  int32_t* dp = c->at<int32_t>(c->y.pos);
+  int32_t* dl = c->at<int32_t>(c->y.len);
+  HIPCHK(hipMemcpyAsync(dp, pos, R * 4, hipMemcpyHostToDevice, c->st));
+  HIPCHK(hipMemcpyAsync(dl, hl.data(), R * 4, hipMemcpyHostToDevice, c->st));
+  // x_in may alias x_out: every kernel reads a residual element before writing it
+  sublayer_rows(c, i, x_in, x_out, R, dp, dl, mx, mode, R > 16);
+  HIPCHK(hipGetLastError());
+  HIPCHK(hipStreamSynchronize(c->st));
+  return KS_OK;
+}
+
+ks_status ks_head_rows(ks_ctx* c, const float* x, int R, float* logits, int32_t* am, float* top1) {
+  REQ(c && x && am && top1, "null pointer");
+  REQ(R >= 1 && R <= c->y.XR, "R out of range");
+  head_rows(c, x, R, logits, am, top1, R > 16);
+  HIPCHK(hipGetLastError());
+  HIPCHK(hipStreamSynchronize(c->st));
+  return KS_OK;
+}
+
+ks_status ks_generate(ks_ctx* c, const int32_t* prompt, int n_prompt, int n_new, int gamma,
+                      int reselect_every, const ks_select_params* p, int32_t* out_tokens,
+                      ks_gen_stats* stats, ks_selection* sel_log, int max_sel_log) {
+  REQ(c && prompt && out_tokens, "null pointer");
+  REQ(n_new >= 1, "n_new must be >= 1");
+  REQ(gamma >= 0 && gamma <= c->lim.gamma_max, "gamma out of range");
+  REQ(gamma == 0 || (p && reselect_every >= 1), "speculative decoding needs params and reselect_every >= 1");
+  if ((long long)n_prompt + n_new + gamma + 1 >= c->md.n_max) {
+    set_error("prompt + generation exceeds the KV cache");
+    return KS_ECAPACITY;
+  }
+  ks_gen_stats st{};
+  auto now = [] { return std::chrono::steady_clock::now(); };
+  auto ms = [](auto a, auto b) { return std::chrono::duration<double, std::milli>(b - a).count(); };
+  const auto tp0 = now();
+  int32_t first = 0;
+  ks_status s = ks_prefill(c, prompt, n_prompt, &first);
+  if (s != KS_OK) return s;
+  const auto t0 = now();
+  st.ms_prefill = ms(tp0, t0);
+  int produced = 1;
+  out_tokens[0] = first;
+  if (gamma == 0) {
+    // greedy AR on the decode kernels; tokens chain through a 64-entry device
+    // ring and are copied out every 63 steps
+    constexpr int RB = 64;
+    int32_t* chain = c->at<int32_t>(c->y.tok);
+    set_i32(chain, first, c->st);
+    const int steps = n_new - 1;
+    std::vector<int32_t> tmp(RB);
+    int flushed = 0;  // out_tokens[0..flushed] are final
+    for (int k = 0; k < steps; ++k) {
+      decode_row(c, chain + (k % RB), c->P + k, nullptr, chain + ((k + 1) % RB), nullptr);
+      if ((k + 1) % (RB - 1) == 0 || k == steps - 1) {
+        HIPCHK(hipMemcpyAsync(tmp.data(), chain, RB * 4, hipMemcpyDeviceToHost, c->st));
+        HIPCHK(hipStreamSynchronize(c->st));
+        for (int t = flushed + 1; t <= k + 1; ++t) out_tokens[t] = tmp[t % RB];
+        flushed = k + 1;
+      }
+    }
+    HIPCHK(hipGetLastError());
+    HIPCHK(hipStreamSynchronize(c->st));
+    c->P += steps;
+    c->s = out_tokens[n_new - 1];
+    c->k_draft = 0;
+    st.ms_total = ms(t0, now());
+    if (stats) *stats = st;
+    return KS_OK;
+  }
+  ks_selection sel{};
+  auto do_select = [&]() -> ks_status {
+    const auto a = now();
+    ks_status r = select_internal(c, p, &sel, nullptr);
+    st.ms_select += ms(a, now());
+    if (r == KS_OK) {
+      if (sel_log && st.n_selections < max_sel_log) sel_log[st.n_selections] = sel;
+      st.n_selections++;
+    }
+    return r;
+  };
+  s = do_select();
+  if (s != KS_OK) return s;
+  int32_t* toks = c->pin;
+  while (produced < n_new) {
+    for (int k = 0; k < gamma; ++k) draft_internal(c, sel.exec);
+    HIPCHK(hipGetLastError());
+    HIPCHK(hipMemcpyAsync(toks, c->at<int32_t>(c->y.tok), (gamma + 1) * 4,
+                          hipMemcpyDeviceToHost, c->st));
+    int a = 0;
+    int32_t pred[16];
+    s = verify_internal(c, toks, gamma, pred, &a);
+    if (s != KS_OK) return s;
+    st.n_rounds++;
+    st.n_drafted += gamma;
+    st.n_accepted += a;
+    const int before = produced;
+    for (int t = 1; t <= a && produced < n_new; ++t) out_tokens[produced++] = toks[t];
+    if (produced < n_new) out_tokens[produced++] = pred[a];
+    if (produced < n_new && produced / reselect_every > before / reselect_every) {
+      s = do_select();
+      if (s != KS_OK) return s;
+    }
+  }
+  HIPCHK(hipStreamSynchronize(c->st));
+  st.ms_total = ms(t0, now());
+  if (stats) *stats = st;
+  return KS_OK;
+}
+
+// ----------------------------------------------------- isolated knapsack
+ks_status ks_knapsack_quantize(const double* t, const double* s, int B, int n, int bins,
+                               int32_t* w, int32_t* q) {
+#pragma clang fp contract(off)
+  REQ(t && s && w && q, "null pointer");
+  REQ(B >= 1 && n >= 1 && bins >= 1, "sizes must be positive");
+  for (size_t k = 0; k < (size_t)B * n; ++k) REQ(t[k] > 0.0 && s[k] > 0.0 && s[k] <= 1.0, "t must be > 0 and s in (0, 1]");
+  for (int b = 0; b < B; ++b) {
+    double delta = 0.0;
+    for (int i = 0; i < n; ++i) delta += t[(size_t)b * n + i];
+    delta /= bins;
+    for (int i = 0; i < n; ++i) {
+      const size_t k = (size_t)b * n + i;
+      const double wf = std::floor(t[k] / delta + 0.5);
+      w[k] = std::max(1, (int)wf);
+      const double ql = -std::log(s[k]) * 16777216.0;
+      q[k] = (int32_t)std::floor(ql + 0.5);
+    }
+  }
+  return KS_OK;
+}
+
+ks_status ks_knapsack_batch(const int32_t* w, const int32_t* q, int B, int n, int C, int max_skip,
+                            int32_t* best, uint64_t* bits, void* stream) {
+  REQ(w && q && best && bits, "null pointer");
+  REQ(B >= 1 && n >= 1 && n <= 4096, "B >= 1 and 1 <= n <= 4096 required");
+  REQ(C >= 0 && C <= 8191, "C must be in [0, 8191]");
+  REQ(max_skip >= 0, "max_skip must be >= 0");
+  knapsack_dp(w, q, B, n, C, max_skip, best, bits, (hipStream_t)stream);
+  HIPCHK(hipGetLastError());
+  return KS_OK;
+}
+
+ks_status ks_knapsack_backtrack(const uint64_t* bits, const int32_t* w, int B, int n, int C,
+                                const int32_t* j, uint8_t* skip, int32_t* err, void* stream) {
+  REQ(bits && w && j && skip && err, "null pointer");
+  REQ(B >= 1 && n >= 1 && C >= 0 && C <= 8191, "sizes out of range");
+  knapsack_backtrack(bits, w, B, n, C, j, skip, err, (hipStream_t)stream);
+  HIPCHK(hipGetLastError());
+  return KS_OK;
+}
+
+ks_status ks_knapsack_batch_select(const int32_t* best, const uint64_t* bits, const int32_t* w,
+                                   const double* s, int B, int n, int C, int D, int32_t* j_star,
+                                   int32_t* gamma_star, double* tpt, uint8_t* skip, void* stream) {
+  REQ(best && bits && w && s && j_star && gamma_star && tpt && skip, "null pointer");
+  REQ(B >= 1 && n >= 1 && n <= 128, "B >= 1 and 1 <= n <= 128 required");
+  REQ(C >= 0 && C <= 8191, "C must be in [0, 8191]");
+  REQ(D >= 1 && D <= 64, "D must be in [1, 64]");
+  knapsack_select(best, bits, w, s, B, n, C, D, j_star, gamma_star, tpt, skip, (hipStream_t)stream);
+  HIPCHK(hipGetLastError());
+  return KS_OK;
+}
+
+}  // extern "C"

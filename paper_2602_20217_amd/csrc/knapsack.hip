@@ -1,0 +1,188 @@
+// Batched integer knapsack over skip budgets (Eq. objective_knapsack in
+// isolation; Single-pass Efficiency and the C/2 prune of Section 3.4).
+//
+// One workgroup per instance.  The row best_{i-1}[0..C] lives in LDS (two
+// ping-pong buffers); for item i every budget j is updated in parallel from
+// best_{i-1}[j] (keep) and best_{i-1}[j - w_i] + q_i (skip, strict).  A wave
+// owns 64 consecutive budgets, so its 64 skip decisions form one 64-bit
+// ballot that a single lane stores: the decision bitmap costs one word per
+// 64 budgets per item.  Integer arithmetic only, so results are exact.
+#include "ks_internal.h"
+
+namespace ks {
+
+constexpr int32_t KINF = 0x7FFFFFFF;
+
+__global__ __launch_bounds__(1024) void k_knap_dp(const int32_t* __restrict__ w,
+                                                  const int32_t* __restrict__ q, int n, int C,
+                                                  int max_skip, int32_t* __restrict__ best,
+                                                  uint64_t* __restrict__ bits) {
+  extern __shared__ int32_t buf[];
+  const int b = blockIdx.x;
+  const int cells = C + 1;
+  const int words = C / 64 + 1;
+  int32_t* cur = buf;
+  int32_t* nxt = buf + cells;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  for (int j = threadIdx.x; j < cells; j += blockDim.x) cur[j] = j == 0 ? 0 : KINF;
+  __syncthreads();
+  for (int i = 0; i < n; ++i) {
+    const int wi = w[(size_t)b * n + i];
+    const int64_t qi = q[(size_t)b * n + i];
+    uint64_t* brow = bits + ((size_t)b * n + i) * words;
+    for (int base = wave * 64; base < words * 64; base += nw * 64) {
+      const int j = base + lane;
+      bool take = false;
+      if (j < cells) {
+        const int32_t keep = cur[j];
+        int32_t v = keep;
+        if (j >= wi && j <= max_skip) {
+          const int32_t src = cur[j - wi];
+          if (src != KINF) {
+            const int64_t cand = (int64_t)src + qi;
+            if (cand < (int64_t)keep) {
+              v = (int32_t)cand;
+              take = true;
+            }
+          }
+        }
+        nxt[j] = v;
+      }
+      const uint64_t ballot = __ballot(take);
+      if (lane == 0) brow[base >> 6] = ballot;
+    }
+    __syncthreads();
+    int32_t* t = cur;
+    cur = nxt;
+    nxt = t;
+  }
+  for (int j = threadIdx.x; j < cells; j += blockDim.x) best[(size_t)b * cells + j] = cur[j];
+}
+
+void knapsack_dp(const int32_t* w, const int32_t* q, int B, int n, int C, int max_skip,
+                 int32_t* best, uint64_t* bits, hipStream_t st) {
+  const size_t lds = 2 * (size_t)(C + 1) * sizeof(int32_t);
+  hipLaunchKernelGGL(k_knap_dp, dim3(B), dim3(1024), lds, st, w, q, n, C, max_skip, best, bits);
+}
+
+__device__ inline int get_bit(const uint64_t* row, int j) { return (int)((row[j >> 6] >> (j & 63)) & 1ull); }
+
+__global__ void k_knap_backtrack(const uint64_t* __restrict__ bits, const int32_t* __restrict__ w,
+                                 int B, int n, int C, const int32_t* __restrict__ jsel,
+                                 uint8_t* __restrict__ skip, int32_t* __restrict__ err) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= B) return;
+  const int words = C / 64 + 1;
+  int j = jsel[b];
+  int bad = (j < 0 || j > C) ? 1 : 0;
+  for (int i = n - 1; i >= 0; --i) {
+    uint8_t sk = 0;
+    if (!bad && get_bit(bits + ((size_t)b * n + i) * words, j)) {
+      sk = 1;
+      j -= w[(size_t)b * n + i];
+      if (j < 0) bad = 1;
+    }
+    skip[(size_t)b * n + i] = sk;
+  }
+  err[b] = (bad || j != 0) ? 1 : 0;
+}
+
+void knapsack_backtrack(const uint64_t* bits, const int32_t* w, int B, int n, int C,
+                        const int32_t* j, uint8_t* skip, int32_t* err, hipStream_t st) {
+  hipLaunchKernelGGL(k_knap_backtrack, dim3((B + 255) / 256), dim3(256), 0, st, bits, w, B, n, C,
+                     j, skip, err);
+}
+
+// Stage 2 with the surrogate acceptance alpha_j = prod_{i skipped} s_i.
+// One workgroup per instance, threads over budgets; each thread keeps the
+// first strict maximum over gamma for its budget, then a tree keeps the
+// largest value and, on equal values, the smallest budget: the same winner as
+// a sequential scan over (j ascending, gamma ascending) with strict ">".
+// Items are limited to 128 so a backtracked mask fits two 64-bit words.
+__global__ __launch_bounds__(256) void k_knap_select(
+    const int32_t* __restrict__ best, const uint64_t* __restrict__ bits,
+    const int32_t* __restrict__ w, const double* __restrict__ s, int n, int C, int D,
+    int32_t* j_star, int32_t* g_star, double* tpt, uint8_t* skip) {
+#pragma clang fp contract(off)
+  __shared__ double sv[256];
+  __shared__ int sj[256], sg[256];
+  const int b = blockIdx.x;
+  const int words = C / 64 + 1;
+  const int32_t* wb = w + (size_t)b * n;
+  const double* sb = s + (size_t)b * n;
+  long long W = 0;
+  for (int i = 0; i < n; ++i) W += wb[i];
+  double bv = 0.0;
+  int bj = 0x7FFFFFFF, bg = 0;
+  for (int j = threadIdx.x; j <= C; j += blockDim.x) {
+    if (best[(size_t)b * (C + 1) + j] == KINF) continue;
+    uint64_t m0 = 0, m1 = 0;
+    int jj = j;
+    for (int i = n - 1; i >= 0 && jj >= 0; --i) {
+      if (get_bit(bits + ((size_t)b * n + i) * words, jj)) {
+        if (i < 64) m0 |= 1ull << i; else m1 |= 1ull << (i - 64);
+        jj -= wb[i];
+      }
+    }
+    if (jj != 0) continue;  // inconsistent decisions: not a candidate
+    double a = 1.0;
+    for (int i = 0; i < n; ++i) {
+      const bool sk = i < 64 ? ((m0 >> i) & 1ull) : ((m1 >> (i - 64)) & 1ull);
+      if (sk) a = a * sb[i];
+    }
+    for (int g = 1; g <= D; ++g) {
+      double e = 0.0, p = 1.0;
+      for (int k = 0; k <= g; ++k) {
+        e = e + p;
+        p = p * a;
+      }
+      const double cost = (double)((long long)g * (W - j) + W);
+      const double v = e / cost;
+      if (v > bv) {  // threads visit their budgets in ascending order
+        bv = v;
+        bj = j;
+        bg = g;
+      }
+    }
+  }
+  sv[threadIdx.x] = bv;
+  sj[threadIdx.x] = bj;
+  sg[threadIdx.x] = bg;
+  __syncthreads();
+  for (int o = 128; o >= 1; o >>= 1) {
+    if (threadIdx.x < o) {
+      const double v2 = sv[threadIdx.x + o];
+      const int j2 = sj[threadIdx.x + o];
+      if (v2 > sv[threadIdx.x] || (v2 == sv[threadIdx.x] && j2 < sj[threadIdx.x])) {
+        sv[threadIdx.x] = v2;
+        sj[threadIdx.x] = j2;
+        sg[threadIdx.x] = sg[threadIdx.x + o];
+      }
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    const int j = sj[0];
+    j_star[b] = j;
+    g_star[b] = sg[0];
+    tpt[b] = sv[0];
+    int jj = j;
+    for (int i = n - 1; i >= 0; --i) {
+      uint8_t sk = 0;
+      if (jj >= 0 && jj <= C && get_bit(bits + ((size_t)b * n + i) * words, jj)) {
+        sk = 1;
+        jj -= wb[i];
+      }
+      skip[(size_t)b * n + i] = sk;
+    }
+  }
+}
+
+void knapsack_select(const int32_t* best, const uint64_t* bits, const int32_t* w,
+                     const double* s, int B, int n, int C, int D, int32_t* j_star,
+                     int32_t* g_star, double* tpt, uint8_t* skip, hipStream_t st) {
+  hipLaunchKernelGGL(k_knap_select, dim3(B), dim3(256), 0, st, best, bits, w, s, n, C, D, j_star,
+                     g_star, tpt, skip);
+}
+
+}  // namespace ks
