@@ -72,6 +72,11 @@ class KsError(RuntimeError):
 
 
 def _load():
+    # PyTorch ships its own HIP runtime (same SONAME as the system one).  Loading
+    # torch first makes the dynamic loader bind the library to that runtime, so
+    # device pointers and streams from torch are valid in the library's calls;
+    # loading the library first would bring a second HIP runtime into the process.
+    import torch  # noqa: F401
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is missing: build it with "
                           "`python -m paper_2602_20217_amd.build` (hipcc, gfx950)")

@@ -95,3 +95,12 @@ def test_product_package_does_not_touch_oracle():
                 txt = open(os.path.join(dirpath, f)).read()
                 assert "import oracle" not in txt and "from oracle" not in txt, f
                 assert "workloads" not in txt, f
+
+
+def test_single_hip_runtime_in_process():
+    """The library binds to the HIP runtime torch loaded: exactly one libamdhip64 and
+    one libhsa-runtime64 are mapped after import."""
+    maps = open("/proc/self/maps").read().splitlines()
+    hip = {l.split()[-1] for l in maps if "libamdhip64" in l}
+    hsa = {l.split()[-1] for l in maps if "libhsa-runtime64" in l}
+    assert len(hip) == 1 and len(hsa) == 1, (hip, hsa)
