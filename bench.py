@@ -1,0 +1,232 @@
+#!/usr/bin/env python
+"""Decode throughput of the self-speculative decode step on one MI355X.
+
+Workload (default): Llama-3-8B-shaped decoder (32 layers, d 4096, 32 query / 8
+kv heads of 128, SwiGLU 14336, vocab 128256), random init, bf16 weights and KV
+cache; 8192-token random-id prompt; 256 generated tokens; draft length 4; the
+skip mask is re-selected every 32 generated tokens by the knapsack DP.
+
+One step = prefill (untimed, restores the state) + the timed generation of
+256 tokens, selections included.  The AR baseline runs the same kernels with
+no drafting.  Prints one JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import dataclasses
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def fit_line(n, t):
+    """least-squares t = a n + b"""
+    import numpy as np
+    A = np.stack([np.asarray(n, float), np.ones(len(n))], 1)
+    (a, b), *_ = np.linalg.lstsq(A, np.asarray(t, float), rcond=None)
+    return float(a), float(b)
+
+
+def latency_sweep(dm, cfg, ctxs, first_tok, steps=6):
+    """Per-sublayer latencies by masked decode steps at several context lengths
+    (Appendix C profiling): t_MLP from MLP-only steps, t_Attn(n) from
+    attention-only steps, both relative to a step that runs no sublayer."""
+    import numpy as np
+    L2 = 2 * cfg.L
+    none = np.zeros(L2, bool)
+    mlp = np.array([i % 2 == 1 for i in range(L2)])
+    attn = ~mlp
+    rows = []
+    for n in ctxs:
+        dm.set_context(n, first_tok)
+        dm.profile_decode(None, 2, per_kernel=False)  # warm
+        t0 = dm.profile_decode(none, steps, per_kernel=False)["ms_step"]
+        tm = dm.profile_decode(mlp, steps, per_kernel=False)["ms_step"]
+        ta = dm.profile_decode(attn, steps, per_kernel=False)["ms_step"]
+        tf = dm.profile_decode(None, steps, per_kernel=False)["ms_step"]
+        rows.append({"n": n, "t_attn_ms": (ta - t0) / cfg.L, "t_mlp_ms": (tm - t0) / cfg.L,
+                     "t_head_ms": t0, "t_step_ms": tf})
+    c2, c3 = fit_line([r["n"] for r in rows], [r["t_attn_ms"] for r in rows])
+    c1 = float(np.mean([r["t_mlp_ms"] for r in rows]))
+    return (c1, c2, c3), rows
+
+
+def cpu_baseline(cfg, ctx, budget_s):
+    """The oracle (float64 NumPy) timed on the host on a bounded sample: decode
+    tokens through 2 of the model's layers at the full context (keys/values
+    from the seeded generator) plus the LM head, scaled to all layers."""
+    import numpy as np
+    import workloads as W
+    from oracle import model as M
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:
+        threads = len(os.sched_getaffinity(0))
+    small = dataclasses.replace(cfg, L=2)
+    model = M.Model(small, W.generate_weights(small, seed=0))
+    cache = M.KVCache(small, ctx + 64)
+    for l in range(2):
+        K, V = W.synthetic_kv(small, ctx, seed=3, layer=l)
+        cache.K[l][:, :ctx] = K
+        cache.V[l][:, :ctx] = V
+    tok = int(W.prompt_ids(cfg.vocab, 1, 9)[0])
+    x = model.embed[[tok]]
+    th = time.perf_counter()
+    M.head(model, x)
+    t_head = time.perf_counter() - th
+    t0 = time.perf_counter()
+    n = 0
+    while True:
+        M.forward(model, cache, [tok], ctx + n)
+        n += 1
+        if time.perf_counter() - t0 > budget_s or n >= 16:
+            break
+    per_tok = (time.perf_counter() - t0) / n
+    est = (per_tok - t_head) * cfg.L / 2 + t_head
+    return {"value": 1.0 / est, "unit": "tok/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{n} float64 oracle decode tokens through 2 of {cfg.L} layers + LM head "
+                      f"at {ctx} context (seeded synthetic KV), per-layer time scaled to "
+                      f"{cfg.L} layers; {per_tok:.2f} s per sampled token"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=2)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--model", default="llama8b")
+    ap.add_argument("--ctx", type=int, default=8192)
+    ap.add_argument("--new", type=int, default=256)
+    ap.add_argument("--gamma", type=int, default=4)
+    ap.add_argument("--reselect", type=int, default=32)
+    ap.add_argument("--cpu-budget", type=float, default=20.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path "
+              "(run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    import workloads as W
+    from paper_2602_20217_amd.engine import DeviceModel, select_params
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    cfg = W.config(args.model)
+    n_max = args.ctx + args.new + 64
+    t = time.time()
+    dm = DeviceModel(cfg, n_max=n_max, gamma_max=max(8, args.gamma), m_rounds=5, cap_max=256,
+                     prefill_chunk=512)
+    W.generate_weights(cfg, seed=0, consume=dm.upload)
+    dm.finalize()
+    log(f"weights generated and packed in {time.time() - t:.1f}s")
+    prompt = W.prompt_ids(cfg.vocab, args.ctx, 1)
+
+    t = time.time()
+    first = dm.prefill(prompt)
+    torch.cuda.synchronize()
+    log(f"prefill {args.ctx} tokens: {time.time() - t:.2f}s")
+    sweep_ctx = sorted({max(64, args.ctx // 8), args.ctx // 4, args.ctx // 2, args.ctx})
+    coeffs, sweep = latency_sweep(dm, cfg, sweep_ctx, first)
+    log(f"latency model c1={coeffs[0]:.4f}ms c2={coeffs[1]:.3e}ms/token c3={coeffs[2]:.4f}ms")
+    params = select_params(coeffs, "paper_min", 0, tau=0.5, prune_half=True, D=10)
+
+    def run(gamma):
+        dm.prefill(prompt)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        out, st, sels = dm.decode(args.new, gamma, args.reselect, params if gamma else None)
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t0) * 1e3, out, st, sels
+
+    ar_ms, ssd_ms, ssd_last, ar_out = [], [], None, None
+    for k in range(args.warmup + args.steps):
+        a_ms, ar_out, _, _ = run(0)
+        s_ms, out, st, sels = run(args.gamma)
+        if k >= args.warmup:
+            ar_ms.append(a_ms)
+            ssd_ms.append(s_ms)
+        ssd_last = (out, st, sels)
+        log(f"step {k}: AR {a_ms:.1f} ms, speculative {s_ms:.1f} ms "
+            f"(select {st.ms_select:.1f} ms, accepted {st.n_accepted}/{st.n_drafted})")
+    out, st, sels = ssd_last
+    same = bool(np.array_equal(out, ar_out))
+
+    # roofline of the dominant kernel: the decode step's gate/up projection
+    prof = dm.profile_decode(None, 16, per_kernel=True)
+    ms_gu = prof["ms"]["gemm_gate_up"]
+    bytes_gu = 2 * cfg.ffn * cfg.d * 2 + cfg.d * 2 * 2 + cfg.ffn * 2 * 2
+    achieved = bytes_gu / (ms_gu * 1e-3) / 1e9
+    wbytes = {"gemm_qkv": (cfg.hq + 2 * cfg.hkv) * cfg.hd * cfg.d * 2,
+              "gemm_o": cfg.d * cfg.hq * cfg.hd * 2, "gemm_gate_up": bytes_gu,
+              "gemm_down": cfg.d * cfg.ffn * 2, "gemm_head": cfg.vocab * cfg.d * 2}
+    kern = {}
+    for name, ms in prof["ms"].items():
+        if prof["launches"][name] == 0:
+            continue
+        e = {"ms": round(ms, 5), "launches_per_token": prof["launches"][name]}
+        if name in wbytes and wbytes[name]:
+            e["GBps"] = round(wbytes[name] / (ms * 1e-3) / 1e9, 1)
+        kern[name] = e
+    P = args.ctx + args.new
+    kv_bytes = P * cfg.hkv * cfg.hd * 2 * 2  # per layer, K and V
+    if prof["ms"]["attn"] > 0:
+        kern["attn"]["GBps"] = round(kv_bytes / ((prof["ms"]["attn"] + prof["ms"]["combine"]) * 1e-3) / 1e9, 1)
+
+    mean_ssd = sum(ssd_ms) / len(ssd_ms)
+    mean_ar = sum(ar_ms) / len(ar_ms)
+    value = args.new / (mean_ssd / 1e3)
+    ar_tps = args.new / (mean_ar / 1e3)
+    token_bytes = (cfg.vocab * cfg.d * 2 + cfg.L * (((cfg.hq + 2 * cfg.hkv) * cfg.hd + cfg.hq * cfg.hd) * cfg.d * 2
+                   + 3 * cfg.ffn * cfg.d * 2) + cfg.L * kv_bytes)
+    res = {
+        "metric": "decode tok/s (bs=1) at 8K ctx, speedup vs AR; achieved HBM GB/s",
+        "value": round(value, 2), "unit": "tok/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(mean_ssd, 2), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded random-init weights, random-id prompt)",
+        "config": {"workload": f"{args.model}: Llama-3-8B-shaped decoder, bf16 weights and KV, "
+                               f"{args.ctx}-token random prompt, {args.new} new tokens, "
+                               f"gamma {args.gamma}, mask re-selected every {args.reselect} tokens",
+                   "global_batch": 1, "seq_len": args.ctx, "new_tokens": args.new,
+                   "gamma": args.gamma, "reselect_every": args.reselect, "parallelism": "none"},
+        "speedup_vs_ar": round(value / ar_tps, 4), "ar_tok_s": round(ar_tps, 2),
+        "ar_ms_per_step": round(mean_ar, 2), "tokens_equal_ar": same,
+        "accepted": st.n_accepted, "drafted": st.n_drafted, "rounds": st.n_rounds,
+        "alpha": round(st.n_accepted / max(1, st.n_drafted), 4),
+        "select_ms": round(st.ms_select, 2), "selections": st.n_selections,
+        "masks": [{"j": s.j_star, "C": s.C, "w_attn": s.w_attn, "w_mlp": s.w_mlp,
+                   "skipped_attn": int(sum(1 for i in range(0, 2 * cfg.L, 2) if not s.exec[i])),
+                   "skipped_mlp": int(sum(1 for i in range(1, 2 * cfg.L, 2) if not s.exec[i])),
+                   "alpha_hat": round(s.alpha_hat, 3), "gamma_star": s.gamma_star} for s in sels],
+        "ar_step_GBps": round(token_bytes / (mean_ar / args.new * 1e-3) / 1e9, 1),
+        "latency_model_ms": {"c1": coeffs[0], "c2": coeffs[1], "c3": coeffs[2], "sweep": sweep},
+        "kernels": kern,
+        "roofline": {"bound": "hbm", "kernel": "k_gemm_skinny<2,16,SWIGLU> (gate/up + SwiGLU, 1 row)",
+                     "achieved": round(achieved, 1), "peak": 8000.0, "unit": "GB/s",
+                     "frac": round(achieved / 8000.0, 4), "traffic": None,
+                     "bytes_per_launch": bytes_gu, "ms_per_launch": round(ms_gu, 5)},
+    }
+    dm.close()
+    del dm
+    torch.cuda.empty_cache()
+    if not args.no_cpu_baseline:
+        t = time.time()
+        res["cpu_baseline"] = cpu_baseline(cfg, args.ctx, args.cpu_budget)
+        log(f"cpu baseline {time.time() - t:.1f}s")
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -262,6 +262,50 @@ ks_status ks_generate(ks_ctx* ctx, const int32_t* prompt, int n_prompt, int n_ne
                       int reselect_every, const ks_select_params* p, int32_t* out_tokens,
                       ks_gen_stats* stats, ks_selection* sel_log, int max_sel_log);
 
+/*
+ * ks_decode: the generation loop of ks_generate without its prefill: continues
+ * from the current state (after ks_prefill, or after an earlier ks_decode) and
+ * returns n_new tokens, the first being the already committed token s.  With
+ * gamma > 0 it selects a mask first (the history must hold at least one block)
+ * and re-selects as ks_generate does.  stats->ms_prefill is 0.
+ */
+ks_status ks_decode(ks_ctx* ctx, int n_new, int gamma, int reselect_every,
+                    const ks_select_params* p, int32_t* out_tokens, ks_gen_stats* stats,
+                    ks_selection* sel_log, int max_sel_log);
+
+/* Kernel classes of the decode step, for ks_profile_decode. */
+enum {
+  KS_KC_EMBED = 0,    /* embedding gather */
+  KS_KC_NORM,         /* RMSNorm into matrix activations */
+  KS_KC_GEMM_QKV,     /* q/k/v projection */
+  KS_KC_QKV_POST,     /* q/k norm, RoPE, key/value store */
+  KS_KC_ATTN,         /* split attention over the cache */
+  KS_KC_COMBINE,      /* merge of attention splits */
+  KS_KC_GEMM_O,       /* output projection + residual */
+  KS_KC_GEMM_GATE_UP, /* gate/up projection + SwiGLU */
+  KS_KC_GEMM_DOWN,    /* down projection + residual */
+  KS_KC_GEMM_HEAD,    /* LM head */
+  KS_KC_ARGMAX,       /* argmax + top-1 probability */
+  KS_KC_OTHER,        /* position fill and small copies */
+  KS_KC_COUNT
+};
+typedef struct ks_kernel_profile {
+  double ms[KS_KC_COUNT];   /* mean duration of one launch of the class */
+  int launches[KS_KC_COUNT];/* launches of the class per decode step */
+  double ms_step;           /* mean wall time of one decode step (events around it) */
+  int steps;
+} ks_kernel_profile;
+/*
+ * ks_profile_decode: runs `steps` single-row decode steps with mask exec (NULL =
+ * every sublayer) at the committed position P and times them with HIP events
+ * on the context stream; with per_kernel = 1 an event pair also brackets every
+ * kernel launch (ms[] and launches[] are filled; otherwise they are 0).  Each
+ * step writes the keys/values of position P (as a draft step would) and
+ * commits nothing.
+ */
+ks_status ks_profile_decode(ks_ctx* ctx, const uint8_t* exec, int steps, int per_kernel,
+                            ks_kernel_profile* out);
+
 /* ---- lower-level calls (per-sublayer parity and latency profiling) ------- */
 /*
  * ks_sublayer_apply: applies sublayer i (1..2L) to R rows of the residual

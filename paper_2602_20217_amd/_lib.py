@@ -65,6 +65,16 @@ class GenStats(C.Structure):
                 ("ms_prefill", C.c_double)]
 
 
+KS_KC_NAMES = ("embed", "norm", "gemm_qkv", "qkv_post", "attn", "combine", "gemm_o",
+               "gemm_gate_up", "gemm_down", "gemm_head", "argmax", "other")
+KS_KC_COUNT = len(KS_KC_NAMES)
+
+
+class KernelProfile(C.Structure):
+    _fields_ = [("ms", C.c_double * KS_KC_COUNT), ("launches", C.c_int * KS_KC_COUNT),
+                ("ms_step", C.c_double), ("steps", C.c_int)]
+
+
 class KsError(RuntimeError):
     def __init__(self, status: int, msg: str):
         super().__init__(f"{STATUS_NAMES.get(status, status)}: {msg}")
@@ -105,6 +115,9 @@ _SIG = {
                                 C.POINTER(SelectionDebug)]),
     "ks_generate": (_I, [_P, _P, _I, _I, _I, _I, C.POINTER(SelectParams), _P,
                          C.POINTER(GenStats), C.POINTER(Selection), _I]),
+    "ks_decode": (_I, [_P, _I, _I, _I, C.POINTER(SelectParams), _P, C.POINTER(GenStats),
+                       C.POINTER(Selection), _I]),
+    "ks_profile_decode": (_I, [_P, _P, _I, _I, C.POINTER(KernelProfile)]),
     "ks_sublayer_apply": (_I, [_P, _I, _P, _P, _P, _I, _I]),
     "ks_head_rows": (_I, [_P, _P, _I, _P, _P, _P]),
     "ks_knapsack_quantize": (_I, [_P, _P, _I, _I, _I, _P, _P]),
@@ -152,6 +165,8 @@ ks_verify = _wrap("ks_verify")
 ks_hidden_cos = _wrap("ks_hidden_cos")
 ks_knapsack_select = _wrap("ks_knapsack_select")
 ks_generate = _wrap("ks_generate")
+ks_decode = _wrap("ks_decode")
+ks_profile_decode = _wrap("ks_profile_decode")
 ks_sublayer_apply = _wrap("ks_sublayer_apply")
 ks_head_rows = _wrap("ks_head_rows")
 ks_knapsack_quantize = _wrap("ks_knapsack_quantize")

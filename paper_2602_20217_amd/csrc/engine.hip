@@ -124,6 +124,10 @@ struct ks_ctx {
   char* ws;
   Layout y;
   int32_t* pin = nullptr;  // pinned host staging: [0,16) draft tokens, [16,32) verify argmax
+  // kernel timing (ks_profile_decode): event pairs around launches
+  bool prof_on = false;
+  std::vector<hipEvent_t> prof_ev;
+  std::vector<std::pair<int, int>> prof_rec;  // (kernel class, first event)
   // decode state
   bool ready = false;
   int P = 0;
@@ -153,6 +157,25 @@ struct ks_ctx {
 
 namespace {
 
+// ---------------------------------------------------------- kernel timing
+int prof_begin(ks_ctx* c, int cls) {
+  if (!c->prof_on) return -1;
+  const int i = 2 * (int)c->prof_rec.size();
+  if (i + 2 > (int)c->prof_ev.size()) return -1;
+  (void)hipEventRecord(c->prof_ev[i], c->st);
+  c->prof_rec.push_back({cls, i});
+  return i;
+}
+void prof_end(ks_ctx* c, int i) {
+  if (i >= 0) (void)hipEventRecord(c->prof_ev[i + 1], c->st);
+}
+#define PROF(c, cls, stmt)              \
+  do {                                  \
+    const int pi_ = prof_begin(c, cls); \
+    stmt;                               \
+    prof_end(c, pi_);                   \
+  } while (0)
+
 // ---------------------------------------------------------- forward pieces
 void gemm(ks_ctx* c, int M, int N, int K, Act A, const void* W, int epi, float* out, int ldo,
           const float* res, int ldres, Act aout, bool batched) {
@@ -171,12 +194,14 @@ void attn_rows(ks_ctx* c, int l, const float* xin, float* xout, int R, const int
   float* qkv = c->at<float>(c->y.qkv);
   float* q = c->at<float>(c->y.q);
   float* kvs = c->at<float>(c->y.kvself);
-  norm_act(xin, d.d, c->attn_norm[l], d.eps, R, d.d, d.dtype, a1, c->st);
-  gemm(c, R, c->y.nqkv, d.d, a1, c->wqkv[l], EPI_STORE, qkv, c->y.nqkv, nullptr, 0, Act{}, batched);
+  PROF(c, KS_KC_NORM, norm_act(xin, d.d, c->attn_norm[l], d.eps, R, d.d, d.dtype, a1, c->st));
+  PROF(c, KS_KC_GEMM_QKV,
+       gemm(c, R, c->y.nqkv, d.d, a1, c->wqkv[l], EPI_STORE, qkv, c->y.nqkv, nullptr, 0, Act{},
+            batched));
   QkvPostArgs qp{R, d.hq, d.hkv, d.hd, d.n_max, d.dtype, d.qk_norm, d.eps, qkv,
                  c->at<float>(c->y.rope), c->q_norm[l], c->k_norm[l], pos, q,
                  c->kc(l), c->vc(l), kvs, mode};
-  qkv_post(qp, c->st);
+  PROF(c, KS_KC_QKV_POST, qkv_post(qp, c->st));
   const int tiles = batched ? BAT_TILES : DEC_TILES;
   const int ns = attn_nsplit(d.n_max, tiles);
   const int step = batched ? PB : 16;
@@ -185,22 +210,29 @@ void attn_rows(ks_ctx* c, int l, const float* xin, float* xout, int R, const int
     AttnArgs aa{rr, d.hq, d.hkv, d.hd, d.n_max, d.dtype,
                 q + (size_t)r0 * d.hq * d.hd, c->kc(l), c->vc(l), len + r0, max_len, tiles,
                 64 / (d.hq / d.hkv) < 16 ? 64 / (d.hq / d.hkv) : 16, c->at<float>(c->y.part), ns};
-    attn_split(aa, c->st);
+    PROF(c, KS_KC_ATTN, attn_split(aa, c->st));
     Act out2 = a2;
     const size_t off = (size_t)r0 * a2.ld * (c->bf() ? 2 : 4);
     out2.hi = (char*)a2.hi + off;
     out2.lo = c->bf() ? (char*)a2.lo + (size_t)r0 * a2.ld * 2 : nullptr;
-    attn_combine(aa, mode == 1 ? kvs + (size_t)r0 * 2 * d.hkv * d.hd : nullptr, out2, c->st);
+    PROF(c, KS_KC_COMBINE,
+         attn_combine(aa, mode == 1 ? kvs + (size_t)r0 * 2 * d.hkv * d.hd : nullptr, out2,
+                      c->st));
   }
-  gemm(c, R, d.d, d.hq * d.hd, a2, c->wo[l], EPI_RESID, xout, d.d, xin, d.d, Act{}, batched);
+  PROF(c, KS_KC_GEMM_O,
+       gemm(c, R, d.d, d.hq * d.hd, a2, c->wo[l], EPI_RESID, xout, d.d, xin, d.d, Act{},
+            batched));
 }
 
 void mlp_rows(ks_ctx* c, int l, const float* xin, float* xout, int R, bool batched) {
   const ks_model_desc& d = c->md;
   const Act a1 = c->act1(), a2 = c->act2();
-  norm_act(xin, d.d, c->mlp_norm[l], d.eps, R, d.d, d.dtype, a1, c->st);
-  gemm(c, R, 2 * d.ffn, d.d, a1, c->wgu[l], EPI_SWIGLU, nullptr, 0, nullptr, 0, a2, batched);
-  gemm(c, R, d.d, d.ffn, a2, c->wdown[l], EPI_RESID, xout, d.d, xin, d.d, Act{}, batched);
+  PROF(c, KS_KC_NORM, norm_act(xin, d.d, c->mlp_norm[l], d.eps, R, d.d, d.dtype, a1, c->st));
+  PROF(c, KS_KC_GEMM_GATE_UP,
+       gemm(c, R, 2 * d.ffn, d.d, a1, c->wgu[l], EPI_SWIGLU, nullptr, 0, nullptr, 0, a2,
+            batched));
+  PROF(c, KS_KC_GEMM_DOWN,
+       gemm(c, R, d.d, d.ffn, a2, c->wdown[l], EPI_RESID, xout, d.d, xin, d.d, Act{}, batched));
 }
 
 void sublayer_rows(ks_ctx* c, int i, const float* xin, float* xout, int R, const int32_t* pos,
@@ -219,10 +251,12 @@ void head_rows(ks_ctx* c, const float* x, int R, float* logits_out, int32_t* am,
   for (int r0 = 0; r0 < R; r0 += step) {
     const int rr = std::min(step, R - r0);
     float* lg = logits_out ? logits_out : c->at<float>(c->y.logits);
-    norm_act(x + (size_t)r0 * d.d, d.d, c->final_norm, d.eps, rr, d.d, d.dtype, a1, c->st);
-    gemm(c, rr, d.vocab, d.d, a1, c->lm_head, EPI_STORE, lg, d.vocab, nullptr, 0, Act{},
-         batched || rr > 16);
-    argmax_rows(lg, rr, d.vocab, am + r0, top1 ? top1 + r0 : nullptr, c->st);
+    PROF(c, KS_KC_NORM,
+         norm_act(x + (size_t)r0 * d.d, d.d, c->final_norm, d.eps, rr, d.d, d.dtype, a1, c->st));
+    PROF(c, KS_KC_GEMM_HEAD,
+         gemm(c, rr, d.vocab, d.d, a1, c->lm_head, EPI_STORE, lg, d.vocab, nullptr, 0, Act{},
+              batched || rr > 16));
+    PROF(c, KS_KC_ARGMAX, argmax_rows(lg, rr, d.vocab, am + r0, top1 ? top1 + r0 : nullptr, c->st));
   }
 }
 
@@ -233,8 +267,8 @@ void decode_row(ks_ctx* c, const int32_t* tok_dev, int p, const uint8_t* exec, i
   float* x = c->at<float>(c->y.x);
   int32_t* pos = c->at<int32_t>(c->y.pos);
   int32_t* len = c->at<int32_t>(c->y.len);
-  fill_pos(pos, len, p, 1, 1, 1, c->st);
-  embed_rows(c->embed, d.dtype, tok_dev, 1, d.d, x, d.d, c->st);
+  PROF(c, KS_KC_OTHER, fill_pos(pos, len, p, 1, 1, 1, c->st));
+  PROF(c, KS_KC_EMBED, embed_rows(c->embed, d.dtype, tok_dev, 1, d.d, x, d.d, c->st));
   for (int i = 1; i <= 2 * d.L; ++i)
     if (!exec || exec[i - 1]) sublayer_rows(c, i, x, x, 1, pos, len, p + 1, 0, false);
   head_rows(c, x, 1, nullptr, am_out, top1_out, false);
@@ -424,6 +458,7 @@ ks_status ks_create(const ks_model_desc* desc, const ks_limits* lim, const ks_we
 ks_status ks_destroy(ks_ctx* c) {
   REQ(c, "ctx is null");
   if (c->pin) (void)hipHostFree(c->pin);
+  for (hipEvent_t e : c->prof_ev) (void)hipEventDestroy(e);
   delete c;
   return KS_OK;
 }
@@ -811,26 +846,15 @@ ks_status ks_head_rows(ks_ctx* c, const float* x, int R, float* logits, int32_t*
   return KS_OK;
 }
 
-ks_status ks_generate(ks_ctx* c, const int32_t* prompt, int n_prompt, int n_new, int gamma,
-                      int reselect_every, const ks_select_params* p, int32_t* out_tokens,
-                      ks_gen_stats* stats, ks_selection* sel_log, int max_sel_log) {
-  REQ(c && prompt && out_tokens, "null pointer");
-  REQ(n_new >= 1, "n_new must be >= 1");
-  REQ(gamma >= 0 && gamma <= c->lim.gamma_max, "gamma out of range");
-  REQ(gamma == 0 || (p && reselect_every >= 1), "speculative decoding needs params and reselect_every >= 1");
-  if ((long long)n_prompt + n_new + gamma + 1 >= c->md.n_max) {
-    set_error("prompt + generation exceeds the KV cache");
-    return KS_ECAPACITY;
-  }
+static ks_status decode_internal(ks_ctx* c, int n_new, int gamma, int reselect_every,
+                                 const ks_select_params* p, int32_t* out_tokens,
+                                 ks_gen_stats* stats, ks_selection* sel_log, int max_sel_log) {
   ks_gen_stats st{};
+  if (stats) st.ms_prefill = stats->ms_prefill;
   auto now = [] { return std::chrono::steady_clock::now(); };
   auto ms = [](auto a, auto b) { return std::chrono::duration<double, std::milli>(b - a).count(); };
-  const auto tp0 = now();
-  int32_t first = 0;
-  ks_status s = ks_prefill(c, prompt, n_prompt, &first);
-  if (s != KS_OK) return s;
   const auto t0 = now();
-  st.ms_prefill = ms(tp0, t0);
+  const int32_t first = c->s;
   int produced = 1;
   out_tokens[0] = first;
   if (gamma == 0) {
@@ -856,6 +880,7 @@ ks_status ks_generate(ks_ctx* c, const int32_t* prompt, int n_prompt, int n_new,
     c->P += steps;
     c->s = out_tokens[n_new - 1];
     c->k_draft = 0;
+    c->blocks.clear();  // AR steps record no history
     st.ms_total = ms(t0, now());
     if (stats) *stats = st;
     return KS_OK;
@@ -871,7 +896,7 @@ ks_status ks_generate(ks_ctx* c, const int32_t* prompt, int n_prompt, int n_new,
     }
     return r;
   };
-  s = do_select();
+  ks_status s = do_select();
   if (s != KS_OK) return s;
   int32_t* toks = c->pin;
   while (produced < n_new) {
@@ -897,6 +922,113 @@ ks_status ks_generate(ks_ctx* c, const int32_t* prompt, int n_prompt, int n_new,
   HIPCHK(hipStreamSynchronize(c->st));
   st.ms_total = ms(t0, now());
   if (stats) *stats = st;
+  return KS_OK;
+}
+
+static ks_status check_decode_args(ks_ctx* c, int n_new, int gamma, int reselect_every,
+                                   const ks_select_params* p, int32_t* out_tokens) {
+  REQ(c && out_tokens, "null pointer");
+  REQ(n_new >= 1, "n_new must be >= 1");
+  REQ(gamma >= 0 && gamma <= c->lim.gamma_max, "gamma out of range");
+  REQ(gamma == 0 || (p && reselect_every >= 1),
+      "speculative decoding needs params and reselect_every >= 1");
+  if (p) {
+    REQ(p->D >= 1 && p->D <= 64, "D must be in [1, 64]");
+    REQ(p->quant_mode == KS_QUANT_PAPER_MIN || p->quant_mode == KS_QUANT_BINS, "bad quant_mode");
+  }
+  return KS_OK;
+}
+
+ks_status ks_decode(ks_ctx* c, int n_new, int gamma, int reselect_every, const ks_select_params* p,
+                    int32_t* out_tokens, ks_gen_stats* stats, ks_selection* sel_log,
+                    int max_sel_log) {
+  ks_status s = check_decode_args(c, n_new, gamma, reselect_every, p, out_tokens);
+  if (s != KS_OK) return s;
+  if (!c->ready || c->k_draft != 0) {
+    set_error("ks_decode needs a committed state with no pending draft");
+    return KS_ESTATE;
+  }
+  if (gamma > 0 && c->blocks.empty()) {
+    set_error("ks_decode with gamma > 0 needs a history (run ks_prefill first)");
+    return KS_ESTATE;
+  }
+  if ((long long)c->P + n_new + gamma + 1 >= c->md.n_max) {
+    set_error("generation exceeds the KV cache");
+    return KS_ECAPACITY;
+  }
+  if (stats) stats->ms_prefill = 0.0;
+  return decode_internal(c, n_new, gamma, reselect_every, p, out_tokens, stats, sel_log,
+                         max_sel_log);
+}
+
+ks_status ks_generate(ks_ctx* c, const int32_t* prompt, int n_prompt, int n_new, int gamma,
+                      int reselect_every, const ks_select_params* p, int32_t* out_tokens,
+                      ks_gen_stats* stats, ks_selection* sel_log, int max_sel_log) {
+  ks_status s = check_decode_args(c, n_new, gamma, reselect_every, p, out_tokens);
+  if (s != KS_OK) return s;
+  REQ(prompt, "null pointer");
+  if ((long long)n_prompt + n_new + gamma + 1 >= c->md.n_max) {
+    set_error("prompt + generation exceeds the KV cache");
+    return KS_ECAPACITY;
+  }
+  const auto tp0 = std::chrono::steady_clock::now();
+  int32_t first = 0;
+  s = ks_prefill(c, prompt, n_prompt, &first);
+  if (s != KS_OK) return s;
+  ks_gen_stats st{};
+  st.ms_prefill =
+      std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - tp0).count();
+  s = decode_internal(c, n_new, gamma, reselect_every, p, out_tokens, &st, sel_log, max_sel_log);
+  if (stats) *stats = st;
+  return s;
+}
+
+ks_status ks_profile_decode(ks_ctx* c, const uint8_t* exec, int steps, int per_kernel,
+                            ks_kernel_profile* out) {
+  REQ(c && out, "null pointer");
+  REQ(steps >= 1, "steps must be >= 1");
+  if (!c->ready) {
+    set_error("ks_profile_decode before ks_prefill / ks_set_context");
+    return KS_ESTATE;
+  }
+  if (c->P + 1 >= c->md.n_max) {
+    set_error("position exceeds the KV cache");
+    return KS_ECAPACITY;
+  }
+  const int need = 2 * (16 * c->md.L + 64);
+  while ((int)c->prof_ev.size() < need + 2) {
+    hipEvent_t e;
+    HIPCHK(hipEventCreate(&e));
+    c->prof_ev.push_back(e);
+  }
+  ks_kernel_profile r{};
+  int32_t* dt = c->at<int32_t>(c->y.tok) + 32;  // scratch slots past the draft chain
+  hipEvent_t e0 = c->prof_ev[c->prof_ev.size() - 2], e1 = c->prof_ev.back();
+  for (int sidx = 0; sidx < steps; ++sidx) {
+    c->prof_rec.clear();
+    set_i32(dt, c->s, c->st);
+    HIPCHK(hipEventRecord(e0, c->st));
+    c->prof_on = per_kernel != 0;
+    decode_row(c, dt, c->P, exec, dt + 1, c->at<float>(c->y.top1));
+    c->prof_on = false;
+    HIPCHK(hipEventRecord(e1, c->st));
+    HIPCHK(hipEventSynchronize(e1));
+    HIPCHK(hipGetLastError());
+    float ms_step = 0.f;
+    HIPCHK(hipEventElapsedTime(&ms_step, e0, e1));
+    r.ms_step += ms_step;
+    for (auto& pr : c->prof_rec) {
+      float m = 0.f;
+      HIPCHK(hipEventElapsedTime(&m, c->prof_ev[pr.second], c->prof_ev[pr.second + 1]));
+      r.ms[pr.first] += m;
+      if (sidx == 0) r.launches[pr.first]++;
+    }
+  }
+  for (int k = 0; k < KS_KC_COUNT; ++k)
+    if (r.launches[k]) r.ms[k] /= (double)steps * r.launches[k];
+  r.ms_step /= steps;
+  r.steps = steps;
+  *out = r;
   return KS_OK;
 }
 

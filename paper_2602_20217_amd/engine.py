@@ -233,6 +233,30 @@ class DeviceModel:
         sels = [log[i] for i in range(min(st.n_selections, max_sel_log))]
         return out, st, sels
 
+    def decode(self, n_new: int, gamma: int, reselect_every: int = 32,
+               params: K.SelectParams | None = None, max_sel_log: int = 256):
+        """Generation loop from the current state (no prefill)."""
+        out = np.zeros(n_new, dtype=np.int32)
+        st = K.GenStats()
+        log = (K.Selection * max_sel_log)()
+        K.ks_decode(self.ctx, n_new, gamma, reselect_every,
+                    C.byref(params) if params is not None else None, out.ctypes.data,
+                    C.byref(st), log, max_sel_log)
+        sels = [log[i] for i in range(min(st.n_selections, max_sel_log))]
+        return out, st, sels
+
+    def profile_decode(self, exec_mask=None, steps: int = 8, per_kernel: bool = True) -> dict:
+        """Mean per-launch duration (ms) of every kernel class of a decode step."""
+        m = None
+        if exec_mask is not None:
+            m = np.ascontiguousarray(np.asarray(exec_mask, dtype=bool).astype(np.uint8))
+        pr = K.KernelProfile()
+        K.ks_profile_decode(self.ctx, m.ctypes.data if m is not None else None, steps,
+                            1 if per_kernel else 0, C.byref(pr))
+        return {"ms": {n: pr.ms[i] for i, n in enumerate(K.KS_KC_NAMES)},
+                "launches": {n: pr.launches[i] for i, n in enumerate(K.KS_KC_NAMES)},
+                "ms_step": pr.ms_step, "steps": pr.steps}
+
     def sublayer_apply(self, i: int, x: torch.Tensor, pos, mode: int = 0, out=None):
         pos = np.ascontiguousarray(pos, dtype=np.int32)
         out = x if out is None else out

@@ -118,10 +118,16 @@ def _tensor_index(kind: str, layer: int) -> int:
 
 
 def round_to_bf16(a: np.ndarray) -> np.ndarray:
-    """Round a float32 array to the nearest bf16 value (ties to even), in place-safe."""
-    u = np.ascontiguousarray(a, dtype=np.float32).view(np.uint32)
-    r = ((u.astype(np.uint64) + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint32) << 16
-    return r.view(np.float32)
+    """Round a float32 array of finite values to the nearest bf16 value (ties to
+    even).  Works in place on float32 input and returns it."""
+    a = np.ascontiguousarray(a, dtype=np.float32)
+    u = a.view(np.uint32)
+    t = u >> 16
+    t &= 1
+    t += 0x7FFF
+    u += t  # finite values cannot wrap: |x| < 2^128 keeps u + 0xFFFF below 2^32
+    u &= 0xFFFF0000
+    return a
 
 
 def bf16_bits(a: np.ndarray) -> np.ndarray:
@@ -159,13 +165,14 @@ def generate_weights(cfg: ModelConfig, seed: int = 0, threads: int | None = None
     out = {}
     with _cf.ThreadPoolExecutor(max_workers=threads) as ex:
         futs = {ex.submit(weight_tensor, cfg, seed, k, l): (k, l) for k, l in names}
-        for f in _cf.as_completed(futs):
-            k, l = futs[f]
+        for f in _cf.as_completed(list(futs)):
+            k, l = futs.pop(f)
             a = f.result()
             if consume is None:
                 out[(k, l)] = a
             else:
                 consume(k, l, a)
+            del a, f  # drop the last references so consumed tensors are freed
     return out if consume is None else None
 
 
