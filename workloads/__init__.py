@@ -163,16 +163,24 @@ def generate_weights(cfg: ModelConfig, seed: int = 0, threads: int | None = None
     names = weight_names(cfg)
     threads = threads or min(16, os.cpu_count() or 1)
     out = {}
+    window = []  # futures in flight, consumed in submission order
     with _cf.ThreadPoolExecutor(max_workers=threads) as ex:
-        futs = {ex.submit(weight_tensor, cfg, seed, k, l): (k, l) for k, l in names}
-        for f in _cf.as_completed(list(futs)):
-            k, l = futs.pop(f)
+        it = iter(names)
+        while True:
+            while len(window) < 2 * threads:
+                nxt = next(it, None)
+                if nxt is None:
+                    break
+                window.append((nxt, ex.submit(weight_tensor, cfg, seed, nxt[0], nxt[1])))
+            if not window:
+                break
+            (k, l), f = window.pop(0)
             a = f.result()
             if consume is None:
                 out[(k, l)] = a
             else:
                 consume(k, l, a)
-            del a, f  # drop the last references so consumed tensors are freed
+            del a, f
     return out if consume is None else None
 
 
