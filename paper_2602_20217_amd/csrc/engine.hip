@@ -209,7 +209,7 @@ void attn_rows(ks_ctx* c, int l, const float* xin, float* xout, int R, const int
     const int rr = std::min(step, R - r0);
     AttnArgs aa{rr, d.hq, d.hkv, d.hd, d.n_max, d.dtype,
                 q + (size_t)r0 * d.hq * d.hd, c->kc(l), c->vc(l), len + r0, max_len, tiles,
-                64 / (d.hq / d.hkv) < 16 ? 64 / (d.hq / d.hkv) : 16, c->at<float>(c->y.part), ns};
+                attn_rows_per_block(d.hq / d.hkv, batched), c->at<float>(c->y.part), ns};
     PROF(c, KS_KC_ATTN, attn_split(aa, c->st));
     Act out2 = a2;
     const size_t off = (size_t)r0 * a2.ld * (c->bf() ? 2 : 4);
@@ -324,7 +324,7 @@ static ks_status check_desc(const ks_model_desc* d) {
   REQ(d, "desc is null");
   REQ(d->L >= 1 && 2 * d->L <= KS_MAX_SUBLAYERS, "L out of range");
   REQ(d->hq >= 1 && d->hkv >= 1 && d->hq % d->hkv == 0, "hq must be a multiple of hkv");
-  REQ(d->hq / d->hkv <= 64, "query heads per kv head must be <= 64");
+  REQ(d->hq / d->hkv <= 32, "query heads per kv head must be <= 32");
   REQ(d->dtype == KS_F32 || d->dtype == KS_BF16, "dtype must be KS_F32 or KS_BF16");
   REQ((d->dtype == KS_BF16 && d->hd == 128) || (d->dtype == KS_F32 && d->hd == 64),
       "supported head dims: 128 for bf16 models, 64 for float32 models");

@@ -64,20 +64,31 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_skinny(
     int nt = nt0 + t < NT ? nt0 + t : NT - 1;
     wb[t] = Wp + (size_t)nt * KT * 512 + lane * 8;
   }
-#pragma unroll 8
-  for (int kt = kb; kt < ke; ++kt) {
-    bf16x8 b[NB];
+  // chunks of CH k-steps: every weight fragment of a chunk is requested before
+  // the first matrix instruction of the chunk
+  constexpr int CH = 8;
+  for (int kc = kb; kc < ke; kc += CH) {
+    const int n = ke - kc < CH ? ke - kc : CH;
+    bf16x8 b[NB][CH];
 #pragma unroll
-    for (int t = 0; t < NB; ++t) b[t] = ld_frag(wb[t] + (size_t)kt * 512);
-    bf16x8 a0 = zero_frag(), a1 = zero_frag();
-    if (rok) {
-      a0 = ld_frag(ah + kt * 32);
-      a1 = ld_frag(al + kt * 32);
-    }
+    for (int u = 0; u < CH; ++u)
 #pragma unroll
-    for (int t = 0; t < NB; ++t) {
-      acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, b[t], acc[t], 0, 0, 0);
-      acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, b[t], acc[t], 0, 0, 0);
+      for (int t = 0; t < NB; ++t)
+        if (u < n) b[t][u] = ld_frag(wb[t] + (size_t)(kc + u) * 512);
+#pragma unroll
+    for (int u = 0; u < CH; ++u) {
+      if (u < n) {
+        bf16x8 a0 = zero_frag(), a1 = zero_frag();
+        if (rok) {
+          a0 = ld_frag(ah + (kc + u) * 32);
+          a1 = ld_frag(al + (kc + u) * 32);
+        }
+#pragma unroll
+        for (int t = 0; t < NB; ++t) {
+          acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, b[t][u], acc[t], 0, 0, 0);
+          acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, b[t][u], acc[t], 0, 0, 0);
+        }
+      }
     }
   }
 

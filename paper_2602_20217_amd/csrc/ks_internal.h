@@ -115,6 +115,7 @@ void attn_split(const AttnArgs& a, hipStream_t st);
 // the attention output as O-projection input activations.
 void attn_combine(const AttnArgs& a, const float* kvself, Act act_out, hipStream_t st);
 int attn_nsplit(int n_positions, int tiles);
+int attn_rows_per_block(int G, bool batched);
 
 // argmax (lowest index on ties) and top-1 probability of each row of logits
 void argmax_rows(const float* logits, int M, int V, int32_t* am, float* top1, hipStream_t st);

@@ -21,13 +21,23 @@ __device__ inline double wsum_d(double v) {
 }
 
 // --------------------------------------------------------------- embedding
-__global__ void k_embed(const void* __restrict__ E, int bf, const int32_t* __restrict__ tok,
-                        int d, float* __restrict__ x, int ldx) {
+// 256 threads per row, 4 elements per thread per step (d % 4 == 0).
+__global__ __launch_bounds__(256) void k_embed(const void* __restrict__ E, int bf,
+                                               const int32_t* __restrict__ tok, int d,
+                                               float* __restrict__ x, int ldx) {
   const int m = blockIdx.x;
   const size_t base = (size_t)tok[m] * d;
-  for (int c = threadIdx.x; c < d; c += blockDim.x) {
-    const float v = bf ? bf2f(((const bf16_t*)E)[base + c]) : ((const float*)E)[base + c];
-    x[(size_t)m * ldx + c] = v;
+  float* xr = x + (size_t)m * ldx;
+  for (int c = 4 * threadIdx.x; c < d; c += 1024) {
+    float4 v;
+    if (bf) {
+      const uint2 u = *(const uint2*)((const bf16_t*)E + base + c);
+      v = make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xFFFF0000u),
+                      __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xFFFF0000u));
+    } else {
+      v = *(const float4*)((const float*)E + base + c);
+    }
+    *(float4*)(xr + c) = v;
   }
 }
 
@@ -39,37 +49,66 @@ void embed_rows(const void* E, int dtype, const int32_t* tok, int M, int d, floa
 }
 
 // ---------------------------------------------------------------- RMSNorm
-// One 256-thread block per row.  Sum of squares: per-thread strided partial
-// sums, then a fixed tree over the block.
+// One 256-thread block per row; a thread holds up to 4 float4 of the row
+// (d <= 4096; wider rows take a strided loop).  Sum of squares: per-thread
+// partials, wave butterfly, then the 4 wave sums added in order.
 __global__ __launch_bounds__(256) void k_norm_act(const float* __restrict__ x, int ldx,
                                                   const float* __restrict__ g, float eps, int d,
                                                   int bf, void* ahi, void* alo, int lda) {
-  __shared__ float red[256];
+  __shared__ float red[4];
   const int m = blockIdx.x;
   const float* xr = x + (size_t)m * ldx;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  constexpr int U = 4;
+  float4 v[U];
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int c = 4 * (threadIdx.x + 256 * u);
+    v[u] = c < d ? *(const float4*)(xr + c) : make_float4(0.f, 0.f, 0.f, 0.f);
+  }
   float scale = 1.0f;
   if (g) {
     float s = 0.f;
-    for (int c = threadIdx.x; c < d; c += 256) s = fmaf(xr[c], xr[c], s);
-    red[threadIdx.x] = s;
-    __syncthreads();
-    for (int o = 128; o >= 1; o >>= 1) {
-      if (threadIdx.x < o) red[threadIdx.x] += red[threadIdx.x + o];
-      __syncthreads();
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      s += v[u].x * v[u].x + v[u].y * v[u].y + v[u].z * v[u].z + v[u].w * v[u].w;
+    for (int c = 4 * (threadIdx.x + 256 * U); c < d; c += 1024) {
+      const float4 t = *(const float4*)(xr + c);
+      s += t.x * t.x + t.y * t.y + t.z * t.z + t.w * t.w;
     }
-    scale = 1.0f / sqrtf(red[0] / (float)d + eps);
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) s += __shfl_xor(s, o);
+    if (lane == 0) red[wave] = s;
+    __syncthreads();
+    scale = 1.0f / sqrtf((red[0] + red[1] + red[2] + red[3]) / (float)d + eps);
   }
-  for (int c = threadIdx.x; c < d; c += 256) {
-    const float a = g ? xr[c] * scale * g[c] : xr[c];
+  auto emit = [&](int c, float4 t) {
+    float a[4] = {t.x, t.y, t.z, t.w};
+    if (g) {
+      const float4 gg = *(const float4*)(g + c);
+      a[0] *= scale * gg.x; a[1] *= scale * gg.y; a[2] *= scale * gg.z; a[3] *= scale * gg.w;
+    }
     const size_t off = (size_t)m * lda + c;
     if (bf) {
-      const bf16_t h = f2bf(a);
-      ((bf16_t*)ahi)[off] = h;
-      ((bf16_t*)alo)[off] = f2bf(a - bf2f(h));
+      uint32_t h[2], l[2];
+#pragma unroll
+      for (int k = 0; k < 2; ++k) {
+        const bf16_t h0 = f2bf(a[2 * k]), h1 = f2bf(a[2 * k + 1]);
+        h[k] = (uint32_t)h0 | ((uint32_t)h1 << 16);
+        l[k] = (uint32_t)f2bf(a[2 * k] - bf2f(h0)) | ((uint32_t)f2bf(a[2 * k + 1] - bf2f(h1)) << 16);
+      }
+      *(uint2*)((bf16_t*)ahi + off) = make_uint2(h[0], h[1]);
+      *(uint2*)((bf16_t*)alo + off) = make_uint2(l[0], l[1]);
     } else {
-      ((float*)ahi)[off] = a;
+      *(float4*)((float*)ahi + off) = make_float4(a[0], a[1], a[2], a[3]);
     }
+  };
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int c = 4 * (threadIdx.x + 256 * u);
+    if (c < d) emit(c, v[u]);
   }
+  for (int c = 4 * (threadIdx.x + 256 * U); c < d; c += 1024) emit(c, *(const float4*)(xr + c));
 }
 
 void norm_act(const float* x, int ldx, const float* g, float eps, int M, int d, int dtype,
@@ -83,19 +122,22 @@ void norm_act(const float* x, int ldx, const float* g, float eps, int M, int d, 
 // One block per row; one wave per head at a time; lane f < hd/2 owns the
 // rotary pair (f, f + hd/2).
 __global__ __launch_bounds__(256) void k_qkv_post(QkvPostArgs a) {
-  const int m = blockIdx.x;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int m = blockIdx.y;
+  const int lane = threadIdx.x & 63;
   const int hd = a.hd, half = hd / 2;
   const int nh = a.hq + 2 * a.hkv;
+  const int hh = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (hh >= nh) return;
   const int pos = a.pos[m];
   const bool act = lane < half;
   const float* src_row = a.qkv + (size_t)m * nh * hd;
   float c = 1.f, s = 0.f;
-  if (act) {
-    c = a.rope_cs[((size_t)pos * half + lane) * 2];
-    s = a.rope_cs[((size_t)pos * half + lane) * 2 + 1];
+  if (act && hh < a.hq + a.hkv) {
+    const float2 cs = *(const float2*)&a.rope_cs[((size_t)pos * half + lane) * 2];
+    c = cs.x;
+    s = cs.y;
   }
-  for (int hh = wave; hh < nh; hh += 4) {
+  {
     const float* src = src_row + (size_t)hh * hd;
     float x0 = act ? src[lane] : 0.f;
     float x1 = act ? src[lane + half] : 0.f;
@@ -113,12 +155,12 @@ __global__ __launch_bounds__(256) void k_qkv_post(QkvPostArgs a) {
       y0 = x0 * c - x1 * s;
       y1 = x1 * c + x0 * s;
     }
-    if (!act) continue;
+    if (!act) return;
     if (hh < a.hq) {
       float* q = a.q_out + ((size_t)m * a.hq + hh) * hd;
       q[lane] = y0;
       q[lane + half] = y1;
-      continue;
+      return;
     }
     const int kv = hh < a.hq + a.hkv ? 0 : 1;
     const int kvh = hh - a.hq - kv * a.hkv;
@@ -146,54 +188,69 @@ __global__ __launch_bounds__(256) void k_qkv_post(QkvPostArgs a) {
 
 void qkv_post(const QkvPostArgs& a, hipStream_t st) {
   if (a.M <= 0) return;
-  hipLaunchKernelGGL(k_qkv_post, dim3(a.M), dim3(256), 0, st, a);
+  const int nh = a.hq + 2 * a.hkv;
+  hipLaunchKernelGGL(k_qkv_post, dim3((nh + 3) / 4, a.M), dim3(256), 0, st, a);
 }
 
 // ------------------------------------------------------------------ argmax
-// Larger value wins; equal values keep the lower index.
+// One pass per element: running (max, first index of max, sum of exp(v - max))
+// per thread over a fixed strided order, then a fixed tree.  Larger value
+// wins; equal values keep the lower index.
+struct AmState {
+  float m;
+  int i;
+  float s;
+};
+__device__ inline void am_push(AmState& a, float v, int i) {
+  if (v > a.m) {
+    a.s = a.s * __expf(a.m - v) + 1.0f;
+    a.m = v;
+    a.i = i;
+  } else {
+    a.s += __expf(v - a.m);
+  }
+}
+__device__ inline AmState am_merge(AmState a, AmState b) {
+  AmState r;
+  if (b.m > a.m || (b.m == a.m && b.i < a.i)) {
+    r.m = b.m;
+    r.i = b.i;
+  } else {
+    r.m = a.m;
+    r.i = a.i;
+  }
+  r.s = a.s * __expf(a.m - r.m) + b.s * __expf(b.m - r.m);
+  return r;
+}
+
 __global__ __launch_bounds__(1024) void k_argmax(const float* __restrict__ logits, int V,
                                                  int32_t* am, float* top1) {
-  __shared__ float sv[1024];
-  __shared__ int si[1024];
+  __shared__ AmState sh[16];
   const int m = blockIdx.x;
   const float* row = logits + (size_t)m * V;
-  float bv = -FLT_MAX;
-  int bi = 0x7FFFFFFF;
-  for (int i = threadIdx.x; i < V; i += 1024) {
-    const float v = row[i];
-    if (v > bv) {
-      bv = v;
-      bi = i;
-    }
+  AmState a{-FLT_MAX, 0x7FFFFFFF, 0.f};
+  const int V4 = V / 4;  // V % 16 == 0
+#pragma unroll 4
+  for (int k = threadIdx.x; k < V4; k += 1024) {
+    const float4 v = *(const float4*)(row + 4 * k);
+    am_push(a, v.x, 4 * k);
+    am_push(a, v.y, 4 * k + 1);
+    am_push(a, v.z, 4 * k + 2);
+    am_push(a, v.w, 4 * k + 3);
   }
-  sv[threadIdx.x] = bv;
-  si[threadIdx.x] = bi;
-  __syncthreads();
-  for (int o = 512; o >= 1; o >>= 1) {
-    if (threadIdx.x < o) {
-      const float v2 = sv[threadIdx.x + o];
-      const int i2 = si[threadIdx.x + o];
-      if (v2 > sv[threadIdx.x] || (v2 == sv[threadIdx.x] && i2 < si[threadIdx.x])) {
-        sv[threadIdx.x] = v2;
-        si[threadIdx.x] = i2;
-      }
-    }
-    __syncthreads();
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    AmState b{__shfl_xor(a.m, o), __shfl_xor(a.i, o), __shfl_xor(a.s, o)};
+    a = am_merge(a, b);
   }
-  const float mx = sv[0];
-  const int arg = si[0];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  if (lane == 0) sh[wave] = a;
   __syncthreads();
-  float s = 0.f;
-  for (int i = threadIdx.x; i < V; i += 1024) s += __expf(row[i] - mx);
-  sv[threadIdx.x] = s;
-  __syncthreads();
-  for (int o = 512; o >= 1; o >>= 1) {
-    if (threadIdx.x < o) sv[threadIdx.x] += sv[threadIdx.x + o];
-    __syncthreads();
-  }
   if (threadIdx.x == 0) {
-    am[m] = arg;
-    if (top1) top1[m] = 1.0f / sv[0];
+    AmState r = sh[0];
+    for (int w = 1; w < 16; ++w) r = am_merge(r, sh[w]);
+    am[m] = r.i;
+    if (top1) top1[m] = 1.0f / r.s;
   }
 }
 
