@@ -8,7 +8,8 @@ import ctypes as C
 import os
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libknapspec.so")
+# KNAPSPEC_LIB selects another build of the same library (e.g. a tuning variant)
+LIB_PATH = os.environ.get("KNAPSPEC_LIB") or os.path.join(HERE, "libknapspec.so")
 
 KS_OK, KS_EINVAL, KS_ENOMEM, KS_ECAPACITY, KS_ESTATE, KS_EHIP = 0, -1, -2, -3, -4, -5
 KS_F32, KS_BF16 = 0, 1

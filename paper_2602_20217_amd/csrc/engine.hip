@@ -45,8 +45,8 @@ using namespace ks;
 namespace {
 
 constexpr int PB = 512;        // rows per batched attention / head pass
-constexpr int DEC_TILES = 1;   // decode/verify: 128 positions per split
-constexpr int BAT_TILES = 8;   // prefill/DP: 1024 positions per split
+constexpr int DEC_TILES = 1;   // decode/verify: 64 positions per split
+constexpr int BAT_TILES = 16;  // prefill/DP: 1024 positions per split
 
 size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
 

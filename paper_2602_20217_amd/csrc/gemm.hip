@@ -37,7 +37,7 @@ __device__ inline void store_split(bf16_t* hi, bf16_t* lo, size_t off, float a) 
 }
 
 // ------------------------------------------------------------------ skinny
-template <int NB, int NW, int EPI>
+template <int NB, int NW, int CH, int EPI>
 __global__ __launch_bounds__(NW * 64) void k_gemm_skinny(
     int M, int N, int K, const bf16_t* __restrict__ Ahi, const bf16_t* __restrict__ Alo,
     int lda, const bf16_t* __restrict__ Wp, float* out, int ldo, const float* res, int ldres,
@@ -66,7 +66,6 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_skinny(
   }
   // chunks of CH k-steps: every weight fragment of a chunk is requested before
   // the first matrix instruction of the chunk
-  constexpr int CH = 8;
   for (int kc = kb; kc < ke; kc += CH) {
     const int n = ke - kc < CH ? ke - kc : CH;
     bf16x8 b[NB][CH];
@@ -124,29 +123,35 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_skinny(
   }
 }
 
-void gemm_bf16_skinny(const GemmArgs& g, hipStream_t st) {
-  constexpr int NW = 16;
+template <int NB, int NW, int CH>
+static void launch_skinny(const GemmArgs& g, hipStream_t st) {
   const int NT = g.N / 16;
   const bf16_t* Ahi = (const bf16_t*)g.A.hi;
   const bf16_t* Alo = (const bf16_t*)g.A.lo;
   const bf16_t* W = (const bf16_t*)g.W;
-  if (g.epi == EPI_SWIGLU) {
-    constexpr int NB = 2;
-    dim3 grid((NT + NB - 1) / NB);
-    hipLaunchKernelGGL((k_gemm_skinny<NB, NW, EPI_SWIGLU>), grid, dim3(NW * 64), 0, st, g.M,
-                       g.N, g.K, Ahi, Alo, g.A.ld, W, g.out, g.ldo, g.res, g.ldres,
-                       (bf16_t*)g.act_out.hi, (bf16_t*)g.act_out.lo, g.act_out.ld);
-  } else if (g.epi == EPI_RESID) {
-    dim3 grid(NT);
-    hipLaunchKernelGGL((k_gemm_skinny<1, NW, EPI_RESID>), grid, dim3(NW * 64), 0, st, g.M, g.N,
-                       g.K, Ahi, Alo, g.A.ld, W, g.out, g.ldo, g.res, g.ldres, nullptr, nullptr,
-                       0);
-  } else {
-    dim3 grid(NT);
-    hipLaunchKernelGGL((k_gemm_skinny<1, NW, EPI_STORE>), grid, dim3(NW * 64), 0, st, g.M, g.N,
-                       g.K, Ahi, Alo, g.A.ld, W, g.out, g.ldo, g.res, g.ldres, nullptr, nullptr,
-                       0);
-  }
+  dim3 grid((NT + NB - 1) / NB), block(NW * 64);
+  if (g.epi == EPI_SWIGLU)
+    hipLaunchKernelGGL((k_gemm_skinny<NB, NW, CH, EPI_SWIGLU>), grid, block, 0, st, g.M, g.N, g.K,
+                       Ahi, Alo, g.A.ld, W, g.out, g.ldo, g.res, g.ldres, (bf16_t*)g.act_out.hi,
+                       (bf16_t*)g.act_out.lo, g.act_out.ld);
+  else if (g.epi == EPI_RESID)
+    hipLaunchKernelGGL((k_gemm_skinny<NB, NW, CH, EPI_RESID>), grid, block, 0, st, g.M, g.N, g.K,
+                       Ahi, Alo, g.A.ld, W, g.out, g.ldo, g.res, g.ldres, nullptr, nullptr, 0);
+  else
+    hipLaunchKernelGGL((k_gemm_skinny<NB, NW, CH, EPI_STORE>), grid, block, 0, st, g.M, g.N, g.K,
+                       Ahi, Alo, g.A.ld, W, g.out, g.ldo, g.res, g.ldres, nullptr, nullptr, 0);
+}
+
+// Launch shape by matrix shape only (never by row count), measured on MI355X
+// with the Llama-8B shapes: gate/up prefers small workgroups that several fit
+// on a CU, the long-K down projection a 16-way K split, the vocabulary head
+// 8 waves, the remaining square-ish products 16 (N <= 4096) or 8 waves.
+void gemm_bf16_skinny(const GemmArgs& g, hipStream_t st) {
+  if (g.epi == EPI_SWIGLU) launch_skinny<2, 4, 4>(g, st);
+  else if (g.K >= 8192) launch_skinny<1, 16, 8>(g, st);
+  else if (g.N >= 65536) launch_skinny<1, 8, 8>(g, st);
+  else if (g.N <= 4096) launch_skinny<1, 16, 8>(g, st);
+  else launch_skinny<1, 8, 8>(g, st);
 }
 
 // ------------------------------------------------------------------- tiled

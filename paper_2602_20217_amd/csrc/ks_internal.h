@@ -96,7 +96,7 @@ struct QkvPostArgs {
 void qkv_post(const QkvPostArgs& a, hipStream_t st);
 
 // Split attention over the cache.  Row m attends cache positions [0, len[m]);
-// splits of 128 positions, `tiles` tiles per split; partial (o[hd], max, sum)
+// splits of 64 * tiles positions; partial (o[hd], max, sum)
 // per (row, q head, split).
 struct AttnArgs {
   int M, hq, hkv, hd, n_max, dtype;
@@ -105,7 +105,7 @@ struct AttnArgs {
   const void* vc;
   const int32_t* len;    // device [M]
   int max_len;           // host upper bound of len[]
-  int tiles;             // 128-position tiles per split
+  int tiles;             // 64-position tiles per split
   int rows_per_block;
   float* part;           // [M][hq][nsplit][hd+2]
   int nsplit;            // stride: splits per (row, head)
