@@ -169,7 +169,8 @@ ks_status ks_pack_matrix(const void* src, void* dst, int N, int K, int dtype, vo
 /*
  * ks_pack_gate_up: gate and up projections, each row-major [ffn][d] (device).
  * KS_F32: dst = [gate rows; up rows] row-major [2 ffn][d].  KS_BF16: packed as
- * a [2 ffn][d] matrix whose 16-row tiles alternate gate tile t, up tile t.
+ * a [2 ffn][d] matrix whose 16-row tile t holds gate rows 8t..8t+7 followed by
+ * up rows 8t..8t+7, so one tile yields 8 SwiGLU outputs.
  */
 ks_status ks_pack_gate_up(const void* gate, const void* up, void* dst, int ffn, int d,
                           int dtype, void* stream);

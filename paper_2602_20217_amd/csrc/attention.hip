@@ -391,10 +391,12 @@ __global__ __launch_bounds__(NWAVE * 64) void k_attn_mfma(
   }
 }
 
-// One wave per (row, query head); output dims lane -> (2 lane, 2 lane + 1) for
-// bf16 caches, lane for float32 caches.  The split maxima are reduced across
-// lanes, then the splits are merged in ascending order (loads of different
-// splits are independent, so they are in flight together).
+// One workgroup of 4 waves per (row, query head); output dims lane -> (2 lane,
+// 2 lane + 1) for bf16 caches, lane for float32 caches.  The split maxima are
+// reduced across the workgroup; wave w then merges splits s = w, w + 4, ...
+// (loads of different splits are independent, so they are in flight together)
+// and the four wave sums are added in wave order.  The row's own key/value
+// (selection rows) joins the max and is added last.
 template <int HD, bool BF>
 __global__ __launch_bounds__(256) void k_attn_combine(int M, int hq, int hkv, int span,
                                                       const float* __restrict__ q,
@@ -404,9 +406,11 @@ __global__ __launch_bounds__(256) void k_attn_combine(int M, int hq, int hkv, in
                                                       bf16_t* ohi, bf16_t* olo, float* of,
                                                       int ldact) {
   constexpr int DPL = HD / 64;
+  __shared__ float s_m[4];
+  __shared__ float s_acc[4][DPL * 64 + 1];
   const int lane = threadIdx.x & 63;
-  const int gid = __builtin_amdgcn_readfirstlane(blockIdx.x * 4 + (threadIdx.x >> 6));
-  if (gid >= M * hq) return;
+  const int wave = threadIdx.x >> 6;
+  const int gid = blockIdx.x;
   const int r = gid / hq, h = gid % hq;
   const int G = hq / hkv;
   const int kvh = h / G;
@@ -416,26 +420,26 @@ __global__ __launch_bounds__(256) void k_attn_combine(int M, int hq, int hkv, in
   const int d0 = BF ? 2 * lane : lane;
 
   float mloc = -FLT_MAX;
-  for (int s = lane; s < ns; s += 64) mloc = fmaxf(mloc, pr[(size_t)s * (HD + 2) + HD]);
-  float mx = wave_max(mloc);
+  for (int s = threadIdx.x; s < ns; s += 256) mloc = fmaxf(mloc, pr[(size_t)s * (HD + 2) + HD]);
+  mloc = wave_max(mloc);
+  if (lane == 0) s_m[wave] = mloc;
+  __syncthreads();
+  float mx = fmaxf(fmaxf(s_m[0], s_m[1]), fmaxf(s_m[2], s_m[3]));
   float sself = 0.f;
-  const float* ks = nullptr;
-  const float* vs = nullptr;
   if (kvself) {
-    ks = kvself + (((size_t)r * 2 + 0) * hkv + kvh) * HD;
-    vs = kvself + (((size_t)r * 2 + 1) * hkv + kvh) * HD;
+    const float* ks = kvself + (((size_t)r * 2 + 0) * hkv + kvh) * HD;
     const float* qv = q + ((size_t)r * hq + h) * HD;
-    float d = 0.f;
+    float dd = 0.f;
 #pragma unroll
-    for (int e = 0; e < DPL; ++e) d = fmaf(qv[d0 + e], ks[d0 + e], d);
-    sself = wave_sum(d) * (1.0f / sqrtf((float)HD));
+    for (int e = 0; e < DPL; ++e) dd = fmaf(qv[d0 + e], ks[d0 + e], dd);
+    sself = wave_sum(dd) * (1.0f / sqrtf((float)HD));
     mx = fmaxf(mx, sself);
   }
   float lsum = 0.f, acc[DPL];
 #pragma unroll
   for (int e = 0; e < DPL; ++e) acc[e] = 0.f;
-#pragma unroll 8
-  for (int s = 0; s < ns; ++s) {
+#pragma unroll 4
+  for (int s = wave; s < ns; s += 4) {
     const float* ps = pr + (size_t)s * (HD + 2);
     const float w = __expf(ps[HD] - mx);
     lsum = fmaf(ps[HD + 1], w, lsum);
@@ -447,7 +451,18 @@ __global__ __launch_bounds__(256) void k_attn_combine(int M, int hq, int hkv, in
       acc[0] = fmaf(ps[d0], w, acc[0]);
     }
   }
+#pragma unroll
+  for (int e = 0; e < DPL; ++e) s_acc[wave][DPL * lane + e] = acc[e];
+  if (lane == 0) s_acc[wave][DPL * 64] = lsum;
+  __syncthreads();
+  if (wave != 0) return;
+#pragma unroll
+  for (int e = 0; e < DPL; ++e)
+    acc[e] = ((s_acc[0][DPL * lane + e] + s_acc[1][DPL * lane + e]) + s_acc[2][DPL * lane + e]) +
+             s_acc[3][DPL * lane + e];
+  lsum = ((s_acc[0][DPL * 64] + s_acc[1][DPL * 64]) + s_acc[2][DPL * 64]) + s_acc[3][DPL * 64];
   if (kvself) {
+    const float* vs = kvself + (((size_t)r * 2 + 1) * hkv + kvh) * HD;
     const float w = __expf(sself - mx);
     lsum += w;
 #pragma unroll
@@ -509,7 +524,7 @@ void attn_split(const AttnArgs& a, hipStream_t st) {
 }
 
 void attn_combine(const AttnArgs& a, const float* kvself, Act act_out, hipStream_t st) {
-  dim3 grid((a.M * a.hq + 3) / 4);
+  dim3 grid(a.M * a.hq);
   const int span = TILE * a.tiles;
   const bool bf = a.dtype == KS_BF16;
 #define KS_COMB(HDV, BFV)                                                                    \

@@ -97,16 +97,17 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_skinny(
   __syncthreads();
 
   if (EPI == EPI_SWIGLU) {
-    for (int idx = threadIdx.x; idx < (NB / 2) * 256; idx += NW * 64) {
-      const int p = idx >> 8, l = (idx >> 2) & 63, v = idx & 3;
+    // tile rows 0..7 are gate rows, 8..15 the matching up rows
+    for (int idx = threadIdx.x; idx < NB * 256; idx += NW * 64) {
+      const int t = idx >> 8, l = (idx >> 2) & 63, v = idx & 3;
       const int m = 4 * (l >> 4) + v;
-      if (m >= M || nt0 + 2 * p + 1 >= NT) continue;
+      if (m >= M || nt0 + t >= NT || (l & 15) >= 8) continue;
       float g = 0.f, u = 0.f;
       for (int w = 0; w < NW; ++w) {
-        g += red[w][2 * p][l][v];
-        u += red[w][2 * p + 1][l][v];
+        g += red[w][t][l][v];
+        u += red[w][t][l + 8][v];
       }
-      const int c = ((nt0 + 2 * p) >> 1) * 16 + (l & 15);
+      const int c = (nt0 + t) * 8 + (l & 15);
       store_split(ohi, olo, (size_t)m * ldact + c, silu_mul(g, u));
     }
   } else {
@@ -143,11 +144,11 @@ static void launch_skinny(const GemmArgs& g, hipStream_t st) {
 }
 
 // Launch shape by matrix shape only (never by row count), measured on MI355X
-// with the Llama-8B shapes: gate/up prefers small workgroups that several fit
-// on a CU, the long-K down projection a 16-way K split, the vocabulary head
-// 8 waves, the remaining square-ish products 16 (N <= 4096) or 8 waves.
+// with the Llama-8B shapes: the wide products (gate/up, vocabulary head) one
+// tile per 8-wave workgroup, the long-K down projection a 16-way K split, the
+// remaining square-ish products 16 (N <= 4096) or 8 waves.
 void gemm_bf16_skinny(const GemmArgs& g, hipStream_t st) {
-  if (g.epi == EPI_SWIGLU) launch_skinny<2, 4, 4>(g, st);
+  if (g.epi == EPI_SWIGLU) launch_skinny<1, 8, 8>(g, st);
   else if (g.K >= 8192) launch_skinny<1, 16, 8>(g, st);
   else if (g.N >= 65536) launch_skinny<1, 8, 8>(g, st);
   else if (g.N <= 4096) launch_skinny<1, 16, 8>(g, st);
@@ -209,16 +210,16 @@ __global__ __launch_bounds__(256) void k_gemm_tiled(int M, int N, int K,
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
       const int m = m0 + i * 16 + 4 * (lane >> 4) + v;
-      if (m >= M) continue;
       if (EPI == EPI_SWIGLU) {
 #pragma unroll
-        for (int p = 0; p < 2; ++p) {
-          if (nt0 + 2 * p + 1 >= NT) continue;
-          const int c = ((nt0 + 2 * p) >> 1) * 16 + (lane & 15);
-          store_split(ohi, olo, (size_t)m * ldact + c,
-                      silu_mul(acc[i][2 * p][v], acc[i][2 * p + 1][v]));
+        for (int t = 0; t < 4; ++t) {
+          const float up = __shfl(acc[i][t][v], (lane & 48) | ((lane + 8) & 15));
+          if (m >= M || !bok[t] || (lane & 15) >= 8) continue;
+          const int c = (nt0 + t) * 8 + (lane & 15);
+          store_split(ohi, olo, (size_t)m * ldact + c, silu_mul(acc[i][t][v], up));
         }
       } else {
+        if (m >= M) continue;
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
           if (!bok[t]) continue;
@@ -316,9 +317,9 @@ __global__ void k_pack(const bf16_t* __restrict__ src0, const bf16_t* __restrict
   const int nt = (int)(tile / KT);
   const bf16_t* src = src0;
   int row = nt * 16 + (l & 15);
-  if (interleave) {  // tile 2t: gate tile t; tile 2t+1: up tile t
-    src = (nt & 1) ? src1 : src0;
-    row = (nt >> 1) * 16 + (l & 15);
+  if (interleave) {  // tile t: gate rows 8t..8t+7, then up rows 8t..8t+7
+    src = (l & 8) ? src1 : src0;
+    row = nt * 8 + (l & 7);
   }
   const u32x4 v = *(const u32x4*)(src + (size_t)row * K + kt * 32 + (l >> 4) * 8);
   *(u32x4*)(dst + f * 8) = v;

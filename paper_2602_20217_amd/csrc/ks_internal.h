@@ -49,8 +49,9 @@ struct Act {
 // GEMM: y[m][n] = sum_k A[m][k] W[n][k] for m < M, n < N (N = rows of W).
 //  EPI_STORE : out[m][n] = y
 //  EPI_RESID : out[m][n] = res[m][n] + y          (out may alias res)
-//  EPI_SWIGLU: W holds interleaved gate/up rows (see ks_pack_gate_up); writes
-//              act_out[m][u] = silu(gate_u) * up_u for u < N/2.
+//  EPI_SWIGLU: W holds gate/up rows interleaved by 8 inside each 16-row tile
+//              (see ks_pack_gate_up); writes act_out[m][u] = silu(gate_u) * up_u
+//              for u < N/2.
 struct GemmArgs {
   int M, N, K;
   Act A;
