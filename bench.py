@@ -111,6 +111,9 @@ def main():
     ap.add_argument("--reselect", type=int, default=32)
     ap.add_argument("--cpu-budget", type=float, default=20.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--profile-kernels", action="store_true",
+                    help="short run for hardware counters: prefill, 16 decode steps and a "
+                         "256 MiB device copy (the reference for counter scaling)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path "
@@ -137,6 +140,20 @@ def main():
     first = dm.prefill(prompt)
     torch.cuda.synchronize()
     log(f"prefill {args.ctx} tokens: {time.time() - t:.2f}s")
+    if args.profile_kernels:
+        # reference of known size for counter scaling: an elementwise product that
+        # reads and writes 256 MiB (its own kernel name in the counter output)
+        copy_bytes = 256 << 20
+        src = torch.empty(copy_bytes // 4, dtype=torch.float32, device="cuda").fill_(1.0)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            torch.mul(src, 1.0, out=dst)
+        torch.cuda.synchronize()
+        prof = dm.profile_decode(None, 16, per_kernel=False)
+        print(json.dumps({"mode": "profile-kernels", "copy_bytes": copy_bytes,
+                          "decode_steps": 16, "ms_step": prof["ms_step"]}), flush=True)
+        dm.close()
+        return
     sweep_ctx = sorted({max(64, args.ctx // 8), args.ctx // 4, args.ctx // 2, args.ctx})
     coeffs, sweep = latency_sweep(dm, cfg, sweep_ctx, first)
     log(f"latency model c1={coeffs[0]:.4f}ms c2={coeffs[1]:.3e}ms/token c3={coeffs[2]:.4f}ms")
@@ -213,7 +230,7 @@ def main():
         "ar_step_GBps": round(token_bytes / (mean_ar / args.new * 1e-3) / 1e9, 1),
         "latency_model_ms": {"c1": coeffs[0], "c2": coeffs[1], "c3": coeffs[2], "sweep": sweep},
         "kernels": kern,
-        "roofline": {"bound": "hbm", "kernel": "k_gemm_skinny<2,16,SWIGLU> (gate/up + SwiGLU, 1 row)",
+        "roofline": {"bound": "hbm", "kernel": "k_gemm_skinny, SwiGLU epilogue (gate/up product, 1 row)",
                      "achieved": round(achieved, 1), "peak": 8000.0, "unit": "GB/s",
                      "frac": round(achieved / 8000.0, 4), "traffic": None,
                      "bytes_per_launch": bytes_gu, "ms_per_launch": round(ms_gu, 5)},
