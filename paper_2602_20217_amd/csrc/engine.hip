@@ -103,7 +103,7 @@ Layout make_layout(const ks_model_desc& d, const ks_limits& lim) {
   y.ge = take((size_t)y.DR * d.d * 4);
   y.dpos = take((size_t)y.DR * 4);
   y.dlen = take((size_t)y.DR * 4);
-  y.sig = take((size_t)2 * y.cells * 8);
+  y.sig = take((size_t)2 * y.DR * 8);
   y.ptrs = take((size_t)4 * (y.cells + 2 * d.L + 2) * 8);
   y.total = o;
   return y;
@@ -667,6 +667,7 @@ static ks_status select_internal(ks_ctx* c, const ks_select_params* p, ks_select
   std::vector<double> se(J + 1), ss(J + 1);
   std::vector<const float*> hs;
   std::vector<float*> hd;
+  std::vector<double> hrow(2 * (size_t)c->y.DR), hsig(2 * (size_t)c->y.cells);
   if (dbg) {
     for (int j = 0; j < dbg->J_cap; ++j) dbg->n_match[j] = -1;
     for (int i = 0; i <= L2; ++i)
@@ -684,12 +685,18 @@ static ks_status select_internal(ks_ctx* c, const ks_select_params* p, ks_select
     const int M = nc * r;
     // execute candidates for every reachable budget
     sublayer_rows(c, i, gprev, E, M, dpos, dlen, n, 1, true);
-    cos_groups_f64(E, X(i), nc, r, d.d, sig, c->st);
-    cos_groups_f64(gprev, X(i), nc, r, d.d, sig + c->y.cells, c->st);
+    // per-row cosines of both candidates against X^(i); the matrix cosine of
+    // Section 2 (mean over the r rows) is taken here, in row order
+    cos_rows(E, X(i), M, r, d.d, sig, c->st);
+    cos_rows(gprev, X(i), M, r, d.d, sig + M, c->st);
     HIPCHK(hipGetLastError());
-    std::vector<double> hsig(2 * (size_t)c->y.cells);
-    HIPCHK(hipMemcpyAsync(hsig.data(), sig, 2 * c->y.cells * 8, hipMemcpyDeviceToHost, c->st));
+    HIPCHK(hipMemcpyAsync(hrow.data(), sig, 2 * (size_t)M * 8, hipMemcpyDeviceToHost, c->st));
     HIPCHK(hipStreamSynchronize(c->st));
+    for (int k = 0; k < 2 * nc; ++k) {
+      double sum = 0.0;
+      for (int t = 0; t < r; ++t) sum += hrow[(size_t)k * r + t];
+      hsig[k < nc ? k : c->y.cells + k - nc] = sum / r;
+    }
     std::fill(idx.begin(), idx.end(), -1);
     for (int k = 0; k < nc; ++k) idx[cells[k]] = k;
     std::vector<int> ncells;

@@ -14,8 +14,9 @@
 // result does not depend on how many rows are in the batch: a verify row and
 // the decode step at the same position produce identical bits.
 //
-// Tiled path (batched rows of the selection DP and of prefill): a 64x64 wave
-// tile of 16x16x32 MFMAs over single bf16 activations.
+// Tiled path (batched rows of the selection DP and of prefill): 128 x 128
+// workgroup tiles staged through LDS, 64 x 64 wave tiles of 16x16x32 MFMAs over
+// single bf16 activations.
 #include "ks_internal.h"
 
 namespace ks {
@@ -156,20 +157,67 @@ void gemm_bf16_skinny(const GemmArgs& g, hipStream_t st) {
 }
 
 // ------------------------------------------------------------------- tiled
-// Block: 4 waves as 2 (rows) x 2 (cols); wave tile 64 rows x 64 cols.
+// Batched rows (prefill chunks, selection DP).  Workgroup tile 128 rows x 128
+// columns, 4 waves as 2 x 2 with 64 x 64 wave tiles (4 x 4 MFMAs).  Each
+// 32-wide k step of A and W is staged in LDS in the MFMA operand order (A:
+// row l%16, k 8(l/16).. of each 16-row tile at byte 16 l; W already arrives in
+// that order), so every fragment read is one conflict-free 16-byte LDS read.
+// The next step's global loads are in flight while the current step's MFMAs
+// run (double-buffered LDS, one barrier per step).  Workgroups that share a
+// weight tile get consecutive logical ids on the same XCD, so the XCD's L2
+// serves the reuse across row blocks.
 template <int EPI>
 __global__ __launch_bounds__(256) void k_gemm_tiled(int M, int N, int K,
                                                     const bf16_t* __restrict__ A, int lda,
                                                     const bf16_t* __restrict__ Wp, float* out,
                                                     int ldo, const float* res, int ldres,
-                                                    bf16_t* ohi, bf16_t* olo, int ldact) {
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
+                                                    bf16_t* ohi, bf16_t* olo, int ldact, int MB) {
+  __shared__ __align__(16) bf16_t As[2][8 * 512];
+  __shared__ __align__(16) bf16_t Bs[2][8 * 512];
   const int KT = K >> 5;
   const int NT = N >> 4;
-  const int m0 = blockIdx.y * 128 + (wave & 1) * 64;
-  const int nt0 = blockIdx.x * 8 + (wave >> 1) * 4;
-  const int kg = lane >> 4;
+  // XCD-aware logical block id (blocks are dealt round-robin over 8 XCDs)
+  const int nblk = gridDim.x;
+  const int bid = blockIdx.x;
+  int lb = bid;
+  if ((nblk & 7) == 0) lb = (bid & 7) * (nblk >> 3) + (bid >> 3);
+  const int mb = lb % MB, nb = lb / MB;
+  const int m0 = mb * 128, nt0 = nb * 8;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave & 1, wn = wave >> 1;
+
+  // staging map: chunk c in [0, 512) of 16 bytes, two per thread per operand
+  //   A: row c/4, k chunk c%4  -> tile row/16, lane (row%16) + 16 (c%4)
+  //   W: tile c/64, lane c%64
+  const int c0 = tid, c1 = tid + 256;
+  const int ar0 = m0 + (c0 >> 2), ar1 = m0 + (c1 >> 2);
+  const bool ak0 = ar0 < M, ak1 = ar1 < M;
+  const bf16_t* as0 = A + (size_t)(ak0 ? ar0 : 0) * lda + (c0 & 3) * 8;
+  const bf16_t* as1 = A + (size_t)(ak1 ? ar1 : 0) * lda + (c1 & 3) * 8;
+  const int ad0 = ((c0 >> 2) >> 4) * 512 + (((c0 >> 2) & 15) + 16 * (c0 & 3)) * 8;
+  const int ad1 = ((c1 >> 2) >> 4) * 512 + (((c1 >> 2) & 15) + 16 * (c1 & 3)) * 8;
+  const bool bk0 = nt0 + (c0 >> 6) < NT, bk1 = nt0 + (c1 >> 6) < NT;
+  const bf16_t* bs0 = Wp + (size_t)(bk0 ? nt0 + (c0 >> 6) : 0) * KT * 512 + (c0 & 63) * 8;
+  const bf16_t* bs1 = Wp + (size_t)(bk1 ? nt0 + (c1 >> 6) : 0) * KT * 512 + (c1 & 63) * 8;
+  const int bd0 = (c0 >> 6) * 512 + (c0 & 63) * 8;
+  const int bd1 = (c1 >> 6) * 512 + (c1 & 63) * 8;
+  // sources are clamped to valid rows/tiles; out-of-range chunks are zeroed
+  // after the load (a load is never skipped, so no pointer select is formed)
+  const uint32_t am0 = ak0 ? ~0u : 0u, am1 = ak1 ? ~0u : 0u;
+  const uint32_t bm0 = bk0 ? ~0u : 0u, bm1 = bk1 ? ~0u : 0u;
+#define KS_MASK4(v, m) make_uint4((v).x & (m), (v).y & (m), (v).z & (m), (v).w & (m))
+  uint4 ra0 = *(const uint4*)as0, ra1 = *(const uint4*)as1;
+  uint4 rb0 = *(const uint4*)bs0, rb1 = *(const uint4*)bs1;
+  ra0 = KS_MASK4(ra0, am0);
+  ra1 = KS_MASK4(ra1, am1);
+  rb0 = KS_MASK4(rb0, bm0);
+  rb1 = KS_MASK4(rb1, bm1);
+  *(uint4*)&As[0][ad0] = ra0;
+  *(uint4*)&As[0][ad1] = ra1;
+  *(uint4*)&Bs[0][bd0] = rb0;
+  *(uint4*)&Bs[0][bd1] = rb1;
+  __syncthreads();
 
   f32x4 acc[4][4];
 #pragma unroll
@@ -177,56 +225,63 @@ __global__ __launch_bounds__(256) void k_gemm_tiled(int M, int N, int K,
 #pragma unroll
     for (int t = 0; t < 4; ++t) acc[i][t] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  const bf16_t* ap[4];
-  bool aok[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int r = m0 + i * 16 + (lane & 15);
-    aok[i] = r < M;
-    ap[i] = A + (size_t)(aok[i] ? r : 0) * lda + kg * 8;
-  }
-  const bf16_t* wp[4];
-  bool bok[4];
-#pragma unroll
-  for (int t = 0; t < 4; ++t) {
-    bok[t] = nt0 + t < NT;
-    wp[t] = Wp + (size_t)(bok[t] ? nt0 + t : 0) * KT * 512 + lane * 8;
-  }
   for (int kt = 0; kt < KT; ++kt) {
+    const int cur = kt & 1;
+    const bool more = kt + 1 < KT;
+    if (more) {
+      ra0 = *(const uint4*)(as0 + (kt + 1) * 32);
+      ra1 = *(const uint4*)(as1 + (kt + 1) * 32);
+      rb0 = *(const uint4*)(bs0 + (size_t)(kt + 1) * 512);
+      rb1 = *(const uint4*)(bs1 + (size_t)(kt + 1) * 512);
+      ra0 = KS_MASK4(ra0, am0);
+      ra1 = KS_MASK4(ra1, am1);
+      rb0 = KS_MASK4(rb0, bm0);
+      rb1 = KS_MASK4(rb1, bm1);
+    }
     bf16x8 a[4], b[4];
 #pragma unroll
-    for (int t = 0; t < 4; ++t) b[t] = bok[t] ? ld_frag(wp[t] + (size_t)kt * 512) : zero_frag();
+    for (int i = 0; i < 4; ++i) a[i] = ld_frag(&As[cur][(4 * wm + i) * 512 + lane * 8]);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) a[i] = aok[i] ? ld_frag(ap[i] + kt * 32) : zero_frag();
+    for (int t = 0; t < 4; ++t) b[t] = ld_frag(&Bs[cur][(4 * wn + t) * 512 + lane * 8]);
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int t = 0; t < 4; ++t)
         acc[i][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[t], acc[i][t], 0, 0, 0);
+    if (more) {
+      *(uint4*)&As[cur ^ 1][ad0] = ra0;
+      *(uint4*)&As[cur ^ 1][ad1] = ra1;
+      *(uint4*)&Bs[cur ^ 1][bd0] = rb0;
+      *(uint4*)&Bs[cur ^ 1][bd1] = rb1;
+    }
+    __syncthreads();
   }
 
+#undef KS_MASK4
+  const int mw = m0 + wm * 64;
+  const int nw = nt0 + wn * 4;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
-      const int m = m0 + i * 16 + 4 * (lane >> 4) + v;
+      const int m = mw + i * 16 + 4 * (lane >> 4) + v;
       if (EPI == EPI_SWIGLU) {
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
           const float up = __shfl(acc[i][t][v], (lane & 48) | ((lane + 8) & 15));
-          if (m >= M || !bok[t] || (lane & 15) >= 8) continue;
-          const int c = (nt0 + t) * 8 + (lane & 15);
+          if (m >= M || nw + t >= NT || (lane & 15) >= 8) continue;
+          const int c = (nw + t) * 8 + (lane & 15);
           store_split(ohi, olo, (size_t)m * ldact + c, silu_mul(acc[i][t][v], up));
         }
       } else {
         if (m >= M) continue;
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
-          if (!bok[t]) continue;
-          const int n = (nt0 + t) * 16 + (lane & 15);
-          float s = acc[i][t][v];
-          if (EPI == EPI_RESID) s += res[(size_t)m * ldres + n];
-          out[(size_t)m * ldo + n] = s;
+          if (nw + t >= NT) continue;
+          const int n = (nw + t) * 16 + (lane & 15);
+          float sv = acc[i][t][v];
+          if (EPI == EPI_RESID) sv += res[(size_t)m * ldres + n];
+          out[(size_t)m * ldo + n] = sv;
         }
       }
     }
@@ -235,19 +290,21 @@ __global__ __launch_bounds__(256) void k_gemm_tiled(int M, int N, int K,
 
 void gemm_bf16_tiled(const GemmArgs& g, hipStream_t st) {
   const int NT = g.N / 16;
-  dim3 grid((NT + 7) / 8, (g.M + 127) / 128);
+  const int MB = (g.M + 127) / 128;
+  const int NBk = (NT + 7) / 8;
+  dim3 grid(MB * NBk);
   const bf16_t* A = (const bf16_t*)g.A.hi;
   const bf16_t* W = (const bf16_t*)g.W;
   if (g.epi == EPI_SWIGLU)
     hipLaunchKernelGGL(k_gemm_tiled<EPI_SWIGLU>, grid, dim3(256), 0, st, g.M, g.N, g.K, A,
                        g.A.ld, W, g.out, g.ldo, g.res, g.ldres, (bf16_t*)g.act_out.hi,
-                       (bf16_t*)g.act_out.lo, g.act_out.ld);
+                       (bf16_t*)g.act_out.lo, g.act_out.ld, MB);
   else if (g.epi == EPI_RESID)
     hipLaunchKernelGGL(k_gemm_tiled<EPI_RESID>, grid, dim3(256), 0, st, g.M, g.N, g.K, A,
-                       g.A.ld, W, g.out, g.ldo, g.res, g.ldres, nullptr, nullptr, 0);
+                       g.A.ld, W, g.out, g.ldo, g.res, g.ldres, nullptr, nullptr, 0, MB);
   else
     hipLaunchKernelGGL(k_gemm_tiled<EPI_STORE>, grid, dim3(256), 0, st, g.M, g.N, g.K, A,
-                       g.A.ld, W, g.out, g.ldo, g.res, g.ldres, nullptr, nullptr, 0);
+                       g.A.ld, W, g.out, g.ldo, g.res, g.ldres, nullptr, nullptr, 0, MB);
 }
 
 // --------------------------------------------------------------------- f32
