@@ -77,7 +77,8 @@ typedef struct ks_limits {
  * Matrix layouts.  Every matrix is logically W[N][K] (out x in), y = W x.
  *  - KS_F32: plain row-major float32.
  *  - KS_BF16: the MFMA tile layout written by ks_pack_matrix (see there).
- *  wqkv     [ (hq + 2 hkv) hd ][ d ]  rows: q heads, then k heads, then v heads
+ *  wqkv     [ (hq + 2 hkv) hd ][ d ]  rows: q heads, then k heads, then v heads;
+ *           bf16: written by ks_pack_qkv (rotary pairs share a tile)
  *  wo       [ d ][ hq hd ]
  *  w_gate_up: written by ks_pack_gate_up from separate gate and up [ffn][d]
  *  w_down   [ d ][ ffn ]
@@ -166,6 +167,17 @@ size_t ks_workspace_bytes(const ks_model_desc* desc, const ks_limits* lim);
  * reads one contiguous KiB.  src and dst must not overlap.
  */
 ks_status ks_pack_matrix(const void* src, void* dst, int N, int K, int dtype, void* stream);
+/*
+ * ks_pack_qkv: the fused q/k/v projection, row-major [(hq + 2 hkv) hd][d]
+ * (device): q heads, then k heads, then v heads, hd rows each.  KS_F32: plain
+ * copy.  KS_BF16 (hd % 16 == 0, d % 32 == 0): packed like ks_pack_matrix after
+ * reordering the rows of every head so that its 16-row tile t holds head rows
+ * 8t..8t+7 followed by hd/2 + 8t..hd/2 + 8t + 7, the rotate-half RoPE pairs
+ * (f, f + hd/2) of the Llama/Qwen decoders; the product's epilogue then owns
+ * both members of each pair.  src and dst must not overlap.
+ */
+ks_status ks_pack_qkv(const void* src, void* dst, int hq, int hkv, int hd, int d, int dtype,
+                      void* stream);
 /*
  * ks_pack_gate_up: gate and up projections, each row-major [ffn][d] (device).
  * KS_F32: dst = [gate rows; up rows] row-major [2 ffn][d].  KS_BF16: packed as

@@ -104,6 +104,7 @@ _SIG = {
     "ks_workspace_bytes": (C.c_size_t, [C.POINTER(ModelDesc), C.POINTER(Limits)]),
     "ks_pack_matrix": (_I, [_P, _P, _I, _I, _I, _P]),
     "ks_pack_gate_up": (_I, [_P, _P, _P, _I, _I, _I, _P]),
+    "ks_pack_qkv": (_I, [_P, _P, _I, _I, _I, _I, _I, _P]),
     "ks_create": (_I, [C.POINTER(ModelDesc), C.POINTER(Limits), C.POINTER(Weights), _P,
                        C.c_size_t, _P, C.c_size_t, _P, C.POINTER(_P)]),
     "ks_destroy": (_I, [_P]),
@@ -157,6 +158,7 @@ def _wrap(name):
 # the same names as the C ABI; status-returning calls raise KsError on failure
 ks_pack_matrix = _wrap("ks_pack_matrix")
 ks_pack_gate_up = _wrap("ks_pack_gate_up")
+ks_pack_qkv = _wrap("ks_pack_qkv")
 ks_create = _wrap("ks_create")
 ks_destroy = _wrap("ks_destroy")
 ks_prefill = _wrap("ks_prefill")

@@ -52,7 +52,7 @@ size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct Layout {
   size_t rope, x, a1hi, a1lo, a2hi, a2lo, qkv, q, kvself, part, logits, am, top1;
-  size_t tok, pos, len, stage, hist, xh, g0, g1, ge, dpos, dlen, sig, ptrs, total;
+  size_t tok, pos, len, stage, hist, xh, g0, g1, ge, dpos, dlen, sig, ptrs, ssq, total;
   int FR, RING, cells, DR, XR, LR, nqkv, a2w, part_rows;
   size_t part_elems;
 };
@@ -105,6 +105,7 @@ Layout make_layout(const ks_model_desc& d, const ks_limits& lim) {
   y.dlen = take((size_t)y.DR * 4);
   y.sig = take((size_t)2 * y.DR * 8);
   y.ptrs = take((size_t)4 * (y.cells + 2 * d.L + 2) * 8);
+  y.ssq = take((size_t)16 * (d.d / 16) * 4);
   y.total = o;
   return y;
 }
@@ -177,31 +178,96 @@ void prof_end(ks_ctx* c, int i) {
   } while (0)
 
 // ---------------------------------------------------------- forward pieces
+// bf16 row products of at most 16 rows (decode, draft, verify) run the skinny
+// kernels.  Their normed inputs arrive as planes x * gain in act1 plus per-tile
+// sums of squares in the ssq buffer, written by whichever kernel produced x
+// (the embedding, a residual epilogue, or act_prep for rows handed in).
+bool skinny(const ks_ctx* c, int M, bool batched) { return c->bf() && !batched && M <= 16; }
+
 void gemm(ks_ctx* c, int M, int N, int K, Act A, const void* W, int epi, float* out, int ldo,
           const float* res, int ldres, Act aout, bool batched) {
   GemmArgs g{M, N, K, A, W, epi, out, ldo, res, ldres, aout};
   if (!c->bf()) gemm_f32(g, c->st);
-  else if (!batched && M <= 16) gemm_bf16_skinny(g, c->st);
+  else if (skinny(c, M, batched)) gemm_bf16_skinny(g, c->st);
+  else gemm_bf16_tiled(g, c->st);
+}
+
+// norm gain feeding sublayer i (1..2L); i = 2L + 1 is the final norm
+const float* gain_of(const ks_ctx* c, int i) {
+  if (i > 2 * c->md.L) return c->final_norm;
+  const int l = (i - 1) / 2;
+  return i % 2 == 1 ? c->attn_norm[l] : c->mlp_norm[l];
+}
+
+// planes and tile sums of rmsnorm input x (R rows) for a skinny normed product
+void prep_rows(ks_ctx* c, const float* x, int R, const float* gain) {
+  PROF(c, KS_KC_NORM,
+       act_prep(x, c->md.d, nullptr, c->md.dtype, nullptr, R, c->md.d, nullptr, gain, c->act1(),
+                c->at<float>(c->y.ssq), c->st));
+}
+
+// skinny normed product over the planes in act1
+GemmArgs normed(ks_ctx* c, int M, int N, const void* W, int epi, float* out, int ldo, Act aout) {
+  const ks_model_desc& d = c->md;
+  GemmArgs g{M, N, d.d, c->act1(), W, epi, out, ldo, nullptr, 0, aout};
+  g.ssq_in = c->at<float>(c->y.ssq);
+  g.nssq = d.d / 16;
+  g.eps = d.eps;
+  return g;
+}
+
+// residual product; on the skinny path with next_gain it also writes the
+// planes and tile sums of its output for the next normed product
+void resid_gemm(ks_ctx* c, int R, int K, Act A, const void* W, float* xout, const float* xin,
+                bool batched, const float* next_gain) {
+  const ks_model_desc& d = c->md;
+  GemmArgs g{R, d.d, K, A, W, EPI_RESID, xout, d.d, xin, d.d, Act{}};
+  if (skinny(c, R, batched) && next_gain) {
+    g.next_gain = next_gain;
+    g.next_act = c->act1();
+    g.next_ssq = c->at<float>(c->y.ssq);
+  }
+  if (!c->bf()) gemm_f32(g, c->st);
+  else if (skinny(c, R, batched)) gemm_bf16_skinny(g, c->st);
   else gemm_bf16_tiled(g, c->st);
 }
 
 // Attention sublayer of layer l on R rows: x_out = x_in + Wo attn(...).
 // mode 0: keys/values stored at pos; mode 1: own key/value (selection DP).
 void attn_rows(ks_ctx* c, int l, const float* xin, float* xout, int R, const int32_t* pos,
-               const int32_t* len, int max_len, int mode, bool batched) {
+               const int32_t* len, int max_len, int mode, bool batched, const float* next_gain) {
   const ks_model_desc& d = c->md;
   const Act a1 = c->act1(), a2 = c->act2();
   float* qkv = c->at<float>(c->y.qkv);
   float* q = c->at<float>(c->y.q);
   float* kvs = c->at<float>(c->y.kvself);
-  PROF(c, KS_KC_NORM, norm_act(xin, d.d, c->attn_norm[l], d.eps, R, d.d, d.dtype, a1, c->st));
-  PROF(c, KS_KC_GEMM_QKV,
-       gemm(c, R, c->y.nqkv, d.d, a1, c->wqkv[l], EPI_STORE, qkv, c->y.nqkv, nullptr, 0, Act{},
-            batched));
-  QkvPostArgs qp{R, d.hq, d.hkv, d.hd, d.n_max, d.dtype, d.qk_norm, d.eps, qkv,
-                 c->at<float>(c->y.rope), c->q_norm[l], c->k_norm[l], pos, q,
-                 c->kc(l), c->vc(l), kvs, mode};
-  PROF(c, KS_KC_QKV_POST, qkv_post(qp, c->st));
+  const float* rope = c->at<float>(c->y.rope);
+  if (skinny(c, R, batched)) {
+    // without q/k norms and for cache writes, RoPE and the key/value stores
+    // are the product's epilogue
+    const bool fused = mode == 0 && !d.qk_norm;
+    GemmArgs g = normed(c, R, c->y.nqkv, c->wqkv[l], fused ? EPI_QKV : EPI_STORE, qkv,
+                        c->y.nqkv, Act{});
+    if (fused)
+      g.qe = QkvEpi{d.hq, d.hkv, d.hd, d.n_max, rope, pos, q, (bf16_t*)c->kc(l),
+                    (bf16_t*)c->vc(l)};
+    PROF(c, KS_KC_GEMM_QKV, gemm_bf16_skinny(g, c->st));
+    if (!fused) {
+      QkvPostArgs qp{R, d.hq, d.hkv, d.hd, d.n_max, d.dtype, d.qk_norm, d.eps, qkv, rope,
+                     c->q_norm[l], c->k_norm[l], pos, q, c->kc(l), c->vc(l), kvs, mode, 1};
+      PROF(c, KS_KC_QKV_POST, qkv_post(qp, c->st));
+    }
+  } else {
+    PROF(c, KS_KC_NORM,
+         norm_act(xin, d.d, c->attn_norm[l], d.eps, R, d.d, d.dtype, a1, c->st));
+    PROF(c, KS_KC_GEMM_QKV,
+         gemm(c, R, c->y.nqkv, d.d, a1, c->wqkv[l], EPI_STORE, qkv, c->y.nqkv, nullptr, 0,
+              Act{}, batched));
+    QkvPostArgs qp{R, d.hq, d.hkv, d.hd, d.n_max, d.dtype, d.qk_norm, d.eps, qkv, rope,
+                   c->q_norm[l], c->k_norm[l], pos, q, c->kc(l), c->vc(l), kvs, mode,
+                   c->bf() ? 1 : 0};
+    PROF(c, KS_KC_QKV_POST, qkv_post(qp, c->st));
+  }
   const int tiles = batched ? BAT_TILES : DEC_TILES;
   const int ns = attn_nsplit(d.n_max, tiles);
   const int step = batched ? PB : 16;
@@ -219,43 +285,60 @@ void attn_rows(ks_ctx* c, int l, const float* xin, float* xout, int R, const int
          attn_combine(aa, mode == 1 ? kvs + (size_t)r0 * 2 * d.hkv * d.hd : nullptr, out2,
                       c->st));
   }
-  PROF(c, KS_KC_GEMM_O,
-       gemm(c, R, d.d, d.hq * d.hd, a2, c->wo[l], EPI_RESID, xout, d.d, xin, d.d, Act{},
-            batched));
+  PROF(c, KS_KC_GEMM_O, resid_gemm(c, R, d.hq * d.hd, a2, c->wo[l], xout, xin, batched, next_gain));
 }
 
-void mlp_rows(ks_ctx* c, int l, const float* xin, float* xout, int R, bool batched) {
+void mlp_rows(ks_ctx* c, int l, const float* xin, float* xout, int R, bool batched,
+              const float* next_gain) {
   const ks_model_desc& d = c->md;
   const Act a1 = c->act1(), a2 = c->act2();
-  PROF(c, KS_KC_NORM, norm_act(xin, d.d, c->mlp_norm[l], d.eps, R, d.d, d.dtype, a1, c->st));
-  PROF(c, KS_KC_GEMM_GATE_UP,
-       gemm(c, R, 2 * d.ffn, d.d, a1, c->wgu[l], EPI_SWIGLU, nullptr, 0, nullptr, 0, a2,
-            batched));
-  PROF(c, KS_KC_GEMM_DOWN,
-       gemm(c, R, d.d, d.ffn, a2, c->wdown[l], EPI_RESID, xout, d.d, xin, d.d, Act{}, batched));
+  if (skinny(c, R, batched)) {
+    PROF(c, KS_KC_GEMM_GATE_UP,
+         gemm_bf16_skinny(normed(c, R, 2 * d.ffn, c->wgu[l], EPI_SWIGLU, nullptr, 0, a2),
+                          c->st));
+  } else {
+    PROF(c, KS_KC_NORM,
+         norm_act(xin, d.d, c->mlp_norm[l], d.eps, R, d.d, d.dtype, a1, c->st));
+    PROF(c, KS_KC_GEMM_GATE_UP,
+         gemm(c, R, 2 * d.ffn, d.d, a1, c->wgu[l], EPI_SWIGLU, nullptr, 0, nullptr, 0, a2,
+              batched));
+  }
+  PROF(c, KS_KC_GEMM_DOWN, resid_gemm(c, R, d.ffn, a2, c->wdown[l], xout, xin, batched, next_gain));
 }
 
+// Sublayer i on R rows.  Skinny path: the planes of x_in for sublayer i's norm
+// must be in act1 (next_gain: also produce those of x_out for the next normed
+// product).
 void sublayer_rows(ks_ctx* c, int i, const float* xin, float* xout, int R, const int32_t* pos,
-                   const int32_t* len, int max_len, int mode, bool batched) {
+                   const int32_t* len, int max_len, int mode, bool batched,
+                   const float* next_gain = nullptr) {
   const int l = (i - 1) / 2;
-  if (i % 2 == 1) attn_rows(c, l, xin, xout, R, pos, len, max_len, mode, batched);
-  else mlp_rows(c, l, xin, xout, R, batched);
+  if (i % 2 == 1) attn_rows(c, l, xin, xout, R, pos, len, max_len, mode, batched, next_gain);
+  else mlp_rows(c, l, xin, xout, R, batched, next_gain);
 }
 
-// final norm + LM head + argmax for R rows (chunked by the logits buffer)
+// final norm + LM head + argmax for R rows (chunked by the logits buffer);
+// prepped: on the skinny path the final-norm planes of x are already in act1
 void head_rows(ks_ctx* c, const float* x, int R, float* logits_out, int32_t* am, float* top1,
-               bool batched) {
+               bool batched, bool prepped = false) {
   const ks_model_desc& d = c->md;
   const Act a1 = c->act1();
   const int step = logits_out ? R : c->y.LR;
   for (int r0 = 0; r0 < R; r0 += step) {
     const int rr = std::min(step, R - r0);
     float* lg = logits_out ? logits_out : c->at<float>(c->y.logits);
-    PROF(c, KS_KC_NORM,
-         norm_act(x + (size_t)r0 * d.d, d.d, c->final_norm, d.eps, rr, d.d, d.dtype, a1, c->st));
-    PROF(c, KS_KC_GEMM_HEAD,
-         gemm(c, rr, d.vocab, d.d, a1, c->lm_head, EPI_STORE, lg, d.vocab, nullptr, 0, Act{},
-              batched || rr > 16));
+    const float* xr = x + (size_t)r0 * d.d;
+    if (skinny(c, rr, batched)) {
+      if (!prepped) prep_rows(c, xr, rr, c->final_norm);
+      PROF(c, KS_KC_GEMM_HEAD,
+           gemm_bf16_skinny(normed(c, rr, d.vocab, c->lm_head, EPI_STORE, lg, d.vocab, Act{}),
+                            c->st));
+    } else {
+      PROF(c, KS_KC_NORM, norm_act(xr, d.d, c->final_norm, d.eps, rr, d.d, d.dtype, a1, c->st));
+      PROF(c, KS_KC_GEMM_HEAD,
+           gemm(c, rr, d.vocab, d.d, a1, c->lm_head, EPI_STORE, lg, d.vocab, nullptr, 0, Act{},
+                true));
+    }
     PROF(c, KS_KC_ARGMAX, argmax_rows(lg, rr, d.vocab, am + r0, top1 ? top1 + r0 : nullptr, c->st));
   }
 }
@@ -264,14 +347,27 @@ void head_rows(ks_ctx* c, const float* x, int R, float* logits_out, int32_t* am,
 void decode_row(ks_ctx* c, const int32_t* tok_dev, int p, const uint8_t* exec, int32_t* am_out,
                 float* top1_out) {
   const ks_model_desc& d = c->md;
+  const int L2 = 2 * d.L;
   float* x = c->at<float>(c->y.x);
   int32_t* pos = c->at<int32_t>(c->y.pos);
   int32_t* len = c->at<int32_t>(c->y.len);
+  auto next_exec = [&](int i) {  // first executed sublayer after i (L2 + 1: the head)
+    int j = i + 1;
+    while (j <= L2 && exec && !exec[j - 1]) ++j;
+    return j;
+  };
   PROF(c, KS_KC_OTHER, fill_pos(pos, len, p, 1, 1, 1, c->st));
-  PROF(c, KS_KC_EMBED, embed_rows(c->embed, d.dtype, tok_dev, 1, d.d, x, d.d, c->st));
-  for (int i = 1; i <= 2 * d.L; ++i)
-    if (!exec || exec[i - 1]) sublayer_rows(c, i, x, x, 1, pos, len, p + 1, 0, false);
-  head_rows(c, x, 1, nullptr, am_out, top1_out, false);
+  if (c->bf()) {
+    PROF(c, KS_KC_EMBED,
+         act_prep(nullptr, d.d, c->embed, d.dtype, tok_dev, 1, d.d, x,
+                  gain_of(c, next_exec(0)), c->act1(), c->at<float>(c->y.ssq), c->st));
+  } else {
+    PROF(c, KS_KC_EMBED, embed_rows(c->embed, d.dtype, tok_dev, 1, d.d, x, d.d, c->st));
+  }
+  for (int i = 1; i <= L2; ++i)
+    if (!exec || exec[i - 1])
+      sublayer_rows(c, i, x, x, 1, pos, len, p + 1, 0, false, gain_of(c, next_exec(i)));
+  head_rows(c, x, 1, nullptr, am_out, top1_out, false, true);
 }
 
 // verify rows of tokens tok_dev[0..R) at positions P..P+R-1, snapshots into stage
@@ -280,31 +376,25 @@ void verify_rows(ks_ctx* c, const int32_t* tok_dev, int R, int32_t* am_out) {
   int32_t* pos = c->at<int32_t>(c->y.pos);
   int32_t* len = c->at<int32_t>(c->y.len);
   fill_pos(pos, len, c->P, R, R, 1, c->st);
-  embed_rows(c->embed, d.dtype, tok_dev, R, d.d, c->stage_row(0, 0), d.d, c->st);
+  if (skinny(c, R, false)) {
+    act_prep(nullptr, d.d, c->embed, d.dtype, tok_dev, R, d.d, c->stage_row(0, 0), gain_of(c, 1),
+             c->act1(), c->at<float>(c->y.ssq), c->st);
+  } else {
+    embed_rows(c->embed, d.dtype, tok_dev, R, d.d, c->stage_row(0, 0), d.d, c->st);
+  }
   for (int i = 1; i <= 2 * d.L; ++i)
     sublayer_rows(c, i, c->stage_row(i - 1, 0), c->stage_row(i, 0), R, pos, len, c->P + R, 0,
-                  false);
-  head_rows(c, c->stage_row(2 * d.L, 0), R, nullptr, am_out, nullptr, false);
+                  false, gain_of(c, i + 1));
+  head_rows(c, c->stage_row(2 * d.L, 0), R, nullptr, am_out, nullptr, false, true);
 }
 
-// copy rows [0, n) of plane set src (row stride ld_src rows per plane) into the
-// history ring at positions p0..p0+n-1 for every sublayer output
+// copy rows [0, n) of plane set src (plane stride plane_stride_rows rows) into
+// the history ring at positions p0..p0+n-1 for every sublayer output
 hipError_t stash_history(ks_ctx* c, const float* src0, size_t plane_stride_rows, int n, int p0) {
   const ks_model_desc& d = c->md;
-  const size_t row_bytes = (size_t)d.d * 4;
-  int done = 0;
-  while (done < n) {
-    const int slot = (p0 + done) % c->y.RING;
-    const int run = std::min(n - done, c->y.RING - slot);
-    for (int i = 0; i <= 2 * d.L; ++i) {
-      hipError_t e = hipMemcpyAsync(c->hist_row(i, slot),
-                                    src0 + ((size_t)i * plane_stride_rows + done) * d.d,
-                                    run * row_bytes, hipMemcpyDeviceToDevice, c->st);
-      if (e != hipSuccess) return e;
-    }
-    done += run;
-  }
-  return hipSuccess;
+  ring_copy(src0, c->at<float>(c->y.hist), plane_stride_rows, 2 * d.L + 1, n, c->y.RING, p0, d.d,
+            true, c->st);
+  return hipGetLastError();
 }
 
 int hist_rows(const ks_ctx* c) {
@@ -369,6 +459,23 @@ ks_status ks_pack_matrix(const void* src, void* dst, int N, int K, int dtype, vo
   }
   REQ(N % 16 == 0 && K % 32 == 0, "bf16 packing needs N % 16 == 0 and K % 32 == 0");
   pack_matrix_bf16((const bf16_t*)src, (bf16_t*)dst, N, K, st);
+  HIPCHK(hipGetLastError());
+  return KS_OK;
+}
+
+ks_status ks_pack_qkv(const void* src, void* dst, int hq, int hkv, int hd, int d, int dtype,
+                      void* stream) {
+  REQ(src && dst, "null pointer");
+  REQ(hq > 0 && hkv > 0 && hd > 0 && d > 0, "sizes must be positive");
+  REQ(dtype == KS_F32 || dtype == KS_BF16, "bad dtype");
+  hipStream_t st = (hipStream_t)stream;
+  const int N = (hq + 2 * hkv) * hd;
+  if (dtype == KS_F32) {
+    HIPCHK(hipMemcpyAsync(dst, src, (size_t)N * d * 4, hipMemcpyDeviceToDevice, st));
+    return KS_OK;
+  }
+  REQ(hd % 16 == 0 && d % 32 == 0, "bf16 packing needs hd % 16 == 0 and d % 32 == 0");
+  pack_qkv_bf16((const bf16_t*)src, (bf16_t*)dst, hq + 2 * hkv, hd, d, st);
   HIPCHK(hipGetLastError());
   return KS_OK;
 }
@@ -639,16 +746,8 @@ static ks_status select_internal(ks_ctx* c, const ks_select_params* p, ks_select
   const int base = n - r;
   float* Xh = c->at<float>(c->y.xh);  // [2L+1][r][d]
   // gather history rows into contiguous planes
-  for (int i = 0; i <= L2; ++i) {
-    int done = 0;
-    while (done < r) {
-      const int slot = (base + done) % c->y.RING;
-      const int run = std::min(r - done, c->y.RING - slot);
-      HIPCHK(hipMemcpyAsync(Xh + ((size_t)i * r + done) * d.d, c->hist_row(i, slot),
-                            (size_t)run * d.d * 4, hipMemcpyDeviceToDevice, c->st));
-      done += run;
-    }
-  }
+  ring_copy(c->at<float>(c->y.hist), Xh, r, L2 + 1, r, c->y.RING, base, d.d, false, c->st);
+  HIPCHK(hipGetLastError());
   auto X = [&](int i) { return Xh + (size_t)i * r * d.d; };
   int32_t* dpos = c->at<int32_t>(c->y.dpos);
   int32_t* dlen = c->at<int32_t>(c->y.dlen);
@@ -838,6 +937,7 @@ ks_status ks_sublayer_apply(ks_ctx* c, int i, const float* x_in, float* x_out, c
   HIPCHK(hipMemcpyAsync(dp, pos, R * 4, hipMemcpyHostToDevice, c->st));
   HIPCHK(hipMemcpyAsync(dl, hl.data(), R * 4, hipMemcpyHostToDevice, c->st));
   // x_in may alias x_out: every kernel reads a residual element before writing it
+  if (skinny(c, R, R > 16)) prep_rows(c, x_in, R, gain_of(c, i));
   sublayer_rows(c, i, x_in, x_out, R, dp, dl, mx, mode, R > 16);
   HIPCHK(hipGetLastError());
   HIPCHK(hipStreamSynchronize(c->st));

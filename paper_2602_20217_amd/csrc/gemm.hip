@@ -38,11 +38,19 @@ __device__ inline void store_split(bf16_t* hi, bf16_t* lo, size_t off, float a) 
 }
 
 // ------------------------------------------------------------------ skinny
-template <int NB, int NW, int CH, int EPI>
+// RMSNorm rides on the producers of the residual stream: the residual
+// epilogue (and the embedding) writes x * gain of the next normed product as
+// hi + lo bf16 planes together with sums of x^2 per 16-column tile.  AN = 1
+// products read those planes like any activation and scale row m by
+// 1/sqrt(sum/K + eps) at the end; the 256 tile sums of a row are added by one
+// wave in a fixed order, whatever the row count.
+template <int NB, int NW, int CH, int EPI, int AN>
 __global__ __launch_bounds__(NW * 64) void k_gemm_skinny(
     int M, int N, int K, const bf16_t* __restrict__ Ahi, const bf16_t* __restrict__ Alo,
     int lda, const bf16_t* __restrict__ Wp, float* out, int ldo, const float* res, int ldres,
-    bf16_t* ohi, bf16_t* olo, int ldact) {
+    bf16_t* ohi, bf16_t* olo, int ldact, const float* __restrict__ ssq_in, int nssq, float eps,
+    const float* __restrict__ next_gain, bf16_t* nhi, bf16_t* nlo, int ldn, float* next_ssq,
+    QkvEpi qe) {
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int KT = K >> 5;
@@ -93,12 +101,22 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_skinny(
   }
 
   __shared__ f32x4 red[NW][NB][64];
+  __shared__ float s_rs[AN ? 16 : 1];
 #pragma unroll
   for (int t = 0; t < NB; ++t) red[wave][t][lane] = acc[t];
+  if (AN) {
+    for (int m = wave; m < M; m += NW) {
+      float t = 0.f;
+      for (int j = lane; j < nssq; j += 64) t += ssq_in[(size_t)m * nssq + j];
+#pragma unroll
+      for (int o = 32; o >= 1; o >>= 1) t += __shfl_xor(t, o);
+      if (lane == 0) s_rs[m] = 1.0f / sqrtf(t / (float)K + eps);
+    }
+  }
   __syncthreads();
 
-  if (EPI == EPI_SWIGLU) {
-    // tile rows 0..7 are gate rows, 8..15 the matching up rows
+  if (EPI == EPI_SWIGLU || EPI == EPI_QKV) {
+    // tile rows 0..7 pair with rows 8..15 (gate/up, or rotary pairs)
     for (int idx = threadIdx.x; idx < NB * 256; idx += NW * 64) {
       const int t = idx >> 8, l = (idx >> 2) & 63, v = idx & 3;
       const int m = 4 * (l >> 4) + v;
@@ -108,40 +126,96 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_skinny(
         g += red[w][t][l][v];
         u += red[w][t][l + 8][v];
       }
-      const int c = (nt0 + t) * 8 + (l & 15);
-      store_split(ohi, olo, (size_t)m * ldact + c, silu_mul(g, u));
+      if (AN) {
+        g *= s_rs[m];
+        u *= s_rs[m];
+      }
+      if (EPI == EPI_SWIGLU) {
+        const int c = (nt0 + t) * 8 + (l & 15);
+        store_split(ohi, olo, (size_t)m * ldact + c, silu_mul(g, u));
+      } else {
+        const int tph = qe.hd >> 4, half = qe.hd >> 1;
+        const int hh = (nt0 + t) / tph;
+        const int f = 8 * ((nt0 + t) % tph) + (l & 15);
+        const int p = qe.pos[m];
+        if (hh < qe.hq + qe.hkv) {
+          const float2 cs = *(const float2*)&qe.rope_cs[((size_t)p * half + f) * 2];
+          const float y0 = g * cs.x - u * cs.y;
+          const float y1 = u * cs.x + g * cs.y;
+          if (hh < qe.hq) {
+            float* q = qe.q_out + ((size_t)m * qe.hq + hh) * qe.hd;
+            q[f] = y0;
+            q[f + half] = y1;
+          } else {
+            bf16_t* k = qe.kc + ((size_t)(hh - qe.hq) * qe.n_max + p) * qe.hd;
+            k[f] = f2bf(y0);
+            k[f + half] = f2bf(y1);
+          }
+        } else {
+          bf16_t* vv = qe.vc + ((size_t)(hh - qe.hq - qe.hkv) * qe.n_max + p) * qe.hd;
+          vv[f] = f2bf(g);
+          vv[f + half] = f2bf(u);
+        }
+      }
     }
   } else {
+    // thread idx < 256 owns (row 4 (l / 16) + v, column l % 16): in a wave the
+    // 16 columns of a row sit on lane bits 2..5, so the tile's sum of squares
+    // for the next norm is a 4-step butterfly
+    static_assert(EPI != EPI_RESID || NB == 1, "next-norm sums assume one tile per block");
+    const bool nn = EPI == EPI_RESID && next_gain != nullptr;
     for (int idx = threadIdx.x; idx < NB * 256; idx += NW * 64) {
       const int t = idx >> 8, l = (idx >> 2) & 63, v = idx & 3;
       const int m = 4 * (l >> 4) + v;
-      if (m >= M || nt0 + t >= NT) continue;
-      float s = 0.f;
-      for (int w = 0; w < NW; ++w) s += red[w][t][l][v];
+      const bool ok = m < M && nt0 + t < NT;
       const int n = (nt0 + t) * 16 + (l & 15);
-      if (EPI == EPI_RESID) s += res[(size_t)m * ldres + n];
-      out[(size_t)m * ldo + n] = s;
+      float s = 0.f;
+      if (ok) {
+        for (int w = 0; w < NW; ++w) s += red[w][t][l][v];
+        if (AN) s *= s_rs[m];
+        if (EPI == EPI_RESID) s += res[(size_t)m * ldres + n];
+        out[(size_t)m * ldo + n] = s;
+      }
+      if (nn) {
+        float sq = s * s;
+        if (ok) store_split(nhi, nlo, (size_t)m * ldn + n, s * next_gain[n]);
+        sq += __shfl_xor(sq, 4);
+        sq += __shfl_xor(sq, 8);
+        sq += __shfl_xor(sq, 16);
+        sq += __shfl_xor(sq, 32);
+        if (ok && (l & 15) == 0) next_ssq[(size_t)m * NT + nt0 + t] = sq;
+      }
     }
   }
 }
 
-template <int NB, int NW, int CH>
-static void launch_skinny(const GemmArgs& g, hipStream_t st) {
+template <int NB, int NW, int CH, int AN>
+static void launch_skinny_an(const GemmArgs& g, hipStream_t st) {
   const int NT = g.N / 16;
   const bf16_t* Ahi = (const bf16_t*)g.A.hi;
   const bf16_t* Alo = (const bf16_t*)g.A.lo;
   const bf16_t* W = (const bf16_t*)g.W;
   dim3 grid((NT + NB - 1) / NB), block(NW * 64);
+#define KS_SKINNY(E, OH, OL, OLD)                                                            \
+  hipLaunchKernelGGL((k_gemm_skinny<NB, NW, CH, E, AN>), grid, block, 0, st, g.M, g.N, g.K,  \
+                     Ahi, Alo, g.A.ld, W, g.out, g.ldo, g.res, g.ldres, OH, OL, OLD,         \
+                     g.ssq_in, g.nssq, g.eps, g.next_gain, (bf16_t*)g.next_act.hi,           \
+                     (bf16_t*)g.next_act.lo, g.next_act.ld, g.next_ssq, g.qe)
   if (g.epi == EPI_SWIGLU)
-    hipLaunchKernelGGL((k_gemm_skinny<NB, NW, CH, EPI_SWIGLU>), grid, block, 0, st, g.M, g.N, g.K,
-                       Ahi, Alo, g.A.ld, W, g.out, g.ldo, g.res, g.ldres, (bf16_t*)g.act_out.hi,
-                       (bf16_t*)g.act_out.lo, g.act_out.ld);
+    KS_SKINNY(EPI_SWIGLU, (bf16_t*)g.act_out.hi, (bf16_t*)g.act_out.lo, g.act_out.ld);
+  else if (g.epi == EPI_QKV)
+    KS_SKINNY(EPI_QKV, nullptr, nullptr, 0);
   else if (g.epi == EPI_RESID)
-    hipLaunchKernelGGL((k_gemm_skinny<NB, NW, CH, EPI_RESID>), grid, block, 0, st, g.M, g.N, g.K,
-                       Ahi, Alo, g.A.ld, W, g.out, g.ldo, g.res, g.ldres, nullptr, nullptr, 0);
+    KS_SKINNY(EPI_RESID, nullptr, nullptr, 0);
   else
-    hipLaunchKernelGGL((k_gemm_skinny<NB, NW, CH, EPI_STORE>), grid, block, 0, st, g.M, g.N, g.K,
-                       Ahi, Alo, g.A.ld, W, g.out, g.ldo, g.res, g.ldres, nullptr, nullptr, 0);
+    KS_SKINNY(EPI_STORE, nullptr, nullptr, 0);
+#undef KS_SKINNY
+}
+
+template <int NB, int NW, int CH>
+static void launch_skinny(const GemmArgs& g, hipStream_t st) {
+  if (g.ssq_in) launch_skinny_an<NB, NW, CH, 1>(g, st);
+  else launch_skinny_an<NB, NW, CH, 0>(g, st);
 }
 
 // Launch shape by matrix shape only (never by row count), measured on MI355X
@@ -362,8 +436,10 @@ void gemm_f32(const GemmArgs& g, hipStream_t st) {
 
 // ----------------------------------------------------------------- packing
 // One thread per 8-element (16-byte) fragment of the destination.
+// mode 0: plain; 1: gate/up 8 + 8 interleave; 2: q/k/v heads of hd rows with
+// tile t of a head holding rows 8t..8t+7 and hd/2 + 8t..hd/2 + 8t + 7
 __global__ void k_pack(const bf16_t* __restrict__ src0, const bf16_t* __restrict__ src1,
-                       bf16_t* __restrict__ dst, int N, int K, int interleave) {
+                       bf16_t* __restrict__ dst, int N, int K, int mode, int hd) {
   const size_t f = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int KT = K >> 5;
   const size_t nfrag = (size_t)N * K / 8;
@@ -374,9 +450,12 @@ __global__ void k_pack(const bf16_t* __restrict__ src0, const bf16_t* __restrict
   const int nt = (int)(tile / KT);
   const bf16_t* src = src0;
   int row = nt * 16 + (l & 15);
-  if (interleave) {  // tile t: gate rows 8t..8t+7, then up rows 8t..8t+7
+  if (mode == 1) {  // tile t: gate rows 8t..8t+7, then up rows 8t..8t+7
     src = (l & 8) ? src1 : src0;
     row = nt * 8 + (l & 7);
+  } else if (mode == 2) {
+    const int tph = hd / 16, h = nt / tph, t = nt % tph;
+    row = h * hd + 8 * t + (l & 7) + (hd / 2) * ((l >> 3) & 1);
   }
   const u32x4 v = *(const u32x4*)(src + (size_t)row * K + kt * 32 + (l >> 4) * 8);
   *(u32x4*)(dst + f * 8) = v;
@@ -385,14 +464,20 @@ __global__ void k_pack(const bf16_t* __restrict__ src0, const bf16_t* __restrict
 void pack_matrix_bf16(const bf16_t* src, bf16_t* dst, int N, int K, hipStream_t st) {
   const size_t nfrag = (size_t)N * K / 8;
   hipLaunchKernelGGL(k_pack, dim3((unsigned)((nfrag + 255) / 256)), dim3(256), 0, st, src,
-                     nullptr, dst, N, K, 0);
+                     nullptr, dst, N, K, 0, 0);
+}
+
+void pack_qkv_bf16(const bf16_t* src, bf16_t* dst, int heads, int hd, int d, hipStream_t st) {
+  const size_t nfrag = (size_t)heads * hd * d / 8;
+  hipLaunchKernelGGL(k_pack, dim3((unsigned)((nfrag + 255) / 256)), dim3(256), 0, st, src,
+                     nullptr, dst, heads * hd, d, 2, hd);
 }
 
 void pack_gate_up_bf16(const bf16_t* gate, const bf16_t* up, bf16_t* dst, int ffn, int d,
                        hipStream_t st) {
   const size_t nfrag = (size_t)2 * ffn * d / 8;
   hipLaunchKernelGGL(k_pack, dim3((unsigned)((nfrag + 255) / 256)), dim3(256), 0, st, gate, up,
-                     dst, 2 * ffn, d, 1);
+                     dst, 2 * ffn, d, 1, 0);
 }
 
 }  // namespace ks

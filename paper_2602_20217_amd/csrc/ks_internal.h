@@ -35,7 +35,7 @@ __host__ __device__ inline bf16_t f2bf(float f) {
 }
 
 // ------------------------------------------------------------------ epilogues
-enum Epi { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2 };
+enum Epi { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_QKV = 3 };
 
 // Activations feeding a matrix product.  bf16 models: two bf16 planes with
 // a = hi + lo (lo = bf16(a - hi)); float32 models: one float plane in hi.
@@ -52,6 +52,18 @@ struct Act {
 //  EPI_SWIGLU: W holds gate/up rows interleaved by 8 inside each 16-row tile
 //              (see ks_pack_gate_up); writes act_out[m][u] = silu(gate_u) * up_u
 //              for u < N/2.
+//  EPI_QKV   : W is the fused q/k/v projection packed by ks_pack_qkv (rotary
+//              pairs f, f + hd/2 of a head in rows 8 apart of one tile); applies
+//              rotate-half RoPE at pos[m] to q and k, writes q (float32) to
+//              q_out[m][hq][hd] and k, v (bf16) to the cache at position pos[m].
+struct QkvEpi {
+  int hq, hkv, hd, n_max;
+  const float* rope_cs;  // [n_max][hd/2][2]
+  const int32_t* pos;    // device [M]
+  float* q_out;
+  bf16_t* kc;            // layer K cache [hkv][n_max][hd]
+  bf16_t* vc;
+};
 struct GemmArgs {
   int M, N, K;
   Act A;
@@ -62,6 +74,20 @@ struct GemmArgs {
   const float* res;
   int ldres;
   Act act_out;
+  // Skinny bf16 path, RMSNorm carried by the producers (see act_prep):
+  //  ssq_in != nullptr: A holds x * gain (not yet divided by rms(x)) and
+  //    ssq_in[m][0..nssq) the partial sums of x^2 of row m; the product scales
+  //    row m by 1/sqrt(sum/K + eps).
+  //  next_gain != nullptr (EPI_RESID): besides out, writes next_act = bf16
+  //    split of out * next_gain and next_ssq[m][n/16] = sum of out^2 over the
+  //    16 columns of each tile (ld d/16), the input of the next normed product.
+  const float* ssq_in = nullptr;
+  int nssq = 0;
+  float eps = 0.f;
+  const float* next_gain = nullptr;
+  Act next_act{};
+  float* next_ssq = nullptr;
+  QkvEpi qe{};
 };
 void gemm_bf16_skinny(const GemmArgs& g, hipStream_t st);  // M <= 16
 void gemm_bf16_tiled(const GemmArgs& g, hipStream_t st);   // any M, A.hi only
@@ -70,10 +96,22 @@ void gemm_f32(const GemmArgs& g, hipStream_t st);          // any M
 void pack_matrix_bf16(const bf16_t* src, bf16_t* dst, int N, int K, hipStream_t st);
 void pack_gate_up_bf16(const bf16_t* gate, const bf16_t* up, bf16_t* dst, int ffn, int d,
                        hipStream_t st);
+// rows of a head reordered so each 16-row tile holds the rotary pairs
+void pack_qkv_bf16(const bf16_t* src, bf16_t* dst, int heads, int hd, int d, hipStream_t st);
+// packed column of head dimension i (rotate-half pairs 8 apart in a 16-row tile)
+__host__ __device__ inline int qkv_perm(int i, int hd) {
+  const int half = hd / 2, f = i % half;
+  return 16 * (f / 8) + (f % 8) + 8 * (i / half);
+}
 
 // x[m][:] = embed[tok[m]][:]
 void embed_rows(const void* E, int dtype, const int32_t* tok, int M, int d, float* x,
                 int ldx, hipStream_t st);
+// RMSNorm input of a skinny product: for row m, x = (E ? embedding row tok[m] :
+// xin row m) is written to xout (when not null and not xin), act = bf16 split of
+// x * gain and ssq[m][j] = sum of x^2 over columns 16 j..16 j + 15 (ld d/16).
+void act_prep(const float* xin, int ldx, const void* E, int dtype, const int32_t* tok, int M,
+              int d, float* xout, const float* gain, Act act, float* ssq, hipStream_t st);
 // act = bf16 split (or f32 copy) of rmsnorm(x) * g ; g == nullptr means no norm (plain
 // conversion).
 void norm_act(const float* x, int ldx, const float* g, float eps, int M, int d, int dtype,
@@ -93,6 +131,7 @@ struct QkvPostArgs {
   void* vc;
   float* kvself;         // [M][2][hkv][hd] (mode 1)
   int mode;
+  int perm;              // qkv columns in the ks_pack_qkv order (bf16 models)
 };
 void qkv_post(const QkvPostArgs& a, hipStream_t st);
 
@@ -128,6 +167,11 @@ void cos_rows(const float* X, const float* Y, int rows, int ry, int d, double* o
               hipStream_t st);
 void cos_groups_f64(const float* X, const float* Y, int groups, int r, int d, double* out,
                     hipStream_t st);
+// history ring <-> contiguous planes for `planes` planes of n rows of d floats
+// (d % 4 == 0): flat row (i, t) at (i * plane_stride + t) * d, ring row (i, t) at
+// (i * RING + (p0 + t) % RING) * d; to_ring copies flat -> ring, else ring -> flat
+void ring_copy(const float* src, float* dst, size_t plane_stride, int planes, int n, int RING,
+               int p0, int d, bool to_ring, hipStream_t st);
 // block copies: dst[i][0..n) = src[i][0..n) via device pointer tables of length cnt
 void copy_rows(const float* const* src, float* const* dst, int cnt, int n, hipStream_t st);
 // pos[c*r + t] = base + t and len[] = pos[] + len_add for c*r + t < total

@@ -48,6 +48,60 @@ void embed_rows(const void* E, int dtype, const int32_t* tok, int M, int d, floa
                      ldx);
 }
 
+// Normed-product input (bf16 models): one block per row; thread c4 owns
+// columns 4 c4..4 c4 + 3, four consecutive threads one 16-column tile whose
+// sum of squares is a 2-step butterfly.  d % 16 == 0.
+__global__ __launch_bounds__(256) void k_act_prep(const float* __restrict__ xin, int ldx,
+                                                  const void* __restrict__ E, int bf,
+                                                  const int32_t* __restrict__ tok, int d,
+                                                  float* xout, const float* __restrict__ gain,
+                                                  bf16_t* hi, bf16_t* lo, int lda, float* ssq) {
+  const int m = blockIdx.x;
+  const size_t eb = E ? (size_t)tok[m] * d : 0;
+  for (int c4 = threadIdx.x; c4 < (d >> 2); c4 += 256) {
+    const int c = 4 * c4;
+    float4 v;
+    if (E) {
+      if (bf) {
+        const uint2 u = *(const uint2*)((const bf16_t*)E + eb + c);
+        v = make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xFFFF0000u),
+                        __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xFFFF0000u));
+      } else {
+        v = *(const float4*)((const float*)E + eb + c);
+      }
+      if (xout) *(float4*)(xout + (size_t)m * ldx + c) = v;
+    } else {
+      v = *(const float4*)(xin + (size_t)m * ldx + c);
+    }
+    const float4 g = *(const float4*)(gain + c);
+    const float a[4] = {v.x * g.x, v.y * g.y, v.z * g.z, v.w * g.w};
+    uint32_t h[2], l[2];
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+      const bf16_t h0 = f2bf(a[2 * k]), h1 = f2bf(a[2 * k + 1]);
+      h[k] = (uint32_t)h0 | ((uint32_t)h1 << 16);
+      l[k] = (uint32_t)f2bf(a[2 * k] - bf2f(h0)) | ((uint32_t)f2bf(a[2 * k + 1] - bf2f(h1)) << 16);
+    }
+    *(uint2*)(hi + (size_t)m * lda + c) = make_uint2(h[0], h[1]);
+    *(uint2*)(lo + (size_t)m * lda + c) = make_uint2(l[0], l[1]);
+    float sq = v.x * v.x;
+    sq = fmaf(v.y, v.y, sq);
+    sq = fmaf(v.z, v.z, sq);
+    sq = fmaf(v.w, v.w, sq);
+    sq += __shfl_xor(sq, 1);
+    sq += __shfl_xor(sq, 2);
+    if ((threadIdx.x & 3) == 0) ssq[(size_t)m * (d >> 4) + (c >> 4)] = sq;
+  }
+}
+
+void act_prep(const float* xin, int ldx, const void* E, int dtype, const int32_t* tok, int M,
+              int d, float* xout, const float* gain, Act act, float* ssq, hipStream_t st) {
+  if (M <= 0) return;
+  hipLaunchKernelGGL(k_act_prep, dim3(M), dim3(256), 0, st, xin, ldx, E,
+                     dtype == KS_BF16 ? 1 : 0, tok, d, xout, gain, (bf16_t*)act.hi,
+                     (bf16_t*)act.lo, act.ld, ssq);
+}
+
 // ---------------------------------------------------------------- RMSNorm
 // One 256-thread block per row; a thread holds up to 4 float4 of the row
 // (d <= 4096; wider rows take a strided loop).  Sum of squares: per-thread
@@ -139,8 +193,10 @@ __global__ __launch_bounds__(256) void k_qkv_post(QkvPostArgs a) {
   }
   {
     const float* src = src_row + (size_t)hh * hd;
-    float x0 = act ? src[lane] : 0.f;
-    float x1 = act ? src[lane + half] : 0.f;
+    const int c0 = a.perm ? qkv_perm(lane, hd) : lane;
+    const int c1 = a.perm ? qkv_perm(lane + half, hd) : lane + half;
+    float x0 = act ? src[c0] : 0.f;
+    float x1 = act ? src[c1] : 0.f;
     float y0 = x0, y1 = x1;
     if (hh < a.hq + a.hkv) {
       if (a.qk_norm) {
@@ -369,6 +425,27 @@ void copy_rows(const float* const* src, float* const* dst, int cnt, int n, hipSt
   if (cnt <= 0 || n <= 0) return;
   const int bx = (n + 255) / 256 < 64 ? (n + 255) / 256 : 64;
   hipLaunchKernelGGL(k_copy_blocks, dim3(bx, cnt), dim3(256), 0, st, src, dst, (size_t)n);
+}
+
+// History ring copies, one launch for every plane: row t < n of plane i,
+// plane[i][t] at flat + (i * plane_stride + t) * d, pairs with ring row
+// ring + (i * RING + (p0 + t) % RING) * d.
+__global__ __launch_bounds__(256) void k_ring_copy(const float* __restrict__ src,
+                                                   float* __restrict__ dst, size_t plane_stride,
+                                                   int RING, int p0, int d, int to_ring) {
+  const int t = blockIdx.x, i = blockIdx.y;
+  const size_t flat = ((size_t)i * plane_stride + t) * d;
+  const size_t ring = ((size_t)i * RING + (p0 + t) % RING) * d;
+  const float4* s4 = (const float4*)(src + (to_ring ? flat : ring));
+  float4* d4 = (float4*)(dst + (to_ring ? ring : flat));
+  for (int c = threadIdx.x; c < d / 4; c += 256) d4[c] = s4[c];
+}
+
+void ring_copy(const float* src, float* dst, size_t plane_stride, int planes, int n, int RING,
+               int p0, int d, bool to_ring, hipStream_t st) {
+  if (n <= 0 || planes <= 0) return;
+  hipLaunchKernelGGL(k_ring_copy, dim3(n, planes), dim3(256), 0, st, src, dst, plane_stride,
+                     RING, p0, d, to_ring ? 1 : 0);
 }
 
 // ------------------------------------------------------------ rotary table

@@ -102,8 +102,11 @@ class DeviceModel:
             p = self._pending.setdefault(("qkv", layer), {})
             p[kind] = a
             if len(p) == 3:
-                cat = np.concatenate([p["wq"], p["wk"], p["wv"]], axis=0)
-                self._pack(self._to_dev(cat), self.w["wqkv"][layer])
+                cat = self._to_dev(np.concatenate([p["wq"], p["wk"], p["wv"]], axis=0))
+                c = self.cfg
+                K.ks_pack_qkv(_ptr(cat), _ptr(self.w["wqkv"][layer]), c.hq, c.hkv, c.hd, c.d,
+                              self.desc.dtype, _stream())
+                torch.cuda.current_stream().synchronize()
                 del self._pending[("qkv", layer)]
         elif kind == "wo":
             self._pack(self._to_dev(a), self.w["wo"][layer])
