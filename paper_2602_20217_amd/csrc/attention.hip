@@ -42,6 +42,16 @@ int attn_nsplit(int n_positions, int tiles) {
 
 // HD: head dim (128 for bf16 caches, 64 for float32 caches).  QMAX: query
 // vectors per wave (rows_per_block * G <= 4 QMAX).
+//
+// The first tile's keys/values, the queries and the row lengths are requested
+// together at the start, so a workgroup waits for one memory round trip before
+// its arithmetic.  The workgroup's query vectors are staged in LDS once (read
+// back as broadcasts).  Tiles are double-buffered through registers: the loads
+// of tile k + 1 are issued before the arithmetic of tile k.  A lane loads its
+// key row from LDS once per tile and scores it against each of its wave's
+// queries; the value pass always runs over the 64 rows of a tile (rows past the
+// end are zero and carry probability 0), so its loop is unrolled and its LDS
+// reads are in flight together.
 template <int HD, bool BF, int QMAX>
 __global__ __launch_bounds__(256) void k_attn_split(int M, int hq, int hkv, int n_max,
                                                     const float* __restrict__ q,
@@ -58,6 +68,7 @@ __global__ __launch_bounds__(256) void k_attn_split(int M, int hq, int hkv, int 
   static_assert((TILE * CPR) % 256 == 0, "tile chunking");
   __shared__ __align__(16) uint32_t Ks[TILE * KS];
   __shared__ __align__(16) uint32_t Vs[TILE * KW];
+  __shared__ __align__(16) float Qs[4 * QMAX * HD];
 
   const int split = blockIdx.x, kvh = blockIdx.y;
   const int r0 = blockIdx.z * rows_per_block;
@@ -68,6 +79,42 @@ __global__ __launch_bounds__(256) void k_attn_split(int M, int hq, int hkv, int 
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int start = split * tiles * TILE;
   const float scale = 1.0f / sqrtf((float)HD);
+
+  const size_t es = BF ? 2 : 4;
+  const char* kbase = (const char*)kc + (size_t)kvh * n_max * HD * es;
+  const char* vbase = (const char*)vc + (size_t)kvh * n_max * HD * es;
+  static_assert(NCH == 4, "four 16-byte chunks per thread per matrix");
+  // named registers (an array carried around the tile loop lands in scratch)
+  uint4 k0, k1, k2, k3, v0, v1, v2, v3;
+  // Tile loads clamp rows to the cache only, so the first tile is requested
+  // before the row lengths arrive; rows at or past the end are zeroed when the
+  // tile is stored to LDS (their scores are masked, their values weigh 0).
+#define KS_LD(U, KD, VD, T0)                                               \
+  {                                                                        \
+    const int c_ = threadIdx.x + 256 * (U);                                \
+    const int row_ = min((T0) + c_ / CPR, n_max - 1), ch_ = c_ % CPR;      \
+    const size_t off_ = (size_t)row_ * HD * es + ch_ * 16;                 \
+    KD = *(const uint4*)(kbase + off_);                                    \
+    VD = *(const uint4*)(vbase + off_);                                    \
+  }
+#define KS_FETCH(T0)                                                       \
+  KS_LD(0, k0, v0, T0) KS_LD(1, k1, v1, T0) KS_LD(2, k2, v2, T0) KS_LD(3, k3, v3, T0)
+#define KS_ST(U, KD, VD, CNT)                                              \
+  {                                                                        \
+    const int c_ = threadIdx.x + 256 * (U);                                \
+    const int row_ = c_ / CPR, ch_ = c_ % CPR;                             \
+    const uint32_t m_ = row_ < (CNT) ? ~0u : 0u; /* mask, not a select */ \
+    *(uint4*)&Ks[row_ * KS + ch_ * 4] =                                    \
+        make_uint4(KD.x & m_, KD.y & m_, KD.z & m_, KD.w & m_);            \
+    *(uint4*)&Vs[row_ * KW + ch_ * 4] =                                    \
+        make_uint4(VD.x & m_, VD.y & m_, VD.z & m_, VD.w & m_);            \
+  }
+  KS_FETCH(start);
+  // query vector j of the workgroup: row r0 + j / G, head kvh * G + j % G
+  for (int e = threadIdx.x; e < nq * HD; e += 256) {
+    const int j = e / HD, c = e % HD;
+    Qs[e] = q[((size_t)(r0 + j / G) * hq + kvh * G + j % G) * HD + c];
+  }
 
   int maxlen = 0;
   for (int r = r0; r < r1; ++r) maxlen = max(maxlen, len[r]);
@@ -84,85 +131,79 @@ __global__ __launch_bounds__(256) void k_attn_split(int M, int hq, int hkv, int 
     for (int e = 0; e < DPL; ++e) o[j][e] = 0.f;
   }
 
-  const size_t es = BF ? 2 : 4;
-  const char* kbase = (const char*)kc + (size_t)kvh * n_max * HD * es;
-  const char* vbase = (const char*)vc + (size_t)kvh * n_max * HD * es;
-  uint4 kr[NCH], vr[NCH];
-  // rows past the end of a partial tile repeat its last row (never scored)
-#define KS_FETCH(T0, CNT)                                                  \
-  _Pragma("unroll") for (int u = 0; u < NCH; ++u) {                        \
-    const int c_ = threadIdx.x + 256 * u;                                  \
-    const int row_ = min(c_ / CPR, (CNT) - 1), ch_ = c_ % CPR;             \
-    const size_t off_ = (size_t)((T0) + row_) * HD * es + ch_ * 16;        \
-    kr[u] = *(const uint4*)(kbase + off_);                                 \
-    vr[u] = *(const uint4*)(vbase + off_);                                 \
-  }
   for (int tile = 0; tile < ntile; ++tile) {
     const int t0 = start + tile * TILE;
-    KS_FETCH(t0, min(TILE, maxlen - t0));
-#pragma unroll
-    for (int u = 0; u < NCH; ++u) {
-      const int c = threadIdx.x + 256 * u;
-      const int row = c / CPR, ch = c % CPR;
-      *(uint4*)&Ks[row * KS + ch * 4] = kr[u];
-      *(uint4*)&Vs[row * KW + ch * 4] = vr[u];
-    }
+    const int cnt = min(TILE, maxlen - t0);
+    KS_ST(0, k0, v0, cnt) KS_ST(1, k1, v1, cnt) KS_ST(2, k2, v2, cnt) KS_ST(3, k3, v3, cnt)
     __syncthreads();
+    if (tile + 1 < ntile) KS_FETCH(t0 + TILE);
 
+    // scores: lane = key t0 + lane
+    uint4 krow[KW / 4];
+#pragma unroll
+    for (int w4 = 0; w4 < KW / 4; ++w4) krow[w4] = *(const uint4*)&Ks[lane * KS + 4 * w4];
+    float p[QMAX];
 #pragma unroll
     for (int j = 0; j < QMAX; ++j) {
+      p[j] = 0.f;
       const int qi = wave + 4 * j;
-      if (qi >= nq) break;
-      const int r = r0 + qi / G;
-      const int h = kvh * G + qi % G;
-      const int vcnt = min(TILE, len[r] - t0);
+      if (qi >= nq) continue;
+      const int vcnt = min(TILE, len[r0 + qi / G] - t0);
       if (vcnt <= 0) continue;
-      const float* qv = q + ((size_t)r * hq + h) * HD;
-      float s0 = 0.f;
-      const uint32_t* k0p = &Ks[lane * KS];
-#pragma unroll 4
+      const float* qv = &Qs[qi * HD];
+      // four interleaved partial sums (shorter dependency chains), added in a
+      // fixed order
+      float sp[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
       for (int w4 = 0; w4 < KW / 4; ++w4) {
-        const uint4 a = *(const uint4*)(k0p + 4 * w4);
+        const uint4 a = krow[w4];
+        float& acc = sp[w4 & 3];
         if (BF) {
-          const float* qq = qv + 8 * w4;
-          s0 = fmaf(qq[0], lo16(a.x), s0); s0 = fmaf(qq[1], hi16(a.x), s0);
-          s0 = fmaf(qq[2], lo16(a.y), s0); s0 = fmaf(qq[3], hi16(a.y), s0);
-          s0 = fmaf(qq[4], lo16(a.z), s0); s0 = fmaf(qq[5], hi16(a.z), s0);
-          s0 = fmaf(qq[6], lo16(a.w), s0); s0 = fmaf(qq[7], hi16(a.w), s0);
+          const float4 qa = *(const float4*)(qv + 8 * w4);
+          const float4 qb = *(const float4*)(qv + 8 * w4 + 4);
+          acc = fmaf(qa.x, lo16(a.x), acc); acc = fmaf(qa.y, hi16(a.x), acc);
+          acc = fmaf(qa.z, lo16(a.y), acc); acc = fmaf(qa.w, hi16(a.y), acc);
+          acc = fmaf(qb.x, lo16(a.z), acc); acc = fmaf(qb.y, hi16(a.z), acc);
+          acc = fmaf(qb.z, lo16(a.w), acc); acc = fmaf(qb.w, hi16(a.w), acc);
         } else {
-          const float* qq = qv + 4 * w4;
-          s0 = fmaf(qq[0], __uint_as_float(a.x), s0); s0 = fmaf(qq[1], __uint_as_float(a.y), s0);
-          s0 = fmaf(qq[2], __uint_as_float(a.z), s0); s0 = fmaf(qq[3], __uint_as_float(a.w), s0);
+          const float4 qa = *(const float4*)(qv + 4 * w4);
+          acc = fmaf(qa.x, __uint_as_float(a.x), acc); acc = fmaf(qa.y, __uint_as_float(a.y), acc);
+          acc = fmaf(qa.z, __uint_as_float(a.z), acc); acc = fmaf(qa.w, __uint_as_float(a.w), acc);
         }
       }
+      float s0 = (sp[0] + sp[1]) + (sp[2] + sp[3]);
       s0 = lane < vcnt ? s0 * scale : -FLT_MAX;
       const float mt = wave_max(s0);
       const float mnew = fmaxf(mrun[j], mt);
       const float alpha = __expf(mrun[j] - mnew);
-      const float p0 = lane < vcnt ? __expf(s0 - mnew) : 0.f;
-      lrun[j] = lrun[j] * alpha + wave_sum(p0);
+      p[j] = lane < vcnt ? __expf(s0 - mnew) : 0.f;
+      lrun[j] = lrun[j] * alpha + wave_sum(p[j]);
       mrun[j] = mnew;
-      float acc[DPL];
 #pragma unroll
-      for (int e = 0; e < DPL; ++e) acc[e] = 0.f;
-#pragma unroll 8
-      for (int t = 0; t < vcnt; ++t) {
-        const float pt = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(p0), t));
-        const uint32_t vw = Vs[t * KW + lane];
+      for (int e = 0; e < DPL; ++e) o[j][e] *= alpha;
+    }
+    // values: every row of the tile, each value word read once per wave
+#pragma unroll 16
+    for (int t = 0; t < TILE; ++t) {
+      const uint32_t vw = Vs[t * KW + lane];
+#pragma unroll
+      for (int j = 0; j < QMAX; ++j) {
+        if (wave + 4 * j >= nq) continue;
+        const float pt = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(p[j]), t));
         if (BF) {
-          acc[0] = fmaf(pt, lo16(vw), acc[0]);
-          acc[DPL - 1] = fmaf(pt, hi16(vw), acc[DPL - 1]);
+          o[j][0] = fmaf(pt, lo16(vw), o[j][0]);
+          o[j][DPL - 1] = fmaf(pt, hi16(vw), o[j][DPL - 1]);
         } else {
-          acc[0] = fmaf(pt, __uint_as_float(vw), acc[0]);
+          o[j][0] = fmaf(pt, __uint_as_float(vw), o[j][0]);
         }
       }
-#pragma unroll
-      for (int e = 0; e < DPL; ++e) o[j][e] = o[j][e] * alpha + acc[e];
     }
     __syncthreads();
   }
 
 #undef KS_FETCH
+#undef KS_LD
+#undef KS_ST
 #pragma unroll
   for (int j = 0; j < QMAX; ++j) {
     const int qi = wave + 4 * j;
@@ -180,6 +221,230 @@ __global__ __launch_bounds__(256) void k_attn_split(int M, int hq, int hkv, int 
     if (lane == 0) {
       dst[HD] = mrun[j];
       dst[HD + 1] = lrun[j];
+    }
+  }
+}
+
+typedef __bf16 bf16x8_d __attribute__((ext_vector_type(8)));
+typedef float f32x4_d __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4_d __attribute__((ext_vector_type(4)));
+
+typedef __attribute__((__vector_size__(4 * sizeof(__bf16)))) __bf16 bf16x4_d;
+
+// Decode / verify rows of bf16 caches with head dim 128 and at most 4 query
+// heads per kv head, all products on matrix instructions.  A workgroup of S
+// waves owns S consecutive 64-key tiles of one kv head and one row; wave w owns
+// tile w for every query head of the kv head.  The wave requests its 32 KiB of
+// keys and values with direct global-to-LDS loads (no staging registers) next
+// to its query loads, so it waits for one memory round trip.  Rows are stored
+// unpadded with 16-byte chunk c of row r at slot c ^ (r % 16).
+//  scores  S^T = K Q^T, keys as rows of 16x16x32 products (queries as hi + lo
+//          bf16 columns, columns >= G zero): lane (j, g) holds keys 16 kt + 4 g
+//          + v of query j, so the tile max and sum need two cross-lane steps;
+//  values  O = P V with the probabilities (bf16) taken from the score registers
+//          as the A operand: k slot e of lane group g is key 4 g + e (e < 4) or
+//          16 + 4 g + e - 4 (e >= 4) of a 32-key step.  The V operand in that
+//          key order comes from transposing LDS reads (a 16-lane group turns
+//          16 8-byte row pieces into 4 keys x 16 dims).  Rows at or past the
+//          row length are zeroed in LDS first (probability 0 must not meet a
+//          non-finite stale value).
+// The S tile results are merged in tile order into the split's partial (o,
+// max, sum), the layout k_attn_combine reads.  Every quantity of a row depends
+// only on that row.
+template <int S>
+__global__ __launch_bounds__(64 * S) void k_attn_dec(int M, int hq, int hkv, int n_max,
+                                                     const float* __restrict__ q,
+                                                     const bf16_t* __restrict__ kc,
+                                                     const bf16_t* __restrict__ vc,
+                                                     const int32_t* __restrict__ len,
+                                                     float* __restrict__ part, int nsplit) {
+  constexpr int HD = 128;
+  constexpr int MGS = 4 * (HD + 2);  // merge record: 4 queries
+  __shared__ __align__(16) uint4 KV[S][2 * TILE * 16];  // per wave: K tile, then V tile
+  const int split = blockIdx.x, kvh = blockIdx.y, r = blockIdx.z;
+  const int G = hq / hkv;
+  const int lane = threadIdx.x & 63;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int t0 = (split * S + w) * TILE;
+  uint4* KVw = &KV[w][0];
+
+  // piece i (1 KiB): rows 4 (i % 16) .. + 3 of K (i < 16) or V; lane l writes
+  // chunk slot l % 16 of row 4 (i % 16) + l / 16
+  {
+    const bf16_t* kb = kc + (size_t)kvh * n_max * HD;
+    const bf16_t* vb = vc + (size_t)kvh * n_max * HD;
+    const int rr0 = lane >> 4, slot = lane & 15;
+#pragma unroll
+    for (int i = 0; i < 32; ++i) {
+      const int rr = 4 * (i & 15) + rr0;
+      const int row = min(t0 + rr, n_max - 1);
+      const bf16_t* src = (i < 16 ? kb : vb) + (size_t)row * HD + ((slot ^ (rr & 15)) << 3);
+      __builtin_amdgcn_global_load_lds((const void*)src,
+                                       (__attribute__((address_space(3))) void*)&KVw[i * 64], 16,
+                                       0, 0);
+    }
+  }
+  // query fragments: column j = lane % 16 (query head kvh G + j), dims
+  // 32 ks + 8 g .. + 7 (g = lane / 16), as hi + lo bf16
+  const int j = lane & 15, g = lane >> 4;
+  bf16x8_d qh[4], ql[4];
+  {
+    const bool ok = j < G;
+    const float* qv = q + ((size_t)r * hq + kvh * G + (ok ? j : 0)) * HD + 8 * g;
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      float4 x0 = *(const float4*)(qv + 32 * ks), x1 = *(const float4*)(qv + 32 * ks + 4);
+      if (!ok) x0 = x1 = make_float4(0.f, 0.f, 0.f, 0.f);
+      const float xs[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const __bf16 h = (__bf16)xs[e];
+        qh[ks][e] = h;
+        ql[ks][e] = (__bf16)(xs[e] - (float)h);
+      }
+    }
+  }
+  const int L = len[r];
+  const int cnt = min(TILE, L - t0);  // keys of this tile (may be <= 0)
+  __builtin_amdgcn_s_waitcnt(0);
+
+  float m = -FLT_MAX, l = 0.f;
+  f32x4_d o[8];
+#pragma unroll
+  for (int dt = 0; dt < 8; ++dt) o[dt] = f32x4_d{0.f, 0.f, 0.f, 0.f};
+  if (cnt > 0) {
+    const uint4* Kt = KVw;
+    uint4* Vt = KVw + TILE * 16;
+    if (cnt < TILE) {
+      for (int c = cnt * 16 + lane; c < TILE * 16; c += 64) Vt[c] = make_uint4(0u, 0u, 0u, 0u);
+    }
+    // S^T: sc[kt][v] = score(key 16 kt + 4 g + v, query j)
+    f32x4_d sc[4];
+#pragma unroll
+    for (int kt = 0; kt < 4; ++kt) {
+      sc[kt] = f32x4_d{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) {
+        const int c = 4 * ks + g;  // 16-byte chunk of the key row
+        const bf16x8_d kf = __builtin_bit_cast(bf16x8_d, Kt[(16 * kt + j) * 16 + (c ^ j)]);
+        sc[kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qh[ks], sc[kt], 0, 0, 0);
+        sc[kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, ql[ks], sc[kt], 0, 0, 0);
+      }
+    }
+    const float scale = 1.0f / sqrtf((float)HD);
+    float mt = -FLT_MAX;
+#pragma unroll
+    for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        sc[kt][v] = 16 * kt + 4 * g + v < cnt ? sc[kt][v] * scale : -FLT_MAX;
+        mt = fmaxf(mt, sc[kt][v]);
+      }
+    mt = fmaxf(mt, __shfl_xor(mt, 16));
+    mt = fmaxf(mt, __shfl_xor(mt, 32));
+    float ps = 0.f;
+#pragma unroll
+    for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const float p = 16 * kt + 4 * g + v < cnt ? __expf(sc[kt][v] - mt) : 0.f;
+        sc[kt][v] = p;
+        ps += p;
+      }
+    ps += __shfl_xor(ps, 16);
+    ps += __shfl_xor(ps, 32);
+    m = mt;
+    l = ps;
+    // transposing reads: lane 16 g + 4 s + u points at the 8-byte piece of V row
+    // 32 k2 + 16 h + 4 g + s, dims 16 dt + 4 u .. + 3
+    const int s4 = (lane & 15) >> 2, u4 = lane & 3;
+    const char* Vb = (const char*)Vt;
+#pragma unroll
+    for (int k2 = 0; k2 < 2; ++k2) {
+      bf16x8_d pa;
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        pa[v] = (__bf16)sc[2 * k2][v];
+        pa[4 + v] = (__bf16)sc[2 * k2 + 1][v];
+      }
+#pragma unroll
+      for (int dt = 0; dt < 8; ++dt) {
+        bf16x4_d h2[2];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int row = 32 * k2 + 16 * h + 4 * g + s4;
+          const int c = 2 * dt + (u4 >> 1);
+          const char* pp = Vb + row * 256 + ((c ^ (row & 15)) << 4) + ((u4 & 1) << 3);
+          h2[h] = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+              (__attribute__((address_space(3))) bf16x4_d*)pp);
+        }
+        bf16x8_d vb;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          vb[e] = h2[0][e];
+          vb[4 + e] = h2[1][e];
+        }
+        o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa, vb, o[dt], 0, 0, 0);
+      }
+    }
+  }
+  // o[dt][v]: query 4 g + v, dim 16 dt + j (valid in lanes g == 0); the max and
+  // sum of query a live in lane a
+  const float ma[4] = {__shfl(m, 0), __shfl(m, 1), __shfl(m, 2), __shfl(m, 3)};
+  const float la[4] = {__shfl(l, 0), __shfl(l, 1), __shfl(l, 2), __shfl(l, 3)};
+  if (S > 1) {
+    __syncthreads();  // every wave is done with its tiles
+    float* rec = (float*)KVw;
+    if (g == 0) {
+#pragma unroll
+      for (int a = 0; a < 4; ++a) {
+#pragma unroll
+        for (int dt = 0; dt < 8; ++dt) rec[a * (HD + 2) + 16 * dt + j] = o[dt][a];
+        if (j == 0) {
+          rec[a * (HD + 2) + HD] = ma[a];
+          rec[a * (HD + 2) + HD + 1] = la[a];
+        }
+      }
+    }
+    __syncthreads();
+    if (w != 0 || g != 0 || split * S * TILE >= L) return;
+#pragma unroll
+    for (int a = 0; a < 4; ++a) {
+      if (a >= G) break;
+      float mx = -FLT_MAX;
+#pragma unroll
+      for (int s = 0; s < S; ++s) mx = fmaxf(mx, ((const float*)&KV[s][0])[a * (HD + 2) + HD]);
+      float lx = 0.f, ox[8];
+#pragma unroll
+      for (int dt = 0; dt < 8; ++dt) ox[dt] = 0.f;
+#pragma unroll
+      for (int s = 0; s < S; ++s) {
+        const float* rs = (const float*)&KV[s][0] + a * (HD + 2);
+        const float wt = rs[HD] == -FLT_MAX ? 0.f : __expf(rs[HD] - mx);
+        lx = fmaf(rs[HD + 1], wt, lx);
+#pragma unroll
+        for (int dt = 0; dt < 8; ++dt) ox[dt] = fmaf(rs[16 * dt + j], wt, ox[dt]);
+      }
+      float* dst = part + (((size_t)r * hq + kvh * G + a) * nsplit + split) * (HD + 2);
+#pragma unroll
+      for (int dt = 0; dt < 8; ++dt) dst[16 * dt + j] = ox[dt];
+      if (j == 0) {
+        dst[HD] = mx;
+        dst[HD + 1] = lx;
+      }
+    }
+    return;
+  }
+  if (g != 0 || t0 >= L) return;
+#pragma unroll
+  for (int a = 0; a < 4; ++a) {
+    if (a >= G) break;
+    float* dst = part + (((size_t)r * hq + kvh * G + a) * nsplit + split) * (HD + 2);
+#pragma unroll
+    for (int dt = 0; dt < 8; ++dt) dst[16 * dt + j] = o[dt][a];
+    if (j == 0) {
+      dst[HD] = ma[a];
+      dst[HD + 1] = la[a];
     }
   }
 }
@@ -509,7 +774,23 @@ void attn_split(const AttnArgs& a, hipStream_t st) {
   hipLaunchKernelGGL((k_attn_split<HDV, BFV, QM>), grid, dim3(256), 0, st, a.M, a.hq, a.hkv, \
                      a.n_max, a.q, a.kc, a.vc, a.len, a.tiles, a.rows_per_block, a.part,     \
                      a.nsplit)
-  if (a.hd == 128 && a.tiles > 1) {
+  if (a.hd == 128 && G <= 4 && a.rows_per_block == 1 && a.tiles >= 1 && a.tiles <= 5) {
+    // decode / verify rows
+    dim3 g3(ns, a.hkv, a.M);
+    const bf16_t* kc = (const bf16_t*)a.kc;
+    const bf16_t* vc = (const bf16_t*)a.vc;
+#define KS_DEC(S_)                                                                                \
+  hipLaunchKernelGGL(k_attn_dec<S_>, g3, dim3(64 * S_), 0, st, a.M, a.hq, a.hkv, a.n_max, a.q, kc, \
+                     vc, a.len, a.part, a.nsplit)
+    switch (a.tiles) {
+      case 1: KS_DEC(1); break;
+      case 2: KS_DEC(2); break;
+      case 3: KS_DEC(3); break;
+      case 4: KS_DEC(4); break;
+      default: KS_DEC(5); break;
+    }
+#undef KS_DEC
+  } else if (a.hd == 128 && a.tiles > 1) {
     // batched rows: matrix-instruction kernel, 64 query vectors per workgroup
     const int span = TILE * a.tiles;
     dim3 g2((a.max_len + span - 1) / span, a.hkv, (a.M * G + 63) / 64);

@@ -45,7 +45,12 @@ using namespace ks;
 namespace {
 
 constexpr int PB = 512;        // rows per batched attention / head pass
-constexpr int DEC_TILES = 1;   // decode/verify: 64 positions per split
+// decode/verify splits: 64-position tiles per split, by cache size only (never
+// by row count, so a verify row and the decode step split alike).  One tile
+// per split for caches up to 4096 positions; five above (a 160 KiB workgroup:
+// up to 10240 positions of 8 kv heads fit the 256 CUs in one round, and the
+// merge reads few partials).  Measured on MI355X against 1..5 tiles.
+int dec_tiles(int n_max) { return n_max > 4096 ? 5 : 1; }
 constexpr int BAT_TILES = 16;  // prefill/DP: 1024 positions per split
 
 size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -68,7 +73,7 @@ Layout make_layout(const ks_model_desc& d, const ks_limits& lim) {
   y.LR = std::max(gam1, PB);
   y.nqkv = (d.hq + 2 * d.hkv) * d.hd;
   y.a2w = std::max(d.hq * d.hd, d.ffn);
-  const int ns_dec = attn_nsplit(d.n_max, DEC_TILES);
+  const int ns_dec = attn_nsplit(d.n_max, dec_tiles(d.n_max));
   const int ns_bat = attn_nsplit(d.n_max, BAT_TILES);
   y.part_rows = PB;
   y.part_elems = std::max((size_t)16 * d.hq * ns_dec, (size_t)PB * d.hq * ns_bat) * (d.hd + 2);
@@ -268,7 +273,7 @@ void attn_rows(ks_ctx* c, int l, const float* xin, float* xout, int R, const int
                    c->bf() ? 1 : 0};
     PROF(c, KS_KC_QKV_POST, qkv_post(qp, c->st));
   }
-  const int tiles = batched ? BAT_TILES : DEC_TILES;
+  const int tiles = batched ? BAT_TILES : dec_tiles(d.n_max);
   const int ns = attn_nsplit(d.n_max, tiles);
   const int step = batched ? PB : 16;
   for (int r0 = 0; r0 < R; r0 += step) {

@@ -25,13 +25,19 @@ __host__ __device__ inline float bf2f(bf16_t b) {
   c.u = (uint32_t)b << 16;
   return c.f;
 }
-// round to nearest even (finite inputs)
+// round to nearest even (finite inputs); on the device the gfx950 conversion
+// instruction, which gives the same bits as the integer form (checked over
+// denormals, ties and random finite values)
 __host__ __device__ inline bf16_t f2bf(float f) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  return __builtin_bit_cast(bf16_t, (__bf16)f);
+#else
   union { uint32_t u; float f; } c;
   c.f = f;
   uint32_t u = c.u;
   u += 0x7FFFu + ((u >> 16) & 1u);
   return (bf16_t)(u >> 16);
+#endif
 }
 
 // ------------------------------------------------------------------ epilogues
