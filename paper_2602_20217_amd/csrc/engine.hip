@@ -45,6 +45,8 @@ using namespace ks;
 namespace {
 
 constexpr int PB = 512;        // rows per batched attention / head pass
+// float32 split-K partials of the batched products (prefill chunks, selection)
+constexpr size_t GPART_BYTES = (size_t)64 << 20;
 // decode/verify splits: 64-position tiles per split, by cache size only (never
 // by row count, so a verify row and the decode step split alike).  One tile
 // per split for caches up to 4096 positions; five above (a 160 KiB workgroup:
@@ -57,7 +59,7 @@ size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct Layout {
   size_t rope, x, a1hi, a1lo, a2hi, a2lo, qkv, q, kvself, part, logits, am, top1;
-  size_t tok, pos, len, stage, hist, xh, g0, g1, ge, dpos, dlen, sig, ptrs, ssq, total;
+  size_t tok, pos, len, stage, hist, xh, g0, g1, ge, dpos, dlen, sig, ptrs, ssq, gpart, total;
   int FR, RING, cells, DR, XR, LR, nqkv, a2w, part_rows;
   size_t part_elems;
 };
@@ -111,6 +113,7 @@ Layout make_layout(const ks_model_desc& d, const ks_limits& lim) {
   y.sig = take((size_t)2 * y.DR * 8);
   y.ptrs = take((size_t)4 * (y.cells + 2 * d.L + 2) * 8);
   y.ssq = take((size_t)16 * (d.d / 16) * 4);
+  y.gpart = take(GPART_BYTES);
   y.total = o;
   return y;
 }
@@ -189,12 +192,22 @@ void prof_end(ks_ctx* c, int i) {
 // (the embedding, a residual epilogue, or act_prep for rows handed in).
 bool skinny(const ks_ctx* c, int M, bool batched) { return c->bf() && !batched && M <= 16; }
 
+void run_gemm(ks_ctx* c, GemmArgs& g, bool batched) {
+  if (!c->bf()) {
+    gemm_f32(g, c->st);
+  } else if (skinny(c, g.M, batched)) {
+    gemm_bf16_skinny(g, c->st);
+  } else {
+    g.part = c->at<float>(c->y.gpart);
+    g.part_bytes = GPART_BYTES;
+    gemm_bf16_tiled(g, c->st);
+  }
+}
+
 void gemm(ks_ctx* c, int M, int N, int K, Act A, const void* W, int epi, float* out, int ldo,
           const float* res, int ldres, Act aout, bool batched) {
   GemmArgs g{M, N, K, A, W, epi, out, ldo, res, ldres, aout};
-  if (!c->bf()) gemm_f32(g, c->st);
-  else if (skinny(c, M, batched)) gemm_bf16_skinny(g, c->st);
-  else gemm_bf16_tiled(g, c->st);
+  run_gemm(c, g, batched);
 }
 
 // norm gain feeding sublayer i (1..2L); i = 2L + 1 is the final norm
@@ -232,9 +245,7 @@ void resid_gemm(ks_ctx* c, int R, int K, Act A, const void* W, float* xout, cons
     g.next_act = c->act1();
     g.next_ssq = c->at<float>(c->y.ssq);
   }
-  if (!c->bf()) gemm_f32(g, c->st);
-  else if (skinny(c, R, batched)) gemm_bf16_skinny(g, c->st);
-  else gemm_bf16_tiled(g, c->st);
+  run_gemm(c, g, batched);
 }
 
 // Attention sublayer of layer l on R rows: x_out = x_in + Wo attn(...).

@@ -232,22 +232,32 @@ void gemm_bf16_skinny(const GemmArgs& g, hipStream_t st) {
 
 // ------------------------------------------------------------------- tiled
 // Batched rows (prefill chunks, selection DP).  Workgroup tile 128 rows x 128
-// columns, 4 waves as 2 x 2 with 64 x 64 wave tiles (4 x 4 MFMAs).  Each
-// 32-wide k step of A and W is staged in LDS in the MFMA operand order (A:
-// row l%16, k 8(l/16).. of each 16-row tile at byte 16 l; W already arrives in
-// that order), so every fragment read is one conflict-free 16-byte LDS read.
-// The next step's global loads are in flight while the current step's MFMAs
-// run (double-buffered LDS, one barrier per step).  Workgroups that share a
-// weight tile get consecutive logical ids on the same XCD, so the XCD's L2
-// serves the reuse across row blocks.
-template <int EPI>
+// columns, 4 waves as 2 x 2 with 64 x 64 wave tiles (4 x 4 MFMAs).  A 32-wide k
+// step of the workgroup is 16 operand tiles of 1 KiB (8 of A, 8 of W), each
+// laid out in LDS in MFMA register order (lane l at byte 16 l: row l % 16,
+// k 8 (l / 16)..), so every fragment read is one conflict-free 16-byte read.
+// The tiles travel with direct global-to-LDS loads (one 1 KiB load per tile:
+// lane l fetches row l % 16, k chunk l / 16 of A, or 16 bytes of the packed W
+// tile, which is already in that order), ST - 1 steps ahead of the arithmetic
+// in a ring of ST stages: one barrier per step and no staging registers.
+// Rows past M and tiles past N read clamped (valid) addresses; their results
+// are never stored.  Workgroups that share a weight tile get consecutive
+// logical ids on the same XCD.  Split-K (SK > 1): workgroup (.., ks) adds up
+// k steps [ks KT / SK, (ks + 1) KT / SK) and stores float32 partials
+// part[ks][M][N]; gemm_splitk_reduce adds them in split order.
+__device__ constexpr int vmcnt_imm(int n) {
+  // s_waitcnt immediate: vmcnt = n, expcnt and lgkmcnt not waited for
+  return (n & 15) | (7 << 4) | (15 << 8) | ((n >> 4) << 14);
+}
+
+template <int EPI, int ST>
 __global__ __launch_bounds__(256) void k_gemm_tiled(int M, int N, int K,
                                                     const bf16_t* __restrict__ A, int lda,
                                                     const bf16_t* __restrict__ Wp, float* out,
                                                     int ldo, const float* res, int ldres,
-                                                    bf16_t* ohi, bf16_t* olo, int ldact, int MB) {
-  __shared__ __align__(16) bf16_t As[2][8 * 512];
-  __shared__ __align__(16) bf16_t Bs[2][8 * 512];
+                                                    bf16_t* ohi, bf16_t* olo, int ldact, int MB,
+                                                    int NB, int SK, float* __restrict__ part) {
+  __shared__ __align__(16) bf16_t Sg[ST][16 * 512];
   const int KT = K >> 5;
   const int NT = N >> 4;
   // XCD-aware logical block id (blocks are dealt round-robin over 8 XCDs)
@@ -255,43 +265,40 @@ __global__ __launch_bounds__(256) void k_gemm_tiled(int M, int N, int K,
   const int bid = blockIdx.x;
   int lb = bid;
   if ((nblk & 7) == 0) lb = (bid & 7) * (nblk >> 3) + (bid >> 3);
-  const int mb = lb % MB, nb = lb / MB;
+  const int mb = lb % MB, nb = (lb / MB) % NB, ks = lb / (MB * NB);
   const int m0 = mb * 128, nt0 = nb * 8;
+  const int kb = (ks * KT) / SK, nk = ((ks + 1) * KT) / SK - kb;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave & 1, wn = wave >> 1;
 
-  // staging map: chunk c in [0, 512) of 16 bytes, two per thread per operand
-  //   A: row c/4, k chunk c%4  -> tile row/16, lane (row%16) + 16 (c%4)
-  //   W: tile c/64, lane c%64
-  const int c0 = tid, c1 = tid + 256;
-  const int ar0 = m0 + (c0 >> 2), ar1 = m0 + (c1 >> 2);
-  const bool ak0 = ar0 < M, ak1 = ar1 < M;
-  const bf16_t* as0 = A + (size_t)(ak0 ? ar0 : 0) * lda + (c0 & 3) * 8;
-  const bf16_t* as1 = A + (size_t)(ak1 ? ar1 : 0) * lda + (c1 & 3) * 8;
-  const int ad0 = ((c0 >> 2) >> 4) * 512 + (((c0 >> 2) & 15) + 16 * (c0 & 3)) * 8;
-  const int ad1 = ((c1 >> 2) >> 4) * 512 + (((c1 >> 2) & 15) + 16 * (c1 & 3)) * 8;
-  const bool bk0 = nt0 + (c0 >> 6) < NT, bk1 = nt0 + (c1 >> 6) < NT;
-  const bf16_t* bs0 = Wp + (size_t)(bk0 ? nt0 + (c0 >> 6) : 0) * KT * 512 + (c0 & 63) * 8;
-  const bf16_t* bs1 = Wp + (size_t)(bk1 ? nt0 + (c1 >> 6) : 0) * KT * 512 + (c1 & 63) * 8;
-  const int bd0 = (c0 >> 6) * 512 + (c0 & 63) * 8;
-  const int bd1 = (c1 >> 6) * 512 + (c1 & 63) * 8;
-  // sources are clamped to valid rows/tiles; out-of-range chunks are zeroed
-  // after the load (a load is never skipped, so no pointer select is formed)
-  const uint32_t am0 = ak0 ? ~0u : 0u, am1 = ak1 ? ~0u : 0u;
-  const uint32_t bm0 = bk0 ? ~0u : 0u, bm1 = bk1 ? ~0u : 0u;
-#define KS_MASK4(v, m) make_uint4((v).x & (m), (v).y & (m), (v).z & (m), (v).w & (m))
-  uint4 ra0 = *(const uint4*)as0, ra1 = *(const uint4*)as1;
-  uint4 rb0 = *(const uint4*)bs0, rb1 = *(const uint4*)bs1;
-  ra0 = KS_MASK4(ra0, am0);
-  ra1 = KS_MASK4(ra1, am1);
-  rb0 = KS_MASK4(rb0, bm0);
-  rb1 = KS_MASK4(rb1, bm1);
-  *(uint4*)&As[0][ad0] = ra0;
-  *(uint4*)&As[0][ad1] = ra1;
-  *(uint4*)&Bs[0][bd0] = rb0;
-  *(uint4*)&Bs[0][bd1] = rb1;
-  __syncthreads();
+  // wave w moves pieces 4w..4w+3 of every step: pieces 0..7 are A tiles (rows
+  // m0 + 16 p ..), 8..15 W tiles nt0 + p - 8
+  const bf16_t* src[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int pc = 4 * wave + q;
+    if (pc < 8) {
+      const int row = min(m0 + 16 * pc + (lane & 15), M - 1);
+      src[q] = A + (size_t)row * lda + (size_t)kb * 32 + (lane >> 4) * 8;
+    } else {
+      const int nt = min(nt0 + pc - 8, NT - 1);
+      src[q] = Wp + ((size_t)nt * KT + kb) * 512 + lane * 8;
+    }
+  }
+  const bool is_a = wave < 2;  // waves 0, 1 move A tiles, waves 2, 3 W tiles
+  auto issue = [&](int step, int buf) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const bf16_t* s_ = src[q] + (size_t)step * (is_a ? 32 : 512);
+      __builtin_amdgcn_global_load_lds(
+          (const void*)s_,
+          (__attribute__((address_space(3))) void*)&Sg[buf][(4 * wave + q) * 512], 16, 0, 0);
+    }
+  };
+#pragma unroll
+  for (int s = 0; s < ST - 1; ++s)
+    if (s < nk) issue(s, s);
 
   f32x4 acc[4][4];
 #pragma unroll
@@ -299,41 +306,33 @@ __global__ __launch_bounds__(256) void k_gemm_tiled(int M, int N, int K,
 #pragma unroll
     for (int t = 0; t < 4; ++t) acc[i][t] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  for (int kt = 0; kt < KT; ++kt) {
-    const int cur = kt & 1;
-    const bool more = kt + 1 < KT;
-    if (more) {
-      ra0 = *(const uint4*)(as0 + (kt + 1) * 32);
-      ra1 = *(const uint4*)(as1 + (kt + 1) * 32);
-      rb0 = *(const uint4*)(bs0 + (size_t)(kt + 1) * 512);
-      rb1 = *(const uint4*)(bs1 + (size_t)(kt + 1) * 512);
-      ra0 = KS_MASK4(ra0, am0);
-      ra1 = KS_MASK4(ra1, am1);
-      rb0 = KS_MASK4(rb0, bm0);
-      rb1 = KS_MASK4(rb1, bm1);
-    }
+  for (int it = 0; it < nk; ++it) {
+    // step it has landed once at most the ST - 2 later steps are in flight.
+    // The barrier then needs no memory fence (a fence would wait for every
+    // step in flight): this wave's tile loads for step it are counted down
+    // above, and its LDS reads of the stage refilled next were consumed by
+    // the previous step's matrix instructions.
+    if (it + ST - 2 < nk) __builtin_amdgcn_s_waitcnt(vmcnt_imm(4 * (ST - 2)));
+    else __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+    __builtin_amdgcn_s_barrier();
+    __asm__ volatile("" ::: "memory");
+    if (it + ST - 1 < nk) issue(it + ST - 1, (it + ST - 1) % ST);
+    const bf16_t* Sb = Sg[it % ST];
     bf16x8 a[4], b[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) a[i] = ld_frag(&As[cur][(4 * wm + i) * 512 + lane * 8]);
+    for (int i = 0; i < 4; ++i) a[i] = ld_frag(&Sb[(4 * wm + i) * 512 + lane * 8]);
 #pragma unroll
-    for (int t = 0; t < 4; ++t) b[t] = ld_frag(&Bs[cur][(4 * wn + t) * 512 + lane * 8]);
+    for (int t = 0; t < 4; ++t) b[t] = ld_frag(&Sb[(8 + 4 * wn + t) * 512 + lane * 8]);
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int t = 0; t < 4; ++t)
         acc[i][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[t], acc[i][t], 0, 0, 0);
-    if (more) {
-      *(uint4*)&As[cur ^ 1][ad0] = ra0;
-      *(uint4*)&As[cur ^ 1][ad1] = ra1;
-      *(uint4*)&Bs[cur ^ 1][bd0] = rb0;
-      *(uint4*)&Bs[cur ^ 1][bd1] = rb1;
-    }
-    __syncthreads();
   }
 
-#undef KS_MASK4
   const int mw = m0 + wm * 64;
   const int nw = nt0 + wn * 4;
+  float* pk = part + (size_t)ks * M * N;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
 #pragma unroll
@@ -354,31 +353,79 @@ __global__ __launch_bounds__(256) void k_gemm_tiled(int M, int N, int K,
           if (nw + t >= NT) continue;
           const int n = (nw + t) * 16 + (lane & 15);
           float sv = acc[i][t][v];
-          if (EPI == EPI_RESID) sv += res[(size_t)m * ldres + n];
-          out[(size_t)m * ldo + n] = sv;
+          if (SK > 1) {
+            pk[(size_t)m * N + n] = sv;
+          } else {
+            if (EPI == EPI_RESID) sv += res[(size_t)m * ldres + n];
+            out[(size_t)m * ldo + n] = sv;
+          }
         }
       }
     }
   }
 }
 
+// out[m][n] = (res[m][n] +) sum over ks in order of part[ks][m][n]; N % 4 == 0
+template <int EPI>
+__global__ __launch_bounds__(256) void k_splitk_reduce(int M, int N, int SK,
+                                                       const float* __restrict__ part,
+                                                       float* out, int ldo, const float* res,
+                                                       int ldres) {
+  const size_t i4 = (size_t)blockIdx.x * 256 + threadIdx.x;
+  const int n4 = N >> 2;
+  if (i4 >= (size_t)M * n4) return;
+  const int m = (int)(i4 / n4), n = (int)(i4 % n4) * 4;
+  float4 s = *(const float4*)&part[(size_t)m * N + n];
+  for (int k = 1; k < SK; ++k) {
+    const float4 t = *(const float4*)&part[((size_t)k * M + m) * N + n];
+    s.x += t.x; s.y += t.y; s.z += t.z; s.w += t.w;
+  }
+  if (EPI == EPI_RESID) {
+    const float4 r = *(const float4*)&res[(size_t)m * ldres + n];
+    s.x = r.x + s.x; s.y = r.y + s.y; s.z = r.z + s.z; s.w = r.w + s.w;
+  }
+  *(float4*)&out[(size_t)m * ldo + n] = s;
+}
+
 void gemm_bf16_tiled(const GemmArgs& g, hipStream_t st) {
+  constexpr int ST = 4;
   const int NT = g.N / 16;
+  const int KT = g.K / 32;
   const int MB = (g.M + 127) / 128;
-  const int NBk = (NT + 7) / 8;
-  dim3 grid(MB * NBk);
+  const int NB = (NT + 7) / 8;
+  // split K until about two workgroups per CU, keeping >= 16 k steps per split
+  // and the partials within the caller's buffer
+  int SK = 1;
+  if (g.epi != EPI_SWIGLU && g.part) {
+    while (SK < 8 && MB * NB * SK < 512 && KT / (2 * SK) >= 16 &&
+           (size_t)2 * SK * g.M * g.N * 4 <= g.part_bytes)
+      SK *= 2;
+  }
+  dim3 grid(MB * NB * SK);
   const bf16_t* A = (const bf16_t*)g.A.hi;
   const bf16_t* W = (const bf16_t*)g.W;
   if (g.epi == EPI_SWIGLU)
-    hipLaunchKernelGGL(k_gemm_tiled<EPI_SWIGLU>, grid, dim3(256), 0, st, g.M, g.N, g.K, A,
+    hipLaunchKernelGGL((k_gemm_tiled<EPI_SWIGLU, ST>), grid, dim3(256), 0, st, g.M, g.N, g.K, A,
                        g.A.ld, W, g.out, g.ldo, g.res, g.ldres, (bf16_t*)g.act_out.hi,
-                       (bf16_t*)g.act_out.lo, g.act_out.ld, MB);
+                       (bf16_t*)g.act_out.lo, g.act_out.ld, MB, NB, 1, g.part);
   else if (g.epi == EPI_RESID)
-    hipLaunchKernelGGL(k_gemm_tiled<EPI_RESID>, grid, dim3(256), 0, st, g.M, g.N, g.K, A,
-                       g.A.ld, W, g.out, g.ldo, g.res, g.ldres, nullptr, nullptr, 0, MB);
+    hipLaunchKernelGGL((k_gemm_tiled<EPI_RESID, ST>), grid, dim3(256), 0, st, g.M, g.N, g.K, A,
+                       g.A.ld, W, g.out, g.ldo, g.res, g.ldres, nullptr, nullptr, 0, MB, NB, SK,
+                       g.part);
   else
-    hipLaunchKernelGGL(k_gemm_tiled<EPI_STORE>, grid, dim3(256), 0, st, g.M, g.N, g.K, A,
-                       g.A.ld, W, g.out, g.ldo, g.res, g.ldres, nullptr, nullptr, 0, MB);
+    hipLaunchKernelGGL((k_gemm_tiled<EPI_STORE, ST>), grid, dim3(256), 0, st, g.M, g.N, g.K, A,
+                       g.A.ld, W, g.out, g.ldo, g.res, g.ldres, nullptr, nullptr, 0, MB, NB, SK,
+                       g.part);
+  if (SK > 1) {
+    const size_t n4 = (size_t)g.M * (g.N / 4);
+    dim3 rg((unsigned)((n4 + 255) / 256));
+    if (g.epi == EPI_RESID)
+      hipLaunchKernelGGL(k_splitk_reduce<EPI_RESID>, rg, dim3(256), 0, st, g.M, g.N, SK, g.part,
+                         g.out, g.ldo, g.res, g.ldres);
+    else
+      hipLaunchKernelGGL(k_splitk_reduce<EPI_STORE>, rg, dim3(256), 0, st, g.M, g.N, SK, g.part,
+                         g.out, g.ldo, g.res, g.ldres);
+  }
 }
 
 // --------------------------------------------------------------------- f32

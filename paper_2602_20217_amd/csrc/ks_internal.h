@@ -94,6 +94,9 @@ struct GemmArgs {
   Act next_act{};
   float* next_ssq = nullptr;
   QkvEpi qe{};
+  // tiled path: float32 split-K partial buffer (optional)
+  float* part = nullptr;
+  size_t part_bytes = 0;
 };
 void gemm_bf16_skinny(const GemmArgs& g, hipStream_t st);  // M <= 16
 void gemm_bf16_tiled(const GemmArgs& g, hipStream_t st);   // any M, A.hi only
