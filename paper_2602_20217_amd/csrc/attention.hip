@@ -21,6 +21,17 @@
 namespace ks {
 
 constexpr int TILE = 64;  // positions per LDS tile of the split kernel
+#ifndef KS_BAT_NW
+#define KS_BAT_NW 8  // waves (16 query vectors each) per batched workgroup
+#endif
+#ifndef KS_BAT_ST
+#define KS_BAT_ST 2  // LDS ring stages of the batched kernel
+#endif
+
+// s_waitcnt immediate: vmcnt = n, expcnt and lgkmcnt not waited for
+__device__ constexpr int vmcnt_imm_a(int n) {
+  return (n & 15) | (7 << 4) | (15 << 8) | ((n >> 4) << 14);
+}
 
 __device__ inline float wave_max(float v) {
 #pragma unroll
@@ -449,6 +460,196 @@ __global__ __launch_bounds__(64 * S) void k_attn_dec(int M, int hq, int hkv, int
   }
 }
 
+// Batched rows (prefill chunks, selection candidates), bf16 caches, head dim
+// 128.  Query vectors of one kv head are ordered qi = row * G + g; wave w of a
+// workgroup owns 16 consecutive ones.  The workgroup walks the 64-key tiles of
+// its split through a ring of ST LDS stages filled by direct global-to-LDS
+// loads ST - 1 tiles ahead (one barrier per tile, no staging registers); rows
+// are stored with 16-byte chunk c of row r at slot c ^ (r % 16).  Per tile and
+// wave: S^T = K Q^T (keys as rows, queries as hi + lo bf16 columns), an online
+// softmax per query column (two cross-lane steps per statistic), then O += P V
+// with the probabilities (bf16) taken from the score registers and the value
+// operand from transposing LDS reads in the same key order.  Tile rows at or
+// past max_len repeat row max_len - 1 (finite; their probability is 0).
+// Partials use the layout of the split kernels.
+template <int NW, int ST>
+__global__ __launch_bounds__(NW * 64) void k_attn_bat(int M, int hq, int hkv, int n_max,
+                                                      const float* __restrict__ q,
+                                                      const bf16_t* __restrict__ kc,
+                                                      const bf16_t* __restrict__ vc,
+                                                      const int32_t* __restrict__ len,
+                                                      int max_len, int span,
+                                                      float* __restrict__ part, int nsplit) {
+  constexpr int HD = 128;
+  constexpr int PPW = 32 / NW;  // 1 KiB pieces per wave per tile
+  __shared__ __align__(16) uint4 KV[ST][2 * TILE * 16];
+  const int split = blockIdx.x, kvh = blockIdx.y;
+  const int G = hq / hkv;
+  const int NQ = M * G;
+  const int lane = threadIdx.x & 63;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int j = lane & 15, g = lane >> 4;
+  const int start = split * span;
+  const int end = min(max_len, start + span);
+  const int ntile = (end - start + TILE - 1) / TILE;  // >= 1: the grid covers max_len
+
+  // piece i (1 KiB) of a tile: rows 4 (i % 16) .. + 3 of K (i < 16) or V
+  const bf16_t* kb = kc + (size_t)kvh * n_max * HD;
+  const bf16_t* vb = vc + (size_t)kvh * n_max * HD;
+  auto issue = [&](int tile, int buf) {
+    const int t0 = start + tile * TILE;
+#pragma unroll
+    for (int u = 0; u < PPW; ++u) {
+      const int i = w * PPW + u;
+      const int rr = 4 * (i & 15) + (lane >> 4);
+      const int row = min(t0 + rr, max_len - 1);
+      const bf16_t* src =
+          (i < 16 ? kb : vb) + (size_t)row * HD + (((lane & 15) ^ (rr & 15)) << 3);
+      __builtin_amdgcn_global_load_lds((const void*)src,
+                                       (__attribute__((address_space(3))) void*)&KV[buf][i * 64],
+                                       16, 0, 0);
+    }
+  };
+#pragma unroll
+  for (int s = 0; s < ST - 1; ++s)
+    if (s < ntile) issue(s, s);
+
+  // query column j of this wave: vector qi = qb + 16 w + j
+  const int qi = blockIdx.z * NW * 16 + 16 * w + j;
+  const bool qok = qi < NQ;
+  const int lim = qok ? min(len[qi / G], end) : 0;  // keys of column j in this split
+  bf16x8_d qh[4], ql[4];
+  {
+    const int row = qok ? qi / G : 0;
+    const int h = kvh * G + (qok ? qi % G : 0);
+    const float* qv = q + ((size_t)row * hq + h) * HD + 8 * g;
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      float4 x0 = *(const float4*)(qv + 32 * ks), x1 = *(const float4*)(qv + 32 * ks + 4);
+      if (!qok) x0 = x1 = make_float4(0.f, 0.f, 0.f, 0.f);
+      const float xs[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const __bf16 hh = (__bf16)xs[e];
+        qh[ks][e] = hh;
+        ql[ks][e] = (__bf16)(xs[e] - (float)hh);
+      }
+    }
+  }
+  const float scale = 1.0f / sqrtf((float)HD);
+  f32x4_d o[8];
+#pragma unroll
+  for (int dt = 0; dt < 8; ++dt) o[dt] = f32x4_d{0.f, 0.f, 0.f, 0.f};
+  float m_run = -FLT_MAX, l_run = 0.f;
+  const int s4 = (lane & 15) >> 2, u4 = lane & 3;
+
+  for (int it = 0; it < ntile; ++it) {
+    // tile it has landed once at most ST - 2 later tiles are in flight; the
+    // barrier needs no fence (see k_gemm_tiled)
+    if (it + ST - 2 < ntile) __builtin_amdgcn_s_waitcnt(vmcnt_imm_a(PPW * (ST - 2)));
+    else __builtin_amdgcn_s_waitcnt(vmcnt_imm_a(0));
+    __builtin_amdgcn_s_barrier();
+    __asm__ volatile("" ::: "memory");
+    if (it + ST - 1 < ntile) issue(it + ST - 1, (it + ST - 1) % ST);
+    const uint4* Kt = &KV[it % ST][0];
+    const char* Vb = (const char*)&KV[it % ST][TILE * 16];
+    const int t0 = start + it * TILE;
+    f32x4_d sc[4];
+#pragma unroll
+    for (int kt = 0; kt < 4; ++kt) {
+      sc[kt] = f32x4_d{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) {
+        const int c = 4 * ks + g;
+        const bf16x8_d kf = __builtin_bit_cast(bf16x8_d, Kt[(16 * kt + j) * 16 + (c ^ j)]);
+        sc[kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qh[ks], sc[kt], 0, 0, 0);
+        sc[kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, ql[ks], sc[kt], 0, 0, 0);
+      }
+    }
+    float mt = -FLT_MAX;
+#pragma unroll
+    for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int key = t0 + 16 * kt + 4 * g + v;
+        sc[kt][v] = key < lim ? sc[kt][v] * scale : -FLT_MAX;
+        mt = fmaxf(mt, sc[kt][v]);
+      }
+    mt = fmaxf(mt, __shfl_xor(mt, 16));
+    mt = fmaxf(mt, __shfl_xor(mt, 32));
+    const float m_new = fmaxf(m_run, mt);
+    const float alpha = m_run == -FLT_MAX ? 0.f : __expf(m_run - m_new);
+    float ps = 0.f;
+#pragma unroll
+    for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int key = t0 + 16 * kt + 4 * g + v;
+        const float p = key < lim ? __expf(sc[kt][v] - m_new) : 0.f;
+        sc[kt][v] = p;
+        ps += p;
+      }
+    ps += __shfl_xor(ps, 16);
+    ps += __shfl_xor(ps, 32);
+    l_run = l_run * alpha + ps;
+    m_run = m_new;
+    // output rows are query columns 4 g + v: rescale by their alpha
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const float av = __shfl(alpha, 4 * g + v);
+#pragma unroll
+      for (int dt = 0; dt < 8; ++dt) o[dt][v] *= av;
+    }
+#pragma unroll
+    for (int k2 = 0; k2 < 2; ++k2) {
+      bf16x8_d pa;
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        pa[v] = (__bf16)sc[2 * k2][v];
+        pa[4 + v] = (__bf16)sc[2 * k2 + 1][v];
+      }
+#pragma unroll
+      for (int dt = 0; dt < 8; ++dt) {
+        bf16x4_d h2[2];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int row = 32 * k2 + 16 * h + 4 * g + s4;
+          const int c = 2 * dt + (u4 >> 1);
+          const char* pp = Vb + row * 256 + ((c ^ (row & 15)) << 4) + ((u4 & 1) << 3);
+          h2[h] = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+              (__attribute__((address_space(3))) bf16x4_d*)pp);
+        }
+        bf16x8_d vbv;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          vbv[e] = h2[0][e];
+          vbv[4 + e] = h2[1][e];
+        }
+        o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa, vbv, o[dt], 0, 0, 0);
+      }
+    }
+  }
+
+  // partials: O rows are query columns 4 g + v, dims 16 dt + j
+  const int qb = blockIdx.z * NW * 16 + 16 * w;
+#pragma unroll
+  for (int v = 0; v < 4; ++v) {
+    const int qv = qb + 4 * g + v;
+    const int lv = __shfl(lim, 4 * g + v);
+    if (qv >= NQ || lv <= start) continue;
+    const int row = qv / G, h = kvh * G + qv % G;
+    float* dst = part + (((size_t)row * hq + h) * nsplit + split) * (HD + 2);
+#pragma unroll
+    for (int dt = 0; dt < 8; ++dt) dst[16 * dt + j] = o[dt][v];
+  }
+  if (g == 0 && qok && lim > start) {
+    const int row = qi / G, h = kvh * G + qi % G;
+    float* dst = part + (((size_t)row * hq + h) * nsplit + split) * (HD + 2);
+    dst[HD] = m_run;
+    dst[HD + 1] = l_run;
+  }
+}
+
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
@@ -793,9 +994,10 @@ void attn_split(const AttnArgs& a, hipStream_t st) {
   } else if (a.hd == 128 && a.tiles > 1) {
     // batched rows: matrix-instruction kernel, 64 query vectors per workgroup
     const int span = TILE * a.tiles;
-    dim3 g2((a.max_len + span - 1) / span, a.hkv, (a.M * G + 63) / 64);
-    hipLaunchKernelGGL(k_attn_mfma<4>, g2, dim3(256), 0, st, a.M, a.hq, a.hkv, a.n_max, a.q,
-                       (const bf16_t*)a.kc, (const bf16_t*)a.vc, a.len, span, a.part, a.nsplit);
+    dim3 g2((a.max_len + span - 1) / span, a.hkv, (a.M * G + 16 * KS_BAT_NW - 1) / (16 * KS_BAT_NW));
+    hipLaunchKernelGGL((k_attn_bat<KS_BAT_NW, KS_BAT_ST>), g2, dim3(64 * KS_BAT_NW), 0, st, a.M,
+                       a.hq, a.hkv, a.n_max, a.q, (const bf16_t*)a.kc, (const bf16_t*)a.vc, a.len,
+                       a.max_len, span, a.part, a.nsplit);
   } else if (a.hd == 128) {
     if (nq <= 4) KS_ATTN(128, true, 1); else KS_ATTN(128, true, 8);
   } else {
