@@ -99,6 +99,136 @@ def cpu_baseline(cfg, ctx, budget_s):
                       f"{cfg.L} layers; {per_tok:.2f} s per sampled token"}
 
 
+def describe(cfg):
+    shape = {"llama8b": "Llama-3-8B-shaped decoder", "qwen8b": "Qwen3-8B-shaped decoder"}
+    return (f"{cfg.name}: {shape.get(cfg.name, 'decoder')} (L {cfg.L}, d {cfg.d}, "
+            f"{cfg.hq}/{cfg.hkv} heads of {cfg.hd}, ffn {cfg.ffn}, vocab {cfg.vocab})")
+
+
+def fill_cache(dm, cfg, n, seed=3):
+    """Seeded synthetic keys/values (std 1.28, like the random-init model's) at
+    positions < n of every layer, generated on the device."""
+    import torch
+    gen = torch.Generator(device="cuda")
+    for l in range(cfg.L):
+        gen.manual_seed(seed * 1000 + l)
+        kk, vv = dm.kv_layer(l)
+        for t in (kk, vv):
+            t[:, :n].copy_(torch.randn(cfg.hkv, n, cfg.hd, generator=gen, device="cuda") * 1.28)
+    torch.cuda.synchronize()
+
+
+def history_rounds(dm, cfg, gamma, tok, rounds=5):
+    """Full-model draft/verify rounds from the current state: every draft is the
+    target's own greedy token, so each round commits gamma + 1 rows of history.
+    Returns the committed token and the mean verify time (ms)."""
+    import numpy as np
+    import torch
+    full = np.ones(2 * cfg.L, dtype=bool)
+    s = tok
+    tv = []
+    for _ in range(rounds):
+        toks = [s]
+        for _ in range(gamma):
+            t, _ = dm.draft_step(full)
+            toks.append(t)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        pred, a = dm.verify(toks)
+        tv.append((time.perf_counter() - t0) * 1e3)
+        s = int(pred[a])
+    return s, sum(tv[1:]) / max(1, len(tv) - 1)
+
+
+def run_sweep(args, cfg):
+    """Context-length x draft-length grid on synthetic caches.  For each context:
+    per-sublayer latencies (masked decode steps); the latency model is fitted over
+    the whole grid; then for each draft length a knapsack selection, the draft and
+    verify rates of the selected mask, and speculative vs autoregressive decode of
+    the same tokens from the same state."""
+    import numpy as np
+    import torch
+    import workloads as W
+    from paper_2602_20217_amd.engine import DeviceModel, select_params
+    ctxs = [int(x) for x in args.sweep_ctx.split(",")]
+    gammas = [int(x) for x in args.sweep_gamma.split(",")]
+    n_new = args.sweep_new
+    n_max = max(ctxs) + n_new + 6 * (max(gammas) + 1) + 64
+    t = time.time()
+    dm = DeviceModel(cfg, n_max=n_max, gamma_max=max(8, max(gammas)), m_rounds=5, cap_max=256,
+                     prefill_chunk=512)
+    W.generate_weights(cfg, seed=0, consume=dm.upload)
+    dm.finalize()
+    log(f"weights generated and packed in {time.time() - t:.1f}s (n_max {n_max})")
+    tok = int(W.prompt_ids(cfg.vocab, 1, 1)[0])
+    L2 = 2 * cfg.L
+    none = np.zeros(L2, bool)
+    mlp = np.array([i % 2 == 1 for i in range(L2)])
+    lat = []
+    for n in ctxs:
+        fill_cache(dm, cfg, n)
+        dm.set_context(n, tok)
+        dm.profile_decode(None, 2, per_kernel=False)
+        t0 = dm.profile_decode(none, 6, per_kernel=False)["ms_step"]
+        tm = dm.profile_decode(mlp, 6, per_kernel=False)["ms_step"]
+        ta = dm.profile_decode(~mlp, 6, per_kernel=False)["ms_step"]
+        tf = dm.profile_decode(None, 6, per_kernel=False)["ms_step"]
+        lat.append({"n": n, "t_attn_ms": (ta - t0) / cfg.L, "t_mlp_ms": (tm - t0) / cfg.L,
+                    "t_head_ms": t0, "t_step_ms": tf})
+        log(f"ctx {n}: t_attn {lat[-1]['t_attn_ms'] * 1e3:.1f} us, t_mlp "
+            f"{lat[-1]['t_mlp_ms'] * 1e3:.1f} us, AR step {tf:.3f} ms")
+    c2, c3 = fit_line([r["n"] for r in lat], [r["t_attn_ms"] for r in lat])
+    c1 = float(np.mean([r["t_mlp_ms"] for r in lat]))
+    params = select_params((c1, c2, c3), "paper_min", 0, tau=0.5, prune_half=True, D=10)
+    points = []
+    for n, lr in zip(ctxs, lat):
+        fill_cache(dm, cfg, n)
+        for gamma in gammas:
+            # AR and speculative decode from the same state (same history rounds)
+            dm.set_context(n, tok)
+            s, _ = history_rounds(dm, cfg, gamma, tok)
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            out_ar, _, _ = dm.decode(n_new, 0)
+            torch.cuda.synchronize()
+            ar_ms = (time.perf_counter() - t0) * 1e3
+            # one selection per point, at the start (its cost grows with the
+            # context: reported apart as well)
+            dm.set_context(n, tok)
+            s, verify_ms = history_rounds(dm, cfg, gamma, tok)
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            out_sd, st, sels = dm.decode(n_new, gamma, n_new, params)
+            torch.cuda.synchronize()
+            sd_ms = (time.perf_counter() - t0) * 1e3
+            mask = np.array([bool(sels[0].exec[i]) for i in range(L2)])
+            draft_ms = dm.profile_decode(mask, 6, per_kernel=False)["ms_step"]
+            pt = {"ctx": n, "gamma": gamma, "t_attn_us": round(lr["t_attn_ms"] * 1e3, 2),
+                  "t_mlp_us": round(lr["t_mlp_ms"] * 1e3, 2),
+                  "draft_ms": round(draft_ms, 4), "draft_tok_s": round(1e3 / draft_ms, 1),
+                  "verify_ms": round(verify_ms, 4),
+                  "verify_tok_s": round((gamma + 1) * 1e3 / verify_ms, 1),
+                  "skipped_attn": int(sum(1 for i in range(0, L2, 2) if not mask[i])),
+                  "skipped_mlp": int(sum(1 for i in range(1, L2, 2) if not mask[i])),
+                  "ar_tok_s": round(n_new * 1e3 / ar_ms, 2),
+                  "spec_tok_s": round(n_new * 1e3 / sd_ms, 2),
+                  "speedup": round(ar_ms / sd_ms, 4),
+                  "speedup_excl_select": round(ar_ms / max(1e-9, sd_ms - st.ms_select), 4),
+                  "select_ms": round(st.ms_select, 1),
+                  "selections": st.n_selections,
+                  "alpha": round(st.n_accepted / max(1, st.n_drafted), 4),
+                  "tokens_equal_ar": bool(np.array_equal(out_ar, out_sd))}
+            points.append(pt)
+            log(json.dumps(pt))
+    res = {"mode": "sweep", "workload": f"{describe(cfg)}, bf16, synthetic caches (seeded, "
+                                        f"std 1.28) of each context length, {n_new} new tokens "
+                                        f"per point after 5 full-model draft/verify rounds of "
+                                        f"history, one knapsack selection per point",
+           "latency_model_ms": {"c1": c1, "c2": c2, "c3": c3, "points": lat}, "points": points}
+    dm.close()
+    print(json.dumps(res), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -114,6 +244,12 @@ def main():
     ap.add_argument("--profile-kernels", action="store_true",
                     help="short run for hardware counters: prefill, 16 decode steps and a "
                          "256 MiB device copy (the reference for counter scaling)")
+    ap.add_argument("--sweep", action="store_true",
+                    help="context x draft-length grid (synthetic caches): per-sublayer "
+                         "latencies, draft/verify rates and speedup over AR at each point")
+    ap.add_argument("--sweep-ctx", default="1024,4096,16384,65536,131072")
+    ap.add_argument("--sweep-gamma", default="2,4,8")
+    ap.add_argument("--sweep-new", type=int, default=64)
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path "
@@ -127,6 +263,8 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     cfg = W.config(args.model)
+    if args.sweep:
+        return run_sweep(args, cfg)
     n_max = args.ctx + args.new + 64
     t = time.time()
     dm = DeviceModel(cfg, n_max=n_max, gamma_max=max(8, args.gamma), m_rounds=5, cap_max=256,
@@ -213,7 +351,7 @@ def main():
         "warmup": args.warmup, "ms_per_step": round(mean_ssd, 2), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic (seeded random-init weights, random-id prompt)",
-        "config": {"workload": f"{args.model}: Llama-3-8B-shaped decoder, bf16 weights and KV, "
+        "config": {"workload": f"{describe(cfg)}, bf16 weights and KV, "
                                f"{args.ctx}-token random prompt, {args.new} new tokens, "
                                f"gamma {args.gamma}, mask re-selected every {args.reselect} tokens",
                    "global_batch": 1, "seq_len": args.ctx, "new_tokens": args.new,

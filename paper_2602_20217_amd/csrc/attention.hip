@@ -242,26 +242,30 @@ typedef uint32_t u32x4_d __attribute__((ext_vector_type(4)));
 
 typedef __attribute__((__vector_size__(4 * sizeof(__bf16)))) __bf16 bf16x4_d;
 
-// Decode / verify rows of bf16 caches with head dim 128 and at most 4 query
-// heads per kv head, all products on matrix instructions.  A workgroup of S
-// waves owns S consecutive 64-key tiles of one kv head and one row; wave w owns
-// tile w for every query head of the kv head.  The wave requests its 32 KiB of
-// keys and values with direct global-to-LDS loads (no staging registers) next
-// to its query loads, so it waits for one memory round trip.  Rows are stored
-// unpadded with 16-byte chunk c of row r at slot c ^ (r % 16).
+// Decode / verify rows of bf16 caches with head dim 128, all products on
+// matrix instructions.  A workgroup of S waves owns S consecutive 64-key tiles
+// of one kv head and RB = 16 / G consecutive rows: its 16 query columns are
+// j = row * G + g (row < RB, G query heads per kv head), so the rows of a
+// verify pass share every key/value load.  Wave w owns tile w.  The wave
+// requests its 32 KiB of keys and values with direct global-to-LDS loads (no
+// staging registers) next to its query loads, so it waits for one memory round
+// trip.  Rows are stored unpadded with 16-byte chunk c of row r at slot
+// c ^ (r % 16).
 //  scores  S^T = K Q^T, keys as rows of 16x16x32 products (queries as hi + lo
-//          bf16 columns, columns >= G zero): lane (j, g) holds keys 16 kt + 4 g
-//          + v of query j, so the tile max and sum need two cross-lane steps;
+//          bf16 columns): lane (j, g) holds keys 16 kt + 4 g + v of column j,
+//          so the tile max and sum need two cross-lane steps; a column only
+//          counts keys below its row's length;
 //  values  O = P V with the probabilities (bf16) taken from the score registers
 //          as the A operand: k slot e of lane group g is key 4 g + e (e < 4) or
 //          16 + 4 g + e - 4 (e >= 4) of a 32-key step.  The V operand in that
 //          key order comes from transposing LDS reads (a 16-lane group turns
 //          16 8-byte row pieces into 4 keys x 16 dims).  Rows at or past the
-//          row length are zeroed in LDS first (probability 0 must not meet a
-//          non-finite stale value).
+//          longest length of the workgroup are zeroed in LDS first
+//          (probability 0 must not meet a non-finite stale value).
 // The S tile results are merged in tile order into the split's partial (o,
-// max, sum), the layout k_attn_combine reads.  Every quantity of a row depends
-// only on that row.
+// max, sum) per query column, the layout k_attn_combine reads.  A column's
+// arithmetic does not depend on the other columns, so a verify row and the
+// decode step at the same position give the same bits.
 template <int S>
 __global__ __launch_bounds__(64 * S) void k_attn_dec(int M, int hq, int hkv, int n_max,
                                                      const float* __restrict__ q,
@@ -270,13 +274,17 @@ __global__ __launch_bounds__(64 * S) void k_attn_dec(int M, int hq, int hkv, int
                                                      const int32_t* __restrict__ len,
                                                      float* __restrict__ part, int nsplit) {
   constexpr int HD = 128;
-  constexpr int MGS = 4 * (HD + 2);  // merge record: 4 queries
+  constexpr int MGS = 16 * (HD + 2);  // merge record: 16 columns
+  static_assert(MGS * 4 <= TILE * 256, "merge record fits a key tile");
   __shared__ __align__(16) uint4 KV[S][2 * TILE * 16];  // per wave: K tile, then V tile
-  const int split = blockIdx.x, kvh = blockIdx.y, r = blockIdx.z;
+  const int split = blockIdx.x, kvh = blockIdx.y;
   const int G = hq / hkv;
+  const int RB = 16 / G;
+  const int r0 = blockIdx.z * RB;
   const int lane = threadIdx.x & 63;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int t0 = (split * S + w) * TILE;
+  const int start = split * S * TILE;
+  const int t0 = start + w * TILE;
   uint4* KVw = &KV[w][0];
 
   // piece i (1 KiB): rows 4 (i % 16) .. + 3 of K (i < 16) or V; lane l writes
@@ -295,17 +303,18 @@ __global__ __launch_bounds__(64 * S) void k_attn_dec(int M, int hq, int hkv, int
                                        0, 0);
     }
   }
-  // query fragments: column j = lane % 16 (query head kvh G + j), dims
+  // query column j = lane % 16: row r0 + j / G, head kvh G + j % G, dims
   // 32 ks + 8 g .. + 7 (g = lane / 16), as hi + lo bf16
   const int j = lane & 15, g = lane >> 4;
+  const int rj = r0 + j / G;
+  const bool qok = rj < M;
   bf16x8_d qh[4], ql[4];
   {
-    const bool ok = j < G;
-    const float* qv = q + ((size_t)r * hq + kvh * G + (ok ? j : 0)) * HD + 8 * g;
+    const float* qv = q + ((size_t)(qok ? rj : r0) * hq + kvh * G + j % G) * HD + 8 * g;
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
       float4 x0 = *(const float4*)(qv + 32 * ks), x1 = *(const float4*)(qv + 32 * ks + 4);
-      if (!ok) x0 = x1 = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (!qok) x0 = x1 = make_float4(0.f, 0.f, 0.f, 0.f);
       const float xs[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
@@ -315,8 +324,11 @@ __global__ __launch_bounds__(64 * S) void k_attn_dec(int M, int hq, int hkv, int
       }
     }
   }
-  const int L = len[r];
-  const int cnt = min(TILE, L - t0);  // keys of this tile (may be <= 0)
+  const int Lj = qok ? len[rj] : 0;  // this column's row length
+  int Lmax = 0;                      // longest row of the workgroup
+  for (int r = r0; r < min(M, r0 + RB); ++r) Lmax = max(Lmax, len[r]);
+  const int cnt = min(TILE, Lmax - t0);  // keys of this tile any column uses (may be <= 0)
+  const int cj = min(TILE, Lj - t0);     // keys of this tile column j uses
   __builtin_amdgcn_s_waitcnt(0);
 
   float m = -FLT_MAX, l = 0.f;
@@ -329,7 +341,7 @@ __global__ __launch_bounds__(64 * S) void k_attn_dec(int M, int hq, int hkv, int
     if (cnt < TILE) {
       for (int c = cnt * 16 + lane; c < TILE * 16; c += 64) Vt[c] = make_uint4(0u, 0u, 0u, 0u);
     }
-    // S^T: sc[kt][v] = score(key 16 kt + 4 g + v, query j)
+    // S^T: sc[kt][v] = score(key 16 kt + 4 g + v, query column j)
     f32x4_d sc[4];
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt) {
@@ -348,7 +360,7 @@ __global__ __launch_bounds__(64 * S) void k_attn_dec(int M, int hq, int hkv, int
     for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
-        sc[kt][v] = 16 * kt + 4 * g + v < cnt ? sc[kt][v] * scale : -FLT_MAX;
+        sc[kt][v] = 16 * kt + 4 * g + v < cj ? sc[kt][v] * scale : -FLT_MAX;
         mt = fmaxf(mt, sc[kt][v]);
       }
     mt = fmaxf(mt, __shfl_xor(mt, 16));
@@ -358,7 +370,7 @@ __global__ __launch_bounds__(64 * S) void k_attn_dec(int M, int hq, int hkv, int
     for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
-        const float p = 16 * kt + 4 * g + v < cnt ? __expf(sc[kt][v] - mt) : 0.f;
+        const float p = 16 * kt + 4 * g + v < cj ? __expf(sc[kt][v] - mt) : 0.f;
         sc[kt][v] = p;
         ps += p;
       }
@@ -399,63 +411,65 @@ __global__ __launch_bounds__(64 * S) void k_attn_dec(int M, int hq, int hkv, int
       }
     }
   }
-  // o[dt][v]: query 4 g + v, dim 16 dt + j (valid in lanes g == 0); the max and
-  // sum of query a live in lane a
-  const float ma[4] = {__shfl(m, 0), __shfl(m, 1), __shfl(m, 2), __shfl(m, 3)};
-  const float la[4] = {__shfl(l, 0), __shfl(l, 1), __shfl(l, 2), __shfl(l, 3)};
+  // o[dt][v]: column 4 g + v, dim 16 dt + j; the max and sum of column c live
+  // in lane c
+  float mv[4], lv[4];
+  int Lv[4];
+#pragma unroll
+  for (int v = 0; v < 4; ++v) {
+    mv[v] = __shfl(m, 4 * g + v);
+    lv[v] = __shfl(l, 4 * g + v);
+    Lv[v] = __shfl(Lj, 4 * g + v);
+  }
   if (S > 1) {
     __syncthreads();  // every wave is done with its tiles
     float* rec = (float*)KVw;
-    if (g == 0) {
 #pragma unroll
-      for (int a = 0; a < 4; ++a) {
+    for (int v = 0; v < 4; ++v) {
+      float* rc = rec + (4 * g + v) * (HD + 2);
 #pragma unroll
-        for (int dt = 0; dt < 8; ++dt) rec[a * (HD + 2) + 16 * dt + j] = o[dt][a];
-        if (j == 0) {
-          rec[a * (HD + 2) + HD] = ma[a];
-          rec[a * (HD + 2) + HD + 1] = la[a];
-        }
+      for (int dt = 0; dt < 8; ++dt) rc[16 * dt + j] = o[dt][v];
+      if (j == 0) {
+        rc[HD] = mv[v];
+        rc[HD + 1] = lv[v];
       }
     }
     __syncthreads();
-    if (w != 0 || g != 0 || split * S * TILE >= L) return;
+    if (w != 0) return;
 #pragma unroll
-    for (int a = 0; a < 4; ++a) {
-      if (a >= G) break;
+    for (int v = 0; v < 4; ++v) {
+      const int col = 4 * g + v;
       float mx = -FLT_MAX;
 #pragma unroll
-      for (int s = 0; s < S; ++s) mx = fmaxf(mx, ((const float*)&KV[s][0])[a * (HD + 2) + HD]);
-      float lx = 0.f, ox[8];
+      for (int s = 0; s < S; ++s)
+        mx = fmaxf(mx, ((const float*)&KV[s][0])[col * (HD + 2) + HD]);
+      float lx = 0.f;
 #pragma unroll
-      for (int dt = 0; dt < 8; ++dt) ox[dt] = 0.f;
+      for (int dt = 0; dt < 8; ++dt) o[dt][v] = 0.f;
 #pragma unroll
       for (int s = 0; s < S; ++s) {
-        const float* rs = (const float*)&KV[s][0] + a * (HD + 2);
+        const float* rs = (const float*)&KV[s][0] + col * (HD + 2);
         const float wt = rs[HD] == -FLT_MAX ? 0.f : __expf(rs[HD] - mx);
         lx = fmaf(rs[HD + 1], wt, lx);
 #pragma unroll
-        for (int dt = 0; dt < 8; ++dt) ox[dt] = fmaf(rs[16 * dt + j], wt, ox[dt]);
+        for (int dt = 0; dt < 8; ++dt) o[dt][v] = fmaf(rs[16 * dt + j], wt, o[dt][v]);
       }
-      float* dst = part + (((size_t)r * hq + kvh * G + a) * nsplit + split) * (HD + 2);
-#pragma unroll
-      for (int dt = 0; dt < 8; ++dt) dst[16 * dt + j] = ox[dt];
-      if (j == 0) {
-        dst[HD] = mx;
-        dst[HD + 1] = lx;
-      }
+      mv[v] = mx;
+      lv[v] = lx;
     }
-    return;
   }
-  if (g != 0 || t0 >= L) return;
+  // write the split's partial of every column whose row reaches this split
 #pragma unroll
-  for (int a = 0; a < 4; ++a) {
-    if (a >= G) break;
-    float* dst = part + (((size_t)r * hq + kvh * G + a) * nsplit + split) * (HD + 2);
+  for (int v = 0; v < 4; ++v) {
+    const int col = 4 * g + v;
+    const int rc = r0 + col / G;
+    if (rc >= M || Lv[v] <= start) continue;
+    float* dst = part + (((size_t)rc * hq + kvh * G + col % G) * nsplit + split) * (HD + 2);
 #pragma unroll
-    for (int dt = 0; dt < 8; ++dt) dst[16 * dt + j] = o[dt][a];
+    for (int dt = 0; dt < 8; ++dt) dst[16 * dt + j] = o[dt][v];
     if (j == 0) {
-      dst[HD] = ma[a];
-      dst[HD + 1] = la[a];
+      dst[HD] = mv[v];
+      dst[HD + 1] = lv[v];
     }
   }
 }
@@ -975,9 +989,10 @@ void attn_split(const AttnArgs& a, hipStream_t st) {
   hipLaunchKernelGGL((k_attn_split<HDV, BFV, QM>), grid, dim3(256), 0, st, a.M, a.hq, a.hkv, \
                      a.n_max, a.q, a.kc, a.vc, a.len, a.tiles, a.rows_per_block, a.part,     \
                      a.nsplit)
-  if (a.hd == 128 && G <= 4 && a.rows_per_block == 1 && a.tiles >= 1 && a.tiles <= 5) {
-    // decode / verify rows
-    dim3 g3(ns, a.hkv, a.M);
+  if (a.hd == 128 && G <= 16 && 16 % G == 0 && a.rows_per_block == 1 && a.tiles >= 1 &&
+      a.tiles <= 5) {
+    // decode / verify rows, 16 / G rows per workgroup
+    dim3 g3(ns, a.hkv, (a.M + 16 / G - 1) / (16 / G));
     const bf16_t* kc = (const bf16_t*)a.kc;
     const bf16_t* vc = (const bf16_t*)a.vc;
 #define KS_DEC(S_)                                                                                \
