@@ -1,0 +1,134 @@
+"""Parity at the full Llama-3-8B shape (bf16, 8K context), in the launch
+configuration the benchmark times (skinny products, 5-tile attention splits).
+
+Sampled outputs the oracle computes one by one: single sublayers (first and last
+layer) on decode (1 row) and verify (5 rows) inputs over a seeded 8K cache, and
+the LM head on two rows; tolerance 2e-2 relative.  Properties that hold at any
+size: full-model drafts are accepted by the verify pass at the same positions,
+and speculative generation (with knapsack selections) emits exactly the
+autoregressive tokens after a real 8K prefill.  Every call goes through the C
+ABI."""
+import dataclasses
+
+import numpy as np
+import pytest
+
+import workloads as W
+from oracle import model as M
+from tests.gpu_helpers import rel_err, margin
+
+pytestmark = pytest.mark.gpu
+torch = pytest.importorskip("torch")
+
+TOL = 2e-2
+CTX = 8192
+LAYERS = (0, 31)
+
+
+@pytest.fixture(scope="module")
+def full():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2602_20217_amd.engine import DeviceModel
+    cfg = W.config("llama8b")
+    print("\n[setup] llama8b weights", flush=True)
+    dm = DeviceModel(cfg, n_max=CTX + 320, gamma_max=8, m_rounds=5, cap_max=256,
+                     prefill_chunk=512)
+    W.generate_weights(cfg, seed=0, consume=dm.upload)
+    dm.finalize()
+    yield cfg, dm
+    dm.close()
+
+
+def _one_layer(cfg, layer):
+    """Oracle model holding layer `layer` of the 8B weights as its only layer."""
+    c1 = dataclasses.replace(cfg, L=1)
+    w = {("embed", -1): np.zeros((16, cfg.d), np.float32),
+         ("lm_head", -1): np.zeros((16, cfg.d), np.float32)}
+    for k in ("wq", "wk", "wv", "wo", "w_gate", "w_up", "w_down"):
+        w[(k, 0)] = W.weight_tensor(cfg, 0, k, layer)
+    return M.Model(c1, w)
+
+
+def _fill(cfg, dm, layer, n):
+    """Seeded keys/values of one layer at positions < n, on the device and in a
+    one-layer oracle cache."""
+    K, V = W.synthetic_kv(cfg, n, seed=3, layer=layer)
+    kk, vv = dm.kv_layer(layer)
+    kk[:, :n] = torch.from_numpy(K).to(torch.bfloat16).cuda()
+    vv[:, :n] = torch.from_numpy(V).to(torch.bfloat16).cuda()
+    torch.cuda.synchronize()
+    cache = M.KVCache(dataclasses.replace(cfg, L=1), CTX + 320)
+    cache.K[0][:, :n] = K
+    cache.V[0][:, :n] = V
+    return cache
+
+
+@pytest.mark.parametrize("layer", LAYERS)
+@pytest.mark.parametrize("R", [1, 5])
+def test_full_size_sublayers(full, layer, R):
+    cfg, dm = full
+    n = CTX - 3  # ragged against the 320-position splits
+    model = _one_layer(cfg, layer)
+    cache = _fill(cfg, dm, layer, n)
+    dm.set_context(n, 0)
+    pos = np.arange(R) + n
+    x = W.synthetic_rows(R, cfg.d, seed=4, std=1.0, index=100 + R + layer)
+    for sub in (1, 2):  # attention, then MLP of the layer
+        i = 2 * layer + sub
+        out = torch.empty(R, cfg.d, device="cuda")
+        dm.sublayer_apply(i, torch.from_numpy(x).cuda(), pos, mode=0, out=out)
+        ref = M.sublayer(model, sub, x.astype(np.float64), pos, cache, mode="write")
+        got = out.cpu().numpy()
+        print(f"[full] layer {layer} sublayer {sub} R {R}: rel err {rel_err(got, ref):.2e}",
+              flush=True)
+        assert rel_err(got, ref) < TOL, (layer, sub, R, rel_err(got, ref))
+        x = got
+
+
+def test_full_size_head(full):
+    cfg, dm = full
+    x = W.synthetic_rows(2, cfg.d, seed=4, std=1.0, index=500)
+    logits, am, top1 = dm.head_rows(torch.from_numpy(x).cuda())
+    lm = W.weight_tensor(cfg, 0, "lm_head").astype(np.float64)
+    h = M.rmsnorm(x.astype(np.float64), np.ones(cfg.d), cfg.eps)
+    ref = h @ lm.T
+    assert rel_err(logits.cpu().numpy(), ref) < TOL
+    am = am.cpu().numpy()
+    for r in range(2):
+        if margin(ref[r]) > TOL * np.max(np.abs(ref[r])):
+            assert am[r] == int(np.argmax(ref[r]))
+
+
+def test_full_size_decode_equals_verify(full):
+    cfg, dm = full
+    n = CTX - 100
+    for l in LAYERS:
+        _fill(cfg, dm, l, n)
+    dm.set_context(n, 7)
+    all_on = np.ones(2 * cfg.L, dtype=bool)
+    drafts = [7]
+    for _ in range(4):
+        t, _ = dm.draft_step(all_on)
+        drafts.append(t)
+    pred, a = dm.verify(drafts)
+    assert a == 4 and list(pred[:4]) == drafts[1:]
+
+
+def test_full_size_speculative_equals_ar(full):
+    from paper_2602_20217_amd.engine import select_params
+    cfg, dm = full
+    prompt = W.prompt_ids(cfg.vocab, CTX, 1)
+    dm.prefill(prompt)
+    ar, _, _ = dm.decode(40, 0)
+    dm.prefill(prompt)
+    params = select_params((0.074, 1.2e-6, 0.035), "paper_min", 0, tau=0.5, prune_half=True,
+                           D=10)
+    sd, st, sels = dm.decode(40, 4, 32, params)
+    assert np.array_equal(ar, sd)
+    assert st.n_selections >= 1
+    for s in sels:
+        skipped_w = sum(s.w_attn if i % 2 == 0 else s.w_mlp
+                        for i in range(2 * cfg.L) if not s.exec[i])
+        assert skipped_w == s.j_star and 0 <= s.j_star <= s.C // 2
+        assert 1 <= s.gamma_star <= 10 and 0.0 <= s.alpha_hat <= 1.0
