@@ -59,7 +59,8 @@ size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct Layout {
   size_t rope, x, a1hi, a1lo, a2hi, a2lo, qkv, q, kvself, part, logits, am, top1;
-  size_t tok, pos, len, stage, hist, xh, g0, g1, ge, dpos, dlen, sig, ptrs, ssq, gpart, total;
+  size_t tok, pos, len, stage, hist, xh, g0, g1, ge, dpos, dlen, sig, ptrs, ssq, gpart;
+  size_t dpc, dpn, dpmean, dpidx, dpbits, dpreach, dpse, dpss, total;
   int FR, RING, cells, DR, XR, LR, nqkv, a2w, part_rows;
   size_t part_elems;
 };
@@ -114,6 +115,16 @@ Layout make_layout(const ks_model_desc& d, const ks_limits& lim) {
   y.ptrs = take((size_t)4 * (y.cells + 2 * d.L + 2) * 8);
   y.ssq = take((size_t)16 * (d.d / 16) * 4);
   y.gpart = take(GPART_BYTES);
+  // model-mode DP state on the device: two cell lists + counts, cell means,
+  // budget index, and per-(stage, budget) bits / reach / cosines
+  y.dpc = take((size_t)2 * y.cells * 4);
+  y.dpn = take(64);
+  y.dpmean = take((size_t)2 * y.cells * 8);
+  y.dpidx = take((size_t)y.cells * 4);
+  y.dpbits = take((size_t)(2 * d.L + 1) * y.cells);
+  y.dpreach = take((size_t)(2 * d.L + 1) * y.cells);
+  y.dpse = take((size_t)(2 * d.L + 1) * y.cells * 8);
+  y.dpss = take((size_t)(2 * d.L + 1) * y.cells * 8);
   y.total = o;
   return y;
 }
@@ -776,83 +787,79 @@ static ks_status select_internal(ks_ctx* c, const ks_select_params* p, ks_select
   float** ptr_dst = (float**)(ptr_src + c->y.cells + 2);
   const size_t cell = (size_t)r * d.d;
   HIPCHK(hipMemcpyAsync(gprev, X(0), cell * 4, hipMemcpyDeviceToDevice, c->st));
-  std::vector<int> cells = {0};       // reachable budgets, ascending
-  std::vector<int> idx(J + 1, -1);    // budget -> compact index
+  // Stage 1 runs on the device stage after stage (k_dp_step), without host
+  // round trips.  Each stage is launched for a bound on the reachable budgets:
+  // every budget is at most min(J, sum of the weights so far); rows of
+  // budgets outside the current list hold stale states that are never scored.
+  const int S_ = c->y.cells;
+  int* dcells = c->at<int>(c->y.dpc);
+  int* dcnt = c->at<int>(c->y.dpn);
+  uint8_t* dbits = c->at<uint8_t>(c->y.dpbits);
+  set_i32(dcells, 0, c->st);  // stage 0: the single budget 0
+  set_i32(dcnt, 1, c->st);
+  int bound = 1, cum = 0;
+  for (int i = 1; i <= L2; ++i) {
+    const int w = (i % 2 == 1) ? wa : wm;
+    const int M = bound * r;
+    // execute candidates for every (possibly) reachable budget
+    sublayer_rows(c, i, gprev, E, M, dpos, dlen, n, 1, true);
+    // per-row cosines of both candidates against X^(i)
+    cos_rows(E, X(i), M, r, d.d, sig, c->st);
+    cos_rows(gprev, X(i), M, r, d.d, sig + M, c->st);
+    cum += w;
+    const int bound_out = std::min(J, cum) + 1;
+    DpStepArgs da{i, J, w, (double)p->tau, r, M, S_, sig,
+                  dcells + ((i - 1) & 1) * S_, dcnt + ((i - 1) & 1),
+                  dcells + (i & 1) * S_, dcnt + (i & 1),
+                  c->at<double>(c->y.dpmean), c->at<int>(c->y.dpidx), dbits,
+                  c->at<uint8_t>(c->y.dpreach), c->at<double>(c->y.dpse),
+                  c->at<double>(c->y.dpss), E, gprev, gnext, X(i), cell, ptr_src, ptr_dst,
+                  bound_out};
+    dp_step(da, c->st);
+    copy_rows(ptr_src, ptr_dst, bound_out, (int)cell, c->st);
+    HIPCHK(hipGetLastError());
+    std::swap(gprev, gnext);
+    bound = bound_out;
+  }
+  // terminal list, decision bits (and the debug record) back to the host
+  int nc_h = 0;
+  HIPCHK(hipMemcpyAsync(&nc_h, dcnt + (L2 & 1), 4, hipMemcpyDeviceToHost, c->st));
+  std::vector<int> cells(S_);
+  HIPCHK(hipMemcpyAsync(cells.data(), dcells + (L2 & 1) * S_, (size_t)S_ * 4,
+                        hipMemcpyDeviceToHost, c->st));
+  std::vector<uint8_t> bits_s((size_t)(L2 + 1) * S_);
+  HIPCHK(hipMemcpyAsync(bits_s.data(), dbits, bits_s.size(), hipMemcpyDeviceToHost, c->st));
+  std::vector<uint8_t> reach_s;
+  std::vector<double> se_s, ss_s;
+  if (dbg) {
+    reach_s.resize(bits_s.size());
+    se_s.resize(bits_s.size());
+    ss_s.resize(bits_s.size());
+    HIPCHK(hipMemcpyAsync(reach_s.data(), c->at<uint8_t>(c->y.dpreach), reach_s.size(),
+                          hipMemcpyDeviceToHost, c->st));
+    HIPCHK(hipMemcpyAsync(se_s.data(), c->at<double>(c->y.dpse), se_s.size() * 8,
+                          hipMemcpyDeviceToHost, c->st));
+    HIPCHK(hipMemcpyAsync(ss_s.data(), c->at<double>(c->y.dpss), ss_s.size() * 8,
+                          hipMemcpyDeviceToHost, c->st));
+  }
+  HIPCHK(hipStreamSynchronize(c->st));
+  cells.resize(nc_h);
   std::vector<uint8_t> bits((size_t)(L2 + 1) * (J + 1), 0);
-  std::vector<double> se(J + 1), ss(J + 1);
-  std::vector<const float*> hs;
-  std::vector<float*> hd;
-  std::vector<double> hrow(2 * (size_t)c->y.DR), hsig(2 * (size_t)c->y.cells);
+  for (int i = 1; i <= L2; ++i)
+    for (int j = 0; j <= J; ++j) bits[(size_t)i * (J + 1) + j] = bits_s[(size_t)i * S_ + j];
   if (dbg) {
     for (int j = 0; j < dbg->J_cap; ++j) dbg->n_match[j] = -1;
+    const double qnan = std::numeric_limits<double>::quiet_NaN();
     for (int i = 0; i <= L2; ++i)
       for (int j = 0; j < dbg->J_cap; ++j) {
         const size_t o = (size_t)i * dbg->J_cap + j;
-        dbg->bits[o] = 0;
-        dbg->reach[o] = (i == 0 && j == 0);
-        dbg->sig_e[o] = std::numeric_limits<double>::quiet_NaN();
-        dbg->sig_s[o] = std::numeric_limits<double>::quiet_NaN();
+        const bool in = i >= 1 && j <= J;
+        const size_t q = (size_t)i * S_ + j;
+        dbg->bits[o] = in ? bits_s[q] : 0;
+        dbg->reach[o] = in ? reach_s[q] : (i == 0 && j == 0);
+        dbg->sig_e[o] = in ? se_s[q] : qnan;
+        dbg->sig_s[o] = in ? ss_s[q] : qnan;
       }
-  }
-  for (int i = 1; i <= L2; ++i) {
-    const int w = (i % 2 == 1) ? wa : wm;
-    const int nc = (int)cells.size();
-    const int M = nc * r;
-    // execute candidates for every reachable budget
-    sublayer_rows(c, i, gprev, E, M, dpos, dlen, n, 1, true);
-    // per-row cosines of both candidates against X^(i); the matrix cosine of
-    // Section 2 (mean over the r rows) is taken here, in row order
-    cos_rows(E, X(i), M, r, d.d, sig, c->st);
-    cos_rows(gprev, X(i), M, r, d.d, sig + M, c->st);
-    HIPCHK(hipGetLastError());
-    HIPCHK(hipMemcpyAsync(hrow.data(), sig, 2 * (size_t)M * 8, hipMemcpyDeviceToHost, c->st));
-    HIPCHK(hipStreamSynchronize(c->st));
-    for (int k = 0; k < 2 * nc; ++k) {
-      double sum = 0.0;
-      for (int t = 0; t < r; ++t) sum += hrow[(size_t)k * r + t];
-      hsig[k < nc ? k : c->y.cells + k - nc] = sum / r;
-    }
-    std::fill(idx.begin(), idx.end(), -1);
-    for (int k = 0; k < nc; ++k) idx[cells[k]] = k;
-    std::vector<int> ncells;
-    hs.clear();
-    hd.clear();
-    for (int j = 0; j <= J; ++j) {
-      const int ie = idx[j];
-      const int is = j >= w ? idx[j - w] : -1;
-      const double sge = ie >= 0 ? hsig[ie] : std::numeric_limits<double>::quiet_NaN();
-      const double sgs = is >= 0 ? hsig[c->y.cells + is] : std::numeric_limits<double>::quiet_NaN();
-      const bool e_ok = ie >= 0 && sge > (double)p->tau;
-      const bool s_ok = is >= 0 && sgs > (double)p->tau;
-      const float* src = nullptr;
-      uint8_t bit = 0;
-      if (j == 0) {
-        src = X(i);  // g[i, 0] = X^(i)
-      } else if (e_ok && (!s_ok || sge >= sgs)) {
-        src = E + (size_t)ie * cell;
-      } else if (s_ok) {
-        src = gprev + (size_t)is * cell;
-        bit = 1;
-      }
-      if (dbg) {
-        const size_t o = (size_t)i * dbg->J_cap + j;
-        dbg->sig_e[o] = sge;
-        dbg->sig_s[o] = sgs;
-        dbg->bits[o] = bit;
-        dbg->reach[o] = src != nullptr;
-      }
-      bits[(size_t)i * (J + 1) + j] = bit;
-      if (src) {
-        hd.push_back(gnext + (size_t)ncells.size() * cell);
-        hs.push_back(src);
-        ncells.push_back(j);
-      }
-    }
-    HIPCHK(hipMemcpyAsync(ptr_src, hs.data(), hs.size() * 8, hipMemcpyHostToDevice, c->st));
-    HIPCHK(hipMemcpyAsync(ptr_dst, hd.data(), hd.size() * 8, hipMemcpyHostToDevice, c->st));
-    copy_rows(ptr_src, ptr_dst, (int)hs.size(), (int)cell, c->st);
-    std::swap(gprev, gnext);
-    cells.swap(ncells);
   }
   // stage 2: argmax rows of terminal states and of X^(2L)
   const int nc = (int)cells.size();

@@ -185,4 +185,77 @@ void knapsack_select(const int32_t* best, const uint64_t* bits, const int32_t* w
                      g_star, tpt, skip);
 }
 
+// ------------------------------------------------------- model-mode step
+// One stage i of the model-mode DP (Section 3.4, Eq. dp_main, pull form), on
+// the device so the stages run without host round trips.  Inputs: the per-row
+// cosines of the executed candidates E (sig[0, M)) and of the skip candidates
+// g[i-1, .] (sig[M, 2M)) against X^(i), M = (bound cells) * r rows, for the
+// reachable budgets cells_in[0..cnt_in) (ascending).  The matrix cosine of a
+// cell is the row mean, summed in row order.  For every budget j <= J: j = 0
+// takes X^(i); otherwise the executed candidate if its cosine exceeds tau and
+// is at least the skip candidate's (ties execute), else the skip candidate
+// g[i-1, j - w] if its cosine exceeds tau (decision bit 1), else j is
+// unreachable.  Writes the decision bits, the debug record (cosines, reach) of
+// row i, the next reachable list and the row-gather table (null beyond the
+// list, up to `bound_out` entries).
+__global__ __launch_bounds__(256) void k_dp_step(
+    int i, int J, int w, double tau, int r, int M, int stride, const double* __restrict__ sig,
+    const int* __restrict__ cells_in, const int* __restrict__ cnt_in, int* cells_out,
+    int* cnt_out, double* mean, int* idx, uint8_t* bits, uint8_t* reach, double* sig_e,
+    double* sig_s, const float* E, const float* gprev, float* gnext, const float* Xi,
+    size_t cell, const float** ptr_src, float** ptr_dst, int bound_out) {
+  const int nc = *cnt_in;
+  for (int k = threadIdx.x; k < 2 * nc; k += blockDim.x) {
+    const double* srow = sig + (k < nc ? 0 : M) + (size_t)(k < nc ? k : k - nc) * r;
+    double sum = 0.0;
+    for (int t = 0; t < r; ++t) sum += srow[t];
+    mean[k] = sum / r;
+  }
+  for (int j = threadIdx.x; j <= J; j += blockDim.x) idx[j] = -1;
+  __syncthreads();
+  for (int k = threadIdx.x; k < nc; k += blockDim.x) idx[cells_in[k]] = k;
+  __syncthreads();
+  if (threadIdx.x != 0) return;
+  const double qnan = __longlong_as_double(0x7FF8000000000000ll);
+  int cnt = 0;
+  for (int j = 0; j <= J; ++j) {
+    const int ie = idx[j];
+    const int is = j >= w ? idx[j - w] : -1;
+    const double sge = ie >= 0 ? mean[ie] : qnan;
+    const double sgs = is >= 0 ? mean[nc + is] : qnan;
+    const bool e_ok = ie >= 0 && sge > tau;
+    const bool s_ok = is >= 0 && sgs > tau;
+    const float* src = nullptr;
+    uint8_t bit = 0;
+    if (j == 0) {
+      src = Xi;
+    } else if (e_ok && (!s_ok || sge >= sgs)) {
+      src = E + (size_t)ie * cell;
+    } else if (s_ok) {
+      src = gprev + (size_t)is * cell;
+      bit = 1;
+    }
+    const size_t o = (size_t)i * stride + j;
+    bits[o] = bit;
+    reach[o] = src != nullptr;
+    sig_e[o] = sge;
+    sig_s[o] = sgs;
+    if (src) {
+      ptr_src[cnt] = src;
+      ptr_dst[cnt] = gnext + (size_t)cnt * cell;
+      cells_out[cnt] = j;
+      ++cnt;
+    }
+  }
+  for (int k = cnt; k < bound_out; ++k) ptr_src[k] = nullptr;
+  *cnt_out = cnt;
+}
+
+void dp_step(const DpStepArgs& a, hipStream_t st) {
+  hipLaunchKernelGGL(k_dp_step, dim3(1), dim3(256), 0, st, a.i, a.J, a.w, a.tau, a.r, a.M,
+                     a.stride, a.sig, a.cells_in, a.cnt_in, a.cells_out, a.cnt_out, a.mean, a.idx,
+                     a.bits, a.reach, a.sig_e, a.sig_s, a.E, a.gprev, a.gnext, a.Xi, a.cell,
+                     a.ptr_src, a.ptr_dst, a.bound_out);
+}
+
 }  // namespace ks

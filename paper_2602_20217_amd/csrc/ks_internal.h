@@ -199,6 +199,33 @@ void knapsack_select(const int32_t* best, const uint64_t* bits, const int32_t* w
                      const double* s, int B, int n, int C, int D, int32_t* j_star,
                      int32_t* g_star, double* tpt, uint8_t* skip, hipStream_t st);
 
+// one stage of the model-mode DP on the device (see k_dp_step)
+struct DpStepArgs {
+  int i, J, w;
+  double tau;
+  int r, M, stride;
+  const double* sig;
+  const int* cells_in;
+  const int* cnt_in;
+  int* cells_out;
+  int* cnt_out;
+  double* mean;    // [2 cells]
+  int* idx;        // [J + 1]
+  uint8_t* bits;   // [2L+1][stride]
+  uint8_t* reach;  // [2L+1][stride]
+  double* sig_e;   // [2L+1][stride]
+  double* sig_s;   // [2L+1][stride]
+  const float* E;
+  const float* gprev;
+  float* gnext;
+  const float* Xi;
+  size_t cell;     // floats per cell (r d)
+  const float** ptr_src;
+  float** ptr_dst;
+  int bound_out;
+};
+void dp_step(const DpStepArgs& a, hipStream_t st);
+
 // ------------------------------------------------------------------ errors
 void set_error(const std::string& msg);
 

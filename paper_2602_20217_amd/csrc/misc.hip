@@ -411,11 +411,13 @@ void cos_rows(const float* X, const float* Y, int rows, int ry, int d, double* o
 }
 
 // ------------------------------------------------------------------- copies
-// dst[i][0..n) = src[i][0..n) for pointer tables of length cnt.
+// dst[i][0..n) = src[i][0..n) for pointer tables of length cnt; a null
+// source marks an unused entry.
 __global__ void k_copy_blocks(const float* const* src, float* const* dst, size_t n) {
   const int i = blockIdx.y;
   const float* s = src[i];
   float* d = dst[i];
+  if (s == nullptr) return;
   for (size_t c = (size_t)blockIdx.x * blockDim.x + threadIdx.x; c < n;
        c += (size_t)gridDim.x * blockDim.x)
     d[c] = s[c];
