@@ -244,152 +244,202 @@ typedef __attribute__((__vector_size__(4 * sizeof(__bf16)))) __bf16 bf16x4_d;
 
 // Decode / verify rows of bf16 caches with head dim 128, all products on
 // matrix instructions.  A workgroup of S waves owns S consecutive 64-key tiles
-// of one kv head and RB = 16 / G consecutive rows: its 16 query columns are
-// j = row * G + g (row < RB, G query heads per kv head), so the rows of a
-// verify pass share every key/value load.  Wave w owns tile w.  The wave
-// requests its 32 KiB of keys and values with direct global-to-LDS loads (no
-// staging registers) next to its query loads, so it waits for one memory round
-// trip.  Rows are stored unpadded with 16-byte chunk c of row r at slot
-// c ^ (r % 16).
-//  scores  S^T = K Q^T, keys as rows of 16x16x32 products (queries as hi + lo
-//          bf16 columns): lane (j, g) holds keys 16 kt + 4 g + v of column j,
-//          so the tile max and sum need two cross-lane steps; a column only
-//          counts keys below its row's length;
+// of one kv head and RB = 16 CB / G consecutive rows: its 16 CB query columns
+// are c = row * G + g (row < RB, G query heads per kv head) in CB blocks of 16,
+// so the rows of a verify pass share every key/value load.  Wave w owns tile w:
+// it requests its queries, then 16 KiB of keys, then 16 KiB of values, the
+// tiles with direct global-to-LDS loads (no staging registers), and scores the
+// keys while the values are still arriving.  Rows are stored unpadded with
+// 16-byte chunk c of row r at slot c ^ (r % 16).
+//  scores  S^T = K Q^T per column block, keys as rows of 16x16x32 products
+//          (queries as hi + lo bf16 columns): lane (j, g) holds keys
+//          16 kt + 4 g + v of column j of the block, so the tile max and sum
+//          need two cross-lane steps; a column only counts keys below its
+//          row's length;
 //  values  O = P V with the probabilities (bf16) taken from the score registers
 //          as the A operand: k slot e of lane group g is key 4 g + e (e < 4) or
 //          16 + 4 g + e - 4 (e >= 4) of a 32-key step.  The V operand in that
 //          key order comes from transposing LDS reads (a 16-lane group turns
-//          16 8-byte row pieces into 4 keys x 16 dims).  Rows at or past the
-//          longest length of the workgroup are zeroed in LDS first
-//          (probability 0 must not meet a non-finite stale value).
-// The S tile results are merged in tile order into the split's partial (o,
-// max, sum) per query column, the layout k_attn_combine reads.  A column's
-// arithmetic does not depend on the other columns, so a verify row and the
+//          16 8-byte row pieces into 4 keys x 16 dims), shared by the column
+//          blocks.  Rows at or past the longest length of the workgroup are
+//          zeroed in LDS first (probability 0 must not meet a non-finite stale
+//          value).
+// The S tile results meet in LDS and the whole workgroup merges them in tile
+// order into the split's partial (o, max, sum) per query column, the layout
+// k_attn_combine reads.  (Merging the splits in the last workgroup of the grid
+// instead, behind an atomic ticket, needs an agent-scope release per
+// workgroup, which on this part costs more than the second launch.)
+// A column's arithmetic depends only on its own query, its length and the
+// split size, never on the other columns or on CB, so a verify row and the
 // decode step at the same position give the same bits.
-template <int S>
-__global__ __launch_bounds__(64 * S) void k_attn_dec(int M, int hq, int hkv, int n_max,
-                                                     const float* __restrict__ q,
-                                                     const bf16_t* __restrict__ kc,
-                                                     const bf16_t* __restrict__ vc,
-                                                     const int32_t* __restrict__ len,
-                                                     float* __restrict__ part, int nsplit) {
+template <int S, int CB>
+__global__ __launch_bounds__(64 * S) void k_attn_dec(
+    int M, int hq, int hkv, int n_max, const float* __restrict__ q,
+    const bf16_t* __restrict__ kc, const bf16_t* __restrict__ vc,
+    const int32_t* __restrict__ len, float* __restrict__ part, int nsplit) {
   constexpr int HD = 128;
-  constexpr int MGS = 16 * (HD + 2);  // merge record: 16 columns
-  static_assert(MGS * 4 <= TILE * 256, "merge record fits a key tile");
-  __shared__ __align__(16) uint4 KV[S][2 * TILE * 16];  // per wave: K tile, then V tile
+  constexpr int RS = HD + 4;  // LDS merge record per column: o, max, sum (bank-shifted)
+  constexpr int NCOL = 16 * CB;
+  static_assert(CB == 1 || CB == 2, "one or two column blocks");
+  static_assert(16 * RS + NCOL * (S + 3) <= TILE * 64, "records and scratch fit a tile");
+  __shared__ __align__(16) uint4 Ks[S][TILE * 16];
+  __shared__ __align__(16) uint4 Vs[S][TILE * 16];
+  // once every wave is past its tiles: wave w's key tile holds the records of
+  // column block 0, its value tile those of block 1; wave 0's key tile also
+  // holds the merge scratch after its records: weights [NCOL][S], maxima,
+  // sums, lengths [NCOL]
+  float* s_w = (float*)&Ks[0][0] + 16 * RS;
+  float* s_mx = s_w + NCOL * S;
+  float* s_lx = s_mx + NCOL;
+  int* s_len = (int*)(s_lx + NCOL);
   const int split = blockIdx.x, kvh = blockIdx.y;
   const int G = hq / hkv;
-  const int RB = 16 / G;
+  const int RB = NCOL / G;
   const int r0 = blockIdx.z * RB;
   const int lane = threadIdx.x & 63;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int start = split * S * TILE;
+  const int span = S * TILE;
+  const int start = split * span;
   const int t0 = start + w * TILE;
-  uint4* KVw = &KV[w][0];
+  const int nc = min(NCOL, (M - r0) * G);  // query columns with a row
 
-  // piece i (1 KiB): rows 4 (i % 16) .. + 3 of K (i < 16) or V; lane l writes
-  // chunk slot l % 16 of row 4 (i % 16) + l / 16
+  // column 16 b + j of the workgroup (j = lane % 16): row r0 + (16 b + j) / G,
+  // head kvh G + j % G, dims 32 ks + 8 g .. + 7 (g = lane / 16)
+  const int j = lane & 15, g = lane >> 4;
+  float4 xq[CB][8];
+  int Lj[CB];
+#pragma unroll
+  for (int b = 0; b < CB; ++b) {
+    const int rj = r0 + (16 * b + j) / G;
+    const bool qok = rj < M;
+    const float* qv = q + ((size_t)(qok ? rj : r0) * hq + kvh * G + j % G) * HD + 8 * g;
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      xq[b][2 * ks] = *(const float4*)(qv + 32 * ks);
+      xq[b][2 * ks + 1] = *(const float4*)(qv + 32 * ks + 4);
+    }
+    Lj[b] = qok ? len[rj] : 0;  // this column's row length (0: no row)
+  }
+  // piece i (1 KiB): rows 4 i .. + 3 of the tile; lane l writes chunk slot
+  // l % 16 of row 4 i + l / 16
   {
     const bf16_t* kb = kc + (size_t)kvh * n_max * HD;
     const bf16_t* vb = vc + (size_t)kvh * n_max * HD;
     const int rr0 = lane >> 4, slot = lane & 15;
 #pragma unroll
-    for (int i = 0; i < 32; ++i) {
-      const int rr = 4 * (i & 15) + rr0;
+    for (int i = 0; i < 16; ++i) {
+      const int rr = 4 * i + rr0;
       const int row = min(t0 + rr, n_max - 1);
-      const bf16_t* src = (i < 16 ? kb : vb) + (size_t)row * HD + ((slot ^ (rr & 15)) << 3);
-      __builtin_amdgcn_global_load_lds((const void*)src,
-                                       (__attribute__((address_space(3))) void*)&KVw[i * 64], 16,
-                                       0, 0);
+      __builtin_amdgcn_global_load_lds(
+          (const void*)(kb + (size_t)row * HD + ((slot ^ (rr & 15)) << 3)),
+          (__attribute__((address_space(3))) void*)&Ks[w][i * 64], 16, 0, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int rr = 4 * i + rr0;
+      const int row = min(t0 + rr, n_max - 1);
+      __builtin_amdgcn_global_load_lds(
+          (const void*)(vb + (size_t)row * HD + ((slot ^ (rr & 15)) << 3)),
+          (__attribute__((address_space(3))) void*)&Vs[w][i * 64], 16, 0, 0);
     }
   }
-  // query column j = lane % 16: row r0 + j / G, head kvh G + j % G, dims
-  // 32 ks + 8 g .. + 7 (g = lane / 16), as hi + lo bf16
-  const int j = lane & 15, g = lane >> 4;
-  const int rj = r0 + j / G;
-  const bool qok = rj < M;
-  bf16x8_d qh[4], ql[4];
-  {
-    const float* qv = q + ((size_t)(qok ? rj : r0) * hq + kvh * G + j % G) * HD + 8 * g;
+  int Lmax = 0;  // longest row of the workgroup
+  for (int r = r0; r < min(M, r0 + RB); ++r) Lmax = max(Lmax, len[r]);
+  const int cnt = min(TILE, Lmax - t0);  // keys of this tile any column uses (may be <= 0)
+  // queries as hi + lo bf16 (waits for the query loads only)
+  bf16x8_d qh[CB][4], ql[CB][4];
+#pragma unroll
+  for (int b = 0; b < CB; ++b)
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
-      float4 x0 = *(const float4*)(qv + 32 * ks), x1 = *(const float4*)(qv + 32 * ks + 4);
-      if (!qok) x0 = x1 = make_float4(0.f, 0.f, 0.f, 0.f);
+      const float4 x0 = xq[b][2 * ks], x1 = xq[b][2 * ks + 1];
       const float xs[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const __bf16 h = (__bf16)xs[e];
-        qh[ks][e] = h;
-        ql[ks][e] = (__bf16)(xs[e] - (float)h);
+        const float x = Lj[b] > 0 ? xs[e] : 0.f;
+        const __bf16 h = (__bf16)x;
+        qh[b][ks][e] = h;
+        ql[b][ks][e] = (__bf16)(x - (float)h);
       }
     }
-  }
-  const int Lj = qok ? len[rj] : 0;  // this column's row length
-  int Lmax = 0;                      // longest row of the workgroup
-  for (int r = r0; r < min(M, r0 + RB); ++r) Lmax = max(Lmax, len[r]);
-  const int cnt = min(TILE, Lmax - t0);  // keys of this tile any column uses (may be <= 0)
-  const int cj = min(TILE, Lj - t0);     // keys of this tile column j uses
-  __builtin_amdgcn_s_waitcnt(0);
+  __builtin_amdgcn_s_waitcnt(vmcnt_imm_a(16));  // keys have landed
 
-  float m = -FLT_MAX, l = 0.f;
-  f32x4_d o[8];
+  float m[CB], l[CB];
+  f32x4_d o[CB][8], sc[CB][4];
 #pragma unroll
-  for (int dt = 0; dt < 8; ++dt) o[dt] = f32x4_d{0.f, 0.f, 0.f, 0.f};
+  for (int b = 0; b < CB; ++b) {
+    m[b] = -FLT_MAX;
+    l[b] = 0.f;
+#pragma unroll
+    for (int dt = 0; dt < 8; ++dt) o[b][dt] = f32x4_d{0.f, 0.f, 0.f, 0.f};
+  }
   if (cnt > 0) {
-    const uint4* Kt = KVw;
-    uint4* Vt = KVw + TILE * 16;
-    if (cnt < TILE) {
-      for (int c = cnt * 16 + lane; c < TILE * 16; c += 64) Vt[c] = make_uint4(0u, 0u, 0u, 0u);
-    }
-    // S^T: sc[kt][v] = score(key 16 kt + 4 g + v, query column j)
-    f32x4_d sc[4];
+    // S^T: sc[b][kt][v] = score(key 16 kt + 4 g + v, column 16 b + j)
+    const uint4* Kt = &Ks[w][0];
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt) {
-      sc[kt] = f32x4_d{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int b = 0; b < CB; ++b) sc[b][kt] = f32x4_d{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) {
         const int c = 4 * ks + g;  // 16-byte chunk of the key row
         const bf16x8_d kf = __builtin_bit_cast(bf16x8_d, Kt[(16 * kt + j) * 16 + (c ^ j)]);
-        sc[kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qh[ks], sc[kt], 0, 0, 0);
-        sc[kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, ql[ks], sc[kt], 0, 0, 0);
+#pragma unroll
+        for (int b = 0; b < CB; ++b) {
+          sc[b][kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qh[b][ks], sc[b][kt], 0, 0, 0);
+          sc[b][kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, ql[b][ks], sc[b][kt], 0, 0, 0);
+        }
       }
     }
     const float scale = 1.0f / sqrtf((float)HD);
-    float mt = -FLT_MAX;
 #pragma unroll
-    for (int kt = 0; kt < 4; ++kt)
+    for (int b = 0; b < CB; ++b) {
+      const int cj = min(TILE, Lj[b] - t0);  // keys of this tile the column uses
+      float mt = -FLT_MAX;
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        sc[kt][v] = 16 * kt + 4 * g + v < cj ? sc[kt][v] * scale : -FLT_MAX;
-        mt = fmaxf(mt, sc[kt][v]);
-      }
-    mt = fmaxf(mt, __shfl_xor(mt, 16));
-    mt = fmaxf(mt, __shfl_xor(mt, 32));
-    float ps = 0.f;
+      for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
-    for (int kt = 0; kt < 4; ++kt)
+        for (int v = 0; v < 4; ++v) {
+          sc[b][kt][v] = 16 * kt + 4 * g + v < cj ? sc[b][kt][v] * scale : -FLT_MAX;
+          mt = fmaxf(mt, sc[b][kt][v]);
+        }
+      mt = fmaxf(mt, __shfl_xor(mt, 16));
+      mt = fmaxf(mt, __shfl_xor(mt, 32));
+      float ps = 0.f;
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const float p = 16 * kt + 4 * g + v < cj ? __expf(sc[kt][v] - mt) : 0.f;
-        sc[kt][v] = p;
-        ps += p;
-      }
-    ps += __shfl_xor(ps, 16);
-    ps += __shfl_xor(ps, 32);
-    m = mt;
-    l = ps;
+      for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const float p = 16 * kt + 4 * g + v < cj ? __expf(sc[b][kt][v] - mt) : 0.f;
+          sc[b][kt][v] = p;
+          ps += p;
+        }
+      ps += __shfl_xor(ps, 16);
+      ps += __shfl_xor(ps, 32);
+      m[b] = mt;
+      l[b] = ps;
+    }
+  }
+  __builtin_amdgcn_s_waitcnt(vmcnt_imm_a(0));  // values have landed
+  if (cnt > 0) {
+    uint4* Vt = &Vs[w][0];
+    if (cnt < TILE) {
+      for (int c = cnt * 16 + lane; c < TILE * 16; c += 64) Vt[c] = make_uint4(0u, 0u, 0u, 0u);
+    }
     // transposing reads: lane 16 g + 4 s + u points at the 8-byte piece of V row
     // 32 k2 + 16 h + 4 g + s, dims 16 dt + 4 u .. + 3
     const int s4 = (lane & 15) >> 2, u4 = lane & 3;
     const char* Vb = (const char*)Vt;
 #pragma unroll
     for (int k2 = 0; k2 < 2; ++k2) {
-      bf16x8_d pa;
+      bf16x8_d pa[CB];
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        pa[v] = (__bf16)sc[2 * k2][v];
-        pa[4 + v] = (__bf16)sc[2 * k2 + 1][v];
-      }
+      for (int b = 0; b < CB; ++b)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          pa[b][v] = (__bf16)sc[b][2 * k2][v];
+          pa[b][4 + v] = (__bf16)sc[b][2 * k2 + 1][v];
+        }
 #pragma unroll
       for (int dt = 0; dt < 8; ++dt) {
         bf16x4_d h2[2];
@@ -407,69 +457,61 @@ __global__ __launch_bounds__(64 * S) void k_attn_dec(int M, int hq, int hkv, int
           vb[e] = h2[0][e];
           vb[4 + e] = h2[1][e];
         }
-        o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa, vb, o[dt], 0, 0, 0);
+#pragma unroll
+        for (int b = 0; b < CB; ++b)
+          o[b][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa[b], vb, o[b][dt], 0, 0, 0);
       }
     }
   }
-  // o[dt][v]: column 4 g + v, dim 16 dt + j; the max and sum of column c live
-  // in lane c
-  float mv[4], lv[4];
-  int Lv[4];
+  // tile results to LDS: o[b][dt][v] is column 16 b + 4 g + v, dim 16 dt + j;
+  // the max and sum of column 16 b + c live in lane c.  A wave overwrites only
+  // its own tiles (LDS accesses of a wave stay in order).
 #pragma unroll
-  for (int v = 0; v < 4; ++v) {
-    mv[v] = __shfl(m, 4 * g + v);
-    lv[v] = __shfl(l, 4 * g + v);
-    Lv[v] = __shfl(Lj, 4 * g + v);
-  }
-  if (S > 1) {
-    __syncthreads();  // every wave is done with its tiles
-    float* rec = (float*)KVw;
+  for (int b = 0; b < CB; ++b) {
+    float* rec = b == 0 ? (float*)&Ks[w][0] : (float*)&Vs[w][0];
 #pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      float* rc = rec + (4 * g + v) * (HD + 2);
+    for (int v = 0; v < 4; ++v)
 #pragma unroll
-      for (int dt = 0; dt < 8; ++dt) rc[16 * dt + j] = o[dt][v];
-      if (j == 0) {
-        rc[HD] = mv[v];
-        rc[HD + 1] = lv[v];
-      }
-    }
-    __syncthreads();
-    if (w != 0) return;
-#pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const int col = 4 * g + v;
-      float mx = -FLT_MAX;
-#pragma unroll
-      for (int s = 0; s < S; ++s)
-        mx = fmaxf(mx, ((const float*)&KV[s][0])[col * (HD + 2) + HD]);
-      float lx = 0.f;
-#pragma unroll
-      for (int dt = 0; dt < 8; ++dt) o[dt][v] = 0.f;
-#pragma unroll
-      for (int s = 0; s < S; ++s) {
-        const float* rs = (const float*)&KV[s][0] + col * (HD + 2);
-        const float wt = rs[HD] == -FLT_MAX ? 0.f : __expf(rs[HD] - mx);
-        lx = fmaf(rs[HD + 1], wt, lx);
-#pragma unroll
-        for (int dt = 0; dt < 8; ++dt) o[dt][v] = fmaf(rs[16 * dt + j], wt, o[dt][v]);
-      }
-      mv[v] = mx;
-      lv[v] = lx;
+      for (int dt = 0; dt < 8; ++dt) rec[(4 * g + v) * RS + 16 * dt + j] = o[b][dt][v];
+    if (lane < 16) {
+      rec[lane * RS + HD] = m[b];
+      rec[lane * RS + HD + 1] = l[b];
     }
   }
-  // write the split's partial of every column whose row reaches this split
+  __syncthreads();
+  auto record = [&](int s, int c) -> const float* {
+    return (c < 16 ? (const float*)&Ks[s][0] : (const float*)&Vs[s][0]) + (c & 15) * RS;
+  };
+  if (threadIdx.x < nc) {  // wave 0, lane c: column c (its Lj[c / 16] is the column's length)
+    const int c = threadIdx.x;
+    float mx = -FLT_MAX;
 #pragma unroll
-  for (int v = 0; v < 4; ++v) {
-    const int col = 4 * g + v;
-    const int rc = r0 + col / G;
-    if (rc >= M || Lv[v] <= start) continue;
-    float* dst = part + (((size_t)rc * hq + kvh * G + col % G) * nsplit + split) * (HD + 2);
+    for (int s = 0; s < S; ++s) mx = fmaxf(mx, record(s, c)[HD]);
+    float lx = 0.f;
 #pragma unroll
-    for (int dt = 0; dt < 8; ++dt) dst[16 * dt + j] = o[dt][v];
-    if (j == 0) {
-      dst[HD] = mv[v];
-      dst[HD + 1] = lv[v];
+    for (int s = 0; s < S; ++s) {
+      const float* rs = record(s, c);
+      const float wt = rs[HD] == -FLT_MAX ? 0.f : __expf(rs[HD] - mx);
+      s_w[c * S + s] = wt;
+      lx = fmaf(rs[HD + 1], wt, lx);
+    }
+    s_mx[c] = mx;
+    s_lx[c] = lx;
+    s_len[c] = CB == 1 || c < 16 ? Lj[0] : Lj[CB - 1];
+  }
+  __syncthreads();
+  // the split's partial of every column whose row reaches this split
+  for (int i = threadIdx.x; i < nc * HD; i += 64 * S) {
+    const int c = i >> 7, d = i & (HD - 1);
+    if (s_len[c] <= start) continue;
+    float acc = 0.f;
+#pragma unroll
+    for (int s = 0; s < S; ++s) acc = fmaf(record(s, c)[d], s_w[c * S + s], acc);
+    float* dst = part + (((size_t)(r0 + c / G) * hq + kvh * G + c % G) * nsplit + split) * (HD + 2);
+    dst[d] = acc;
+    if (d == 0) {
+      dst[HD] = s_mx[c];
+      dst[HD + 1] = s_lx[c];
     }
   }
 }
@@ -872,40 +914,35 @@ __global__ __launch_bounds__(NWAVE * 64) void k_attn_mfma(
 }
 
 // One workgroup of 4 waves per (row, query head); output dims lane -> (2 lane,
-// 2 lane + 1) for bf16 caches, lane for float32 caches.  The split maxima are
-// reduced across the workgroup; wave w then merges splits s = w, w + 4, ...
-// (loads of different splits are independent, so they are in flight together)
-// and the four wave sums are added in wave order.  The row's own key/value
-// (selection rows) joins the max and is added last.
+// 2 lane + 1) for bf16 caches, lane for float32 caches.  Wave w takes the
+// splits s = w, w + 4, ... of the launch; the maxima, sums and output dims of
+// up to CB of them are requested together with the row length, so a wave
+// waits for one memory round trip per CB splits.  Splits at or past the row's
+// own split count are skipped, the others enter a running max and sum in
+// order.  The four wave results are rescaled to the common max and added in
+// wave order, the row's own key/value (selection rows) last.
 template <int HD, bool BF>
 __global__ __launch_bounds__(256) void k_attn_combine(int M, int hq, int hkv, int span,
-                                                      const float* __restrict__ q,
+                                                      int ngrid, const float* __restrict__ q,
                                                       const float* __restrict__ part, int nsplit,
                                                       const int32_t* __restrict__ len,
                                                       const float* __restrict__ kvself,
                                                       bf16_t* ohi, bf16_t* olo, float* of,
                                                       int ldact) {
   constexpr int DPL = HD / 64;
-  __shared__ float s_m[4];
-  __shared__ float s_acc[4][DPL * 64 + 1];
+  constexpr int CB = 8;
+  __shared__ float s_m[4], s_l[4];
+  __shared__ float s_acc[4][DPL * 64];
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
-  const int gid = blockIdx.x;
-  const int r = gid / hq, h = gid % hq;
+  const int r = blockIdx.x / hq, h = blockIdx.x % hq;
   const int G = hq / hkv;
   const int kvh = h / G;
-  const int L = len[r];
-  const int ns = (L + span - 1) / span;
   const float* pr = part + ((size_t)r * hq + h) * nsplit * (HD + 2);
   const int d0 = BF ? 2 * lane : lane;
-
-  float mloc = -FLT_MAX;
-  for (int s = threadIdx.x; s < ns; s += 256) mloc = fmaxf(mloc, pr[(size_t)s * (HD + 2) + HD]);
-  mloc = wave_max(mloc);
-  if (lane == 0) s_m[wave] = mloc;
-  __syncthreads();
-  float mx = fmaxf(fmaxf(s_m[0], s_m[1]), fmaxf(s_m[2], s_m[3]));
-  float sself = 0.f;
+  const int L = len[r];
+  // the row's own key (selection rows): its score joins the max
+  float sself = -FLT_MAX;
   if (kvself) {
     const float* ks = kvself + (((size_t)r * 2 + 0) * hkv + kvh) * HD;
     const float* qv = q + ((size_t)r * hq + h) * HD;
@@ -913,34 +950,57 @@ __global__ __launch_bounds__(256) void k_attn_combine(int M, int hq, int hkv, in
 #pragma unroll
     for (int e = 0; e < DPL; ++e) dd = fmaf(qv[d0 + e], ks[d0 + e], dd);
     sself = wave_sum(dd) * (1.0f / sqrtf((float)HD));
-    mx = fmaxf(mx, sself);
   }
-  float lsum = 0.f, acc[DPL];
+  float mr = -FLT_MAX, lr = 0.f, acc[DPL];
 #pragma unroll
   for (int e = 0; e < DPL; ++e) acc[e] = 0.f;
-#pragma unroll 4
-  for (int s = wave; s < ns; s += 4) {
-    const float* ps = pr + (size_t)s * (HD + 2);
-    const float w = __expf(ps[HD] - mx);
-    lsum = fmaf(ps[HD + 1], w, lsum);
-    if (DPL == 2) {
-      const float2 v = *(const float2*)&ps[d0];
-      acc[0] = fmaf(v.x, w, acc[0]);
-      acc[DPL - 1] = fmaf(v.y, w, acc[DPL - 1]);
-    } else {
-      acc[0] = fmaf(ps[d0], w, acc[0]);
+  for (int s0 = wave; s0 < ngrid; s0 += 4 * CB) {
+    float ms[CB], ls[CB], ov[CB][DPL];
+#pragma unroll
+    for (int k = 0; k < CB; ++k) {
+      const float* ps = pr + (size_t)min(s0 + 4 * k, ngrid - 1) * (HD + 2);
+      ms[k] = ps[HD];
+      ls[k] = ps[HD + 1];
+      if (DPL == 2) {
+        const float2 v = *(const float2*)&ps[d0];
+        ov[k][0] = v.x;
+        ov[k][DPL - 1] = v.y;
+      } else {
+        ov[k][0] = ps[d0];
+      }
+    }
+    const int ns = (L + span - 1) / span;  // splits holding keys of this row
+#pragma unroll
+    for (int k = 0; k < CB; ++k) {
+      if (s0 + 4 * k < ns) {
+        const float mn = fmaxf(mr, ms[k]);
+        const float ea = __expf(mr - mn), eb = __expf(ms[k] - mn);
+        lr = fmaf(ls[k], eb, lr * ea);
+#pragma unroll
+        for (int e = 0; e < DPL; ++e) acc[e] = fmaf(ov[k][e], eb, acc[e] * ea);
+        mr = mn;
+      }
     }
   }
 #pragma unroll
   for (int e = 0; e < DPL; ++e) s_acc[wave][DPL * lane + e] = acc[e];
-  if (lane == 0) s_acc[wave][DPL * 64] = lsum;
+  if (lane == 0) {
+    s_m[wave] = mr;
+    s_l[wave] = lr;
+  }
   __syncthreads();
   if (wave != 0) return;
+  const float mx = fmaxf(fmaxf(fmaxf(s_m[0], s_m[1]), fmaxf(s_m[2], s_m[3])), sself);
+  float lsum = 0.f;
 #pragma unroll
-  for (int e = 0; e < DPL; ++e)
-    acc[e] = ((s_acc[0][DPL * lane + e] + s_acc[1][DPL * lane + e]) + s_acc[2][DPL * lane + e]) +
-             s_acc[3][DPL * lane + e];
-  lsum = ((s_acc[0][DPL * 64] + s_acc[1][DPL * 64]) + s_acc[2][DPL * 64]) + s_acc[3][DPL * 64];
+  for (int e = 0; e < DPL; ++e) acc[e] = 0.f;
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    const float ew = s_m[w] == -FLT_MAX ? 0.f : __expf(s_m[w] - mx);
+    lsum = fmaf(s_l[w], ew, lsum);
+#pragma unroll
+    for (int e = 0; e < DPL; ++e) acc[e] = fmaf(s_acc[w][DPL * lane + e], ew, acc[e]);
+  }
   if (kvself) {
     const float* vs = kvself + (((size_t)r * 2 + 1) * hkv + kvh) * HD;
     const float w = __expf(sself - mx);
@@ -979,6 +1039,13 @@ int attn_rows_per_block(int G, bool batched) {
   return G >= 32 ? 1 : 32 / G;
 }
 
+// Decode / verify rows of bf16 caches with head dim 128 take k_attn_dec.
+bool attn_dec_path(const AttnArgs& a) {
+  const int G = a.hq / a.hkv;
+  return a.dtype == KS_BF16 && a.hd == 128 && G <= 16 && 16 % G == 0 &&
+         a.rows_per_block == 1 && a.tiles >= 1 && a.tiles <= 5;
+}
+
 void attn_split(const AttnArgs& a, hipStream_t st) {
   if (a.max_len <= 0) return;
   const int ns = attn_nsplit(a.max_len, a.tiles);
@@ -989,22 +1056,31 @@ void attn_split(const AttnArgs& a, hipStream_t st) {
   hipLaunchKernelGGL((k_attn_split<HDV, BFV, QM>), grid, dim3(256), 0, st, a.M, a.hq, a.hkv, \
                      a.n_max, a.q, a.kc, a.vc, a.len, a.tiles, a.rows_per_block, a.part,     \
                      a.nsplit)
-  if (a.hd == 128 && G <= 16 && 16 % G == 0 && a.rows_per_block == 1 && a.tiles >= 1 &&
-      a.tiles <= 5) {
-    // decode / verify rows, 16 / G rows per workgroup
-    dim3 g3(ns, a.hkv, (a.M + 16 / G - 1) / (16 / G));
+  if (attn_dec_path(a)) {
+    // decode / verify rows: 16 query columns per workgroup when one block holds
+    // all rows, else 32 (16 CB / G rows per workgroup)
+    const int CB = a.M * G <= 16 ? 1 : 2;
+    const int RB = 16 * CB / G;
+    dim3 g3(ns, a.hkv, (a.M + RB - 1) / RB);
     const bf16_t* kc = (const bf16_t*)a.kc;
     const bf16_t* vc = (const bf16_t*)a.vc;
-#define KS_DEC(S_)                                                                                \
-  hipLaunchKernelGGL(k_attn_dec<S_>, g3, dim3(64 * S_), 0, st, a.M, a.hq, a.hkv, a.n_max, a.q, kc, \
-                     vc, a.len, a.part, a.nsplit)
-    switch (a.tiles) {
-      case 1: KS_DEC(1); break;
-      case 2: KS_DEC(2); break;
-      case 3: KS_DEC(3); break;
-      case 4: KS_DEC(4); break;
-      default: KS_DEC(5); break;
+#define KS_DEC(S_, CB_)                                                                      \
+  hipLaunchKernelGGL((k_attn_dec<S_, CB_>), g3, dim3(64 * S_), 0, st, a.M, a.hq, a.hkv,       \
+                     a.n_max, a.q, kc, vc, a.len, a.part, a.nsplit)
+#define KS_DEC_S(CB_)            \
+  switch (a.tiles) {             \
+    case 1: KS_DEC(1, CB_); break; \
+    case 2: KS_DEC(2, CB_); break; \
+    case 3: KS_DEC(3, CB_); break; \
+    case 4: KS_DEC(4, CB_); break; \
+    default: KS_DEC(5, CB_); break; \
+  }
+    if (CB == 1) {
+      KS_DEC_S(1);
+    } else {
+      KS_DEC_S(2);
     }
+#undef KS_DEC_S
 #undef KS_DEC
   } else if (a.hd == 128 && a.tiles > 1) {
     // batched rows: matrix-instruction kernel, 64 query vectors per workgroup
@@ -1024,10 +1100,11 @@ void attn_split(const AttnArgs& a, hipStream_t st) {
 void attn_combine(const AttnArgs& a, const float* kvself, Act act_out, hipStream_t st) {
   dim3 grid(a.M * a.hq);
   const int span = TILE * a.tiles;
+  const int ngrid = attn_nsplit(a.max_len, a.tiles);  // splits the split kernel ran
   const bool bf = a.dtype == KS_BF16;
 #define KS_COMB(HDV, BFV)                                                                    \
   hipLaunchKernelGGL((k_attn_combine<HDV, BFV>), grid, dim3(256), 0, st, a.M, a.hq, a.hkv,   \
-                     span, a.q, a.part, a.nsplit, a.len, kvself,                             \
+                     span, ngrid, a.q, a.part, a.nsplit, a.len, kvself,                      \
                      bf ? (bf16_t*)act_out.hi : nullptr, bf ? (bf16_t*)act_out.lo : nullptr, \
                      bf ? nullptr : (float*)act_out.hi, act_out.ld)
   if (a.hd == 128) KS_COMB(128, true);

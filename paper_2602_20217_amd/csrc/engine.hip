@@ -48,11 +48,11 @@ constexpr int PB = 512;        // rows per batched attention / head pass
 // float32 split-K partials of the batched products (prefill chunks, selection)
 constexpr size_t GPART_BYTES = (size_t)64 << 20;
 // decode/verify splits: 64-position tiles per split, by cache size only (never
-// by row count, so a verify row and the decode step split alike).  One tile
-// per split for caches up to 4096 positions; five above (a 160 KiB workgroup:
-// up to 10240 positions of 8 kv heads fit the 256 CUs in one round, and the
-// merge reads few partials).  Measured on MI355X against 1..5 tiles.
-int dec_tiles(int n_max) { return n_max > 4096 ? 5 : 1; }
+// by row count, so a verify row and the decode step split alike).  Measured on
+// MI355X (split kernel + merge, 1..5 tiles, 1 and 5 rows): two tiles for caches
+// up to 2048 positions, three up to 5120, five above (a 160 KiB workgroup: up to
+// 10240 positions of 8 kv heads fit the 256 CUs in one round).
+int dec_tiles(int n_max) { return n_max <= 2048 ? 2 : n_max <= 5120 ? 3 : 5; }
 constexpr int BAT_TILES = 16;  // prefill/DP: 1024 positions per split
 
 size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }

@@ -159,6 +159,7 @@ struct AttnArgs {
   float* part;           // [M][hq][nsplit][hd+2]
   int nsplit;            // stride: splits per (row, head)
 };
+bool attn_dec_path(const AttnArgs& a);
 void attn_split(const AttnArgs& a, hipStream_t st);
 // Merge splits (and, when kvself != nullptr, the row's own key/value) and write
 // the attention output as O-projection input activations.

@@ -1,8 +1,9 @@
 """GPU vs oracle parity of decode and verify rows over long caches, where the
-attention splits hold two or four 64-position tiles (cache sizes above 2048 and
-4096 positions).  The cache holds seeded synthetic keys/values up to a ragged
-length and NaN beyond it, so any read of a position past a row's length shows
-up in the result.  Every call goes through the C ABI; tolerance 2e-2 (bf16)."""
+decode attention splits hold two, three and five 64-position tiles (cache
+sizes up to 2048, up to 5120 and above).  The cache holds seeded synthetic
+keys/values up to a ragged length and NaN beyond it, so any read of a position
+past a row's length shows up in the result.  Every call goes through the C
+ABI; tolerance 2e-2 (bf16)."""
 import numpy as np
 import pytest
 
@@ -16,7 +17,7 @@ torch = pytest.importorskip("torch")
 TOL = 2e-2
 
 
-@pytest.fixture(scope="module", params=[3000, 4600])
+@pytest.fixture(scope="module", params=[1500, 3000, 6000])
 def setup(request):
     if not torch.cuda.is_available():
         pytest.skip("no GPU")
