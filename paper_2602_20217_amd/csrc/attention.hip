@@ -943,7 +943,7 @@ __global__ __launch_bounds__(256) void k_attn_combine(int M, int hq, int hkv, in
   const int L = len[r];
   // the row's own key (selection rows): its score joins the max
   float sself = -FLT_MAX;
-  if (kvself) {
+  if (kvself && wave == 0) {
     const float* ks = kvself + (((size_t)r * 2 + 0) * hkv + kvh) * HD;
     const float* qv = q + ((size_t)r * hq + h) * HD;
     float dd = 0.f;
@@ -958,15 +958,21 @@ __global__ __launch_bounds__(256) void k_attn_combine(int M, int hq, int hkv, in
     float ms[CB], ls[CB], ov[CB][DPL];
 #pragma unroll
     for (int k = 0; k < CB; ++k) {
-      const float* ps = pr + (size_t)min(s0 + 4 * k, ngrid - 1) * (HD + 2);
-      ms[k] = ps[HD];
-      ls[k] = ps[HD + 1];
-      if (DPL == 2) {
-        const float2 v = *(const float2*)&ps[d0];
-        ov[k][0] = v.x;
-        ov[k][DPL - 1] = v.y;
-      } else {
-        ov[k][0] = ps[d0];
+      ms[k] = -FLT_MAX;
+      ls[k] = 0.f;
+#pragma unroll
+      for (int e = 0; e < DPL; ++e) ov[k][e] = 0.f;
+      if (s0 + 4 * k < ngrid) {  // wave-uniform: only splits the launch ran
+        const float* ps = pr + (size_t)(s0 + 4 * k) * (HD + 2);
+        ms[k] = ps[HD];
+        ls[k] = ps[HD + 1];
+        if (DPL == 2) {
+          const float2 v = *(const float2*)&ps[d0];
+          ov[k][0] = v.x;
+          ov[k][DPL - 1] = v.y;
+        } else {
+          ov[k][0] = ps[d0];
+        }
       }
     }
     const int ns = (L + span - 1) / span;  // splits holding keys of this row

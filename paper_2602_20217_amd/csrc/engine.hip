@@ -804,8 +804,7 @@ static ks_status select_internal(ks_ctx* c, const ks_select_params* p, ks_select
     // execute candidates for every (possibly) reachable budget
     sublayer_rows(c, i, gprev, E, M, dpos, dlen, n, 1, true);
     // per-row cosines of both candidates against X^(i)
-    cos_rows(E, X(i), M, r, d.d, sig, c->st);
-    cos_rows(gprev, X(i), M, r, d.d, sig + M, c->st);
+    cos_rows2(E, gprev, X(i), M, r, d.d, sig, sig + M, c->st);
     cum += w;
     const int bound_out = std::min(J, cum) + 1;
     DpStepArgs da{i, J, w, (double)p->tau, r, M, S_, sig,

@@ -219,13 +219,15 @@ static void launch_skinny(const GemmArgs& g, hipStream_t st) {
 }
 
 // Launch shape by matrix shape only (never by row count), measured on MI355X
-// with the Llama-8B shapes: the wide products (gate/up, vocabulary head) one
-// tile per 8-wave workgroup, the long-K down projection a 16-way K split, the
-// remaining square-ish products 16 (N <= 4096) or 8 waves.
+// with the Llama-8B shapes (cold weights, 4/8/16 waves x 4/8/16-deep chunks):
+// gate/up one tile per 4-wave workgroup in 4-deep chunks (1792 workgroups of
+// 4 waves are all resident at once, 7 per CU, so no second round trails); the
+// vocabulary head 8 waves, 4-deep; the long-K down projection a 16-way K split;
+// the remaining square-ish products 16 (N <= 4096) or 8 waves, 8-deep.
 void gemm_bf16_skinny(const GemmArgs& g, hipStream_t st) {
-  if (g.epi == EPI_SWIGLU) launch_skinny<1, 8, 8>(g, st);
+  if (g.epi == EPI_SWIGLU) launch_skinny<1, 4, 4>(g, st);
   else if (g.K >= 8192) launch_skinny<1, 16, 8>(g, st);
-  else if (g.N >= 65536) launch_skinny<1, 8, 8>(g, st);
+  else if (g.N >= 65536) launch_skinny<1, 8, 4>(g, st);
   else if (g.N <= 4096) launch_skinny<1, 16, 8>(g, st);
   else launch_skinny<1, 8, 8>(g, st);
 }

@@ -215,40 +215,53 @@ __global__ __launch_bounds__(256) void k_dp_step(
   __syncthreads();
   for (int k = threadIdx.x; k < nc; k += blockDim.x) idx[cells_in[k]] = k;
   __syncthreads();
-  if (threadIdx.x != 0) return;
+  // every budget decides in parallel; the reached budgets are compacted in
+  // ascending order with a workgroup scan, 256 budgets at a time
+  __shared__ int s_wsum[4];
   const double qnan = __longlong_as_double(0x7FF8000000000000ll);
-  int cnt = 0;
-  for (int j = 0; j <= J; ++j) {
-    const int ie = idx[j];
-    const int is = j >= w ? idx[j - w] : -1;
-    const double sge = ie >= 0 ? mean[ie] : qnan;
-    const double sgs = is >= 0 ? mean[nc + is] : qnan;
-    const bool e_ok = ie >= 0 && sge > tau;
-    const bool s_ok = is >= 0 && sgs > tau;
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  int base = 0;
+  for (int j0 = 0; j0 <= J; j0 += 256) {
+    const int j = j0 + threadIdx.x;
     const float* src = nullptr;
-    uint8_t bit = 0;
-    if (j == 0) {
-      src = Xi;
-    } else if (e_ok && (!s_ok || sge >= sgs)) {
-      src = E + (size_t)ie * cell;
-    } else if (s_ok) {
-      src = gprev + (size_t)is * cell;
-      bit = 1;
+    if (j <= J) {
+      const int ie = idx[j];
+      const int is = j >= w ? idx[j - w] : -1;
+      const double sge = ie >= 0 ? mean[ie] : qnan;
+      const double sgs = is >= 0 ? mean[nc + is] : qnan;
+      const bool e_ok = ie >= 0 && sge > tau;
+      const bool s_ok = is >= 0 && sgs > tau;
+      uint8_t bit = 0;
+      if (j == 0) {
+        src = Xi;
+      } else if (e_ok && (!s_ok || sge >= sgs)) {
+        src = E + (size_t)ie * cell;
+      } else if (s_ok) {
+        src = gprev + (size_t)is * cell;
+        bit = 1;
+      }
+      const size_t o = (size_t)i * stride + j;
+      bits[o] = bit;
+      reach[o] = src != nullptr;
+      sig_e[o] = sge;
+      sig_s[o] = sgs;
     }
-    const size_t o = (size_t)i * stride + j;
-    bits[o] = bit;
-    reach[o] = src != nullptr;
-    sig_e[o] = sge;
-    sig_s[o] = sgs;
+    const unsigned long long bal = __ballot(src != nullptr);
+    if (lane == 0) s_wsum[wv] = __popcll(bal);
+    __syncthreads();
+    int off = base;
+    for (int q = 0; q < wv; ++q) off += s_wsum[q];
     if (src) {
-      ptr_src[cnt] = src;
-      ptr_dst[cnt] = gnext + (size_t)cnt * cell;
-      cells_out[cnt] = j;
-      ++cnt;
+      const int p = off + __popcll(bal & ((1ull << lane) - 1ull));
+      ptr_src[p] = src;
+      ptr_dst[p] = gnext + (size_t)p * cell;
+      cells_out[p] = j;
     }
+    base += s_wsum[0] + s_wsum[1] + s_wsum[2] + s_wsum[3];
+    __syncthreads();
   }
-  for (int k = cnt; k < bound_out; ++k) ptr_src[k] = nullptr;
-  *cnt_out = cnt;
+  for (int k = base + threadIdx.x; k < bound_out; k += blockDim.x) ptr_src[k] = nullptr;
+  if (threadIdx.x == 0) *cnt_out = base;
 }
 
 void dp_step(const DpStepArgs& a, hipStream_t st) {

@@ -175,6 +175,8 @@ void cos_groups(const float* X, const float* Y, int groups, int r, int d, float*
 // per-row cosine with float64 accumulation: out[t] = cos(X[t], Y[t % ry])
 void cos_rows(const float* X, const float* Y, int rows, int ry, int d, double* out,
               hipStream_t st);
+void cos_rows2(const float* X1, const float* X2, const float* Y, int rows, int ry, int d,
+               double* out1, double* out2, hipStream_t st);
 void cos_groups_f64(const float* X, const float* Y, int groups, int r, int d, double* out,
                     hipStream_t st);
 // history ring <-> contiguous planes for `planes` planes of n rows of d floats

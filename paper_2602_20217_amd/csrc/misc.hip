@@ -410,6 +410,28 @@ void cos_rows(const float* X, const float* Y, int rows, int ry, int d, double* o
   hipLaunchKernelGGL(k_cos_rows, dim3((rows + 3) / 4), dim3(256), 0, st, X, Y, rows, ry, d, out);
 }
 
+// Both candidate sets of a DP stage in one launch: rows t < rows of X1 into
+// out1, of X2 into out2, each against Y row t % ry.
+__global__ __launch_bounds__(256) void k_cos_rows2(const float* __restrict__ X1,
+                                                   const float* __restrict__ X2,
+                                                   const float* __restrict__ Y, int rows, int ry,
+                                                   int d, double* out1, double* out2) {
+  const int lane = threadIdx.x & 63;
+  const int t2 = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t2 >= 2 * rows) return;
+  const bool second = t2 >= rows;
+  const int t = second ? t2 - rows : t2;
+  const double c = row_cos((second ? X2 : X1) + (size_t)t * d, Y + (size_t)(t % ry) * d, d, lane);
+  if (lane == 0) (second ? out2 : out1)[t] = c;
+}
+
+void cos_rows2(const float* X1, const float* X2, const float* Y, int rows, int ry, int d,
+               double* out1, double* out2, hipStream_t st) {
+  if (rows <= 0) return;
+  hipLaunchKernelGGL(k_cos_rows2, dim3((2 * rows + 3) / 4), dim3(256), 0, st, X1, X2, Y, rows,
+                     ry, d, out1, out2);
+}
+
 // ------------------------------------------------------------------- copies
 // dst[i][0..n) = src[i][0..n) for pointer tables of length cnt; a null
 // source marks an unused entry.
