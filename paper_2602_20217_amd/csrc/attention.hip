@@ -27,6 +27,9 @@ constexpr int TILE = 64;  // positions per LDS tile of the split kernel
 #ifndef KS_BAT_ST
 #define KS_BAT_ST 2  // LDS ring stages of the batched kernel
 #endif
+#ifndef KS_BAT_CB
+#define KS_BAT_CB 1  // 16-vector query blocks per wave of the batched kernel
+#endif
 
 // s_waitcnt immediate: vmcnt = n, expcnt and lgkmcnt not waited for
 __device__ constexpr int vmcnt_imm_a(int n) {
@@ -346,7 +349,9 @@ __global__ __launch_bounds__(64 * S) void k_attn_dec(
   int Lmax = 0;  // longest row of the workgroup
   for (int r = r0; r < min(M, r0 + RB); ++r) Lmax = max(Lmax, len[r]);
   const int cnt = min(TILE, Lmax - t0);  // keys of this tile any column uses (may be <= 0)
-  // queries as hi + lo bf16 (waits for the query loads only)
+  // queries as hi + lo bf16 (waits for the query loads only), scaled by
+  // log2(e) / sqrt(HD): scores in base-2 units, probabilities powers of two
+  const float qscale = 1.4426950408889634f / sqrtf((float)HD);
   bf16x8_d qh[CB][4], ql[CB][4];
 #pragma unroll
   for (int b = 0; b < CB; ++b)
@@ -356,7 +361,7 @@ __global__ __launch_bounds__(64 * S) void k_attn_dec(
       const float xs[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const float x = Lj[b] > 0 ? xs[e] : 0.f;
+        const float x = Lj[b] > 0 ? xs[e] * qscale : 0.f;
         const __bf16 h = (__bf16)x;
         qh[b][ks][e] = h;
         ql[b][ks][e] = (__bf16)(x - (float)h);
@@ -391,7 +396,6 @@ __global__ __launch_bounds__(64 * S) void k_attn_dec(
         }
       }
     }
-    const float scale = 1.0f / sqrtf((float)HD);
 #pragma unroll
     for (int b = 0; b < CB; ++b) {
       const int cj = min(TILE, Lj[b] - t0);  // keys of this tile the column uses
@@ -400,7 +404,7 @@ __global__ __launch_bounds__(64 * S) void k_attn_dec(
       for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
-          sc[b][kt][v] = 16 * kt + 4 * g + v < cj ? sc[b][kt][v] * scale : -FLT_MAX;
+          sc[b][kt][v] = 16 * kt + 4 * g + v < cj ? sc[b][kt][v] : -FLT_MAX;
           mt = fmaxf(mt, sc[b][kt][v]);
         }
       mt = fmaxf(mt, __shfl_xor(mt, 16));
@@ -410,7 +414,7 @@ __global__ __launch_bounds__(64 * S) void k_attn_dec(
       for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
-          const float p = 16 * kt + 4 * g + v < cj ? __expf(sc[b][kt][v] - mt) : 0.f;
+          const float p = 16 * kt + 4 * g + v < cj ? __builtin_amdgcn_exp2f(sc[b][kt][v] - mt) : 0.f;
           sc[b][kt][v] = p;
           ps += p;
         }
@@ -491,7 +495,7 @@ __global__ __launch_bounds__(64 * S) void k_attn_dec(
 #pragma unroll
     for (int s = 0; s < S; ++s) {
       const float* rs = record(s, c);
-      const float wt = rs[HD] == -FLT_MAX ? 0.f : __expf(rs[HD] - mx);
+      const float wt = rs[HD] == -FLT_MAX ? 0.f : __builtin_amdgcn_exp2f(rs[HD] - mx);
       s_w[c * S + s] = wt;
       lx = fmaf(rs[HD + 1], wt, lx);
     }
@@ -510,7 +514,7 @@ __global__ __launch_bounds__(64 * S) void k_attn_dec(
     float* dst = part + (((size_t)(r0 + c / G) * hq + kvh * G + c % G) * nsplit + split) * (HD + 2);
     dst[d] = acc;
     if (d == 0) {
-      dst[HD] = s_mx[c];
+      dst[HD] = s_mx[c] * 0.6931471805599453f;  // back to natural-log units
       dst[HD + 1] = s_lx[c];
     }
   }
@@ -518,17 +522,25 @@ __global__ __launch_bounds__(64 * S) void k_attn_dec(
 
 // Batched rows (prefill chunks, selection candidates), bf16 caches, head dim
 // 128.  Query vectors of one kv head are ordered qi = row * G + g; wave w of a
-// workgroup owns 16 consecutive ones.  The workgroup walks the 64-key tiles of
+// workgroup owns 16 CB consecutive ones in CB column blocks (each key fragment
+// and each transposed value read from LDS feeds CB matrix instructions; one
+// block measured fastest, as two need 240 VGPRs).  The workgroup walks the
+// 64-key tiles of
 // its split through a ring of ST LDS stages filled by direct global-to-LDS
 // loads ST - 1 tiles ahead (one barrier per tile, no staging registers); rows
 // are stored with 16-byte chunk c of row r at slot c ^ (r % 16).  Per tile and
 // wave: S^T = K Q^T (keys as rows, queries as hi + lo bf16 columns), an online
 // softmax per query column (two cross-lane steps per statistic), then O += P V
 // with the probabilities (bf16) taken from the score registers and the value
-// operand from transposing LDS reads in the same key order.  Tile rows at or
-// past max_len repeat row max_len - 1 (finite; their probability is 0).
-// Partials use the layout of the split kernels.
-template <int NW, int ST>
+// operand from transposing LDS reads in the same key order.  The softmax is
+// kept light, as the vector ALU and not the matrix unit bounds this kernel:
+// scores arrive in base-2 units (queries pre-scaled), keys are masked only in
+// tiles that reach past the shortest column of the wave, and the rescale of
+// the running output is skipped when no column's max moved (its factor would
+// be exactly 1).  Tile rows at or past max_len repeat row max_len - 1 (finite;
+// their probability is 0).  Partials use the layout of the split kernels
+// (max in natural-log units).
+template <int NW, int ST, int CB>
 __global__ __launch_bounds__(NW * 64) void k_attn_bat(int M, int hq, int hkv, int n_max,
                                                       const float* __restrict__ q,
                                                       const bf16_t* __restrict__ kc,
@@ -538,6 +550,7 @@ __global__ __launch_bounds__(NW * 64) void k_attn_bat(int M, int hq, int hkv, in
                                                       float* __restrict__ part, int nsplit) {
   constexpr int HD = 128;
   constexpr int PPW = 32 / NW;  // 1 KiB pieces per wave per tile
+  constexpr int QW = 16 * CB;   // query vectors per wave
   __shared__ __align__(16) uint4 KV[ST][2 * TILE * 16];
   const int split = blockIdx.x, kvh = blockIdx.y;
   const int G = hq / hkv;
@@ -570,12 +583,20 @@ __global__ __launch_bounds__(NW * 64) void k_attn_bat(int M, int hq, int hkv, in
   for (int s = 0; s < ST - 1; ++s)
     if (s < ntile) issue(s, s);
 
-  // query column j of this wave: vector qi = qb + 16 w + j
-  const int qi = blockIdx.z * NW * 16 + 16 * w + j;
-  const bool qok = qi < NQ;
-  const int lim = qok ? min(len[qi / G], end) : 0;  // keys of column j in this split
-  bf16x8_d qh[4], ql[4];
-  {
+  // query column j of block b of this wave: vector qb + 16 b + j.  Queries are
+  // scaled by log2(e) / sqrt(HD), so scores are in base-2 units and the
+  // probabilities are plain powers of two.
+  const float qscale = 1.4426950408889634f / sqrtf((float)HD);
+  const int qb = (blockIdx.z * NW + w) * QW;
+  int lim[CB];      // keys of the column in this split
+  int lim_min = end;  // fewest keys over the wave's columns with a query
+  bf16x8_d qh[CB][4], ql[CB][4];
+#pragma unroll
+  for (int b = 0; b < CB; ++b) {
+    const int qi = qb + 16 * b + j;
+    const bool qok = qi < NQ;
+    lim[b] = qok ? min(len[qi / G], end) : 0;
+    lim_min = min(lim_min, qok ? lim[b] : end);
     const int row = qok ? qi / G : 0;
     const int h = kvh * G + (qok ? qi % G : 0);
     const float* qv = q + ((size_t)row * hq + h) * HD + 8 * g;
@@ -586,84 +607,112 @@ __global__ __launch_bounds__(NW * 64) void k_attn_bat(int M, int hq, int hkv, in
       const float xs[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const __bf16 hh = (__bf16)xs[e];
-        qh[ks][e] = hh;
-        ql[ks][e] = (__bf16)(xs[e] - (float)hh);
+        const float x = xs[e] * qscale;
+        const __bf16 hh = (__bf16)x;
+        qh[b][ks][e] = hh;
+        ql[b][ks][e] = (__bf16)(x - (float)hh);
       }
     }
   }
-  const float scale = 1.0f / sqrtf((float)HD);
-  f32x4_d o[8];
 #pragma unroll
-  for (int dt = 0; dt < 8; ++dt) o[dt] = f32x4_d{0.f, 0.f, 0.f, 0.f};
-  float m_run = -FLT_MAX, l_run = 0.f;
+  for (int o_ = 32; o_ >= 1; o_ >>= 1) lim_min = min(lim_min, __shfl_xor(lim_min, o_));
+  f32x4_d o[CB][8];
+  float m_run[CB], l_run[CB];
+#pragma unroll
+  for (int b = 0; b < CB; ++b) {
+    m_run[b] = -FLT_MAX;
+    l_run[b] = 0.f;
+#pragma unroll
+    for (int dt = 0; dt < 8; ++dt) o[b][dt] = f32x4_d{0.f, 0.f, 0.f, 0.f};
+  }
   const int s4 = (lane & 15) >> 2, u4 = lane & 3;
 
-  for (int it = 0; it < ntile; ++it) {
+  auto step = [&](int it, int buf) {
     // tile it has landed once at most ST - 2 later tiles are in flight; the
     // barrier needs no fence (see k_gemm_tiled)
     if (it + ST - 2 < ntile) __builtin_amdgcn_s_waitcnt(vmcnt_imm_a(PPW * (ST - 2)));
     else __builtin_amdgcn_s_waitcnt(vmcnt_imm_a(0));
     __builtin_amdgcn_s_barrier();
     __asm__ volatile("" ::: "memory");
-    if (it + ST - 1 < ntile) issue(it + ST - 1, (it + ST - 1) % ST);
-    const uint4* Kt = &KV[it % ST][0];
-    const char* Vb = (const char*)&KV[it % ST][TILE * 16];
+    if (it + ST - 1 < ntile) issue(it + ST - 1, (buf + ST - 1) % ST);
+    const uint4* Kt = &KV[buf][0];
+    const char* Vb = (const char*)&KV[buf][TILE * 16];
     const int t0 = start + it * TILE;
-    f32x4_d sc[4];
+    // keys past a column's length only in tiles that reach past the shortest
+    // column of the wave (wave-uniform)
+    const bool edge = t0 + TILE > lim_min;
+    // S^T per column block; each key fragment feeds every block
+    f32x4_d sc[CB][4];
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt) {
-      sc[kt] = f32x4_d{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int b = 0; b < CB; ++b) sc[b][kt] = f32x4_d{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) {
         const int c = 4 * ks + g;
         const bf16x8_d kf = __builtin_bit_cast(bf16x8_d, Kt[(16 * kt + j) * 16 + (c ^ j)]);
-        sc[kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qh[ks], sc[kt], 0, 0, 0);
-        sc[kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, ql[ks], sc[kt], 0, 0, 0);
+#pragma unroll
+        for (int b = 0; b < CB; ++b) {
+          sc[b][kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qh[b][ks], sc[b][kt], 0, 0, 0);
+          sc[b][kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, ql[b][ks], sc[b][kt], 0, 0, 0);
+        }
       }
     }
-    float mt = -FLT_MAX;
+    bf16x8_d pa[CB][2];
 #pragma unroll
-    for (int kt = 0; kt < 4; ++kt)
+    for (int b = 0; b < CB; ++b) {
+      if (edge) {
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int key = t0 + 16 * kt + 4 * g + v;
-        sc[kt][v] = key < lim ? sc[kt][v] * scale : -FLT_MAX;
-        mt = fmaxf(mt, sc[kt][v]);
+        for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+          for (int v = 0; v < 4; ++v)
+            if (t0 + 16 * kt + 4 * g + v >= lim[b]) sc[b][kt][v] = -FLT_MAX;
       }
-    mt = fmaxf(mt, __shfl_xor(mt, 16));
-    mt = fmaxf(mt, __shfl_xor(mt, 32));
-    const float m_new = fmaxf(m_run, mt);
-    const float alpha = m_run == -FLT_MAX ? 0.f : __expf(m_run - m_new);
-    float ps = 0.f;
+      float mt = -FLT_MAX;
 #pragma unroll
-    for (int kt = 0; kt < 4; ++kt)
+      for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int key = t0 + 16 * kt + 4 * g + v;
-        const float p = key < lim ? __expf(sc[kt][v] - m_new) : 0.f;
-        sc[kt][v] = p;
-        ps += p;
+        for (int v = 0; v < 4; ++v) mt = fmaxf(mt, sc[b][kt][v]);
+      mt = fmaxf(mt, __shfl_xor(mt, 16));
+      mt = fmaxf(mt, __shfl_xor(mt, 32));
+      const float m_new = fmaxf(m_run[b], mt);
+      float ps = 0.f;
+#pragma unroll
+      for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          // masked scores give 2^(-huge) = 0
+          const float p = __builtin_amdgcn_exp2f(sc[b][kt][v] - m_new);
+          sc[b][kt][v] = p;
+          ps += p;
+        }
+      ps += __shfl_xor(ps, 16);
+      ps += __shfl_xor(ps, 32);
+      // a column whose max moved rescales its sum and output rows; when no
+      // column of the wave moved the factor is exactly 1 and is skipped
+      if (__ballot(m_new != m_run[b])) {
+        const float alpha = m_run[b] == -FLT_MAX ? 0.f : __builtin_amdgcn_exp2f(m_run[b] - m_new);
+        l_run[b] *= alpha;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const float av = __shfl(alpha, 4 * g + v);
+#pragma unroll
+          for (int dt = 0; dt < 8; ++dt) o[b][dt][v] *= av;
+        }
       }
-    ps += __shfl_xor(ps, 16);
-    ps += __shfl_xor(ps, 32);
-    l_run = l_run * alpha + ps;
-    m_run = m_new;
-    // output rows are query columns 4 g + v: rescale by their alpha
+      l_run[b] += ps;
+      m_run[b] = m_new;
 #pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const float av = __shfl(alpha, 4 * g + v);
+      for (int k2 = 0; k2 < 2; ++k2)
 #pragma unroll
-      for (int dt = 0; dt < 8; ++dt) o[dt][v] *= av;
+        for (int v = 0; v < 4; ++v) {
+          pa[b][k2][v] = (__bf16)sc[b][2 * k2][v];
+          pa[b][k2][4 + v] = (__bf16)sc[b][2 * k2 + 1][v];
+        }
     }
+    // O += P V; each transposed value operand feeds every block
 #pragma unroll
     for (int k2 = 0; k2 < 2; ++k2) {
-      bf16x8_d pa;
-#pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        pa[v] = (__bf16)sc[2 * k2][v];
-        pa[4 + v] = (__bf16)sc[2 * k2 + 1][v];
-      }
 #pragma unroll
       for (int dt = 0; dt < 8; ++dt) {
         bf16x4_d h2[2];
@@ -681,28 +730,40 @@ __global__ __launch_bounds__(NW * 64) void k_attn_bat(int M, int hq, int hkv, in
           vbv[e] = h2[0][e];
           vbv[4 + e] = h2[1][e];
         }
-        o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa, vbv, o[dt], 0, 0, 0);
+#pragma unroll
+        for (int b = 0; b < CB; ++b)
+          o[b][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa[b][k2], vbv, o[b][dt], 0, 0, 0);
       }
     }
+  };
+  // the ring position is a constant of each unrolled copy
+  for (int it0 = 0; it0 < ntile; it0 += ST) {
+#pragma unroll
+    for (int u = 0; u < ST; ++u)
+      if (it0 + u < ntile) step(it0 + u, u);
   }
 
-  // partials: O rows are query columns 4 g + v, dims 16 dt + j
-  const int qb = blockIdx.z * NW * 16 + 16 * w;
+  // partials: O rows of block b are query columns 16 b + 4 g + v, dims 16 dt + j;
+  // the max goes back to natural-log units
 #pragma unroll
-  for (int v = 0; v < 4; ++v) {
-    const int qv = qb + 4 * g + v;
-    const int lv = __shfl(lim, 4 * g + v);
-    if (qv >= NQ || lv <= start) continue;
-    const int row = qv / G, h = kvh * G + qv % G;
-    float* dst = part + (((size_t)row * hq + h) * nsplit + split) * (HD + 2);
+  for (int b = 0; b < CB; ++b) {
 #pragma unroll
-    for (int dt = 0; dt < 8; ++dt) dst[16 * dt + j] = o[dt][v];
-  }
-  if (g == 0 && qok && lim > start) {
-    const int row = qi / G, h = kvh * G + qi % G;
-    float* dst = part + (((size_t)row * hq + h) * nsplit + split) * (HD + 2);
-    dst[HD] = m_run;
-    dst[HD + 1] = l_run;
+    for (int v = 0; v < 4; ++v) {
+      const int qv = qb + 16 * b + 4 * g + v;
+      const int lv = __shfl(lim[b], 4 * g + v);
+      if (qv >= NQ || lv <= start) continue;
+      const int row = qv / G, h = kvh * G + qv % G;
+      float* dst = part + (((size_t)row * hq + h) * nsplit + split) * (HD + 2);
+#pragma unroll
+      for (int dt = 0; dt < 8; ++dt) dst[16 * dt + j] = o[b][dt][v];
+    }
+    const int qi = qb + 16 * b + j;
+    if (g == 0 && qi < NQ && lim[b] > start) {
+      const int row = qi / G, h = kvh * G + qi % G;
+      float* dst = part + (((size_t)row * hq + h) * nsplit + split) * (HD + 2);
+      dst[HD] = m_run[b] * 0.6931471805599453f;
+      dst[HD + 1] = l_run[b];
+    }
   }
 }
 
@@ -712,205 +773,6 @@ typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 __device__ inline uint32_t pack2(float a, float b) {
   return (uint32_t)f2bf(a) | ((uint32_t)f2bf(b) << 16);
-}
-
-// Batched-row attention with matrix instructions (bf16 cache, head dim 128),
-// used for prefill chunks and the candidate rows of the selection DP.
-//
-// Query vectors of one kv head are ordered qi = row * G + g; a wave owns 16
-// consecutive ones, a workgroup NWAVE waves.  Per 64-key tile of the split, K
-// (rows padded to 272 bytes) and V (transposed, rows padded to 136 bytes) are
-// staged in LDS.  Scores are computed transposed, S^T = K Q^T, with keys as the
-// rows of 16x16x32 MFMAs: a lane then holds 16 scores of a single query vector,
-// so the softmax statistics need only two cross-lane steps, and the
-// probabilities are already laid out as the A operand of O += P V (the k index
-// of that product is permuted identically in P and V).  Queries enter as hi +
-// lo bf16 pairs; probabilities as bf16.  Partials use the layout of the split
-// kernel above.
-template <int NWAVE>
-__global__ __launch_bounds__(NWAVE * 64) void k_attn_mfma(
-    int M, int hq, int hkv, int n_max, const float* __restrict__ q,
-    const bf16_t* __restrict__ kc, const bf16_t* __restrict__ vc,
-    const int32_t* __restrict__ len, int span, float* __restrict__ part, int nsplit) {
-  constexpr int HD = 128;
-  constexpr int KT = 64;          // keys per tile
-  constexpr int KSTR = HD + 8;    // K row stride (bf16)
-  constexpr int VSTR = KT + 4;    // transposed V row stride (bf16)
-  constexpr int NT = NWAVE * 64;  // threads
-  constexpr int NCH = KT * 16 / NT;
-  static_assert((KT * 16) % NT == 0, "staging");
-  constexpr float NEG = -1.0e30f;
-  __shared__ __align__(16) bf16_t Ks[KT * KSTR];
-  __shared__ __align__(16) bf16_t Vt[HD * VSTR];
-  __shared__ int s_len[NWAVE * 16];
-
-  const int split = blockIdx.x, kvh = blockIdx.y;
-  const int G = hq / hkv;
-  const int NQ = M * G;
-  const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int qb = blockIdx.z * NWAVE * 16;
-  const int j = lane & 15, g4 = lane >> 4;
-  const int start = split * span;
-  const float scale = 1.0f / sqrtf((float)HD);
-
-  for (int t = threadIdx.x; t < NWAVE * 16; t += NT) {
-    const int qi = qb + t;
-    s_len[t] = qi < NQ ? len[qi / G] : 0;
-  }
-  __syncthreads();
-  int maxlen = 0;
-  for (int t = 0; t < NWAVE * 16; ++t) maxlen = max(maxlen, s_len[t]);
-  const int end = min(maxlen, start + span);
-  if (start >= end) return;
-
-  const int qi = qb + wave * 16 + j;
-  const int lim = min(s_len[wave * 16 + j], end);  // keys of column j in this split
-  bf16x8_t qh[4], ql[4];
-  {
-    const bool ok = qi < NQ;
-    const int row = ok ? qi / G : 0;
-    const int h = kvh * G + (ok ? qi % G : 0);
-    const float* qv = q + ((size_t)row * hq + h) * HD + 8 * g4;
-#pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-      float4 x0 = make_float4(0.f, 0.f, 0.f, 0.f), x1 = x0;
-      if (ok) {
-        x0 = *(const float4*)(qv + 32 * ks);
-        x1 = *(const float4*)(qv + 32 * ks + 4);
-      }
-      const float xs[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
-      u32x4_t hv, lv;
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        const float a = xs[2 * k], b = xs[2 * k + 1];
-        const bf16_t ha = f2bf(a), hb = f2bf(b);
-        hv[k] = (uint32_t)ha | ((uint32_t)hb << 16);
-        lv[k] = pack2(a - bf2f(ha), b - bf2f(hb));
-      }
-      qh[ks] = __builtin_bit_cast(bf16x8_t, hv);
-      ql[ks] = __builtin_bit_cast(bf16x8_t, lv);
-    }
-  }
-  f32x4_t o[8];
-#pragma unroll
-  for (int dt = 0; dt < 8; ++dt) o[dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  float m_run = NEG, l_run = 0.f;
-
-  const bf16_t* kbase = kc + (size_t)kvh * n_max * HD;
-  const bf16_t* vbase = vc + (size_t)kvh * n_max * HD;
-  for (int t0 = start; t0 < end; t0 += KT) {
-    const int cnt = min(KT, end - t0);
-    uint4 kr[NCH], vr[NCH];
-#pragma unroll
-    for (int u = 0; u < NCH; ++u) {
-      const int c = threadIdx.x + NT * u;
-      const int r = min(c >> 4, cnt - 1), ch = c & 15;
-      const size_t off = (size_t)(t0 + r) * HD + ch * 8;
-      kr[u] = *(const uint4*)(kbase + off);
-      vr[u] = *(const uint4*)(vbase + off);
-    }
-#pragma unroll
-    for (int u = 0; u < NCH; ++u) {
-      const int c = threadIdx.x + NT * u;
-      const int r = c >> 4, ch = c & 15;
-      *(uint4*)&Ks[r * KSTR + ch * 8] = kr[u];
-      const uint32_t w[4] = {vr[u].x, vr[u].y, vr[u].z, vr[u].w};
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        Vt[(ch * 8 + 2 * e) * VSTR + r] = (bf16_t)(w[e] & 0xFFFF);
-        Vt[(ch * 8 + 2 * e + 1) * VSTR + r] = (bf16_t)(w[e] >> 16);
-      }
-    }
-    __syncthreads();
-
-    // S^T = K Q^T: s[kt][v] = score(key t0 + 16 kt + 4 g4 + v, query column j)
-    f32x4_t s[4];
-#pragma unroll
-    for (int kt = 0; kt < 4; ++kt) {
-      s[kt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
-        const bf16x8_t a = __builtin_bit_cast(
-            bf16x8_t, *(const u32x4_t*)&Ks[(16 * kt + j) * KSTR + 32 * ks + 8 * g4]);
-        s[kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qh[ks], s[kt], 0, 0, 0);
-        s[kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, ql[ks], s[kt], 0, 0, 0);
-      }
-    }
-    float mt = NEG;
-#pragma unroll
-    for (int kt = 0; kt < 4; ++kt)
-#pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int key = t0 + 16 * kt + 4 * g4 + v;
-        s[kt][v] = key < lim ? s[kt][v] * scale : NEG;
-        mt = fmaxf(mt, s[kt][v]);
-      }
-    mt = fmaxf(mt, __shfl_xor(mt, 16));
-    mt = fmaxf(mt, __shfl_xor(mt, 32));
-    const float m_new = fmaxf(m_run, mt);
-    const float alpha = __expf(m_run - m_new);
-    float ps = 0.f;
-#pragma unroll
-    for (int kt = 0; kt < 4; ++kt)
-#pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int key = t0 + 16 * kt + 4 * g4 + v;
-        const float p = key < lim ? __expf(s[kt][v] - m_new) : 0.f;
-        s[kt][v] = p;
-        ps += p;
-      }
-    ps += __shfl_xor(ps, 16);
-    ps += __shfl_xor(ps, 32);
-    l_run = l_run * alpha + ps;
-    m_run = m_new;
-    // rows of O are query vectors 4 g4 + v: rescale by their alpha
-#pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const float av = __shfl(alpha, 4 * g4 + v);
-#pragma unroll
-      for (int dt = 0; dt < 8; ++dt) o[dt][v] *= av;
-    }
-    // O += P V over two 32-key steps; element e of a lane group g4 is key
-    // 4 g4 + e (e < 4) or 16 + 4 g4 + e - 4 (e >= 4) of the step
-#pragma unroll
-    for (int k2 = 0; k2 < 2; ++k2) {
-      u32x4_t pv;
-      pv[0] = pack2(s[2 * k2][0], s[2 * k2][1]);
-      pv[1] = pack2(s[2 * k2][2], s[2 * k2][3]);
-      pv[2] = pack2(s[2 * k2 + 1][0], s[2 * k2 + 1][1]);
-      pv[3] = pack2(s[2 * k2 + 1][2], s[2 * k2 + 1][3]);
-      const bf16x8_t pa = __builtin_bit_cast(bf16x8_t, pv);
-#pragma unroll
-      for (int dt = 0; dt < 8; ++dt) {
-        const bf16_t* vrow = &Vt[(16 * dt + j) * VSTR + 32 * k2 + 4 * g4];
-        const uint2 lo = *(const uint2*)vrow;
-        const uint2 hi = *(const uint2*)(vrow + 16);
-        const u32x4_t bv = {lo.x, lo.y, hi.x, hi.y};
-        o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa, __builtin_bit_cast(bf16x8_t, bv),
-                                                        o[dt], 0, 0, 0);
-      }
-    }
-    __syncthreads();
-  }
-
-  // partials: O rows are query vectors 4 g4 + v, columns dims 16 dt + j
-#pragma unroll
-  for (int v = 0; v < 4; ++v) {
-    const int t = wave * 16 + 4 * g4 + v;
-    const int qv = qb + t;
-    if (qv >= NQ || s_len[t] <= start) continue;
-    const int row = qv / G, h = kvh * G + qv % G;
-    float* dst = part + (((size_t)row * hq + h) * nsplit + split) * (HD + 2);
-#pragma unroll
-    for (int dt = 0; dt < 8; ++dt) dst[16 * dt + j] = o[dt][v];
-  }
-  if (g4 == 0 && qi < NQ && s_len[wave * 16 + j] > start) {
-    const int row = qi / G, h = kvh * G + qi % G;
-    float* dst = part + (((size_t)row * hq + h) * nsplit + split) * (HD + 2);
-    dst[HD] = m_run;
-    dst[HD + 1] = l_run;
-  }
 }
 
 // One workgroup of 4 waves per (row, query head); output dims lane -> (2 lane,
@@ -1091,10 +953,11 @@ void attn_split(const AttnArgs& a, hipStream_t st) {
   } else if (a.hd == 128 && a.tiles > 1) {
     // batched rows: matrix-instruction kernel, 64 query vectors per workgroup
     const int span = TILE * a.tiles;
-    dim3 g2((a.max_len + span - 1) / span, a.hkv, (a.M * G + 16 * KS_BAT_NW - 1) / (16 * KS_BAT_NW));
-    hipLaunchKernelGGL((k_attn_bat<KS_BAT_NW, KS_BAT_ST>), g2, dim3(64 * KS_BAT_NW), 0, st, a.M,
-                       a.hq, a.hkv, a.n_max, a.q, (const bf16_t*)a.kc, (const bf16_t*)a.vc, a.len,
-                       a.max_len, span, a.part, a.nsplit);
+    constexpr int QWG = 16 * KS_BAT_NW * KS_BAT_CB;  // query vectors per workgroup
+    dim3 g2((a.max_len + span - 1) / span, a.hkv, (a.M * G + QWG - 1) / QWG);
+    hipLaunchKernelGGL((k_attn_bat<KS_BAT_NW, KS_BAT_ST, KS_BAT_CB>), g2, dim3(64 * KS_BAT_NW), 0,
+                       st, a.M, a.hq, a.hkv, a.n_max, a.q, (const bf16_t*)a.kc,
+                       (const bf16_t*)a.vc, a.len, a.max_len, span, a.part, a.nsplit);
   } else if (a.hd == 128) {
     if (nq <= 4) KS_ATTN(128, true, 1); else KS_ATTN(128, true, 8);
   } else {
