@@ -233,9 +233,9 @@ void gemm_bf16_skinny(const GemmArgs& g, hipStream_t st) {
 }
 
 // ------------------------------------------------------------------- tiled
-// Batched rows (prefill chunks, selection DP).  Workgroup tile 128 rows x 128
-// columns, 4 waves as 2 x 2 with 64 x 64 wave tiles (4 x 4 MFMAs).  A 32-wide k
-// step of the workgroup is 16 operand tiles of 1 KiB (8 of A, 8 of W), each
+// Batched rows (prefill chunks, selection DP).  Workgroup tile 64 NWM rows x
+// 16 NWN WN columns, NWM x NWN waves with 64 x 16 WN wave tiles (4 x WN MFMAs).
+// A 32-wide k step of the workgroup is 4 NWM + NWN WN operand tiles of 1 KiB, each
 // laid out in LDS in MFMA register order (lane l at byte 16 l: row l % 16,
 // k 8 (l / 16)..), so every fragment read is one conflict-free 16-byte read.
 // The tiles travel with direct global-to-LDS loads (one 1 KiB load per tile:
@@ -252,14 +252,20 @@ __device__ constexpr int vmcnt_imm(int n) {
   return (n & 15) | (7 << 4) | (15 << 8) | ((n >> 4) << 14);
 }
 
-template <int EPI, int ST>
-__global__ __launch_bounds__(256) void k_gemm_tiled(int M, int N, int K,
+template <int EPI, int ST, int WN, int NWM, int NWN>
+__global__ __launch_bounds__(64 * NWM * NWN) void k_gemm_tiled(int M, int N, int K,
                                                     const bf16_t* __restrict__ A, int lda,
                                                     const bf16_t* __restrict__ Wp, float* out,
                                                     int ldo, const float* res, int ldres,
                                                     bf16_t* ohi, bf16_t* olo, int ldact, int MB,
                                                     int NB, int SK, float* __restrict__ part) {
-  __shared__ __align__(16) bf16_t Sg[ST][16 * 512];
+  constexpr int WM = 4;           // 16-row fragments per wave (64 rows)
+  constexpr int NWV = NWM * NWN;  // waves: NWM along M, NWN along N
+  constexpr int PA = NWM * WM;    // A pieces per step: 64 NWM rows
+  constexpr int PB = NWN * WN;   // W pieces per step: 16 NWN WN columns
+  constexpr int PPW = (PA + PB) / NWV;
+  static_assert((PA + PB) % NWV == 0, "pieces split evenly over the waves");
+  __shared__ __align__(16) bf16_t Sg[ST][(PA + PB) * 512];
   const int KT = K >> 5;
   const int NT = N >> 4;
   // XCD-aware logical block id (blocks are dealt round-robin over 8 XCDs)
@@ -268,45 +274,47 @@ __global__ __launch_bounds__(256) void k_gemm_tiled(int M, int N, int K,
   int lb = bid;
   if ((nblk & 7) == 0) lb = (bid & 7) * (nblk >> 3) + (bid >> 3);
   const int mb = lb % MB, nb = (lb / MB) % NB, ks = lb / (MB * NB);
-  const int m0 = mb * 128, nt0 = nb * 8;
+  const int m0 = mb * 64 * NWM, nt0 = nb * PB;
   const int kb = (ks * KT) / SK, nk = ((ks + 1) * KT) / SK - kb;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave & 1, wn = wave >> 1;
+  const int wm = wave % NWM, wn = wave / NWM;
 
-  // wave w moves pieces 4w..4w+3 of every step: pieces 0..7 are A tiles (rows
-  // m0 + 16 p ..), 8..15 W tiles nt0 + p - 8
-  const bf16_t* src[4];
+  // wave w moves pieces PPW w .. + PPW - 1 of every step: pieces 0..PA-1 are A
+  // tiles (rows m0 + 16 p ..), the rest W tiles nt0 + p - PA
+  const bf16_t* src[PPW];
+  int adv[PPW];  // elements per k step
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const int pc = 4 * wave + q;
-    if (pc < 8) {
+  for (int q = 0; q < PPW; ++q) {
+    const int pc = PPW * wave + q;
+    if (pc < PA) {
       const int row = min(m0 + 16 * pc + (lane & 15), M - 1);
       src[q] = A + (size_t)row * lda + (size_t)kb * 32 + (lane >> 4) * 8;
+      adv[q] = 32;
     } else {
-      const int nt = min(nt0 + pc - 8, NT - 1);
+      const int nt = min(nt0 + pc - PA, NT - 1);
       src[q] = Wp + ((size_t)nt * KT + kb) * 512 + lane * 8;
+      adv[q] = 512;
     }
   }
-  const bool is_a = wave < 2;  // waves 0, 1 move A tiles, waves 2, 3 W tiles
   auto issue = [&](int step, int buf) {
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const bf16_t* s_ = src[q] + (size_t)step * (is_a ? 32 : 512);
+    for (int q = 0; q < PPW; ++q) {
+      const bf16_t* s_ = src[q] + (size_t)step * adv[q];
       __builtin_amdgcn_global_load_lds(
           (const void*)s_,
-          (__attribute__((address_space(3))) void*)&Sg[buf][(4 * wave + q) * 512], 16, 0, 0);
+          (__attribute__((address_space(3))) void*)&Sg[buf][(PPW * wave + q) * 512], 16, 0, 0);
     }
   };
 #pragma unroll
   for (int s = 0; s < ST - 1; ++s)
     if (s < nk) issue(s, s);
 
-  f32x4 acc[4][4];
+  f32x4 acc[WM][WN];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < WM; ++i)
 #pragma unroll
-    for (int t = 0; t < 4; ++t) acc[i][t] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int t = 0; t < WN; ++t) acc[i][t] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   for (int it = 0; it < nk; ++it) {
     // step it has landed once at most the ST - 2 later steps are in flight.
@@ -314,35 +322,35 @@ __global__ __launch_bounds__(256) void k_gemm_tiled(int M, int N, int K,
     // step in flight): this wave's tile loads for step it are counted down
     // above, and its LDS reads of the stage refilled next were consumed by
     // the previous step's matrix instructions.
-    if (it + ST - 2 < nk) __builtin_amdgcn_s_waitcnt(vmcnt_imm(4 * (ST - 2)));
+    if (it + ST - 2 < nk) __builtin_amdgcn_s_waitcnt(vmcnt_imm(PPW * (ST - 2)));
     else __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
     __builtin_amdgcn_s_barrier();
     __asm__ volatile("" ::: "memory");
     if (it + ST - 1 < nk) issue(it + ST - 1, (it + ST - 1) % ST);
     const bf16_t* Sb = Sg[it % ST];
-    bf16x8 a[4], b[4];
+    bf16x8 a[WM], b[WN];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) a[i] = ld_frag(&Sb[(4 * wm + i) * 512 + lane * 8]);
+    for (int i = 0; i < WM; ++i) a[i] = ld_frag(&Sb[(WM * wm + i) * 512 + lane * 8]);
 #pragma unroll
-    for (int t = 0; t < 4; ++t) b[t] = ld_frag(&Sb[(8 + 4 * wn + t) * 512 + lane * 8]);
+    for (int t = 0; t < WN; ++t) b[t] = ld_frag(&Sb[(PA + WN * wn + t) * 512 + lane * 8]);
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < WM; ++i)
 #pragma unroll
-      for (int t = 0; t < 4; ++t)
+      for (int t = 0; t < WN; ++t)
         acc[i][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[t], acc[i][t], 0, 0, 0);
   }
 
   const int mw = m0 + wm * 64;
-  const int nw = nt0 + wn * 4;
+  const int nw = nt0 + wn * WN;
   float* pk = part + (size_t)ks * M * N;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
+  for (int i = 0; i < WM; ++i) {
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
       const int m = mw + i * 16 + 4 * (lane >> 4) + v;
       if (EPI == EPI_SWIGLU) {
 #pragma unroll
-        for (int t = 0; t < 4; ++t) {
+        for (int t = 0; t < WN; ++t) {
           const float up = __shfl(acc[i][t][v], (lane & 48) | ((lane + 8) & 15));
           if (m >= M || nw + t >= NT || (lane & 15) >= 8) continue;
           const int c = (nw + t) * 8 + (lane & 15);
@@ -351,7 +359,7 @@ __global__ __launch_bounds__(256) void k_gemm_tiled(int M, int N, int K,
       } else {
         if (m >= M) continue;
 #pragma unroll
-        for (int t = 0; t < 4; ++t) {
+        for (int t = 0; t < WN; ++t) {
           if (nw + t >= NT) continue;
           const int n = (nw + t) * 16 + (lane & 15);
           float sv = acc[i][t][v];
@@ -389,12 +397,12 @@ __global__ __launch_bounds__(256) void k_splitk_reduce(int M, int N, int SK,
   *(float4*)&out[(size_t)m * ldo + n] = s;
 }
 
-void gemm_bf16_tiled(const GemmArgs& g, hipStream_t st) {
-  constexpr int ST = 4;
+template <int ST, int WN, int NWM, int NWN>
+static void launch_tiled(const GemmArgs& g, hipStream_t st) {
   const int NT = g.N / 16;
   const int KT = g.K / 32;
-  const int MB = (g.M + 127) / 128;
-  const int NB = (NT + 7) / 8;
+  const int MB = (g.M + 64 * NWM - 1) / (64 * NWM);
+  const int NB = (NT + NWN * WN - 1) / (NWN * WN);
   // split K until about two workgroups per CU, keeping >= 16 k steps per split
   // and the partials within the caller's buffer
   int SK = 1;
@@ -407,17 +415,17 @@ void gemm_bf16_tiled(const GemmArgs& g, hipStream_t st) {
   const bf16_t* A = (const bf16_t*)g.A.hi;
   const bf16_t* W = (const bf16_t*)g.W;
   if (g.epi == EPI_SWIGLU)
-    hipLaunchKernelGGL((k_gemm_tiled<EPI_SWIGLU, ST>), grid, dim3(256), 0, st, g.M, g.N, g.K, A,
-                       g.A.ld, W, g.out, g.ldo, g.res, g.ldres, (bf16_t*)g.act_out.hi,
+    hipLaunchKernelGGL((k_gemm_tiled<EPI_SWIGLU, ST, WN, NWM, NWN>), grid, dim3(64 * NWM * NWN), 0, st, g.M, g.N,
+                       g.K, A, g.A.ld, W, g.out, g.ldo, g.res, g.ldres, (bf16_t*)g.act_out.hi,
                        (bf16_t*)g.act_out.lo, g.act_out.ld, MB, NB, 1, g.part);
   else if (g.epi == EPI_RESID)
-    hipLaunchKernelGGL((k_gemm_tiled<EPI_RESID, ST>), grid, dim3(256), 0, st, g.M, g.N, g.K, A,
-                       g.A.ld, W, g.out, g.ldo, g.res, g.ldres, nullptr, nullptr, 0, MB, NB, SK,
-                       g.part);
+    hipLaunchKernelGGL((k_gemm_tiled<EPI_RESID, ST, WN, NWM, NWN>), grid, dim3(64 * NWM * NWN), 0, st, g.M, g.N, g.K,
+                       A, g.A.ld, W, g.out, g.ldo, g.res, g.ldres, nullptr, nullptr, 0, MB, NB,
+                       SK, g.part);
   else
-    hipLaunchKernelGGL((k_gemm_tiled<EPI_STORE, ST>), grid, dim3(256), 0, st, g.M, g.N, g.K, A,
-                       g.A.ld, W, g.out, g.ldo, g.res, g.ldres, nullptr, nullptr, 0, MB, NB, SK,
-                       g.part);
+    hipLaunchKernelGGL((k_gemm_tiled<EPI_STORE, ST, WN, NWM, NWN>), grid, dim3(64 * NWM * NWN), 0, st, g.M, g.N, g.K,
+                       A, g.A.ld, W, g.out, g.ldo, g.res, g.ldres, nullptr, nullptr, 0, MB, NB,
+                       SK, g.part);
   if (SK > 1) {
     const size_t n4 = (size_t)g.M * (g.N / 4);
     dim3 rg((unsigned)((n4 + 255) / 256));
@@ -428,6 +436,27 @@ void gemm_bf16_tiled(const GemmArgs& g, hipStream_t st) {
       hipLaunchKernelGGL(k_splitk_reduce<EPI_STORE>, rg, dim3(256), 0, st, g.M, g.N, SK, g.part,
                          g.out, g.ldo, g.res, g.ldres);
   }
+}
+
+// Workgroup tile 128 x 256 (8 waves of 64 x 64), 3 stages: measured on MI355X
+// at the selection shapes (400..1225 rows of the Llama-8B products) against
+// 128 x 128 / 4 waves (up to 1.3x slower: it moves 33% more operand bytes per
+// flop through the CU's load path), 256 x 128, 256 x 256, 64 x 128 wave tiles
+// and 2..5 stages.
+#ifndef KS_TILED_WN
+#define KS_TILED_WN 4
+#endif
+#ifndef KS_TILED_ST
+#define KS_TILED_ST 3
+#endif
+#ifndef KS_TILED_NWN
+#define KS_TILED_NWN 4
+#endif
+#ifndef KS_TILED_NWM
+#define KS_TILED_NWM 2
+#endif
+void gemm_bf16_tiled(const GemmArgs& g, hipStream_t st) {
+  launch_tiled<KS_TILED_ST, KS_TILED_WN, KS_TILED_NWM, KS_TILED_NWN>(g, st);
 }
 
 // --------------------------------------------------------------------- f32
