@@ -520,6 +520,283 @@ __global__ __launch_bounds__(64 * S) void k_attn_dec(
   }
 }
 
+// Decode / verify rows over long bf16 caches (head dim 128): a streaming
+// variant of k_attn_dec.  A workgroup of NW waves owns NW * tpw consecutive
+// 64-key tiles of one kv head (the split) and the same 16 CB query columns as
+// k_attn_dec.  Wave w walks tiles i NW + w (i < tpw, stopping at the longest
+// row of the workgroup); the key fragment of a 16x16x32 product is 16
+// contiguous bytes per lane, so keys go straight from memory into registers,
+// and values through the wave's own two-stage LDS ring (direct global-to-LDS
+// loads, rows at slot c ^ (r % 16)).  Tile i + 1's keys and values are
+// requested before tile i is computed, so every wave keeps two tiles in
+// flight and no barrier is needed until the end.  Per tile: S^T = K Q^T on
+// matrix instructions, an online base-2 softmax per column (queries
+// pre-scaled by log2(e) / sqrt(HD); keys masked only in tiles that reach past
+// the shortest column of the wave; the running output rescaled only when some
+// column's max moved, as the factor is otherwise exactly 1), then O += P V with
+// the value operand from transposing LDS reads.  The NW wave results are merged
+// in wave order into the split's partial, exactly as in k_attn_dec.  A column's
+// arithmetic depends only on its own query, its length and the split size, so
+// a verify row and the decode step at the same position give the same bits.
+template <int NW, int CB>
+__global__ __launch_bounds__(64 * NW) void k_attn_stream(
+    int M, int hq, int hkv, int n_max, const float* __restrict__ q,
+    const bf16_t* __restrict__ kc, const bf16_t* __restrict__ vc,
+    const int32_t* __restrict__ len, float* __restrict__ part, int nsplit, int tpw) {
+  constexpr int HD = 128;
+  constexpr int RS = HD + 4;  // LDS merge record per column: o, max, sum (bank-shifted)
+  constexpr int NCOL = 16 * CB;
+  static_assert(CB == 1 || CB == 2, "one or two column blocks");
+  static_assert(16 * RS + NCOL * (NW + 3) <= TILE * 64, "records and scratch fit a stage");
+  // the two ring stages are separate arrays, so the compiler can tell that the
+  // loads into one stage never alias reads of the other
+  __shared__ __align__(16) uint4 Vr0[NW][TILE * 16];
+  __shared__ __align__(16) uint4 Vr1[NW][TILE * 16];
+  const int split = blockIdx.x, kvh = blockIdx.y;
+  const int G = hq / hkv;
+  const int RB = NCOL / G;
+  const int r0 = blockIdx.z * RB;
+  const int lane = threadIdx.x & 63;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int start = split * NW * tpw * TILE;
+  const int nc = min(NCOL, (M - r0) * G);  // query columns with a row
+  const int j = lane & 15, g = lane >> 4;
+
+  // queries (column 16 b + j: row r0 + (16 b + j) / G, head kvh G + j % G, dims
+  // 32 ks + 8 g .. + 7) as hi + lo bf16, scaled to base-2 units
+  const float qscale = 1.4426950408889634f / sqrtf((float)HD);
+  int Lj[CB];
+  int lim_min = INT_MAX;  // shortest column of the workgroup with a row
+  bf16x8_d qh[CB][4], ql[CB][4];
+#pragma unroll
+  for (int b = 0; b < CB; ++b) {
+    const int rj = r0 + (16 * b + j) / G;
+    const bool qok = rj < M;
+    Lj[b] = qok ? len[rj] : 0;
+    if (qok) lim_min = min(lim_min, Lj[b]);
+    const float* qv = q + ((size_t)(qok ? rj : r0) * hq + kvh * G + j % G) * HD + 8 * g;
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      const float4 x0 = *(const float4*)(qv + 32 * ks), x1 = *(const float4*)(qv + 32 * ks + 4);
+      const float xs[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float x = qok ? xs[e] * qscale : 0.f;
+        const __bf16 h = (__bf16)x;
+        qh[b][ks][e] = h;
+        ql[b][ks][e] = (__bf16)(x - (float)h);
+      }
+    }
+  }
+#pragma unroll
+  for (int o_ = 32; o_ >= 1; o_ >>= 1) lim_min = min(lim_min, __shfl_xor(lim_min, o_));
+  int Lmax = 0;  // longest row of the workgroup
+  for (int r = r0; r < min(M, r0 + RB); ++r) Lmax = max(Lmax, len[r]);
+  // tiles of this wave holding a key below Lmax
+  const int first = start + w * TILE;
+  const int ntl = Lmax > first ? min(tpw, (Lmax - first + NW * TILE - 1) / (NW * TILE)) : 0;
+
+  const bf16_t* kb = kc + (size_t)kvh * n_max * HD;
+  const bf16_t* vb = vc + (size_t)kvh * n_max * HD;
+  bf16x8_d kr[2][16];  // key fragments of two tiles: [kt * 4 + ks]
+  auto issue = [&](int i, int buf) {
+    const int t0 = first + i * NW * TILE;
+#pragma unroll
+    for (int kt = 0; kt < 4; ++kt) {
+      const int row = min(t0 + 16 * kt + j, n_max - 1);
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks)
+        kr[buf][kt * 4 + ks] =
+            __builtin_bit_cast(bf16x8_d, *(const uint4*)(kb + (size_t)row * HD + 32 * ks + 8 * g));
+    }
+    const int rr0 = lane >> 4, slot = lane & 15;
+#pragma unroll
+    for (int p = 0; p < 16; ++p) {
+      const int rr = 4 * p + rr0;
+      const int row = min(t0 + rr, n_max - 1);
+      __builtin_amdgcn_global_load_lds(
+          (const void*)(vb + (size_t)row * HD + ((slot ^ (rr & 15)) << 3)),
+          (__attribute__((address_space(3))) void*)&(buf ? Vr1 : Vr0)[w][p * 64], 16, 0, 0);
+    }
+  };
+
+  float m_run[CB], l_run[CB];
+  f32x4_d o[CB][8];
+#pragma unroll
+  for (int b = 0; b < CB; ++b) {
+    m_run[b] = -FLT_MAX;
+    l_run[b] = 0.f;
+#pragma unroll
+    for (int dt = 0; dt < 8; ++dt) o[b][dt] = f32x4_d{0.f, 0.f, 0.f, 0.f};
+  }
+  const int s4 = (lane & 15) >> 2, u4 = lane & 3;
+  auto step = [&](int i, int buf) {
+    const bool more = i + 1 < ntl;
+    if (more) issue(i + 1, buf ^ 1);
+    const int t0 = first + i * NW * TILE;
+    const bool edge = t0 + TILE > lim_min;
+    f32x4_d sc[CB][4];
+#pragma unroll
+    for (int kt = 0; kt < 4; ++kt) {
+#pragma unroll
+      for (int b = 0; b < CB; ++b) sc[b][kt] = f32x4_d{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+        for (int b = 0; b < CB; ++b) {
+          sc[b][kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kr[buf][kt * 4 + ks], qh[b][ks],
+                                                              sc[b][kt], 0, 0, 0);
+          sc[b][kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kr[buf][kt * 4 + ks], ql[b][ks],
+                                                              sc[b][kt], 0, 0, 0);
+        }
+    }
+    bf16x8_d pa[CB][2];
+#pragma unroll
+    for (int b = 0; b < CB; ++b) {
+      if (edge) {
+#pragma unroll
+        for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+          for (int v = 0; v < 4; ++v)
+            if (t0 + 16 * kt + 4 * g + v >= Lj[b]) sc[b][kt][v] = -FLT_MAX;
+      }
+      float mt = -FLT_MAX;
+#pragma unroll
+      for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) mt = fmaxf(mt, sc[b][kt][v]);
+      mt = fmaxf(mt, __shfl_xor(mt, 16));
+      mt = fmaxf(mt, __shfl_xor(mt, 32));
+      const float m_new = fmaxf(m_run[b], mt);
+      float ps = 0.f;
+#pragma unroll
+      for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const float p = __builtin_amdgcn_exp2f(sc[b][kt][v] - m_new);
+          sc[b][kt][v] = p;
+          ps += p;
+        }
+      ps += __shfl_xor(ps, 16);
+      ps += __shfl_xor(ps, 32);
+      if (__ballot(m_new != m_run[b])) {
+        const float alpha = m_run[b] == -FLT_MAX ? 0.f : __builtin_amdgcn_exp2f(m_run[b] - m_new);
+        l_run[b] *= alpha;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const float av = __shfl(alpha, 4 * g + v);
+#pragma unroll
+          for (int dt = 0; dt < 8; ++dt) o[b][dt][v] *= av;
+        }
+      }
+      l_run[b] += ps;
+      m_run[b] = m_new;
+#pragma unroll
+      for (int k2 = 0; k2 < 2; ++k2)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          pa[b][k2][v] = (__bf16)sc[b][2 * k2][v];
+          pa[b][k2][4 + v] = (__bf16)sc[b][2 * k2 + 1][v];
+        }
+    }
+    // this tile's values have landed once at most the next tile's loads are in flight
+    if (more) __builtin_amdgcn_s_waitcnt(vmcnt_imm_a(32));
+    else __builtin_amdgcn_s_waitcnt(vmcnt_imm_a(0));
+    uint4* Vt = &(buf ? Vr1 : Vr0)[w][0];
+    const int cnt = min(TILE, Lmax - t0);
+    if (cnt < TILE) {
+      for (int c = cnt * 16 + lane; c < TILE * 16; c += 64) Vt[c] = make_uint4(0u, 0u, 0u, 0u);
+    }
+    const char* Vb = (const char*)Vt;
+#pragma unroll
+    for (int k2 = 0; k2 < 2; ++k2) {
+#pragma unroll
+      for (int dt = 0; dt < 8; ++dt) {
+        bf16x4_d h2[2];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int row = 32 * k2 + 16 * h + 4 * g + s4;
+          const int c = 2 * dt + (u4 >> 1);
+          const char* pp = Vb + row * 256 + ((c ^ (row & 15)) << 4) + ((u4 & 1) << 3);
+          h2[h] = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+              (__attribute__((address_space(3))) bf16x4_d*)pp);
+        }
+        bf16x8_d vbv;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          vbv[e] = h2[0][e];
+          vbv[4 + e] = h2[1][e];
+        }
+#pragma unroll
+        for (int b = 0; b < CB; ++b)
+          o[b][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa[b][k2], vbv, o[b][dt], 0, 0, 0);
+      }
+    }
+  };
+  if (ntl > 0) issue(0, 0);
+  // the ring position is a constant of each unrolled copy
+  for (int i0 = 0; i0 < ntl; i0 += 2) {
+    step(i0, 0);
+    if (i0 + 1 < ntl) step(i0 + 1, 1);
+  }
+
+  // wave results to LDS (the wave's own stages: block b in stage b): o[b][dt][v]
+  // is column 16 b + 4 g + v, dim 16 dt + j; the max and sum of column
+  // 16 b + c live in lane c.  Wave 0's first stage also holds the merge scratch.
+  float* s_w = (float*)&Vr0[0][0] + 16 * RS;
+  float* s_mx = s_w + NCOL * NW;
+  float* s_lx = s_mx + NCOL;
+  int* s_len = (int*)(s_lx + NCOL);
+#pragma unroll
+  for (int b = 0; b < CB; ++b) {
+    float* rec = b == 0 ? (float*)&Vr0[w][0] : (float*)&Vr1[w][0];
+#pragma unroll
+    for (int v = 0; v < 4; ++v)
+#pragma unroll
+      for (int dt = 0; dt < 8; ++dt) rec[(4 * g + v) * RS + 16 * dt + j] = o[b][dt][v];
+    if (lane < 16) {
+      rec[lane * RS + HD] = m_run[b];
+      rec[lane * RS + HD + 1] = l_run[b];
+    }
+  }
+  __syncthreads();
+  auto record = [&](int s, int c) -> const float* {
+    return (c < 16 ? (const float*)&Vr0[s][0] : (const float*)&Vr1[s][0]) + (c & 15) * RS;
+  };
+  if (threadIdx.x < nc) {  // wave 0, lane c: column c (its Lj[c / 16] is the column's length)
+    const int c = threadIdx.x;
+    float mx = -FLT_MAX;
+#pragma unroll
+    for (int s = 0; s < NW; ++s) mx = fmaxf(mx, record(s, c)[HD]);
+    float lx = 0.f;
+#pragma unroll
+    for (int s = 0; s < NW; ++s) {
+      const float* rs = record(s, c);
+      const float wt = rs[HD] == -FLT_MAX ? 0.f : __builtin_amdgcn_exp2f(rs[HD] - mx);
+      s_w[c * NW + s] = wt;
+      lx = fmaf(rs[HD + 1], wt, lx);
+    }
+    s_mx[c] = mx;
+    s_lx[c] = lx;
+    s_len[c] = CB == 1 || c < 16 ? Lj[0] : Lj[CB - 1];
+  }
+  __syncthreads();
+  // the split's partial of every column whose row reaches this split
+  for (int i = threadIdx.x; i < nc * HD; i += 64 * NW) {
+    const int c = i >> 7, d = i & (HD - 1);
+    if (s_len[c] <= start) continue;
+    float acc = 0.f;
+#pragma unroll
+    for (int s = 0; s < NW; ++s) acc = fmaf(record(s, c)[d], s_w[c * NW + s], acc);
+    float* dst = part + (((size_t)(r0 + c / G) * hq + kvh * G + c % G) * nsplit + split) * (HD + 2);
+    dst[d] = acc;
+    if (d == 0) {
+      dst[HD] = s_mx[c] * 0.6931471805599453f;  // back to natural-log units
+      dst[HD + 1] = s_lx[c];
+    }
+  }
+}
+
 // Batched rows (prefill chunks, selection candidates), bf16 caches, head dim
 // 128.  Query vectors of one kv head are ordered qi = row * G + g; wave w of a
 // workgroup owns 16 CB consecutive ones in CB column blocks (each key fragment
@@ -907,11 +1184,14 @@ int attn_rows_per_block(int G, bool batched) {
   return G >= 32 ? 1 : 32 / G;
 }
 
-// Decode / verify rows of bf16 caches with head dim 128 take k_attn_dec.
+// Decode / verify rows of bf16 caches with head dim 128 take k_attn_dec (1..5
+// tiles per split) or k_attn_stream (splits of a multiple of STREAM_NW tiles
+// above that).
+constexpr int STREAM_NW = 4;
 bool attn_dec_path(const AttnArgs& a) {
   const int G = a.hq / a.hkv;
   return a.dtype == KS_BF16 && a.hd == 128 && G <= 16 && 16 % G == 0 &&
-         a.rows_per_block == 1 && a.tiles >= 1 && a.tiles <= 5;
+         a.rows_per_block == 1 && a.tiles >= 1 && (a.tiles <= 5 || a.tiles % STREAM_NW == 0);
 }
 
 void attn_split(const AttnArgs& a, hipStream_t st) {
@@ -943,7 +1223,15 @@ void attn_split(const AttnArgs& a, hipStream_t st) {
     case 4: KS_DEC(4, CB_); break; \
     default: KS_DEC(5, CB_); break; \
   }
-    if (CB == 1) {
+    if (a.tiles > 5) {
+      const int tpw = a.tiles / STREAM_NW;
+      if (CB == 1)
+        hipLaunchKernelGGL((k_attn_stream<STREAM_NW, 1>), g3, dim3(64 * STREAM_NW), 0, st, a.M,
+                           a.hq, a.hkv, a.n_max, a.q, kc, vc, a.len, a.part, a.nsplit, tpw);
+      else
+        hipLaunchKernelGGL((k_attn_stream<STREAM_NW, 2>), g3, dim3(64 * STREAM_NW), 0, st, a.M,
+                           a.hq, a.hkv, a.n_max, a.q, kc, vc, a.len, a.part, a.nsplit, tpw);
+    } else if (CB == 1) {
       KS_DEC_S(1);
     } else {
       KS_DEC_S(2);

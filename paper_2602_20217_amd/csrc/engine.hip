@@ -47,12 +47,23 @@ namespace {
 constexpr int PB = 512;        // rows per batched attention / head pass
 // float32 split-K partials of the batched products (prefill chunks, selection)
 constexpr size_t GPART_BYTES = (size_t)64 << 20;
-// decode/verify splits: 64-position tiles per split, by cache size only (never
-// by row count, so a verify row and the decode step split alike).  Measured on
-// MI355X (split kernel + merge, 1..5 tiles, 1 and 5 rows): two tiles for caches
-// up to 2048 positions, three up to 5120, five above (a 160 KiB workgroup: up to
-// 10240 positions of 8 kv heads fit the 256 CUs in one round).
-int dec_tiles(int n_max) { return n_max <= 2048 ? 2 : n_max <= 5120 ? 3 : 5; }
+// decode/verify splits: 64-position tiles per split, by the model's cache size
+// and kv heads only (never by row count, so a verify row and the decode step
+// split alike).  Measured on MI355X (split kernel + merge, 1 and 5 rows): the
+// one-tile-per-wave kernel with two tiles for caches up to 2048 positions,
+// three up to 5120, five up to 12288 (a 160 KiB workgroup: up to 10240
+// positions of 8 kv heads fit the 256 CUs in one round); above, the streaming
+// kernel with 4 waves and as many tiles per wave (at least 2) as keep the
+// splits of all kv heads to one round of 256 workgroups.
+int dec_tiles(int n_max, int hkv) {
+  if (n_max <= 2048) return 2;
+  if (n_max <= 5120) return 3;
+  if (n_max <= 12288) return 5;
+  const int n_tiles = (n_max + 63) / 64;
+  const int splits = std::max(1, 256 / hkv);
+  const int tpw = (n_tiles + 4 * splits - 1) / (4 * splits);
+  return 4 * std::max(2, tpw);
+}
 constexpr int BAT_TILES = 16;  // prefill/DP: 1024 positions per split
 
 size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -76,7 +87,7 @@ Layout make_layout(const ks_model_desc& d, const ks_limits& lim) {
   y.LR = std::max(gam1, PB);
   y.nqkv = (d.hq + 2 * d.hkv) * d.hd;
   y.a2w = std::max(d.hq * d.hd, d.ffn);
-  const int ns_dec = attn_nsplit(d.n_max, dec_tiles(d.n_max));
+  const int ns_dec = attn_nsplit(d.n_max, dec_tiles(d.n_max, d.hkv));
   const int ns_bat = attn_nsplit(d.n_max, BAT_TILES);
   y.part_rows = PB;
   y.part_elems = std::max((size_t)16 * d.hq * ns_dec, (size_t)PB * d.hq * ns_bat) * (d.hd + 2);
@@ -295,7 +306,7 @@ void attn_rows(ks_ctx* c, int l, const float* xin, float* xout, int R, const int
                    c->bf() ? 1 : 0};
     PROF(c, KS_KC_QKV_POST, qkv_post(qp, c->st));
   }
-  const int tiles = batched ? BAT_TILES : dec_tiles(d.n_max);
+  const int tiles = batched ? BAT_TILES : dec_tiles(d.n_max, d.hkv);
   const int ns = attn_nsplit(d.n_max, tiles);
   const int step = batched ? PB : 16;
   for (int r0 = 0; r0 < R; r0 += step) {

@@ -1,6 +1,8 @@
 """GPU vs oracle parity of decode and verify rows over long caches, where the
 decode attention splits hold two, three and five 64-position tiles (cache
-sizes up to 2048, up to 5120 and above).  The cache holds seeded synthetic
+sizes up to 2048, up to 5120 and up to 12288), and beyond that the streaming
+kernel walks two or three tiles per wave (14000 and 70000 positions with the
+two kv heads of the small model).  The cache holds seeded synthetic
 keys/values up to a ragged length and NaN beyond it, so any read of a position
 past a row's length shows up in the result.  Every call goes through the C
 ABI; tolerance 2e-2 (bf16)."""
@@ -17,7 +19,7 @@ torch = pytest.importorskip("torch")
 TOL = 2e-2
 
 
-@pytest.fixture(scope="module", params=[1500, 3000, 6000])
+@pytest.fixture(scope="module", params=[1500, 3000, 6000, 14000, 70000])
 def setup(request):
     if not torch.cuda.is_available():
         pytest.skip("no GPU")
