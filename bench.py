@@ -172,19 +172,24 @@ def run_sweep(args, cfg):
     ctxs = [int(x) for x in args.sweep_ctx.split(",")]
     gammas = [int(x) for x in args.sweep_gamma.split(",")]
     n_new = args.sweep_new
-    n_max = max(ctxs) + n_new + 6 * (max(gammas) + 1) + 64
+    # one context per length over the same weights, each with the cache a
+    # deployment at that length would allocate
+    spare = n_new + 6 * (max(gammas) + 1) + 64
     t = time.time()
-    dm = DeviceModel(cfg, n_max=n_max, gamma_max=max(8, max(gammas)), m_rounds=5, cap_max=256,
-                     prefill_chunk=512)
-    W.generate_weights(cfg, seed=0, consume=dm.upload)
-    dm.finalize()
-    log(f"weights generated and packed in {time.time() - t:.1f}s (n_max {n_max})")
+    base = DeviceModel(cfg, n_max=min(ctxs) + spare, gamma_max=max(8, max(gammas)), m_rounds=5,
+                       cap_max=256, prefill_chunk=512)
+    W.generate_weights(cfg, seed=0, consume=base.upload)
+    base.finalize()
+    models = {n: base if n + spare == base.desc.n_max else base.resized(n + spare) for n in ctxs}
+    log(f"weights generated and packed in {time.time() - t:.1f}s (caches of "
+        f"{', '.join(str(n + spare) for n in ctxs)} positions)")
     tok = int(W.prompt_ids(cfg.vocab, 1, 1)[0])
     L2 = 2 * cfg.L
     none = np.zeros(L2, bool)
     mlp = np.array([i % 2 == 1 for i in range(L2)])
     lat = []
     for n in ctxs:
+        dm = models[n]
         fill_cache(dm, cfg, n)
         dm.set_context(n, tok)
         dm.profile_decode(None, 2, per_kernel=False)
@@ -201,6 +206,7 @@ def run_sweep(args, cfg):
     params = select_params((c1, c2, c3), "paper_min", 0, tau=0.5, prune_half=True, D=10)
     points = []
     for n, lr in zip(ctxs, lat):
+        dm = models[n]
         fill_cache(dm, cfg, n)
         for gamma in gammas:
             # AR and speculative decode from the same state (same history rounds)
@@ -244,7 +250,9 @@ def run_sweep(args, cfg):
                                         f"per point after 5 full-model draft/verify rounds of "
                                         f"history, one knapsack selection per point",
            "latency_model_ms": {"c1": c1, "c2": c2, "c3": c3, "points": lat}, "points": points}
-    dm.close()
+    for m in models.values():
+        m.close()
+    base.close()
     print(json.dumps(res), flush=True)
 
 

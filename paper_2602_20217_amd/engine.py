@@ -155,6 +155,29 @@ class DeviceModel:
         torch.cuda.current_stream().synchronize()
         return self
 
+    def resized(self, n_max: int) -> "DeviceModel":
+        """A second context over the same uploaded weights, with its own KV cache
+        of n_max positions and workspace (the decode attention splits follow the
+        cache size, so a deployment sizes the cache to its context)."""
+        if self.ctx is None:
+            raise RuntimeError("finalize() the weights first")
+        other = DeviceModel.__new__(DeviceModel)
+        other.cfg, other.dev, other.bf = self.cfg, self.dev, self.bf
+        d = self.desc
+        other.desc = K.ModelDesc(d.L, d.d, d.hq, d.hkv, d.hd, d.ffn, d.vocab, n_max, d.qk_norm,
+                                 d.dtype, d.eps, d.rope_theta)
+        other.lim = self.lim
+        kvb = K.ks_kv_cache_bytes(C.byref(other.desc))
+        wsb = K.ks_workspace_bytes(C.byref(other.desc), C.byref(other.lim))
+        if kvb == 0 or wsb == 0:
+            raise K.KsError(K.KS_EINVAL, K.last_error())
+        other.kv = torch.zeros(kvb, dtype=torch.uint8, device=self.dev)
+        other.ws = torch.zeros(wsb, dtype=torch.uint8, device=self.dev)
+        other.w, other.gains = self.w, self.gains
+        other._pending, other._done = {}, set(self._done)
+        other.ctx = None
+        return other.finalize()
+
     def close(self):
         if self.ctx is not None:
             K.ks_destroy(self.ctx)
