@@ -271,6 +271,9 @@ def main():
     ap.add_argument("--profile-kernels", action="store_true",
                     help="short run for hardware counters: prefill, 16 decode steps and a "
                          "256 MiB device copy (the reference for counter scaling)")
+    ap.add_argument("--profile-select", action="store_true",
+                    help="isolated knapsack selections (model-mode DP) at the workload's "
+                         "shape after a prefill, for traces and counters of the DP")
     ap.add_argument("--sweep", action="store_true",
                     help="context x draft-length grid (synthetic caches): per-sublayer "
                          "latencies, draft/verify rates and speedup over AR at each point")
@@ -322,6 +325,24 @@ def main():
     sweep_ctx = sorted({max(64, args.ctx // 8), args.ctx // 4, args.ctx // 2, args.ctx})
     coeffs, sweep = latency_sweep(dm, cfg, sweep_ctx, first)
     log(f"latency model c1={coeffs[0]:.4f}ms c2={coeffs[1]:.3e}ms/token c3={coeffs[2]:.4f}ms")
+    if args.profile_select:
+        # isolated selections on the prompt's history rows (the workload's first
+        # selection), for per-kernel traces and counters of the DP
+        params = select_params(coeffs, "paper_min", 0, tau=0.5, prune_half=True, D=10)
+        dm.prefill(prompt)
+        times = []
+        for k in range(args.warmup + args.steps):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            sel = dm.select(params)
+            torch.cuda.synchronize()
+            if k >= args.warmup:
+                times.append(round((time.perf_counter() - t0) * 1e3, 2))
+        print(json.dumps({"mode": "profile-select", "C": sel.C, "w_attn": sel.w_attn,
+                          "w_mlp": sel.w_mlp, "cells": sel.n_cells, "rows": sel.n_rows,
+                          "j": sel.j_star, "select_ms": times}), flush=True)
+        dm.close()
+        return
     params = select_params(coeffs, "paper_min", 0, tau=0.5, prune_half=True, D=10)
 
     def run(gamma):
@@ -387,7 +408,9 @@ def main():
         "ar_ms_per_step": round(mean_ar, 2), "tokens_equal_ar": same,
         "accepted": st.n_accepted, "drafted": st.n_drafted, "rounds": st.n_rounds,
         "alpha": round(st.n_accepted / max(1, st.n_drafted), 4),
+        "tokens_per_round": round((st.n_accepted + st.n_rounds) / max(1, st.n_rounds), 3),
         "select_ms": round(st.ms_select, 2), "selections": st.n_selections,
+        "select_overhead_pct": round(100.0 * st.ms_select / max(1e-9, ssd_ms[-1]), 2),
         "masks": [{"j": s.j_star, "C": s.C, "w_attn": s.w_attn, "w_mlp": s.w_mlp,
                    "skipped_attn": int(sum(1 for i in range(0, 2 * cfg.L, 2) if not s.exec[i])),
                    "skipped_mlp": int(sum(1 for i in range(1, 2 * cfg.L, 2) if not s.exec[i])),

@@ -1025,6 +1025,16 @@ static ks_status decode_internal(ks_ctx* c, int n_new, int gamma, int reselect_e
     if (stats) *stats = st;
     return KS_OK;
   }
+  // the first selection of a generation uses the last m (gamma + 1) prompt rows
+  // (the prefill keeps m (gamma_max + 1), as it does not know gamma yet)
+  if (c->blocks.size() == 1) {
+    auto& b = c->blocks.front();
+    const int cap = c->lim.m_rounds * (gamma + 1);
+    if (b.second > cap) {
+      b.first += b.second - cap;
+      b.second = cap;
+    }
+  }
   ks_selection sel{};
   auto do_select = [&]() -> ks_status {
     const auto a = now();

@@ -222,3 +222,24 @@ def test_generate_ssd_equals_ar_and_oracle(setup):
             np.testing.assert_array_equal(np.array(sg.exec[:2 * cfg.L], dtype=bool),
                                           sref.exec_mask)
             assert sg.j_star == sref.j_star and sg.gamma_star == sref.gamma_star
+
+
+def test_first_selection_uses_gamma_rows(setup):
+    """With a draft length below gamma_max, the first selection of a generation
+    uses the last m (gamma + 1) prompt rows (here 15 of the 25 the prefill
+    keeps): the selections equal the oracle's, which keeps exactly those."""
+    name, cfg, dm, model = setup
+    if cfg.dtype != "f32":
+        pytest.skip("selection identity is pinned on the fp32 model")
+    c, mode, bins = LAT[name]
+    from paper_2602_20217_amd.engine import select_params
+    prompt = _prompt(cfg, 96, seed=2)
+    ssd, st, sels = dm.generate(prompt, 24, gamma=2, reselect_every=8,
+                                params=select_params(c, mode, bins))
+    out, log = GEN.generate(model, prompt, 24, gamma=2, T=8, lat=c, quant_mode=mode, bins=bins)
+    assert list(ssd) == out
+    assert len(log.selections) == len(sels) >= 2
+    for (_, P, wts, sref), sg in zip(log.selections, sels):
+        np.testing.assert_array_equal(np.array(sg.exec[:2 * cfg.L], dtype=bool),
+                                      sref.exec_mask)
+        assert sg.j_star == sref.j_star and sg.gamma_star == sref.gamma_star
