@@ -274,6 +274,9 @@ def main():
     ap.add_argument("--profile-select", action="store_true",
                     help="isolated knapsack selections (model-mode DP) at the workload's "
                          "shape after a prefill, for traces and counters of the DP")
+    ap.add_argument("--select-coeffs", default="",
+                    help="c1,c2,c3 (ms) for --profile-select instead of the fitted ones "
+                         "(a profiler's own overhead distorts the fit)")
     ap.add_argument("--sweep", action="store_true",
                     help="context x draft-length grid (synthetic caches): per-sublayer "
                          "latencies, draft/verify rates and speedup over AR at each point")
@@ -297,7 +300,10 @@ def main():
         return run_sweep(args, cfg)
     n_max = args.ctx + args.new + 64
     t = time.time()
-    dm = DeviceModel(cfg, n_max=n_max, gamma_max=max(8, args.gamma), m_rounds=5, cap_max=256,
+    # the selection profile keeps exactly the m (gamma + 1) history rows a
+    # generation's selections use
+    gmax = args.gamma if args.profile_select else max(8, args.gamma)
+    dm = DeviceModel(cfg, n_max=n_max, gamma_max=gmax, m_rounds=5, cap_max=256,
                      prefill_chunk=512)
     W.generate_weights(cfg, seed=0, consume=dm.upload)
     dm.finalize()
@@ -328,6 +334,8 @@ def main():
     if args.profile_select:
         # isolated selections on the prompt's history rows (the workload's first
         # selection), for per-kernel traces and counters of the DP
+        if args.select_coeffs:
+            coeffs = tuple(float(x) for x in args.select_coeffs.split(","))
         params = select_params(coeffs, "paper_min", 0, tau=0.5, prune_half=True, D=10)
         dm.prefill(prompt)
         times = []
