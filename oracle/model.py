@@ -257,13 +257,17 @@ class Round:
     emitted: list
 
 
-def ssd_round(model: Model, st: State, exec_mask, gamma: int, m_rounds: int = 5) -> Round:
+def ssd_round(model: Model, st: State, exec_mask, gamma: int, m_rounds: int = 5,
+              tau_conf: float = 0.0) -> Round:
     """One greedy self-speculative round (Section 2.1).
 
-    Draft: gamma steps of f^(S) starting from s at position P; executed attention
-    sublayers store their keys/values at P+k.  Verify: the full model on
-    [s, d_1..d_gamma] at positions P..P+gamma, overwriting those keys/values.
-    Accept the longest prefix with d_i = y_{i-1}; emit d_1..d_a and y_a.
+    Draft: up to gamma steps of f^(S) starting from s at position P; executed
+    attention sublayers store their keys/values at P+k.  With tau_conf > 0 the
+    drafting stops after the first draft token whose top-1 probability is below
+    tau_conf (the dynamic drafting exit of Section 3, TPT maximization; that token
+    is still verified).  Verify: the full model on [s, d_1..d_g] at positions
+    P..P+g (g drafts), overwriting those keys/values.  Accept the longest prefix
+    with d_i = y_{i-1}; emit d_1..d_a and y_a.
     """
     drafts, tops = [], []
     t = st.s
@@ -272,10 +276,13 @@ def ssd_round(model: Model, st: State, exec_mask, gamma: int, m_rounds: int = 5)
         t = int(fw.argmax[0])
         drafts.append(t)
         tops.append(float(fw.top1[0]))
+        if tau_conf > 0 and not tops[-1] >= tau_conf:
+            break
+    g = len(drafts)
     fv = forward(model, st.cache, [st.s] + drafts, st.P)
     y = fv.argmax
     a = 0
-    while a < gamma and drafts[a] == y[a]:
+    while a < g and drafts[a] == y[a]:
         a += 1
     emitted = drafts[:a] + [int(y[a])]
     pos = st.P + np.arange(a + 1)

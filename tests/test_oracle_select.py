@@ -156,3 +156,62 @@ def test_generate_equals_ar_tiny():
     ref = M.generate_ar(model, prompt, 20, 128)
     assert out == ref
     assert len(log.selections) >= 2
+
+
+def _tiny_gen(**kw):
+    cfg = W.config("tiny")
+    model = M.Model(cfg, W.generate_weights(cfg, seed=0))
+    prompt = W.prompt_ids(cfg.vocab, 64, 1)
+    out, log = GEN.generate(model, prompt, 24, gamma=4, T=8, lat=W.TINY_LATENCY,
+                            quant_mode="bins", bins=64, **kw)
+    return model, prompt, out, log
+
+
+def test_dynamic_exit_zero_threshold_is_fixed_gamma():
+    """tau_conf = 0 leaves every round at the configured gamma."""
+    _, _, out0, log0 = _tiny_gen()
+    _, _, out1, log1 = _tiny_gen(tau_conf=0.0)
+    assert out0 == out1 and log0.accepted == log1.accepted
+    assert all(g == 4 for g in log1.drafted[:-1])
+
+
+def test_dynamic_exit_threshold_above_one_drafts_one_token():
+    """A top-1 probability never reaches 1.01, so every round drafts exactly one
+    token; greedy output still equals AR (Section 2.1)."""
+    model, prompt, out, log = _tiny_gen(tau_conf=1.01)
+    assert set(log.drafted) == {1}
+    assert out == M.generate_ar(model, prompt, 24, 128)
+
+
+def test_dynamic_exit_stops_at_first_low_confidence_draft():
+    """Each round's drafts: all but the last reach tau_conf, and the round stops
+    early only on a draft below it (checked on the round records)."""
+    cfg = W.config("tiny")
+    model = M.Model(cfg, W.generate_weights(cfg, seed=0))
+    prompt = W.prompt_ids(cfg.vocab, 64, 1)
+    st = M.prefill(model, prompt, 200, 25)
+    mask = [True, False] * 4
+    tops = []
+    for _ in range(3):
+        rd = M.ssd_round(model, st, mask, 4, 5, tau_conf=0.0)
+        tops += rd.draft_top1
+    tau = float(np.median(tops))  # a threshold that splits the observed confidences
+    st = M.prefill(model, prompt, 200, 25)
+    stopped_early = 0
+    for _ in range(6):
+        rd = M.ssd_round(model, st, mask, 4, 5, tau_conf=tau)
+        assert all(p >= tau for p in rd.draft_top1[:-1])
+        if len(rd.drafts) < 4:
+            stopped_early += 1
+            assert rd.draft_top1[-1] < tau
+        assert 0 <= rd.n_accepted <= len(rd.drafts)
+    assert stopped_early >= 1
+
+
+def test_gamma_from_selection_caps_rounds():
+    """gamma_source 'selected': every round drafts at most min(gamma*, gamma)
+    tokens of the selection in force; output equals AR."""
+    model, prompt, out, log = _tiny_gen(gamma_source="selected")
+    assert out == M.generate_ar(model, prompt, 24, 128)
+    caps = [max(1, min(4, s[3].gamma_star)) for s in log.selections]
+    assert max(log.drafted) <= max(caps)
