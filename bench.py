@@ -266,6 +266,11 @@ def main():
     ap.add_argument("--new", type=int, default=256)
     ap.add_argument("--gamma", type=int, default=4)
     ap.add_argument("--reselect", type=int, default=32)
+    ap.add_argument("--tau-conf", type=float, default=0.0,
+                    help="dynamic drafting exit below this top-1 probability (paper: 0.7; "
+                         "0 keeps the fixed draft length of the workload)")
+    ap.add_argument("--gamma-source", default="fixed", choices=("fixed", "selected"),
+                    help="draft cap per round: --gamma, or min(gamma*, --gamma)")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-kernels", action="store_true",
@@ -307,6 +312,7 @@ def main():
                      prefill_chunk=512)
     W.generate_weights(cfg, seed=0, consume=dm.upload)
     dm.finalize()
+    dm.set_draft_policy(args.tau_conf, args.gamma_source)
     log(f"weights generated and packed in {time.time() - t:.1f}s")
     prompt = W.prompt_ids(cfg.vocab, args.ctx, 1)
 
@@ -411,7 +417,9 @@ def main():
                                f"{args.ctx}-token random prompt, {args.new} new tokens, "
                                f"gamma {args.gamma}, mask re-selected every {args.reselect} tokens",
                    "global_batch": 1, "seq_len": args.ctx, "new_tokens": args.new,
-                   "gamma": args.gamma, "reselect_every": args.reselect, "parallelism": "none"},
+                   "gamma": args.gamma, "reselect_every": args.reselect, "parallelism": "none",
+                   "draft_policy": {"tau_conf": args.tau_conf,
+                                    "gamma_source": args.gamma_source}},
         "speedup_vs_ar": round(value / ar_tps, 4), "ar_tok_s": round(ar_tps, 2),
         "ar_ms_per_step": round(mean_ar, 2), "tokens_equal_ar": same,
         "accepted": st.n_accepted, "drafted": st.n_drafted, "rounds": st.n_rounds,

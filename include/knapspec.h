@@ -286,6 +286,27 @@ ks_status ks_decode(ks_ctx* ctx, int n_new, int gamma, int reselect_every,
                     const ks_select_params* p, int32_t* out_tokens, ks_gen_stats* stats,
                     ks_selection* sel_log, int max_sel_log);
 
+/*
+ * Draft policy of the generation loop (ks_generate, ks_decode) of a context
+ * (Section 3, TPT maximization, dynamic drafting exit):
+ *  tau_conf > 0: a round stops drafting after its first draft token whose
+ *    top-1 probability is below tau_conf (paper: 0.7); that token is still
+ *    verified.  Each draft step then reads its top-1 probability back (one
+ *    stream synchronisation per draft step).  0 keeps every round at its cap.
+ *  gamma_source KS_GAMMA_FIXED: rounds draft up to the call's gamma;
+ *    KS_GAMMA_SELECTED: up to min(gamma*, gamma) of the selection in force
+ *    (gamma* from the stage-2 grid, Section 3).
+ * A new context starts with {0, KS_GAMMA_FIXED}: the call's gamma every round.
+ * Errors: KS_EINVAL for a null pointer, a negative or non-finite tau_conf or
+ * an unknown gamma_source (the policy is then unchanged).
+ */
+enum { KS_GAMMA_FIXED = 0, KS_GAMMA_SELECTED = 1 };
+typedef struct ks_draft_policy {
+  float tau_conf;
+  int gamma_source;
+} ks_draft_policy;
+ks_status ks_set_draft_policy(ks_ctx* ctx, const ks_draft_policy* p);
+
 /* Kernel classes of the decode step, for ks_profile_decode. */
 enum {
   KS_KC_EMBED = 0,    /* embedding gather */

@@ -29,6 +29,7 @@ class GenLog:
     selections: list = field(default_factory=list)   # (produced, P, weights, Selection)
     accepted: list = field(default_factory=list)     # n_accepted per round
     drafted: list = field(default_factory=list)      # draft tokens per round
+    draft_top1: list = field(default_factory=list)   # top-1 probabilities of each round's drafts
 
 
 def generate(model: M.Model, prompt, n_new: int, gamma: int, T: int, lat,
@@ -54,6 +55,7 @@ def generate(model: M.Model, prompt, n_new: int, gamma: int, T: int, lat,
         rd = M.ssd_round(model, st, sel.exec_mask, cap, m_rounds, tau_conf)
         log.accepted.append(rd.n_accepted)
         log.drafted.append(len(rd.drafts))
+        log.draft_top1.append(rd.draft_top1)
         if len(st.out) < n_new and len(st.out) // T > before // T:
             sel = choose()
     return st.out[:n_new], log

@@ -60,6 +60,13 @@ class SelectionDebug(C.Structure):
                 ("sig_s", C.POINTER(C.c_double)), ("n_match", C.POINTER(C.c_int))]
 
 
+KS_GAMMA_FIXED, KS_GAMMA_SELECTED = 0, 1
+
+
+class DraftPolicy(C.Structure):
+    _fields_ = [("tau_conf", C.c_float), ("gamma_source", C.c_int)]
+
+
 class GenStats(C.Structure):
     _fields_ = [("n_rounds", C.c_int), ("n_selections", C.c_int), ("n_drafted", C.c_int),
                 ("n_accepted", C.c_int), ("ms_total", C.c_double), ("ms_select", C.c_double),
@@ -119,6 +126,7 @@ _SIG = {
                          C.POINTER(GenStats), C.POINTER(Selection), _I]),
     "ks_decode": (_I, [_P, _I, _I, _I, C.POINTER(SelectParams), _P, C.POINTER(GenStats),
                        C.POINTER(Selection), _I]),
+    "ks_set_draft_policy": (_I, [_P, C.POINTER(DraftPolicy)]),
     "ks_profile_decode": (_I, [_P, _P, _I, _I, C.POINTER(KernelProfile)]),
     "ks_sublayer_apply": (_I, [_P, _I, _P, _P, _P, _I, _I]),
     "ks_head_rows": (_I, [_P, _P, _I, _P, _P, _P]),
@@ -169,6 +177,7 @@ ks_hidden_cos = _wrap("ks_hidden_cos")
 ks_knapsack_select = _wrap("ks_knapsack_select")
 ks_generate = _wrap("ks_generate")
 ks_decode = _wrap("ks_decode")
+ks_set_draft_policy = _wrap("ks_set_draft_policy")
 ks_profile_decode = _wrap("ks_profile_decode")
 ks_sublayer_apply = _wrap("ks_sublayer_apply")
 ks_head_rows = _wrap("ks_head_rows")

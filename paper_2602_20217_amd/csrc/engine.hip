@@ -165,6 +165,8 @@ struct ks_ctx {
   int32_t s = 0;
   int k_draft = 0;
   std::deque<std::pair<int, int>> blocks;  // (first position, rows)
+  float tau_conf = 0.f;                    // draft policy (ks_set_draft_policy)
+  int gamma_source = KS_GAMMA_FIXED;
 
   template <typename T>
   T* at(size_t off) const { return (T*)(ws + off); }
@@ -746,6 +748,16 @@ ks_status ks_verify(ks_ctx* c, const int32_t* tokens, int gamma, int32_t* out_pr
   return verify_internal(c, tokens, gamma, out_pred, out_a);
 }
 
+ks_status ks_set_draft_policy(ks_ctx* c, const ks_draft_policy* p) {
+  REQ(c && p, "null pointer");
+  REQ(std::isfinite(p->tau_conf) && p->tau_conf >= 0.f, "tau_conf must be finite and >= 0");
+  REQ(p->gamma_source == KS_GAMMA_FIXED || p->gamma_source == KS_GAMMA_SELECTED,
+      "gamma_source must be KS_GAMMA_FIXED or KS_GAMMA_SELECTED");
+  c->tau_conf = p->tau_conf;
+  c->gamma_source = p->gamma_source;
+  return KS_OK;
+}
+
 ks_status ks_hidden_cos(const float* X, const float* Y, int groups, int r, int d, float* out,
                         void* stream) {
   REQ(X && Y && out, "null pointer");
@@ -1049,17 +1061,33 @@ static ks_status decode_internal(ks_ctx* c, int n_new, int gamma, int reselect_e
   ks_status s = do_select();
   if (s != KS_OK) return s;
   int32_t* toks = c->pin;
+  float* top1_h = (float*)(c->pin + 64);
   while (produced < n_new) {
-    for (int k = 0; k < gamma; ++k) draft_internal(c, sel.exec);
+    // draft cap of the round, then the dynamic exit on the draft's top-1
+    // probability (Section 3, TPT maximization)
+    const int cap = c->gamma_source == KS_GAMMA_SELECTED
+                        ? std::max(1, std::min(gamma, sel.gamma_star))
+                        : gamma;
+    int g = 0;
+    while (g < cap) {
+      draft_internal(c, sel.exec);
+      ++g;
+      if (c->tau_conf > 0.f) {
+        HIPCHK(hipMemcpyAsync(top1_h, c->at<float>(c->y.top1) + g - 1, 4, hipMemcpyDeviceToHost,
+                              c->st));
+        HIPCHK(hipStreamSynchronize(c->st));
+        if (!(*top1_h >= c->tau_conf)) break;
+      }
+    }
     HIPCHK(hipGetLastError());
-    HIPCHK(hipMemcpyAsync(toks, c->at<int32_t>(c->y.tok), (gamma + 1) * 4,
-                          hipMemcpyDeviceToHost, c->st));
+    HIPCHK(hipMemcpyAsync(toks, c->at<int32_t>(c->y.tok), (g + 1) * 4, hipMemcpyDeviceToHost,
+                          c->st));
     int a = 0;
     int32_t pred[16];
-    s = verify_internal(c, toks, gamma, pred, &a);
+    s = verify_internal(c, toks, g, pred, &a);
     if (s != KS_OK) return s;
     st.n_rounds++;
-    st.n_drafted += gamma;
+    st.n_drafted += g;
     st.n_accepted += a;
     const int before = produced;
     for (int t = 1; t <= a && produced < n_new; ++t) out_tokens[produced++] = toks[t];

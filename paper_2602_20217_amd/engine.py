@@ -247,6 +247,12 @@ class DeviceModel:
                              C.byref(dbg) if dbg is not None else None)
         return (out, self._dbg) if debug_cells else out
 
+    def set_draft_policy(self, tau_conf: float = 0.0, gamma_source: str = "fixed"):
+        """Dynamic drafting exit below tau_conf (0 disables) and the draft cap of
+        each round: the call's gamma ("fixed") or min(gamma*, gamma) ("selected")."""
+        src = {"fixed": K.KS_GAMMA_FIXED, "selected": K.KS_GAMMA_SELECTED}[gamma_source]
+        K.ks_set_draft_policy(self.ctx, C.byref(K.DraftPolicy(tau_conf, src)))
+
     def generate(self, prompt, n_new: int, gamma: int, reselect_every: int = 32,
                  params: K.SelectParams | None = None, max_sel_log: int = 256):
         p = np.ascontiguousarray(prompt, dtype=np.int32)

@@ -243,3 +243,54 @@ def test_first_selection_uses_gamma_rows(setup):
         np.testing.assert_array_equal(np.array(sg.exec[:2 * cfg.L], dtype=bool),
                                       sref.exec_mask)
         assert sg.j_star == sref.j_star and sg.gamma_star == sref.gamma_star
+
+
+@pytest.mark.parametrize("tau_mode,source", [("above", "fixed"), ("median", "fixed"),
+                                             ("zero", "selected"), ("median", "selected")])
+def test_draft_policy(setup, tau_mode, source):
+    """Dynamic drafting exit and the gamma* cap (Section 3, TPT maximization):
+    tokens equal AR on every model; on the fp32 model the rounds (draft counts,
+    acceptances) and the selections equal the oracle's wherever no draft's top-1
+    probability lies within 1e-3 (relative) of the threshold."""
+    name, cfg, dm, model = setup
+    c, mode, bins = LAT[name]
+    from paper_2602_20217_amd.engine import select_params
+    params = select_params(c, mode, bins)
+    prompt = _prompt(cfg, 96, seed=3)
+    ar, _, _ = dm.generate(prompt, 24, gamma=0)
+    if tau_mode == "above":
+        tau = 1.01
+    elif tau_mode == "zero":
+        tau = 0.0
+    else:
+        _, log0 = GEN.generate(model, prompt, 24, gamma=4, T=8, lat=c, quant_mode=mode,
+                               bins=bins)
+        # the midpoint of the widest gap between observed confidences in their
+        # middle half: a threshold that splits them with a margin
+        tops = np.sort([p for r in log0.draft_top1 for p in r])
+        lo, hi = len(tops) // 4, max(len(tops) // 4 + 1, 3 * len(tops) // 4)
+        i = lo + int(np.argmax(np.diff(tops[lo:hi + 1])))
+        tau = float(0.5 * (tops[i] + tops[i + 1]))
+    try:
+        dm.set_draft_policy(tau, source)
+        sd, st, sels = dm.generate(prompt, 24, gamma=4, reselect_every=8, params=params)
+    finally:
+        dm.set_draft_policy(0.0, "fixed")
+    np.testing.assert_array_equal(sd, ar)
+    assert st.n_drafted <= 4 * st.n_rounds
+    if tau_mode == "above":
+        assert st.n_drafted == st.n_rounds
+    if cfg.dtype != "f32":
+        return
+    out, log = GEN.generate(model, prompt, 24, gamma=4, T=8, lat=c, quant_mode=mode, bins=bins,
+                            tau_conf=tau, gamma_source=source)
+    assert list(sd) == out
+    if tau > 0 and min(abs(p - tau) for r in log.draft_top1 for p in r) < 1e-3 * tau:
+        pytest.skip("a draft confidence lies within 1e-3 (relative) of the threshold")
+    assert st.n_rounds == len(log.drafted)
+    assert st.n_drafted == sum(log.drafted) and st.n_accepted == sum(log.accepted)
+    assert len(sels) == len(log.selections)
+    for (_, P, wts, sref), sg in zip(log.selections, sels):
+        np.testing.assert_array_equal(np.array(sg.exec[:2 * cfg.L], dtype=bool),
+                                      sref.exec_mask)
+        assert sg.gamma_star == sref.gamma_star
