@@ -202,8 +202,8 @@ ks_status ks_destroy(ks_ctx* ctx);
 /*
  * ks_prefill (Section 2; setup step): runs the prompt tokens (host int32[n],
  * 1 <= n < n_max) through the full model, fills the KV cache for positions
- * 0..n-1 and commits the target's greedy token s at position n (no keys/values
- * yet).  The last min(n, m_rounds (gamma_max+1)) rows of every sublayer output
+ * 0..n-1 and commits the target's greedy (or, after ks_set_sampling, sampled)
+ * token s at position n (no keys/values yet).  The last min(n, m_rounds (gamma_max+1)) rows of every sublayer output
  * X^(0..2L) become the first history block.  Resets all decode state.
  */
 ks_status ks_prefill(ks_ctx* ctx, const int32_t* tokens, int n, int32_t* out_first_token);
@@ -306,6 +306,86 @@ typedef struct ks_draft_policy {
   int gamma_source;
 } ks_draft_policy;
 ks_status ks_set_draft_policy(ks_ctx* ctx, const ks_draft_policy* p);
+
+/* ---- speculative sampling ------------------------------------------------ */
+/*
+ * Sampling mode of verification (Section 2.1 with sampled drafts; the paper's
+ * sampling experiments use temperature 0.7, top-k 50, top-p 0.95).
+ *
+ * Filter of one logits row: keep the top_k largest logits (ties: lower token
+ * id first), softmax of logit / temperature over them (float32), keep the
+ * shortest prefix in that order whose cumulative probability reaches top_p,
+ * renormalise.  A table row holds count entries (ids, probs) in that order;
+ * table rows are KS_SAMPLE_KMAX entries apart.  A draw with uniform u takes
+ * the first entry whose cumulative probability exceeds u (the last entry if
+ * rounding leaves none).  Logits must be finite.
+ *
+ * Uniforms: u = (w >> 8) * 2^-24, w the first output word of Philox4x32-10
+ * (Salmon, Moraes, Dror, Shaw, SC 2011) at counter (pos, purpose, 0, 0) under
+ * key (seed & 0xffffffff, seed >> 32).  Purposes: 0 draft draw, 1 acceptance
+ * test, 2 target draw (residual, bonus, autoregressive and prefill tokens);
+ * pos is the position of the token being produced.
+ *
+ * Acceptance chain of a round from committed position P with drafts d_1..d_g
+ * (d_i at position P+i, drawn from draft table q_i) and target tables
+ * p_0..p_g of the verify rows: for i = 1..g, d_i is accepted iff
+ * u(P+i, 1) < min(1, p_{i-1}(d_i) / q_i(d_i)); at the first rejection the
+ * round emits a token drawn with u(P+i, 2) from max(0, p_{i-1} - q_i) over
+ * p_{i-1}'s table, normalised (from p_{i-1} itself if that is zero
+ * everywhere); when every draft is accepted it emits a token drawn from p_g
+ * with u(P+g+1, 2).  The emitted tokens then follow the target's filtered
+ * distribution.
+ */
+enum { KS_SAMPLE_KMAX = 128 };
+typedef struct ks_sampling {
+  float temperature;  /* > 0 samples; <= 0 (ks_set_sampling only): greedy */
+  int top_k;          /* 1..KS_SAMPLE_KMAX, at most vocab */
+  float top_p;        /* (0, 1] */
+  uint64_t seed;
+} ks_sampling;
+/*
+ * ks_set_sampling: token choice of the context.  s = NULL or temperature <= 0:
+ * greedy (the default of a new context).  Otherwise ks_prefill draws its token
+ * from the filter of the last prompt row, ks_draft_step draws draft k from the
+ * draft model's filter and keeps its table, ks_verify runs the acceptance chain
+ * above (it then needs the gamma drafts of ks_draft_step since the last
+ * verify; out_pred holds the accepted drafts, the emitted token and -1 after
+ * it), and ks_generate / ks_decode sample every token (gamma = 0: each token
+ * from the target's filter).  The knapsack selection is unchanged.  Errors:
+ * KS_EINVAL for a non-finite temperature or top_k / top_p out of range.
+ */
+ks_status ks_set_sampling(ks_ctx* ctx, const ks_sampling* s);
+/*
+ * ks_sample_workspace_bytes: device workspace of ks_sample_filter for rows rows
+ * of vocab logits; 0 if the sizes are unsupported (vocab too large for top_k:
+ * about 4096 * min(128, 8192 / top_k) logits at most).
+ */
+size_t ks_sample_workspace_bytes(int rows, int vocab, int top_k);
+/*
+ * ks_sample_filter: the filter of rows rows of logits (device float32, row r
+ * at logits + r * ld) into tables ids / probs (device [rows][KS_SAMPLE_KMAX])
+ * and counts (device int32 [rows]).  top1 (optional, device float32 [rows]):
+ * the unfiltered softmax maximum (temperature 1).  tokens (optional, device
+ * int32 [rows]): row r drawn with u(pos0 + r, purpose).  Asynchronous.
+ */
+ks_status ks_sample_filter(const float* logits, int rows, int vocab, int ld, const ks_sampling* s,
+                           int pos0, int purpose, int32_t* ids, float* probs, int32_t* counts,
+                           float* top1, int32_t* tokens, void* workspace, size_t workspace_bytes,
+                           void* stream);
+/*
+ * ks_spec_accept: the acceptance chain of one round on device tables (p: rows
+ * 0..gamma, q: rows 0..gamma-1 for d_1..d_gamma, layout of ks_sample_filter),
+ * drafts device int32 [gamma] (d_1..d_gamma), pos0 = P; counts in
+ * [1, KS_SAMPLE_KMAX] (others are clamped).  Writes out (device
+ * int32 [2]) = {accepted drafts a, emitted token}.  Asynchronous.
+ */
+ks_status ks_spec_accept(const int32_t* p_ids, const float* p_probs, const int32_t* p_counts,
+                         const int32_t* q_ids, const float* q_probs, const int32_t* q_counts,
+                         const int32_t* drafts, int gamma, uint64_t seed, int pos0, int32_t* out,
+                         void* stream);
+/* ks_sample_uniforms: out[i] = u(pos[i], purpose) (device arrays).  Asynchronous. */
+ks_status ks_sample_uniforms(uint64_t seed, const int32_t* pos, int n, int purpose, float* out,
+                             void* stream);
 
 /* Kernel classes of the decode step, for ks_profile_decode. */
 enum {

@@ -67,6 +67,14 @@ class DraftPolicy(C.Structure):
     _fields_ = [("tau_conf", C.c_float), ("gamma_source", C.c_int)]
 
 
+KS_SAMPLE_KMAX = 128
+
+
+class Sampling(C.Structure):
+    _fields_ = [("temperature", C.c_float), ("top_k", C.c_int), ("top_p", C.c_float),
+                ("seed", C.c_uint64)]
+
+
 class GenStats(C.Structure):
     _fields_ = [("n_rounds", C.c_int), ("n_selections", C.c_int), ("n_drafted", C.c_int),
                 ("n_accepted", C.c_int), ("ms_total", C.c_double), ("ms_select", C.c_double),
@@ -127,6 +135,12 @@ _SIG = {
     "ks_decode": (_I, [_P, _I, _I, _I, C.POINTER(SelectParams), _P, C.POINTER(GenStats),
                        C.POINTER(Selection), _I]),
     "ks_set_draft_policy": (_I, [_P, C.POINTER(DraftPolicy)]),
+    "ks_set_sampling": (_I, [_P, C.POINTER(Sampling)]),
+    "ks_sample_workspace_bytes": (C.c_size_t, [_I, _I, _I]),
+    "ks_sample_filter": (_I, [_P, _I, _I, _I, C.POINTER(Sampling), _I, _I, _P, _P, _P, _P, _P,
+                              _P, C.c_size_t, _P]),
+    "ks_spec_accept": (_I, [_P, _P, _P, _P, _P, _P, _P, _I, C.c_uint64, _I, _P, _P]),
+    "ks_sample_uniforms": (_I, [C.c_uint64, _P, _I, _I, _P, _P]),
     "ks_profile_decode": (_I, [_P, _P, _I, _I, C.POINTER(KernelProfile)]),
     "ks_sublayer_apply": (_I, [_P, _I, _P, _P, _P, _I, _I]),
     "ks_head_rows": (_I, [_P, _P, _I, _P, _P, _P]),
@@ -178,6 +192,11 @@ ks_knapsack_select = _wrap("ks_knapsack_select")
 ks_generate = _wrap("ks_generate")
 ks_decode = _wrap("ks_decode")
 ks_set_draft_policy = _wrap("ks_set_draft_policy")
+ks_set_sampling = _wrap("ks_set_sampling")
+ks_sample_filter = _wrap("ks_sample_filter")
+ks_spec_accept = _wrap("ks_spec_accept")
+ks_sample_uniforms = _wrap("ks_sample_uniforms")
+ks_sample_workspace_bytes = lib.ks_sample_workspace_bytes
 ks_profile_decode = _wrap("ks_profile_decode")
 ks_sublayer_apply = _wrap("ks_sublayer_apply")
 ks_head_rows = _wrap("ks_head_rows")

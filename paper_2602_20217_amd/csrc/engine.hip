@@ -71,7 +71,8 @@ size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
 struct Layout {
   size_t rope, x, a1hi, a1lo, a2hi, a2lo, qkv, q, kvself, part, logits, am, top1;
   size_t tok, pos, len, stage, hist, xh, g0, g1, ge, dpos, dlen, sig, ptrs, ssq, gpart;
-  size_t dpc, dpn, dpmean, dpidx, dpbits, dpreach, dpse, dpss, total;
+  size_t dpc, dpn, dpmean, dpidx, dpbits, dpreach, dpse, dpss;
+  size_t vws, tab_ids, tab_pr, tab_cnt, sres, total;
   int FR, RING, cells, DR, XR, LR, nqkv, a2w, part_rows;
   size_t part_elems;
 };
@@ -136,6 +137,13 @@ Layout make_layout(const ks_model_desc& d, const ks_limits& lim) {
   y.dpreach = take((size_t)(2 * d.L + 1) * y.cells);
   y.dpse = take((size_t)(2 * d.L + 1) * y.cells * 8);
   y.dpss = take((size_t)(2 * d.L + 1) * y.cells * 8);
+  // vocabulary reductions: chunk partials / candidates, and the sampling tables
+  // (rows 0..gamma_max: target rows of a verify; rows gamma_max+1..: drafts)
+  y.vws = take(std::max(argmax_ws_bytes(y.LR, d.vocab), sample_ws_bytes_max(gam1)));
+  y.tab_ids = take((size_t)2 * gam1 * KS_SAMPLE_KMAX * 4);
+  y.tab_pr = take((size_t)2 * gam1 * KS_SAMPLE_KMAX * 4);
+  y.tab_cnt = take((size_t)2 * gam1 * 4);
+  y.sres = take(64);
   y.total = o;
   return y;
 }
@@ -167,6 +175,7 @@ struct ks_ctx {
   std::deque<std::pair<int, int>> blocks;  // (first position, rows)
   float tau_conf = 0.f;                    // draft policy (ks_set_draft_policy)
   int gamma_source = KS_GAMMA_FIXED;
+  ks_sampling samp{};                      // temperature <= 0: greedy
 
   template <typename T>
   T* at(size_t off) const { return (T*)(ws + off); }
@@ -185,6 +194,18 @@ struct ks_ctx {
   }
   float* stage_row(int i, int k) const {
     return at<float>(y.stage) + ((size_t)i * (lim.gamma_max + 1) + k) * md.d;
+  }
+  bool sampling() const { return samp.temperature > 0.f; }
+  // sampling tables: row t of the target (verify) set, row gamma_max + 1 + t of
+  // the draft set
+  int32_t* tab_ids(int row) const { return at<int32_t>(y.tab_ids) + (size_t)row * KS_SAMPLE_KMAX; }
+  float* tab_pr(int row) const { return at<float>(y.tab_pr) + (size_t)row * KS_SAMPLE_KMAX; }
+  int32_t* tab_cnt(int row) const { return at<int32_t>(y.tab_cnt) + row; }
+  int qrow(int k) const { return lim.gamma_max + 1 + k; }
+  // filter of `row` (tables at table row trow), optional draw at position pos
+  SampleSpec spec(int trow, float* top1, int32_t* tok, int pos, int purpose) const {
+    return SampleSpec{samp.temperature, samp.top_k, samp.top_p, samp.seed, tab_ids(trow),
+                      tab_pr(trow), tab_cnt(trow), top1, tok, pos, purpose};
   }
 };
 
@@ -359,8 +380,9 @@ void sublayer_rows(ks_ctx* c, int i, const float* xin, float* xout, int R, const
 
 // final norm + LM head + argmax for R rows (chunked by the logits buffer);
 // prepped: on the skinny path the final-norm planes of x are already in act1
+// (sampling: ss != nullptr, R <= gamma_max + 1, tables / draws as ss says)
 void head_rows(ks_ctx* c, const float* x, int R, float* logits_out, int32_t* am, float* top1,
-               bool batched, bool prepped = false) {
+               bool batched, bool prepped = false, const SampleSpec* ss = nullptr) {
   const ks_model_desc& d = c->md;
   const Act a1 = c->act1();
   const int step = logits_out ? R : c->y.LR;
@@ -379,13 +401,23 @@ void head_rows(ks_ctx* c, const float* x, int R, float* logits_out, int32_t* am,
            gemm(c, rr, d.vocab, d.d, a1, c->lm_head, EPI_STORE, lg, d.vocab, nullptr, 0, Act{},
                 true));
     }
-    PROF(c, KS_KC_ARGMAX, argmax_rows(lg, rr, d.vocab, am + r0, top1 ? top1 + r0 : nullptr, c->st));
+    if (ss) {
+      PROF(c, KS_KC_ARGMAX, sample_rows(lg, rr, d.vocab, d.vocab, *ss, c->ws + c->y.vws, c->st));
+      continue;
+    }
+    for (int a0 = 0; a0 < rr; a0 += c->y.LR) {
+      const int ra = std::min(c->y.LR, rr - a0);
+      PROF(c, KS_KC_ARGMAX,
+           argmax_rows(lg + (size_t)a0 * d.vocab, ra, d.vocab, d.vocab, am + r0 + a0,
+                       top1 ? top1 + r0 + a0 : nullptr, c->ws + c->y.vws, c->st));
+    }
   }
 }
 
 // one decode row at position p from token tok_dev[0]; writes argmax to am_out
+// (ss: sample the token instead, see head_rows)
 void decode_row(ks_ctx* c, const int32_t* tok_dev, int p, const uint8_t* exec, int32_t* am_out,
-                float* top1_out) {
+                float* top1_out, const SampleSpec* ss = nullptr) {
   const ks_model_desc& d = c->md;
   const int L2 = 2 * d.L;
   float* x = c->at<float>(c->y.x);
@@ -407,11 +439,12 @@ void decode_row(ks_ctx* c, const int32_t* tok_dev, int p, const uint8_t* exec, i
   for (int i = 1; i <= L2; ++i)
     if (!exec || exec[i - 1])
       sublayer_rows(c, i, x, x, 1, pos, len, p + 1, 0, false, gain_of(c, next_exec(i)));
-  head_rows(c, x, 1, nullptr, am_out, top1_out, false, true);
+  head_rows(c, x, 1, nullptr, am_out, top1_out, false, true, ss);
 }
 
 // verify rows of tokens tok_dev[0..R) at positions P..P+R-1, snapshots into stage
-void verify_rows(ks_ctx* c, const int32_t* tok_dev, int R, int32_t* am_out) {
+void verify_rows(ks_ctx* c, const int32_t* tok_dev, int R, int32_t* am_out,
+                 const SampleSpec* ss = nullptr) {
   const ks_model_desc& d = c->md;
   int32_t* pos = c->at<int32_t>(c->y.pos);
   int32_t* len = c->at<int32_t>(c->y.len);
@@ -425,7 +458,7 @@ void verify_rows(ks_ctx* c, const int32_t* tok_dev, int R, int32_t* am_out) {
   for (int i = 1; i <= 2 * d.L; ++i)
     sublayer_rows(c, i, c->stage_row(i - 1, 0), c->stage_row(i, 0), R, pos, len, c->P + R, 0,
                   false, gain_of(c, i + 1));
-  head_rows(c, c->stage_row(2 * d.L, 0), R, nullptr, am_out, nullptr, false, true);
+  head_rows(c, c->stage_row(2 * d.L, 0), R, nullptr, am_out, nullptr, false, true, ss);
 }
 
 // copy rows [0, n) of plane set src (plane stride plane_stride_rows rows) into
@@ -462,6 +495,7 @@ static ks_status check_desc(const ks_model_desc* d) {
   REQ(d->ffn >= 32 && d->ffn % 32 == 0, "ffn must be a positive multiple of 32");
   REQ((d->hq * d->hd) % 32 == 0, "hq*hd must be a multiple of 32");
   REQ(d->vocab >= 16 && d->vocab % 16 == 0, "vocab must be a positive multiple of 16");
+  REQ(vocab_fits(d->vocab, 0), "vocab must be at most 524288");
   REQ(d->n_max >= 2, "n_max must be >= 2");
   REQ(d->eps >= 0.f, "eps must be >= 0");
   REQ(d->rope_theta > 0.0, "rope_theta must be > 0");
@@ -642,7 +676,11 @@ ks_status ks_prefill(ks_ctx* c, const int32_t* tokens, int n, int32_t* out_first
         p += run;
       }
     }
-    if (c0 + R == n) head_rows(c, x + (size_t)(R - 1) * d.d, 1, nullptr, am, nullptr, false);
+    if (c0 + R == n) {
+      const SampleSpec ss = c->spec(0, nullptr, am, n, 2);
+      head_rows(c, x + (size_t)(R - 1) * d.d, 1, nullptr, am, nullptr, false, false,
+                c->sampling() ? &ss : nullptr);
+    }
   }
   HIPCHK(hipGetLastError());
   int32_t first = 0;
@@ -677,8 +715,11 @@ ks_status ks_set_context(ks_ctx* c, int n_cached, int32_t last_token) {
 static ks_status draft_internal(ks_ctx* c, const uint8_t* exec) {
   int32_t* dt = c->at<int32_t>(c->y.tok);
   if (c->k_draft == 0) set_i32(dt, c->s, c->st);
-  decode_row(c, dt + c->k_draft, c->P + c->k_draft, exec, dt + c->k_draft + 1,
-             c->at<float>(c->y.top1) + c->k_draft);
+  float* top1 = c->at<float>(c->y.top1) + c->k_draft;
+  const SampleSpec ss =
+      c->spec(c->qrow(c->k_draft), top1, dt + c->k_draft + 1, c->P + c->k_draft + 1, 0);
+  decode_row(c, dt + c->k_draft, c->P + c->k_draft, exec, dt + c->k_draft + 1, top1,
+             c->sampling() ? &ss : nullptr);
   c->k_draft++;
   return KS_OK;
 }
@@ -712,13 +753,31 @@ static ks_status verify_internal(ks_ctx* c, const int32_t* toks, int gamma, int3
                                  int* out_a) {
   const int R = gamma + 1;
   int32_t* am = c->at<int32_t>(c->y.am);
-  verify_rows(c, c->at<int32_t>(c->y.tok), R, am);
-  HIPCHK(hipGetLastError());
+  int32_t* tok = c->at<int32_t>(c->y.tok);
   int32_t* y = c->pin + 16;
-  HIPCHK(hipMemcpyAsync(y, am, R * 4, hipMemcpyDeviceToHost, c->st));
-  HIPCHK(hipStreamSynchronize(c->st));
   int a = 0;
-  while (a < gamma && toks[a + 1] == y[a]) ++a;
+  if (c->sampling()) {
+    // target tables of rows 0..gamma, then the acceptance chain against the
+    // draft tables the draft steps left (Section 2.1, speculative sampling)
+    const SampleSpec ss = c->spec(0, nullptr, nullptr, 0, 0);
+    verify_rows(c, tok, R, am, &ss);
+    int32_t* res = c->at<int32_t>(c->y.sres);
+    const int q0 = c->qrow(0);
+    spec_accept(c->tab_ids(0), c->tab_pr(0), c->tab_cnt(0), c->tab_ids(q0), c->tab_pr(q0),
+                c->tab_cnt(q0), tok + 1, gamma, c->samp.seed, c->P, res, c->st);
+    HIPCHK(hipGetLastError());
+    HIPCHK(hipMemcpyAsync(y, res, 8, hipMemcpyDeviceToHost, c->st));
+    HIPCHK(hipStreamSynchronize(c->st));
+    a = y[0];
+    const int32_t fin = y[1];
+    for (int i = 0; i < R; ++i) y[i] = i < a ? toks[i + 1] : (i == a ? fin : -1);
+  } else {
+    verify_rows(c, tok, R, am);
+    HIPCHK(hipGetLastError());
+    HIPCHK(hipMemcpyAsync(y, am, R * 4, hipMemcpyDeviceToHost, c->st));
+    HIPCHK(hipStreamSynchronize(c->st));
+    while (a < gamma && toks[a + 1] == y[a]) ++a;
+  }
   HIPCHK(stash_history(c, c->stage_row(0, 0), c->lim.gamma_max + 1, a + 1, c->P));
   c->blocks.push_back({c->P, a + 1});
   while ((int)c->blocks.size() > c->lim.m_rounds) c->blocks.pop_front();
@@ -738,6 +797,18 @@ ks_status ks_verify(ks_ctx* c, const int32_t* tokens, int gamma, int32_t* out_pr
   }
   REQ(gamma >= 0 && gamma <= c->lim.gamma_max, "gamma out of range");
   REQ(tokens[0] == c->s, "tokens[0] must be the committed token");
+  if (c->sampling() && c->k_draft != gamma) {
+    set_error("sampling verify needs the gamma drafts of ks_draft_step since the last verify");
+    return KS_ESTATE;
+  }
+  if (c->sampling() && gamma > 0) {
+    // the acceptance chain reads the drafts' tables: the tokens must be those drafts
+    int32_t* dh = c->pin + 32;
+    HIPCHK(hipMemcpyAsync(dh, c->at<int32_t>(c->y.tok), (gamma + 1) * 4, hipMemcpyDeviceToHost,
+                          c->st));
+    HIPCHK(hipStreamSynchronize(c->st));
+    for (int t = 1; t <= gamma; ++t) REQ(tokens[t] == dh[t], "sampling verify: tokens must be the drafts");
+  }
   for (int t = 0; t <= gamma; ++t) REQ(tokens[t] >= 0 && tokens[t] < c->md.vocab, "token id out of range");
   if (c->P + gamma + 1 >= c->md.n_max) {
     set_error("verify positions exceed the KV cache");
@@ -755,6 +826,85 @@ ks_status ks_set_draft_policy(ks_ctx* c, const ks_draft_policy* p) {
       "gamma_source must be KS_GAMMA_FIXED or KS_GAMMA_SELECTED");
   c->tau_conf = p->tau_conf;
   c->gamma_source = p->gamma_source;
+  return KS_OK;
+}
+
+ks_status ks_set_sampling(ks_ctx* c, const ks_sampling* s) {
+  REQ(c, "ctx is null");
+  if (c->k_draft != 0) {
+    set_error("ks_set_sampling with a pending draft (verify it first)");
+    return KS_ESTATE;
+  }
+  if (!s || !(s->temperature > 0.f)) {
+    REQ(!s || std::isfinite(s->temperature), "temperature must be finite");
+    c->samp = ks_sampling{};
+    return KS_OK;
+  }
+  REQ(std::isfinite(s->temperature), "temperature must be finite");
+  REQ(s->top_k >= 1 && s->top_k <= KS_SAMPLE_KMAX && s->top_k <= c->md.vocab,
+      "top_k must be in [1, min(KS_SAMPLE_KMAX, vocab)]");
+  REQ(s->top_p > 0.f && s->top_p <= 1.f, "top_p must be in (0, 1]");
+  REQ(vocab_fits(c->md.vocab, s->top_k), "vocabulary too large for the sampling filter");
+  c->samp = *s;
+  return KS_OK;
+}
+
+static ks_status check_sampling(const ks_sampling* s, int vocab) {
+  REQ(s, "null pointer");
+  REQ(std::isfinite(s->temperature) && s->temperature > 0.f, "temperature must be finite and > 0");
+  REQ(s->top_k >= 1 && s->top_k <= KS_SAMPLE_KMAX && s->top_k <= vocab,
+      "top_k must be in [1, min(KS_SAMPLE_KMAX, vocab)]");
+  REQ(s->top_p > 0.f && s->top_p <= 1.f, "top_p must be in (0, 1]");
+  REQ(vocab_fits(vocab, s->top_k), "vocabulary too large for the sampling filter");
+  return KS_OK;
+}
+
+size_t ks_sample_workspace_bytes(int rows, int vocab, int top_k) {
+  if (rows < 1 || vocab < 1 || top_k < 1 || top_k > KS_SAMPLE_KMAX || top_k > vocab ||
+      !vocab_fits(vocab, top_k))
+    return 0;
+  return sample_ws_bytes(rows, vocab, top_k);
+}
+
+ks_status ks_sample_filter(const float* logits, int rows, int vocab, int ld, const ks_sampling* s,
+                           int pos0, int purpose, int32_t* ids, float* probs, int32_t* counts,
+                           float* top1, int32_t* tokens, void* workspace, size_t ws_bytes,
+                           void* stream) {
+  REQ(logits && ids && probs && counts && workspace, "null pointer");
+  REQ(rows >= 1 && rows <= 65535 && vocab >= 1 && ld >= vocab, "sizes out of range");
+  ks_status st = check_sampling(s, vocab);
+  if (st != KS_OK) return st;
+  REQ(pos0 >= 0 && purpose >= 0, "pos0 and purpose must be >= 0");
+  if (ws_bytes < sample_ws_bytes(rows, vocab, s->top_k)) {
+    set_error("workspace smaller than ks_sample_workspace_bytes");
+    return KS_ENOMEM;
+  }
+  const SampleSpec ss{s->temperature, s->top_k, s->top_p, s->seed, ids, probs, counts, top1,
+                      tokens, pos0, purpose};
+  sample_rows(logits, rows, vocab, ld, ss, workspace, (hipStream_t)stream);
+  HIPCHK(hipGetLastError());
+  return KS_OK;
+}
+
+ks_status ks_spec_accept(const int32_t* p_ids, const float* p_probs, const int32_t* p_counts,
+                         const int32_t* q_ids, const float* q_probs, const int32_t* q_counts,
+                         const int32_t* drafts, int gamma, uint64_t seed, int pos0, int32_t* out,
+                         void* stream) {
+  REQ(p_ids && p_probs && p_counts && out, "null pointer");
+  REQ(gamma == 0 || (q_ids && q_probs && q_counts && drafts), "null pointer");
+  REQ(gamma >= 0 && gamma <= 1024 && pos0 >= 0, "gamma must be in [0, 1024], pos0 >= 0");
+  spec_accept(p_ids, p_probs, p_counts, q_ids, q_probs, q_counts, drafts, gamma, seed, pos0, out,
+              (hipStream_t)stream);
+  HIPCHK(hipGetLastError());
+  return KS_OK;
+}
+
+ks_status ks_sample_uniforms(uint64_t seed, const int32_t* pos, int n, int purpose, float* out,
+                             void* stream) {
+  REQ(n >= 0 && purpose >= 0, "n and purpose must be >= 0");
+  REQ(n == 0 || (pos && out), "null pointer");
+  uniforms(seed, pos, n, purpose, out, (hipStream_t)stream);
+  HIPCHK(hipGetLastError());
   return KS_OK;
 }
 
@@ -1019,7 +1169,9 @@ static ks_status decode_internal(ks_ctx* c, int n_new, int gamma, int reselect_e
     std::vector<int32_t> tmp(RB);
     int flushed = 0;  // out_tokens[0..flushed] are final
     for (int k = 0; k < steps; ++k) {
-      decode_row(c, chain + (k % RB), c->P + k, nullptr, chain + ((k + 1) % RB), nullptr);
+      const SampleSpec ss = c->spec(0, nullptr, chain + ((k + 1) % RB), c->P + k + 1, 2);
+      decode_row(c, chain + (k % RB), c->P + k, nullptr, chain + ((k + 1) % RB), nullptr,
+                 c->sampling() ? &ss : nullptr);
       if ((k + 1) % (RB - 1) == 0 || k == steps - 1) {
         HIPCHK(hipMemcpyAsync(tmp.data(), chain, RB * 4, hipMemcpyDeviceToHost, c->st));
         HIPCHK(hipStreamSynchronize(c->st));

@@ -167,8 +167,40 @@ void attn_combine(const AttnArgs& a, const float* kvself, Act act_out, hipStream
 int attn_nsplit(int n_positions, int tiles);
 int attn_rows_per_block(int G, bool batched);
 
-// argmax (lowest index on ties) and top-1 probability of each row of logits
-void argmax_rows(const float* logits, int M, int V, int32_t* am, float* top1, hipStream_t st);
+// ---------------------------------------------------- vocabulary reductions
+// argmax (lowest index on ties) and top-1 probability of each of M rows of V
+// logits (rows ld floats apart); ws: argmax_ws_bytes(M, V) device bytes
+size_t argmax_ws_bytes(int M, int V);
+void argmax_rows(const float* logits, int M, int V, int ld, int32_t* am, float* top1, void* ws,
+                 hipStream_t st);
+// Sampling filter of R rows: tables of the top_k largest logits (ties by lower
+// id), softmax at the temperature, shortest prefix reaching top_p, ids / probs
+// rows KS_SAMPLE_KMAX apart, count[r] entries; top1 (optional) = unfiltered
+// softmax maximum; tok (optional) = draw of row r with the Philox uniform of
+// (seed, pos0 + r, purpose).  ws: sample_ws_bytes(R, V, top_k) device bytes.
+struct SampleSpec {
+  float temperature;
+  int top_k;
+  float top_p;
+  uint64_t seed;
+  int32_t* ids;
+  float* probs;
+  int32_t* count;
+  float* top1;
+  int32_t* tok;
+  int pos0;
+  int purpose;
+};
+bool vocab_fits(int V, int top_k);  // top_k = 0: the argmax reduction
+size_t sample_ws_bytes(int R, int V, int top_k);
+size_t sample_ws_bytes_max(int R);  // any top_k <= KS_SAMPLE_KMAX
+void sample_rows(const float* logits, int R, int V, int ld, const SampleSpec& s, void* ws,
+                 hipStream_t st);
+// acceptance chain of one speculative sampling round; out = {a, token}
+void spec_accept(const int32_t* pid, const float* ppr, const int32_t* pcnt, const int32_t* qid,
+                 const float* qpr, const int32_t* qcnt, const int32_t* drafts, int g,
+                 uint64_t seed, int pos0, int32_t* out, hipStream_t st);
+void uniforms(uint64_t seed, const int32_t* pos, int n, int purpose, float* out, hipStream_t st);
 // out[g] = mean_t cos(X[g][t], Y[t])
 void cos_groups(const float* X, const float* Y, int groups, int r, int d, float* out,
                 hipStream_t st);

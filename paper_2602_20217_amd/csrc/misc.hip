@@ -252,69 +252,6 @@ void qkv_post(const QkvPostArgs& a, hipStream_t st) {
 // One pass per element: running (max, first index of max, sum of exp(v - max))
 // per thread over a fixed strided order, then a fixed tree.  Larger value
 // wins; equal values keep the lower index.
-struct AmState {
-  float m;
-  int i;
-  float s;
-};
-__device__ inline void am_push(AmState& a, float v, int i) {
-  if (v > a.m) {
-    a.s = a.s * __expf(a.m - v) + 1.0f;
-    a.m = v;
-    a.i = i;
-  } else {
-    a.s += __expf(v - a.m);
-  }
-}
-__device__ inline AmState am_merge(AmState a, AmState b) {
-  AmState r;
-  if (b.m > a.m || (b.m == a.m && b.i < a.i)) {
-    r.m = b.m;
-    r.i = b.i;
-  } else {
-    r.m = a.m;
-    r.i = a.i;
-  }
-  r.s = a.s * __expf(a.m - r.m) + b.s * __expf(b.m - r.m);
-  return r;
-}
-
-__global__ __launch_bounds__(1024) void k_argmax(const float* __restrict__ logits, int V,
-                                                 int32_t* am, float* top1) {
-  __shared__ AmState sh[16];
-  const int m = blockIdx.x;
-  const float* row = logits + (size_t)m * V;
-  AmState a{-FLT_MAX, 0x7FFFFFFF, 0.f};
-  const int V4 = V / 4;  // V % 16 == 0
-#pragma unroll 4
-  for (int k = threadIdx.x; k < V4; k += 1024) {
-    const float4 v = *(const float4*)(row + 4 * k);
-    am_push(a, v.x, 4 * k);
-    am_push(a, v.y, 4 * k + 1);
-    am_push(a, v.z, 4 * k + 2);
-    am_push(a, v.w, 4 * k + 3);
-  }
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) {
-    AmState b{__shfl_xor(a.m, o), __shfl_xor(a.i, o), __shfl_xor(a.s, o)};
-    a = am_merge(a, b);
-  }
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  if (lane == 0) sh[wave] = a;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    AmState r = sh[0];
-    for (int w = 1; w < 16; ++w) r = am_merge(r, sh[w]);
-    am[m] = r.i;
-    if (top1) top1[m] = 1.0f / r.s;
-  }
-}
-
-void argmax_rows(const float* logits, int M, int V, int32_t* am, float* top1, hipStream_t st) {
-  if (M <= 0) return;
-  hipLaunchKernelGGL(k_argmax, dim3(M), dim3(1024), 0, st, logits, V, am, top1);
-}
-
 // ------------------------------------------------------------------ cosine
 // One wave per row: <x, y>, |x|^2, |y|^2 accumulated in float64 (every
 // float32 product is exact in float64).  Rows of a multiple of 4 floats at

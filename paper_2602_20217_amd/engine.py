@@ -253,6 +253,12 @@ class DeviceModel:
         src = {"fixed": K.KS_GAMMA_FIXED, "selected": K.KS_GAMMA_SELECTED}[gamma_source]
         K.ks_set_draft_policy(self.ctx, C.byref(K.DraftPolicy(tau_conf, src)))
 
+    def set_sampling(self, temperature: float = 0.0, top_k: int = 50, top_p: float = 0.95,
+                     seed: int = 0):
+        """Speculative sampling with the T / top-k / top-p filter and Philox
+        stream `seed`; temperature <= 0 returns to greedy decoding."""
+        K.ks_set_sampling(self.ctx, C.byref(K.Sampling(temperature, top_k, top_p, seed)))
+
     def generate(self, prompt, n_new: int, gamma: int, reselect_every: int = 32,
                  params: K.SelectParams | None = None, max_sel_log: int = 256):
         p = np.ascontiguousarray(prompt, dtype=np.int32)
@@ -312,6 +318,43 @@ def hidden_cos(X: torch.Tensor, Y: torch.Tensor) -> torch.Tensor:
     G, r, d = X.shape
     out = torch.empty(G, dtype=torch.float32, device=X.device)
     K.ks_hidden_cos(_ptr(X), _ptr(Y), G, r, d, _ptr(out), _stream())
+    return out
+
+
+def sample_filter(logits: torch.Tensor, temperature: float, top_k: int, top_p: float,
+                  seed: int = 0, pos0: int | None = None, purpose: int = 2):
+    """Filter tables (ids, probs, counts), unfiltered top-1 probability and, when
+    pos0 is given, the draw of row r at position pos0 + r."""
+    R, V = logits.shape
+    dev = logits.device
+    s = K.Sampling(temperature, top_k, top_p, seed)
+    ws_b = K.ks_sample_workspace_bytes(R, V, top_k)  # 0: the call reports the bad argument
+    ws = torch.empty(max(ws_b, 256), dtype=torch.uint8, device=dev)
+    ids = torch.empty(R, K.KS_SAMPLE_KMAX, dtype=torch.int32, device=dev)
+    probs = torch.empty(R, K.KS_SAMPLE_KMAX, dtype=torch.float32, device=dev)
+    cnt = torch.empty(R, dtype=torch.int32, device=dev)
+    top1 = torch.empty(R, dtype=torch.float32, device=dev)
+    tok = torch.empty(R, dtype=torch.int32, device=dev) if pos0 is not None else None
+    K.ks_sample_filter(_ptr(logits), R, V, logits.stride(0), C.byref(s), pos0 or 0, purpose,
+                       _ptr(ids), _ptr(probs), _ptr(cnt), _ptr(top1),
+                       _ptr(tok) if tok is not None else None, _ptr(ws), ws_b, _stream())
+    return ids, probs, cnt, top1, tok
+
+
+def spec_accept(p_ids, p_probs, p_cnt, q_ids, q_probs, q_cnt, drafts: torch.Tensor, seed: int,
+                pos0: int):
+    """Acceptance chain of one round on device tables: (accepted drafts, token)."""
+    g = drafts.numel()
+    out = torch.empty(2, dtype=torch.int32, device=p_ids.device)
+    K.ks_spec_accept(_ptr(p_ids), _ptr(p_probs), _ptr(p_cnt), _ptr(q_ids), _ptr(q_probs),
+                     _ptr(q_cnt), _ptr(drafts), g, seed, pos0, _ptr(out), _stream())
+    a, t = out.cpu().tolist()
+    return a, t
+
+
+def sample_uniforms(seed: int, pos: torch.Tensor, purpose: int) -> torch.Tensor:
+    out = torch.empty(pos.numel(), dtype=torch.float32, device=pos.device)
+    K.ks_sample_uniforms(seed, _ptr(pos), pos.numel(), purpose, _ptr(out), _stream())
     return out
 
 

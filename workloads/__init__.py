@@ -230,3 +230,15 @@ def synthetic_rows(rows: int, d: int, seed: int = 4, std: float = 1.0, index: in
     """Random residual-stream rows [rows, d], float32."""
     g = np.random.Generator(np.random.PCG64([seed, 2000 + index]))
     return g.standard_normal((rows, d), dtype=np.float32) * np.float32(std)
+
+
+def synthetic_logits(rows: int, vocab: int, seed: int = 5, std: float = 3.0, ties: bool = False,
+                     index: int = 0):
+    """Random LM-head outputs [rows, vocab], float32: normal with the given std;
+    ties=True rounds them to multiples of 1/4, so equal logits occur at the top
+    and across the top-k boundary."""
+    g = np.random.Generator(np.random.PCG64([seed, 3000 + index]))
+    z = g.standard_normal((rows, vocab), dtype=np.float32) * np.float32(std)
+    if ties:
+        z = np.round(z * 4.0).astype(np.float32) / np.float32(4.0)
+    return z
