@@ -271,6 +271,9 @@ def main():
                          "0 keeps the fixed draft length of the workload)")
     ap.add_argument("--gamma-source", default="fixed", choices=("fixed", "selected"),
                     help="draft cap per round: --gamma, or min(gamma*, --gamma)")
+    ap.add_argument("--sample", default="",
+                    help="T,top_k,top_p[,seed]: speculative sampling (paper's sampling "
+                         "setting: 0.7,50,0.95) instead of greedy decoding")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-kernels", action="store_true",
@@ -313,6 +316,12 @@ def main():
     W.generate_weights(cfg, seed=0, consume=dm.upload)
     dm.finalize()
     dm.set_draft_policy(args.tau_conf, args.gamma_source)
+    sampling = None
+    if args.sample:
+        f = args.sample.split(",")
+        sampling = {"temperature": float(f[0]), "top_k": int(f[1]), "top_p": float(f[2]),
+                    "seed": int(f[3]) if len(f) > 3 else 0}
+        dm.set_sampling(**sampling)
     log(f"weights generated and packed in {time.time() - t:.1f}s")
     prompt = W.prompt_ids(cfg.vocab, args.ctx, 1)
 
@@ -378,7 +387,8 @@ def main():
         log(f"step {k}: AR {a_ms:.1f} ms, speculative {s_ms:.1f} ms "
             f"(select {st.ms_select:.1f} ms, accepted {st.n_accepted}/{st.n_drafted})")
     out, st, sels = ssd_last
-    same = bool(np.array_equal(out, ar_out))
+    # greedy: the speculative tokens equal the AR tokens; sampling draws differ
+    same = None if sampling else bool(np.array_equal(out, ar_out))
 
     # roofline of the dominant kernel: the decode step's gate/up projection
     prof = dm.profile_decode(None, 16, per_kernel=True)
@@ -419,7 +429,9 @@ def main():
                    "global_batch": 1, "seq_len": args.ctx, "new_tokens": args.new,
                    "gamma": args.gamma, "reselect_every": args.reselect, "parallelism": "none",
                    "draft_policy": {"tau_conf": args.tau_conf,
-                                    "gamma_source": args.gamma_source}},
+                                    "gamma_source": args.gamma_source},
+                   "decoding": ({"mode": "speculative sampling", **sampling} if sampling
+                                else {"mode": "greedy"})},
         "speedup_vs_ar": round(value / ar_tps, 4), "ar_tok_s": round(ar_tps, 2),
         "ar_ms_per_step": round(mean_ar, 2), "tokens_equal_ar": same,
         "accepted": st.n_accepted, "drafted": st.n_drafted, "rounds": st.n_rounds,

@@ -132,3 +132,49 @@ def test_full_size_speculative_equals_ar(full):
                         for i in range(2 * cfg.L) if not s.exec[i])
         assert skipped_w == s.j_star and 0 <= s.j_star <= s.C // 2
         assert 1 <= s.gamma_star <= 10 and 0.0 <= s.alpha_hat <= 1.0
+
+
+def test_full_size_sampling_filter(full):
+    """T 0.7 / top-k 50 / top-p 0.95 tables and draws of two rows of 128256
+    head logits, against the oracle's filter of the same logits."""
+    from oracle import sampling as S
+    from paper_2602_20217_amd.engine import sample_filter
+    cfg, dm = full
+    x = W.synthetic_rows(2, cfg.d, seed=4, std=1.0, index=501)
+    logits, _, _ = dm.head_rows(torch.from_numpy(x).cuda())
+    ids, probs, cnt, top1, tok = [t.cpu().numpy() for t in
+                                  sample_filter(logits, 0.7, 50, 0.95, seed=9, pos0=CTX)]
+    lg = logits.cpu().numpy().astype(np.float64)
+    for r in range(2):
+        prm = S.SamplingParams(0.7, 50, 0.95, 9)
+        mg = []
+        rid, rpr = S.filtered(lg[r], prm, mg)
+        if min(mg) <= 1e-5:
+            continue
+        assert cnt[r] == len(rid) and ids[r, :cnt[r]].tolist() == rid.tolist()
+        np.testing.assert_allclose(probs[r, :cnt[r]], rpr, rtol=2e-5, atol=1e-7)
+        assert top1[r] == pytest.approx(1.0 / np.sum(np.exp(lg[r] - lg[r].max())), rel=1e-4)
+        dmg = []
+        t_ref = S.draw(rid, rpr, S.uniform(9, CTX + r, 2), dmg)
+        if min(dmg, default=1.0) > 1e-5:
+            assert tok[r] == t_ref
+
+
+def test_full_size_top_k_one_sampling_is_greedy(full):
+    """Speculative sampling with top-k 1 accepts exactly as greedy verification
+    does: after the 8K prefill it emits the autoregressive tokens."""
+    from paper_2602_20217_amd.engine import select_params
+    cfg, dm = full
+    prompt = W.prompt_ids(cfg.vocab, CTX, 1)
+    dm.prefill(prompt)
+    ar, _, _ = dm.decode(40, 0)
+    params = select_params((0.074, 1.2e-6, 0.035), "paper_min", 0, tau=0.5, prune_half=True,
+                           D=10)
+    dm.set_sampling(0.7, 1, 0.95, 4)
+    try:
+        dm.prefill(prompt)
+        sd, st, _ = dm.decode(40, 4, 32, params)
+    finally:
+        dm.set_sampling(0.0)
+    assert np.array_equal(ar, sd)
+    assert st.n_rounds >= 1
