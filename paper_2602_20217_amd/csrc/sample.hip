@@ -71,13 +71,26 @@ __device__ inline VStat st_merge(VStat a, VStat b) {
   r.pad = 0;
   return r;
 }
+template <int CTRL>
+__device__ inline VStat st_rot(VStat a) {
+  const int m = __builtin_amdgcn_update_dpp(0, __float_as_int(a.m), CTRL, 0xF, 0xF, false);
+  const int s = __builtin_amdgcn_update_dpp(0, __float_as_int(a.s), CTRL, 0xF, 0xF, false);
+  const int i = __builtin_amdgcn_update_dpp(0, a.i, CTRL, 0xF, 0xF, false);
+  return VStat{__int_as_float(m), __int_as_float(s), i, 0};
+}
+__device__ inline VStat st_lane(VStat a, int l) {
+  return VStat{__int_as_float(__builtin_amdgcn_readlane(__float_as_int(a.m), l)),
+               __int_as_float(__builtin_amdgcn_readlane(__float_as_int(a.s), l)),
+               __builtin_amdgcn_readlane(a.i, l), 0};
+}
+// wave reduction (every lane gets the result): row rotations (DPP), then the
+// four row results (merge is commutative and associative up to rounding)
 __device__ inline VStat st_wave(VStat a) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) {
-    VStat b{__shfl_xor(a.m, o), __shfl_xor(a.s, o), __shfl_xor(a.i, o), 0};
-    a = st_merge(a, b);
-  }
-  return a;
+  a = st_merge(a, st_rot<0x128>(a));
+  a = st_merge(a, st_rot<0x124>(a));
+  a = st_merge(a, st_rot<0x122>(a));
+  a = st_merge(a, st_rot<0x121>(a));
+  return st_merge(st_merge(st_lane(a, 0), st_lane(a, 16)), st_merge(st_lane(a, 32), st_lane(a, 48)));
 }
 
 // Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC 2011): first output word of
@@ -99,31 +112,65 @@ __device__ inline float philox_uniform(uint32_t k0, uint32_t k1, uint32_t pos, u
   return (float)(c0 >> 8) * (1.0f / 16777216.0f);
 }
 
-template <typename T>
-__device__ inline T wave_incl_scan(T x, int lane) {
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const T t = __shfl_up(x, o);
-    if (lane >= o) x += t;
-  }
+// Cross-lane steps on DPP lane moves (no LDS round trip).  dpp(x, ctrl, rows):
+// the value of the lane the control names, 0 where the source lane lies
+// outside the row or the destination row is masked off.
+template <int CTRL, int ROWS = 0xF, bool BOUND = true>
+__device__ inline int dpp_i(int x) {
+  return __builtin_amdgcn_update_dpp(0, x, CTRL, ROWS, 0xF, BOUND);
+}
+template <int CTRL, int ROWS = 0xF, bool BOUND = true>
+__device__ inline float dpp_f(float x) {
+  return __int_as_float(dpp_i<CTRL, ROWS, BOUND>(__float_as_int(x)));
+}
+constexpr int ROW_SHR1 = 0x111, ROW_SHR2 = 0x112, ROW_SHR4 = 0x114, ROW_SHR8 = 0x118;
+constexpr int ROW_ROR1 = 0x121, ROW_ROR2 = 0x122, ROW_ROR4 = 0x124, ROW_ROR8 = 0x128;
+constexpr int ROW_BCAST15 = 0x142, ROW_BCAST31 = 0x143;
+
+// inclusive prefix sum over the 64 lanes: scans of the four 16-lane rows, then
+// lane 15 added into row 1 and 3, lane 31 into rows 2 and 3
+__device__ inline int wave_scan(int x) {
+  x += dpp_i<ROW_SHR1>(x);
+  x += dpp_i<ROW_SHR2>(x);
+  x += dpp_i<ROW_SHR4>(x);
+  x += dpp_i<ROW_SHR8>(x);
+  x += dpp_i<ROW_BCAST15, 0xA, false>(x);
+  x += dpp_i<ROW_BCAST31, 0xC, false>(x);
   return x;
 }
-__device__ inline float wave_sum(float x) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) x += __shfl_xor(x, o);
+__device__ inline float wave_scan(float x) {
+  x += dpp_f<ROW_SHR1>(x);
+  x += dpp_f<ROW_SHR2>(x);
+  x += dpp_f<ROW_SHR4>(x);
+  x += dpp_f<ROW_SHR8>(x);
+  x += dpp_f<ROW_BCAST15, 0xA, false>(x);
+  x += dpp_f<ROW_BCAST31, 0xC, false>(x);
   return x;
+}
+__device__ inline float lane_f(float x, int l) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), l));
+}
+// wave-uniform sum / max: row rotations, then the four row results
+__device__ inline float wave_sum(float x) {
+  x += dpp_f<ROW_ROR8>(x);
+  x += dpp_f<ROW_ROR4>(x);
+  x += dpp_f<ROW_ROR2>(x);
+  x += dpp_f<ROW_ROR1>(x);
+  return (lane_f(x, 0) + lane_f(x, 16)) + (lane_f(x, 32) + lane_f(x, 48));
 }
 __device__ inline float wave_max(float x) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) x = fmaxf(x, __shfl_xor(x, o));
-  return x;
+  x = fmaxf(x, dpp_f<ROW_ROR8>(x));
+  x = fmaxf(x, dpp_f<ROW_ROR4>(x));
+  x = fmaxf(x, dpp_f<ROW_ROR2>(x));
+  x = fmaxf(x, dpp_f<ROW_ROR1>(x));
+  return fmaxf(fmaxf(lane_f(x, 0), lane_f(x, 16)), fmaxf(lane_f(x, 32), lane_f(x, 48)));
 }
 
 // Exclusive prefix over the block of v (thread order) and the block total.
 template <int NT>
 __device__ inline int block_excl_scan(int v, int* sh, int& total) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int x = wave_incl_scan(v, lane);
+  const int x = wave_scan(v);
   if (lane == 63) sh[wave] = x;
   __syncthreads();
   int base = 0, tot = 0;
@@ -138,10 +185,35 @@ __device__ inline int block_excl_scan(int v, int* sh, int& total) {
   return base + x - v;
 }
 
+// Histogram update of the wave's lanes with pred set.  agg (the top digit,
+// where a selection's keys mostly agree and same-address LDS atomics would
+// serialise): the lanes sharing the first two distinct digits of the wave add
+// their count through one lane each, the rest one by one; otherwise every lane
+// adds its own.
+__device__ inline void hist_add(int* hist, bool pred, uint32_t d, bool agg) {
+  if (!agg) {
+    if (pred) atomicAdd(&hist[d], 1);
+    return;
+  }
+  const int lane = threadIdx.x & 63;
+  uint64_t act = __ballot(pred);
+#pragma unroll
+  for (int round = 0; round < 2; ++round) {
+    if (!act) return;  // wave-uniform
+    const int leader = __ffsll((unsigned long long)act) - 1;
+    const uint32_t dl = (uint32_t)__builtin_amdgcn_readlane((int)d, leader);
+    const uint64_t same = __ballot(pred && d == dl);
+    if (lane == leader) atomicAdd(&hist[dl], (int)__popcll(same));
+    act &= ~same;
+    pred = pred && d != dl;
+  }
+  if (pred) atomicAdd(&hist[d], 1);
+}
+
 // k-th largest key (k = want on entry, 1 <= want <= number of valid keys) of
 // the block's valid keys: on return thr is that key and want the number of
 // keys equal to thr that belong to the top k (keys above thr number k - want).
-// Key e of a thread is valid iff e < nv[thread] (nv <= E).
+// Key e of a thread is valid iff e < nv (nv <= E).
 template <int NT, int E>
 __device__ inline void radix_kth(const uint32_t (&key)[E], int nv, int* hist, int* sh,
                                  uint32_t& thr, int& want) {
@@ -153,29 +225,25 @@ __device__ inline void radix_kth(const uint32_t (&key)[E], int nv, int* hist, in
     __syncthreads();
 #pragma unroll
     for (int e = 0; e < E; ++e)
-      if (e < nv && (key[e] & himask) == prefix) atomicAdd(&hist[(key[e] >> shift) & 255u], 1);
+      hist_add(hist, e < nv && (key[e] & himask) == prefix, (key[e] >> shift) & 255u,
+               shift == 24);
     __syncthreads();
     if (threadIdx.x < 64) {
-      // lane l holds digits 4l..4l+3; suffix sums from the top digit down
-      const int h0 = hist[4 * lane], h1 = hist[4 * lane + 1], h2 = hist[4 * lane + 2],
-                h3 = hist[4 * lane + 3];
-      const int tot = h0 + h1 + h2 + h3;
-      int s = tot;
-#pragma unroll
-      for (int o = 1; o < 64; o <<= 1) {
-        const int t = __shfl_down(s, o);
-        if (lane + o < 64) s += t;
-      }
-      int above = s - tot;  // keys in digits above 4l+3
+      // lane l holds digits 255 - 4l down to 252 - 4l; the prefix sum over the
+      // lanes counts the keys from the top digit down
+      const int4 q = *(const int4*)&hist[252 - 4 * lane];
+      const int h[4] = {q.w, q.z, q.y, q.x};  // digits 255 - 4l - j
+      const int tot = h[0] + h[1] + h[2] + h[3];
+      const int s = wave_scan(tot);
+      int above = s - tot;  // keys in digits above 255 - 4l
       if (above < want && want <= s) {
-        const int h[4] = {h0, h1, h2, h3};
-        int d = 4 * lane;
-        for (int b = 3; b >= 0; --b) {
-          if (above + h[b] >= want) {
-            d = 4 * lane + b;
+        int d = 252 - 4 * lane;
+        for (int j = 0; j < 4; ++j) {
+          if (above + h[j] >= want) {
+            d = 255 - 4 * lane - j;
             break;
           }
-          above += h[b];
+          above += h[j];
         }
         sh[0] = d;
         sh[1] = want - above;
@@ -190,52 +258,79 @@ __device__ inline void radix_kth(const uint32_t (&key)[E], int nv, int* hist, in
   thr = prefix;
 }
 
-// Index-ordered compaction of the top k: element (e, thread) has index
-// e * NT + thread; selected are all keys above thr and the first `want` keys
-// equal to thr.  all: select every valid element.  Calls put(slot, e).
+// Index-ordered compaction of the top k.  Thread t holds the consecutive
+// elements t * c .. t * c + nv - 1 (c per thread, nv <= c valid) in key[0..nv);
+// selected are all keys above thr and the first `want` keys equal to thr
+// (all: every valid element).  One block scan; calls put(slot, e), slot < k.
 template <int NT, int E, typename F>
-__device__ inline void compact_top(const uint32_t (&key)[E], int nv, int en, bool all, uint32_t thr,
+__device__ inline void compact_top(const uint32_t (&key)[E], int nv, bool all, uint32_t thr,
                                    int want, int* sh, F put) {
-  int gt_run = 0, eq_run = 0;
+  int cg = 0, ce = 0;
 #pragma unroll
   for (int e = 0; e < E; ++e) {
-    if (e < en) {  // uniform over the block
-      const bool valid = e < nv;
-      const bool gt = valid && (all || key[e] > thr);
-      const bool eq = valid && !all && key[e] == thr;
-      int total = 0;
-      const int ex = block_excl_scan<NT>((int)gt | ((int)eq << 16), sh, total);
-      const int gtb = gt_run + (ex & 0xFFFF), eqb = eq_run + (ex >> 16);
-      if (gt) put(gtb + min(eqb, want), e);
-      if (eq && eqb < want) put(gtb + eqb, e);  // slots stay below k
-      gt_run += total & 0xFFFF;
-      eq_run += total >> 16;
+    if (e < nv) {
+      cg += (all || key[e] > thr) ? 1 : 0;
+      ce += (!all && key[e] == thr) ? 1 : 0;
+    }
+  }
+  int total = 0;
+  const int ex = block_excl_scan<NT>(cg | (ce << 16), sh, total);
+  int gtb = ex & 0xFFFF, eqb = ex >> 16;
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    if (e < nv) {
+      if (all || key[e] > thr) {
+        put(gtb + min(eqb, want), e);
+        ++gtb;
+      } else if (key[e] == thr) {
+        if (eqb < want) put(gtb + eqb, e);
+        ++eqb;
+      }
     }
   }
 }
 
+// candidates of a row: NB * k (key, id) pairs, rows an even number of pairs
+// apart so that every row starts 16-byte aligned
+__host__ __device__ inline int cand_stride(int NB, int k) { return (NB * k + 1) & ~1; }
+
 // grid (NB, rows), SCAN_NT threads.  Row r of logits (ld floats apart), chunk
-// b = ids [b * chunk, min(V, (b + 1) * chunk)).  k > 0: also the chunk's top-k
-// candidates (keys, ids) in id order at cand[(r * NB + b) * k ..], padded with
-// (0, INT_MAX) when the chunk is shorter than k.
+// b = ids [b * chunk, min(V, (b + 1) * chunk)); thread t reads the c = chunk /
+// SCAN_NT consecutive logits from t * c.  k > 0: also the chunk's top-k
+// candidates, (key, id) pairs in id order at cand[r * stride + b * k ..],
+// padded with (0, INT_MAX) when the chunk is shorter than k.
 __global__ __launch_bounds__(SCAN_NT) void k_vocab_scan(const float* __restrict__ logits, int ld,
                                                         int V, int chunk, int k, VStat* stat,
-                                                        uint32_t* ckey, int32_t* cid) {
-  __shared__ int hist[256];
+                                                        uint2* cand) {
+  __shared__ __align__(16) int hist[256];
   __shared__ int sh[8];
   __shared__ VStat sred[SCAN_NT / 64];
   const int b = blockIdx.x, NB = gridDim.x, r = blockIdx.y, t = threadIdx.x;
   const int j0 = b * chunk;
   const int n = min(chunk, V - j0);
-  const float* row = logits + (size_t)r * ld + j0;
+  const int c = chunk / SCAN_NT;  // chunk is a multiple of SCAN_NT
+  const int i0 = t * c;           // first element of this thread within the chunk
+  const int nv = max(0, min(c, n - i0));
+  const float* row = logits + (size_t)r * ld + j0 + i0;
   float v[SCAN_E];
-  VStat a{-FLT_MAX, 0.f, 0x7FFFFFFF, 0};
-  const int nv = n > t ? (n - t + SCAN_NT - 1) / SCAN_NT : 0;
+  const bool vec = ((((uintptr_t)row) & 15) == 0) && (c & 3) == 0;
 #pragma unroll
-  for (int e = 0; e < SCAN_E; ++e) {
-    v[e] = e < nv ? row[t + e * SCAN_NT] : -FLT_MAX;
-    if (e < nv) st_push(a, v[e], j0 + t + e * SCAN_NT);
+  for (int e = 0; e < SCAN_E; e += 4) {
+    if (vec && e + 4 <= nv) {
+      const float4 q = *(const float4*)(row + e);
+      v[e] = q.x;
+      v[e + 1] = q.y;
+      v[e + 2] = q.z;
+      v[e + 3] = q.w;
+    } else {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) v[e + u] = e + u < nv ? row[e + u] : -FLT_MAX;
+    }
   }
+  VStat a{-FLT_MAX, 0.f, 0x7FFFFFFF, 0};
+#pragma unroll
+  for (int e = 0; e < SCAN_E; ++e)
+    if (e < nv) st_push(a, v[e], j0 + i0 + e);
   a = st_wave(a);
   if ((t & 63) == 0) sred[t >> 6] = a;
   __syncthreads();
@@ -253,18 +348,11 @@ __global__ __launch_bounds__(SCAN_NT) void k_vocab_scan(const float* __restrict_
   uint32_t thr = 0u;
   int want = k;
   if (!all) radix_kth<SCAN_NT, SCAN_E>(key, nv, hist, sh, thr, want);
-  const size_t base = ((size_t)r * NB + b) * k;
-  const int en = (n + SCAN_NT - 1) / SCAN_NT;
-  compact_top<SCAN_NT, SCAN_E>(key, nv, en, all, thr, want, sh, [&](int slot, int e) {
-    if (slot < k) {
-      ckey[base + slot] = key[e];
-      cid[base + slot] = j0 + t + e * SCAN_NT;
-    }
+  uint2* out = cand + (size_t)r * cand_stride(NB, k) + (size_t)b * k;
+  compact_top<SCAN_NT, SCAN_E>(key, nv, all, thr, want, sh, [&](int slot, int e) {
+    if (slot < k) out[slot] = make_uint2(key[e], (uint32_t)(j0 + i0 + e));
   });
-  for (int s = min(n, k) + t; s < k; s += SCAN_NT) {
-    ckey[base + s] = 0u;
-    cid[base + s] = 0x7FFFFFFF;
-  }
+  for (int s = min(n, k) + t; s < k; s += SCAN_NT) out[s] = make_uint2(0u, 0x7FFFFFFFu);
 }
 
 // grid rows, 128 threads: argmax (lowest id on ties) and top-1 probability of
@@ -288,8 +376,7 @@ __global__ __launch_bounds__(128) void k_argmax_merge(const VStat* stat, int NB,
 struct RowArgs {
   const VStat* stat;
   int NB;
-  const uint32_t* ckey;
-  const int32_t* cid;
+  const uint2* cand;
   int k;
   float temperature, top_p;
   uint32_t seed_lo, seed_hi;
@@ -305,9 +392,9 @@ struct RowArgs {
 // (entry l in w0, entry l + 64 in w1): the first entry whose cumulative weight
 // exceeds u, else the last one.  Returns the entry index.
 __device__ inline int wave_draw(float w0, float w1, int n, float u, int lane) {
-  const float c0 = wave_incl_scan(lane < n ? w0 : 0.f, lane);
-  const float t0 = __shfl(c0, 63);
-  const float c1 = t0 + wave_incl_scan(lane + 64 < n ? w1 : 0.f, lane);
+  const float c0 = wave_scan(lane < n ? w0 : 0.f);
+  const float t0 = lane_f(c0, 63);
+  const float c1 = t0 + wave_scan(lane + 64 < n ? w1 : 0.f);
   const uint64_t b0 = __ballot(lane < n && c0 > u);
   if (b0) return __ffsll((unsigned long long)b0) - 1;
   const uint64_t b1 = __ballot(lane + 64 < n && c1 > u);
@@ -319,13 +406,34 @@ __device__ inline int wave_draw(float w0, float w1, int n, float u, int lane) {
 // (logit desc, id asc); softmax at temperature T; top-p cut; table write and
 // optional draw.
 __global__ __launch_bounds__(ROW_NT) void k_sample_row(RowArgs A) {
-  __shared__ int hist[256];
+  __shared__ __align__(16) int hist[256];
   __shared__ int sh[16];
-  __shared__ uint32_t sk[KS_SAMPLE_KMAX], ok[KS_SAMPLE_KMAX];
-  __shared__ int32_t si[KS_SAMPLE_KMAX], oi[KS_SAMPLE_KMAX];
+  __shared__ __align__(16) uint32_t sk[KS_SAMPLE_KMAX];
+  __shared__ __align__(16) int32_t si[KS_SAMPLE_KMAX];
+  __shared__ uint32_t ok[KS_SAMPLE_KMAX];
+  __shared__ int32_t oi[KS_SAMPLE_KMAX];
+  __shared__ int srank[KS_SAMPLE_KMAX];
   __shared__ VStat sred[ROW_NT / 64];
   const int r = blockIdx.x, t = threadIdx.x, lane = t & 63;
   const int k = A.k, n = A.NB * k;
+  // candidates first (their loads overlap the partials' merge): thread t holds
+  // the c consecutive pairs from t * c, c even, two pairs per 16-byte load
+  const uint2* cr = A.cand + (size_t)r * cand_stride(A.NB, k);
+  const int c = 2 * ((n + 2 * ROW_NT - 1) / (2 * ROW_NT));
+  const int i0 = t * c;
+  const int nv = max(0, min(c, n - i0));
+  uint32_t key[ROW_E];
+  int32_t cand_id[ROW_E];
+#pragma unroll
+  for (int e = 0; e < ROW_E; e += 2) {
+    uint4 q = make_uint4(0u, 0x7FFFFFFFu, 0u, 0x7FFFFFFFu);
+    if (e < nv) q = *(const uint4*)(cr + i0 + e);  // pair e + 1 is inside the padded row
+    key[e] = q.x;
+    cand_id[e] = (int32_t)q.y;
+    key[e + 1] = q.z;
+    cand_id[e + 1] = (int32_t)q.w;
+  }
+  if (t < KS_SAMPLE_KMAX) srank[t] = 0;
   if (A.top1) {
     VStat a{-FLT_MAX, 0.f, 0x7FFFFFFF, 0};
     for (int b = t; b < A.NB; b += ROW_NT) a = st_merge(a, A.stat[(size_t)r * A.NB + b]);
@@ -339,31 +447,42 @@ __global__ __launch_bounds__(ROW_NT) void k_sample_row(RowArgs A) {
       A.top1[r] = 1.0f / s.s;
     }
   }
-  const uint32_t* ck = A.ckey + (size_t)r * n;
-  const int32_t* ci = A.cid + (size_t)r * n;
-  uint32_t key[ROW_E];
-  const int nv = n > t ? (n - t + ROW_NT - 1) / ROW_NT : 0;
-#pragma unroll
-  for (int e = 0; e < ROW_E; ++e) key[e] = e < nv ? ck[t + e * ROW_NT] : 0u;
   const bool all = n <= k;
   uint32_t thr = 0u;
   int want = k;
   if (!all) radix_kth<ROW_NT, ROW_E>(key, nv, hist, sh, thr, want);
-  compact_top<ROW_NT, ROW_E>(key, nv, (n + ROW_NT - 1) / ROW_NT, all, thr, want, sh,
-                             [&](int slot, int e) {
-                               if (slot < k) {
-                                 sk[slot] = key[e];
-                                 si[slot] = ci[t + e * ROW_NT];
-                               }
-                             });
+  compact_top<ROW_NT, ROW_E>(key, nv, all, thr, want, sh, [&](int slot, int e) {
+    if (slot < k) {
+      sk[slot] = key[e];
+      si[slot] = cand_id[e];
+    }
+  });
   __syncthreads();
-  if (t < k) {  // rank of entry t in (key desc, id asc)
-    const uint32_t mk = sk[t];
-    const int32_t mi = si[t];
-    int rank = 0;
-    for (int j = 0; j < k; ++j) rank += (sk[j] > mk || (sk[j] == mk && si[j] < mi)) ? 1 : 0;
-    ok[rank] = mk;
-    oi[rank] = mi;
+  {  // rank of entry i in (key desc, id asc), counted by 4 threads of 32 entries each
+    const int i = t & (KS_SAMPLE_KMAX - 1), part = t / KS_SAMPLE_KMAX;
+    if (i < k) {
+      const uint32_t mk = sk[i];
+      const int32_t mi = si[i];
+      int cnt = 0;
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        const int j = part * 32 + 4 * q;
+        if (j < k) {
+          const uint4 kk = *(const uint4*)&sk[j];
+          const int4 ii = *(const int4*)&si[j];
+          cnt += (kk.x > mk || (kk.x == mk && ii.x < mi)) ? 1 : 0;
+          cnt += (j + 1 < k && (kk.y > mk || (kk.y == mk && ii.y < mi))) ? 1 : 0;
+          cnt += (j + 2 < k && (kk.z > mk || (kk.z == mk && ii.z < mi))) ? 1 : 0;
+          cnt += (j + 3 < k && (kk.w > mk || (kk.w == mk && ii.w < mi))) ? 1 : 0;
+        }
+      }
+      if (cnt) atomicAdd(&srank[i], cnt);
+    }
+  }
+  __syncthreads();
+  if (t < k) {
+    ok[srank[t]] = sk[t];
+    oi[srank[t]] = si[t];
   }
   __syncthreads();
   if (t >= 64) return;
@@ -372,10 +491,10 @@ __global__ __launch_bounds__(ROW_NT) void k_sample_row(RowArgs A) {
   const float inv_t = 1.0f / A.temperature;
   const float e0 = lane < k ? expf((key_f(ok[lane]) - l0) * inv_t) : 0.f;
   const float e1 = lane + 64 < k ? expf((key_f(ok[lane + 64]) - l0) * inv_t) : 0.f;
-  const float c0 = wave_incl_scan(e0, lane);
-  const float t0 = __shfl(c0, 63);
-  const float c1 = t0 + wave_incl_scan(e1, lane);
-  const float sk_all = k > 64 ? __shfl(c1, k - 65) : __shfl(c0, k - 1);
+  const float c0 = wave_scan(e0);
+  const float t0 = lane_f(c0, 63);
+  const float c1 = t0 + wave_scan(e1);
+  const float sk_all = k > 64 ? lane_f(c1, k - 65) : lane_f(c0, k - 1);
   int m = k;
   if (A.top_p < 1.0f) {
     const float cut = A.top_p * sk_all;
@@ -385,7 +504,7 @@ __global__ __launch_bounds__(ROW_NT) void k_sample_row(RowArgs A) {
                          : (b1 ? 64 + __ffsll((unsigned long long)b1) - 1 : k - 1);
     m = first + 1;
   }
-  const float sm = m > 64 ? __shfl(c1, m - 65) : __shfl(c0, m - 1);
+  const float sm = m > 64 ? lane_f(c1, m - 65) : lane_f(c0, m - 1);
   const float p0 = lane < m ? e0 / sm : 0.f;
   const float p1 = lane + 64 < m ? e1 / sm : 0.f;
   int32_t* ids = A.ids + (size_t)r * KS_SAMPLE_KMAX;
@@ -493,7 +612,7 @@ Chunking chunking(int V, int k) {
   const int nb_max = k > 0 ? std::min(NB_MAX, CAND_MAX / k) : NB_MAX;
   int nb = std::min(nb_max, std::max(1, (V + 1023) / 1024));
   int chunk = (V + nb - 1) / nb;
-  chunk = (chunk + 3) & ~3;
+  chunk = (chunk + SCAN_NT - 1) / SCAN_NT * SCAN_NT;  // whole logits per thread
   nb = (V + chunk - 1) / chunk;
   return {nb, chunk};
 }
@@ -511,11 +630,11 @@ size_t argmax_ws_bytes(int M, int V) {
 
 size_t sample_ws_bytes(int R, int V, int k) {
   const Chunking ch = chunking(V, k);
-  return (size_t)R * ch.NB * sizeof(VStat) + (size_t)R * ch.NB * k * 8;
+  return (size_t)R * ch.NB * sizeof(VStat) + (size_t)R * cand_stride(ch.NB, k) * 8;
 }
 
 size_t sample_ws_bytes_max(int R) {
-  return (size_t)R * NB_MAX * sizeof(VStat) + (size_t)R * CAND_MAX * 8;
+  return (size_t)R * NB_MAX * sizeof(VStat) + (size_t)R * (CAND_MAX + 2) * 8;
 }
 
 void argmax_rows(const float* logits, int M, int V, int ld, int32_t* am, float* top1, void* ws,
@@ -527,7 +646,7 @@ void argmax_rows(const float* logits, int M, int V, int ld, int32_t* am, float* 
     const int mm = std::min(65535, M - m0);
     hipLaunchKernelGGL(k_vocab_scan, dim3(ch.NB, mm), dim3(SCAN_NT), 0, st,
                        logits + (size_t)m0 * ld, ld, V, ch.chunk, 0, stat + (size_t)m0 * ch.NB,
-                       nullptr, nullptr);
+                       nullptr);
   }
   hipLaunchKernelGGL(k_argmax_merge, dim3(M), dim3(128), 0, st, stat, ch.NB, am, top1);
 }
@@ -538,11 +657,10 @@ void sample_rows(const float* logits, int R, int V, int ld, const SampleSpec& s,
   const int k = s.top_k;
   const Chunking ch = chunking(V, k);
   VStat* stat = (VStat*)ws;
-  uint32_t* ckey = (uint32_t*)((char*)ws + (size_t)R * ch.NB * sizeof(VStat));
-  int32_t* cid = (int32_t*)(ckey + (size_t)R * ch.NB * k);
+  uint2* cand = (uint2*)((char*)ws + (size_t)R * ch.NB * sizeof(VStat));  // 16-byte aligned
   hipLaunchKernelGGL(k_vocab_scan, dim3(ch.NB, R), dim3(SCAN_NT), 0, st, logits, ld, V, ch.chunk,
-                     k, stat, ckey, cid);
-  RowArgs A{stat, ch.NB, ckey, cid, k, s.temperature, s.top_p, (uint32_t)s.seed,
+                     k, stat, cand);
+  RowArgs A{stat, ch.NB, cand, k, s.temperature, s.top_p, (uint32_t)s.seed,
             (uint32_t)(s.seed >> 32), s.ids, s.probs, s.count, s.top1, s.tok, s.pos0, s.purpose};
   hipLaunchKernelGGL(k_sample_row, dim3(R), dim3(ROW_NT), 0, st, A);
 }
