@@ -118,6 +118,68 @@ def cpu_baseline(cfg, ctx, budget_s):
                       f"{cfg.L} layers; {per_tok:.2f} s per sampled token"}
 
 
+# int32 vector ALU peak: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz, one op per lane per clock
+INT32_VALU_OPS = 256 * 4 * 16 * 2.4e9
+KNAP_OPS_PER_CELL = 3  # one add, one compare, one select per cell update
+
+
+def knapsack_leg(steps, warmup):
+    """The isolated knapsack batch (1024 instances x 72 items x 4097 budgets,
+    Llama-8B-shaped latencies, 4096 bins, skipped weight <= 2048): DP with
+    decision bits, then stage 2 (backtrack + TPT grid, D = 10), timed with HIP
+    events on the launch stream."""
+    import torch
+    import workloads as W
+    from paper_2602_20217_amd.engine import (knapsack_quantize, knapsack_batch,
+                                             knapsack_batch_select)
+    inst = W.knapsack_instances(B=1024, n_items=72, seed=2)
+    w, q = knapsack_quantize(inst["t"], inst["s"], 4096)
+    C, max_skip, B, n = 4096, 2048, w.shape[0], w.shape[1]
+    wd, qd = torch.from_numpy(w).cuda(), torch.from_numpy(q).cuda()
+    sd = torch.from_numpy(inst["s"]).cuda()
+    for _ in range(warmup):
+        best, bits = knapsack_batch(wd, qd, C, max_skip)
+        knapsack_batch_select(best, bits, wd, sd, C, 10)
+    torch.cuda.synchronize()
+    # back-to-back launches between the events, so host submission gaps are
+    # hidden behind the queued work
+    e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    reps = 10
+    e[0].record()
+    for _ in range(reps * steps):
+        best, bits = knapsack_batch(wd, qd, C, max_skip)
+    e[1].record()
+    for _ in range(reps * steps):
+        knapsack_batch_select(best, bits, wd, sd, C, 10)
+    e[2].record()
+    e[2].synchronize()
+    ms_dp = e[0].elapsed_time(e[1]) / (reps * steps)
+    ms_sel = e[1].elapsed_time(e[2]) / (reps * steps)
+    cells = B * n * (C + 1)
+    ops = KNAP_OPS_PER_CELL * cells / (ms_dp * 1e-3)
+    return {"workload": f"{B} instances x {n} items x {C + 1} budgets, skipped weight <= {max_skip}",
+            "ms_dp": round(ms_dp, 4), "ms_stage2": round(ms_sel, 4),
+            "cell_updates_per_s": round(cells / (ms_dp * 1e-3), 1),
+            "roofline": {"bound": "alu", "kernel": "k_knap_dp", "achieved": round(ops / 1e12, 3),
+                         "peak": round(INT32_VALU_OPS / 1e12, 3), "unit": "Tops/s (int32)",
+                         "frac": round(ops / INT32_VALU_OPS, 4),
+                         "ops_per_cell": KNAP_OPS_PER_CELL}}, (w, q, C, max_skip)
+
+
+def knapsack_cpu_baseline(w, q, C, max_skip, rows=256):
+    """The oracle's vectorised DP timed on the host over the first `rows`
+    instances of the same batch."""
+    import numpy as np
+    from oracle import additive as A
+    t0 = time.perf_counter()
+    A.knapsack_dp(np.ascontiguousarray(w[:rows]), np.ascontiguousarray(q[:rows]), C, max_skip)
+    dt = time.perf_counter() - t0
+    cells = rows * w.shape[1] * (C + 1)
+    return {"value": round(cells / dt, 1), "unit": "cell updates/s",
+            "cores": len(os.sched_getaffinity(0)), "kind": "oracle",
+            "sample": f"oracle DP over {rows} of {w.shape[0]} instances ({dt:.2f} s)"}
+
+
 def describe(cfg):
     shape = {"llama8b": "Llama-3-8B-shaped decoder", "qwen8b": "Qwen3-8B-shaped decoder"}
     return (f"{cfg.name}: {shape.get(cfg.name, 'decoder')} (L {cfg.L}, d {cfg.d}, "
@@ -275,6 +337,8 @@ def main():
                     help="T,top_k,top_p[,seed]: speculative sampling (paper's sampling "
                          "setting: 0.7,50,0.95) instead of greedy decoding")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
+    ap.add_argument("--no-knapsack", action="store_true",
+                    help="skip the isolated knapsack batch leg")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-kernels", action="store_true",
                     help="short run for hardware counters: prefill, 16 decode steps and a "
@@ -454,9 +518,16 @@ def main():
     dm.close()
     del dm
     torch.cuda.empty_cache()
+    knap_in = None
+    if not args.no_knapsack:
+        res["knapsack_batch"], knap_in = knapsack_leg(max(args.steps, 5), max(args.warmup, 1))
+        log(f"knapsack batch: DP {res['knapsack_batch']['ms_dp']:.3f} ms, "
+            f"stage 2 {res['knapsack_batch']['ms_stage2']:.3f} ms")
     if not args.no_cpu_baseline:
         t = time.time()
         res["cpu_baseline"] = cpu_baseline(cfg, args.ctx, args.cpu_budget)
+        if knap_in is not None:
+            res["knapsack_batch"]["cpu_baseline"] = knapsack_cpu_baseline(*knap_in)
         log(f"cpu baseline {time.time() - t:.1f}s")
     print(json.dumps(res), flush=True)
 

@@ -459,7 +459,8 @@ ks_status ks_knapsack_quantize(const double* t, const double* s, int B, int n, i
  * i = 0..n-1: skip item i at budget j iff j >= w_i and
  * best_{i-1}[j - w_i] + q_i < best_{i-1}[j] (strict; ties keep the item).
  * bits[b][i][j/64] bit j%64 records that decision (uint64 words, C/64 + 1 per
- * item).  Requires C <= 16383, n <= 4096, total loss < 2^31.  Asynchronous.
+ * item).  Requires C <= 8191, n <= 4096, w and q >= 0 (negative entries are
+ * read as 0) and total loss < 2^31.  Asynchronous.
  */
 ks_status ks_knapsack_batch(const int32_t* w, const int32_t* q, int B, int n, int C,
                             int max_skip, int32_t* best, uint64_t* bits, void* stream);

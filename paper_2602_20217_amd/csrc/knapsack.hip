@@ -1,68 +1,115 @@
 // Batched integer knapsack over skip budgets (Eq. objective_knapsack in
 // isolation; Single-pass Efficiency and the C/2 prune of Section 3.4).
 //
-// One workgroup per instance.  The row best_{i-1}[0..C] lives in LDS (two
-// ping-pong buffers); for item i every budget j is updated in parallel from
-// best_{i-1}[j] (keep) and best_{i-1}[j - w_i] + q_i (skip, strict).  A wave
-// owns 64 consecutive budgets, so its 64 skip decisions form one 64-bit
-// ballot that a single lane stores: the decision bitmap costs one word per
-// 64 budgets per item.  Integer arithmetic only, so results are exact.
+// One 256-thread workgroup per instance.  Thread t keeps budgets t + 256 e
+// (e < E) of the current row best_{i-1} in registers and mirrors them into
+// one of two LDS rows; for item i every budget j is updated in parallel from
+// its own best_{i-1}[j] (keep) and best_{i-1}[j - w_i] + q_i (skip, strict),
+// the latter read from LDS, so a cell update costs one LDS read and one LDS
+// write.  A wave owns 64 consecutive budgets per slot e, so its 64 skip
+// decisions form one 64-bit ballot that a single lane stores: the decision
+// bitmap costs one word per 64 budgets per item.  Integer arithmetic only, so
+// results are exact.
 #include "ks_internal.h"
 
 namespace ks {
 
 constexpr int32_t KINF = 0x7FFFFFFF;
 
-__global__ __launch_bounds__(1024) void k_knap_dp(const int32_t* __restrict__ w,
-                                                  const int32_t* __restrict__ q, int n, int C,
-                                                  int max_skip, int32_t* __restrict__ best,
-                                                  uint64_t* __restrict__ bits) {
-  extern __shared__ int32_t buf[];
-  const int b = blockIdx.x;
-  const int cells = C + 1;
-  const int words = C / 64 + 1;
-  int32_t* cur = buf;
-  int32_t* nxt = buf + cells;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
-  for (int j = threadIdx.x; j < cells; j += blockDim.x) cur[j] = j == 0 ? 0 : KINF;
-  __syncthreads();
-  for (int i = 0; i < n; ++i) {
-    const int wi = w[(size_t)b * n + i];
-    const int64_t qi = q[(size_t)b * n + i];
-    uint64_t* brow = bits + ((size_t)b * n + i) * words;
-    for (int base = wave * 64; base < words * 64; base += nw * 64) {
-      const int j = base + lane;
-      bool take = false;
-      if (j < cells) {
-        const int32_t keep = cur[j];
-        int32_t v = keep;
-        if (j >= wi && j <= max_skip) {
-          const int32_t src = cur[j - wi];
-          if (src != KINF) {
-            const int64_t cand = (int64_t)src + qi;
-            if (cand < (int64_t)keep) {
-              v = (int32_t)cand;
-              take = true;
-            }
-          }
-        }
-        nxt[j] = v;
-      }
-      const uint64_t ballot = __ballot(take);
-      if (lane == 0) brow[base >> 6] = ballot;
+template <int E, int Q>
+__device__ inline void knap_slots(const uint32_t (&cand)[E], int32_t (&v)[E], uint32_t& wlo,
+                                  uint32_t& whi) {
+  if constexpr (Q < E) {
+    const bool take = cand[Q] < (uint32_t)v[Q];
+    v[Q] = take ? (int32_t)cand[Q] : v[Q];
+    const uint64_t ballot = __ballot(take);
+    if ((threadIdx.x & 63) == Q) {
+      wlo = (uint32_t)ballot;
+      whi = (uint32_t)(ballot >> 32);
     }
-    __syncthreads();
-    int32_t* t = cur;
-    cur = nxt;
-    nxt = t;
+    knap_slots<E, Q + 1>(cand, v, wlo, whi);
   }
-  for (int j = threadIdx.x; j < cells; j += blockDim.x) best[(size_t)b * cells + j] = cur[j];
+}
+
+template <int E>
+__global__ __launch_bounds__(256) void k_knap_dp(const int32_t* __restrict__ w,
+                                                 const int32_t* __restrict__ q, int n, int C,
+                                                 int max_skip, int32_t* __restrict__ best,
+                                                 uint64_t* __restrict__ bits) {
+  // two LDS rows of 256 E + 1 entries: slot e of thread t is budget 256 e + t,
+  // entry 256 E a sentinel that stays INF (budgets past C stay INF too)
+  extern __shared__ int32_t buf[];
+  constexpr int ROW = 256 * E + 1;
+  const int b = blockIdx.x, t = threadIdx.x;
+  const int lane = t & 63, wave = t >> 6;
+  const int words = C / 64 + 1;
+  int32_t* row0 = buf;
+  int32_t* row1 = buf + ROW;
+  int32_t v[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    v[e] = e * 256 + t == 0 ? 0 : KINF;
+    row0[e * 256 + t] = v[e];
+  }
+  if (t == 0) row0[256 * E] = row1[256 * E] = KINF;
+  __syncthreads();
+  const int32_t* wb = w + (size_t)b * n;
+  const int32_t* qb = q + (size_t)b * n;
+  // jv[e]: budget of slot e, or -1 where no skip can land (beyond C or max_skip)
+  const int jmax = min(C, max_skip);
+  int jv[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) jv[e] = e * 256 + t <= jmax ? e * 256 + t : -1;
+  auto item = [&](int i, const int32_t* src_row, int32_t* dst_row) {
+    const int wi = max(wb[i], 0);                 // negative weights are read as 0
+    const uint32_t qi = (uint32_t)max(qb[i], 0);  // so are negative losses
+    // all reads first (one wait), then the updates, then all writes.  Skip
+    // candidate of slot e: row entry jv[e] - w_i, or the sentinel (entry 256 E)
+    // when that is negative (unsigned min).  An INF candidate never wins:
+    // INF + q_i >= INF >= best, all below 2^32.
+    uint32_t cand[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e)
+      cand[e] = (uint32_t)src_row[min((uint32_t)(jv[e] - wi), (uint32_t)(256 * E))] + qi;
+    uint32_t wlo = 0, whi = 0;  // lane e: the 64 decisions of slot e of this wave
+    knap_slots<E, 0>(cand, v, wlo, whi);
+#pragma unroll
+    for (int e = 0; e < E; ++e) dst_row[e * 256 + t] = v[e];
+    const int word = 4 * lane + wave;  // lane e stores word 4 e + wave
+    if (lane < E && word < words)
+      bits[((size_t)b * n + i) * words + word] = ((uint64_t)whi << 32) | wlo;
+    __syncthreads();
+  };
+  int i = 0;
+  for (; i + 1 < n; i += 2) {  // fixed rows per half step: addresses fold into offsets
+    item(i, row0, row1);
+    item(i + 1, row1, row0);
+  }
+  if (i < n) item(i, row0, row1);
+  const int cells = C + 1;
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const int j = e * 256 + t;
+    if (j < cells) best[(size_t)b * cells + j] = v[e];
+  }
+}
+
+template <int E>
+static void launch_knap_dp(const int32_t* w, const int32_t* q, int B, int n, int C, int max_skip,
+                           int32_t* best, uint64_t* bits, hipStream_t st) {
+  const size_t lds = 2 * (size_t)(256 * E + 1) * sizeof(int32_t);
+  hipLaunchKernelGGL(k_knap_dp<E>, dim3(B), dim3(256), lds, st, w, q, n, C, max_skip, best, bits);
 }
 
 void knapsack_dp(const int32_t* w, const int32_t* q, int B, int n, int C, int max_skip,
                  int32_t* best, uint64_t* bits, hipStream_t st) {
-  const size_t lds = 2 * (size_t)(C + 1) * sizeof(int32_t);
-  hipLaunchKernelGGL(k_knap_dp, dim3(B), dim3(1024), lds, st, w, q, n, C, max_skip, best, bits);
+  // slots per thread: 256 E budgets cover the C / 64 + 1 decision words
+  const int need = (C / 64 + 1) * 64;
+  if (need <= 256 * 2) launch_knap_dp<2>(w, q, B, n, C, max_skip, best, bits, st);
+  else if (need <= 256 * 4) launch_knap_dp<4>(w, q, B, n, C, max_skip, best, bits, st);
+  else if (need <= 256 * 8) launch_knap_dp<8>(w, q, B, n, C, max_skip, best, bits, st);
+  else if (need <= 256 * 17) launch_knap_dp<17>(w, q, B, n, C, max_skip, best, bits, st);
+  else launch_knap_dp<32>(w, q, B, n, C, max_skip, best, bits, st);  // C <= 8191
 }
 
 __device__ inline int get_bit(const uint64_t* row, int j) { return (int)((row[j >> 6] >> (j & 63)) & 1ull); }
@@ -98,70 +145,101 @@ void knapsack_backtrack(const uint64_t* bits, const int32_t* w, int B, int n, in
 // first strict maximum over gamma for its budget, then a tree keeps the
 // largest value and, on equal values, the smallest budget: the same winner as
 // a sequential scan over (j ascending, gamma ascending) with strict ">".
-// Items are limited to 128 so a backtracked mask fits two 64-bit words.
+// The instance's decision words (and w, s) are staged in LDS when they fit;
+// a thread walks four of its budgets' backtracks side by side so their
+// dependent reads overlap.  Items are limited to 128 so a backtracked mask
+// fits two 64-bit words.
+template <bool BITS_IN_LDS>
 __global__ __launch_bounds__(256) void k_knap_select(
     const int32_t* __restrict__ best, const uint64_t* __restrict__ bits,
     const int32_t* __restrict__ w, const double* __restrict__ s, int n, int C, int D,
     int32_t* j_star, int32_t* g_star, double* tpt, uint8_t* skip) {
 #pragma clang fp contract(off)
+  extern __shared__ uint64_t lbits[];
   __shared__ double sv[256];
   __shared__ int sj[256], sg[256];
-  const int b = blockIdx.x;
+  __shared__ int32_t sw[128];
+  __shared__ double ss[128];
+  const int b = blockIdx.x, tid = threadIdx.x;
   const int words = C / 64 + 1;
-  const int32_t* wb = w + (size_t)b * n;
-  const double* sb = s + (size_t)b * n;
+  const uint64_t* gb = bits + (size_t)b * n * words;
+  if (BITS_IN_LDS)
+    for (int k = tid; k < n * words; k += 256) lbits[k] = gb[k];
+  for (int i = tid; i < n; i += 256) {
+    sw[i] = w[(size_t)b * n + i];
+    ss[i] = s[(size_t)b * n + i];
+  }
+  __syncthreads();
+  const uint64_t* bb = BITS_IN_LDS ? lbits : gb;
   long long W = 0;
-  for (int i = 0; i < n; ++i) W += wb[i];
+  for (int i = 0; i < n; ++i) W += sw[i];
   double bv = 0.0;
   int bj = 0x7FFFFFFF, bg = 0;
-  for (int j = threadIdx.x; j <= C; j += blockDim.x) {
-    if (best[(size_t)b * (C + 1) + j] == KINF) continue;
-    uint64_t m0 = 0, m1 = 0;
-    int jj = j;
-    for (int i = n - 1; i >= 0 && jj >= 0; --i) {
-      if (get_bit(bits + ((size_t)b * n + i) * words, jj)) {
-        if (i < 64) m0 |= 1ull << i; else m1 |= 1ull << (i - 64);
-        jj -= wb[i];
+  constexpr int G = 4;
+  for (int k0 = 0; k0 * 256 <= C; k0 += G) {
+    int jj[G], j0[G];
+    uint64_t m0[G], m1[G];
+    bool live[G];
+#pragma unroll
+    for (int u = 0; u < G; ++u) {
+      j0[u] = (k0 + u) * 256 + tid;
+      live[u] = j0[u] <= C && best[(size_t)b * (C + 1) + j0[u]] != KINF;
+      jj[u] = j0[u];
+      m0[u] = m1[u] = 0;
+    }
+    if (!(live[0] || live[1] || live[2] || live[3])) continue;
+    for (int i = n - 1; i >= 0; --i) {
+      const int wi = sw[i];
+#pragma unroll
+      for (int u = 0; u < G; ++u) {
+        if (live[u] && jj[u] >= 0 && jj[u] <= C &&
+            ((bb[i * words + (jj[u] >> 6)] >> (jj[u] & 63)) & 1ull)) {
+          if (i < 64) m0[u] |= 1ull << i; else m1[u] |= 1ull << (i - 64);
+          jj[u] -= wi;
+        }
       }
     }
-    if (jj != 0) continue;  // inconsistent decisions: not a candidate
-    double a = 1.0;
-    for (int i = 0; i < n; ++i) {
-      const bool sk = i < 64 ? ((m0 >> i) & 1ull) : ((m1 >> (i - 64)) & 1ull);
-      if (sk) a = a * sb[i];
-    }
-    for (int g = 1; g <= D; ++g) {
-      double e = 0.0, p = 1.0;
-      for (int k = 0; k <= g; ++k) {
+#pragma unroll
+    for (int u = 0; u < G; ++u) {  // ascending budgets
+      if (!live[u] || jj[u] != 0) continue;  // inconsistent decisions: not a candidate
+      double a = 1.0;
+      for (int i = 0; i < n; ++i) {
+        const bool sk = i < 64 ? ((m0[u] >> i) & 1ull) : ((m1[u] >> (i - 64)) & 1ull);
+        if (sk) a = a * ss[i];
+      }
+      // e_g = 1 + a + ... + a^g, summed in ascending powers; one running sum
+      // over g gives the same additions in the same order as summing anew
+      double e = 1.0, p = a;
+      for (int g = 1; g <= D; ++g) {
         e = e + p;
         p = p * a;
-      }
-      const double cost = (double)((long long)g * (W - j) + W);
-      const double v = e / cost;
-      if (v > bv) {  // threads visit their budgets in ascending order
-        bv = v;
-        bj = j;
-        bg = g;
+        const double cost = (double)((long long)g * (W - j0[u]) + W);
+        const double v = e / cost;
+        if (v > bv) {
+          bv = v;
+          bj = j0[u];
+          bg = g;
+        }
       }
     }
   }
-  sv[threadIdx.x] = bv;
-  sj[threadIdx.x] = bj;
-  sg[threadIdx.x] = bg;
+  sv[tid] = bv;
+  sj[tid] = bj;
+  sg[tid] = bg;
   __syncthreads();
   for (int o = 128; o >= 1; o >>= 1) {
-    if (threadIdx.x < o) {
-      const double v2 = sv[threadIdx.x + o];
-      const int j2 = sj[threadIdx.x + o];
-      if (v2 > sv[threadIdx.x] || (v2 == sv[threadIdx.x] && j2 < sj[threadIdx.x])) {
-        sv[threadIdx.x] = v2;
-        sj[threadIdx.x] = j2;
-        sg[threadIdx.x] = sg[threadIdx.x + o];
+    if (tid < o) {
+      const double v2 = sv[tid + o];
+      const int j2 = sj[tid + o];
+      if (v2 > sv[tid] || (v2 == sv[tid] && j2 < sj[tid])) {
+        sv[tid] = v2;
+        sj[tid] = j2;
+        sg[tid] = sg[tid + o];
       }
     }
     __syncthreads();
   }
-  if (threadIdx.x == 0) {
+  if (tid == 0) {
     const int j = sj[0];
     j_star[b] = j;
     g_star[b] = sg[0];
@@ -169,9 +247,9 @@ __global__ __launch_bounds__(256) void k_knap_select(
     int jj = j;
     for (int i = n - 1; i >= 0; --i) {
       uint8_t sk = 0;
-      if (jj >= 0 && jj <= C && get_bit(bits + ((size_t)b * n + i) * words, jj)) {
+      if (jj >= 0 && jj <= C && ((bb[i * words + (jj >> 6)] >> (jj & 63)) & 1ull)) {
         sk = 1;
-        jj -= wb[i];
+        jj -= sw[i];
       }
       skip[(size_t)b * n + i] = sk;
     }
@@ -181,8 +259,13 @@ __global__ __launch_bounds__(256) void k_knap_select(
 void knapsack_select(const int32_t* best, const uint64_t* bits, const int32_t* w,
                      const double* s, int B, int n, int C, int D, int32_t* j_star,
                      int32_t* g_star, double* tpt, uint8_t* skip, hipStream_t st) {
-  hipLaunchKernelGGL(k_knap_select, dim3(B), dim3(256), 0, st, best, bits, w, s, n, C, D, j_star,
-                     g_star, tpt, skip);
+  const size_t lds = (size_t)n * (C / 64 + 1) * 8;
+  if (lds <= 48 * 1024)
+    hipLaunchKernelGGL(k_knap_select<true>, dim3(B), dim3(256), lds, st, best, bits, w, s, n, C, D,
+                       j_star, g_star, tpt, skip);
+  else
+    hipLaunchKernelGGL(k_knap_select<false>, dim3(B), dim3(256), 0, st, best, bits, w, s, n, C, D,
+                       j_star, g_star, tpt, skip);
 }
 
 // ------------------------------------------------------- model-mode step
