@@ -245,3 +245,37 @@ def test_sampling_step_calls_and_top_k_one(tiny):
         dm.verify([s1, d1])
     finally:
         dm.set_sampling(0.0)
+
+
+def test_sampling_with_dynamic_exit_matches_oracle(tiny):
+    """Sampling mode under the draft policy: with tau_conf above 1 every round
+    drafts one token; with the selection's gamma* cap rounds stay below it; the
+    tokens, acceptances and round lengths equal the oracle's for seeds whose
+    decisions clear the margin."""
+    from paper_2602_20217_amd.engine import select_params
+    cfg, dm, model = tiny
+    prompt = W.prompt_ids(cfg.vocab, 128, 3)
+    compared = 0
+    for tau, source in ((1.01, "fixed"), (0.0, "selected")):
+        for seed in range(1, 6):
+            prm = S.SamplingParams(0.7, 50, 0.95, seed)
+            mg = []
+            ref, log = S.generate(model, prompt, 24, 4, 8, W.TINY_LATENCY, prm,
+                                  quant_mode="bins", bins=64, n_max=320, tau_conf=tau,
+                                  gamma_source=source, margins=mg)
+            dm.set_sampling(0.7, 50, 0.95, seed)
+            dm.set_draft_policy(tau, source)
+            try:
+                out, st, _ = dm.generate(prompt, 24, gamma=4, reselect_every=8,
+                                         params=select_params(W.TINY_LATENCY, "bins", 64))
+            finally:
+                dm.set_sampling(0.0)
+                dm.set_draft_policy(0.0, "fixed")
+            if tau > 1.0:
+                assert st.n_drafted == st.n_rounds  # one draft per round
+            if min(mg) <= MARGIN:
+                continue
+            compared += 1
+            assert out.tolist() == ref, (tau, source, seed)
+            assert st.n_drafted == sum(log.drafted) and st.n_accepted == sum(log.accepted)
+    assert compared >= 3
