@@ -216,7 +216,8 @@ ks_status ks_prefill(ks_ctx* ctx, const int32_t* tokens, int n, int32_t* out_fir
 ks_status ks_set_context(ks_ctx* ctx, int n_cached, int32_t last_token);
 
 /*
- * ks_draft_step (Section 2.1, draft model f^(S)): one greedy draft token.  The
+ * ks_draft_step (Section 2.1, draft model f^(S)): one draft token, the argmax
+ * (or, after ks_set_sampling, a draw from the draft's filtered distribution).  The
  * k-th call since the last verify (k = 0, 1, ...) processes, at position P+k,
  * the committed token s (k = 0) or the previous draft token; executed attention
  * sublayers store their keys/values at P+k.  exec: host uint8[2L] mask S.
@@ -233,6 +234,8 @@ ks_status ks_draft_step(ks_ctx* ctx, const uint8_t* exec, int32_t* out_token,
  * y_a (a+1 tokens); the new s is y_a at position P+a+1.  The rows 0..a of every
  * sublayer output become a history block (the last m_rounds blocks are kept).
  * out_pred: host int32[gamma+1] target argmaxes; out_n_accepted: a.
+ * After ks_set_sampling the pass runs the acceptance chain of speculative
+ * sampling instead (see there).
  */
 ks_status ks_verify(ks_ctx* ctx, const int32_t* tokens, int gamma, int32_t* out_pred,
                     int* out_n_accepted);
@@ -399,7 +402,7 @@ enum {
   KS_KC_GEMM_GATE_UP, /* gate/up projection + SwiGLU */
   KS_KC_GEMM_DOWN,    /* down projection + residual */
   KS_KC_GEMM_HEAD,    /* LM head */
-  KS_KC_ARGMAX,       /* argmax + top-1 probability */
+  KS_KC_ARGMAX,       /* vocabulary reduction: argmax + top-1 probability, or the sampling filter */
   KS_KC_OTHER,        /* position fill and small copies */
   KS_KC_COUNT
 };
