@@ -28,3 +28,54 @@ def margin(logits_row):
     """Top-1 minus top-2 logit."""
     s = np.sort(np.asarray(logits_row))
     return float(s[-1] - s[-2])
+
+
+def one_layer_model(cfg, layer, seed=0):
+    """Oracle model holding layer `layer` of the seeded weights as its only
+    layer (embedding and head zero: only sublayers 1 and 2 are evaluated)."""
+    import dataclasses
+    c1 = dataclasses.replace(cfg, L=1)
+    w = {("embed", -1): np.zeros((16, cfg.d), np.float32),
+         ("lm_head", -1): np.zeros((16, cfg.d), np.float32)}
+    for k in ("wq", "wk", "wv", "wo", "w_gate", "w_up", "w_down"):
+        w[(k, 0)] = W.weight_tensor(cfg, seed, k, layer)
+    return M.Model(c1, w)
+
+
+def fill_layer(cfg, dm, layer, n, n_max, seed=3):
+    """Seeded keys/values of one layer at positions < n, written to the device
+    cache and to a one-layer oracle cache of n_max positions."""
+    import dataclasses
+    import torch
+    K, V = W.synthetic_kv(cfg, n, seed=seed, layer=layer)
+    kk, vv = dm.kv_layer(layer)
+    kk[:, :n] = torch.from_numpy(K).to(kk.dtype).cuda()
+    vv[:, :n] = torch.from_numpy(V).to(vv.dtype).cuda()
+    torch.cuda.synchronize()
+    cache = M.KVCache(dataclasses.replace(cfg, L=1), n_max)
+    cache.K[0][:, :n] = K
+    cache.V[0][:, :n] = V
+    return cache
+
+
+def check_sublayers(cfg, dm, model, cache, layer, n, R, tol, tag, seed_index=0):
+    """Attention then MLP of `layer` on R rows at positions n.. through the C
+    ABI (mode 0: rows store their keys/values, then attend) against the
+    one-layer oracle; returns the relative errors."""
+    import torch
+    dm.set_context(n, 0)
+    pos = np.arange(R) + n
+    x = W.synthetic_rows(R, cfg.d, seed=4, std=1.0, index=seed_index + 100 + R + layer)
+    errs = []
+    for sub in (1, 2):
+        i = 2 * layer + sub
+        out = torch.empty(R, cfg.d, device="cuda")
+        dm.sublayer_apply(i, torch.from_numpy(x).cuda(), pos, mode=0, out=out)
+        ref = M.sublayer(model, sub, x.astype(np.float64), pos, cache, mode="write")
+        got = out.cpu().numpy()
+        e = rel_err(got, ref)
+        print(f"[{tag}] layer {layer} sublayer {sub} R {R}: rel err {e:.2e}", flush=True)
+        assert e < tol, (tag, layer, sub, R, e)
+        errs.append(e)
+        x = got
+    return errs

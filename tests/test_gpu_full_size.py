@@ -1,12 +1,15 @@
-"""Parity at the full Llama-3-8B shape (bf16, 8K context), in the launch
-configuration the benchmark times (skinny products, 5-tile attention splits).
+"""Parity at the full Llama-3-8B shape (bf16), in the launch configurations the
+benchmark times: the 8K workload (skinny products, 5-tile attention splits) and
+a 128K-position context (streaming attention splits, as in the context sweep).
 
 Sampled outputs the oracle computes one by one: single sublayers (first and last
-layer) on decode (1 row) and verify (5 rows) inputs over a seeded 8K cache, and
-the LM head on two rows; tolerance 2e-2 relative.  Properties that hold at any
-size: full-model drafts are accepted by the verify pass at the same positions,
-and speculative generation (with knapsack selections) emits exactly the
-autoregressive tokens after a real 8K prefill.  Every call goes through the C
+layer) on decode (1 row) and verify (5 rows) inputs over seeded caches of
+8189 and 131067 positions, the LM head on two rows (tolerance 2e-2 relative),
+and the sampling filter of head logits against the oracle's filter of the same
+logits.  Properties that hold at any size: full-model drafts are accepted by
+the verify pass at the same positions, and speculative generation (with
+knapsack selections) emits exactly the autoregressive tokens after a real 8K
+prefill, greedy and as sampling with top-k 1.  Every call goes through the C
 ABI."""
 import dataclasses
 
@@ -15,7 +18,7 @@ import pytest
 
 import workloads as W
 from oracle import model as M
-from tests.gpu_helpers import rel_err, margin
+from tests.gpu_helpers import rel_err, margin, one_layer_model, fill_layer, check_sublayers
 
 pytestmark = pytest.mark.gpu
 torch = pytest.importorskip("torch")
@@ -41,27 +44,11 @@ def full():
 
 
 def _one_layer(cfg, layer):
-    """Oracle model holding layer `layer` of the 8B weights as its only layer."""
-    c1 = dataclasses.replace(cfg, L=1)
-    w = {("embed", -1): np.zeros((16, cfg.d), np.float32),
-         ("lm_head", -1): np.zeros((16, cfg.d), np.float32)}
-    for k in ("wq", "wk", "wv", "wo", "w_gate", "w_up", "w_down"):
-        w[(k, 0)] = W.weight_tensor(cfg, 0, k, layer)
-    return M.Model(c1, w)
+    return one_layer_model(cfg, layer)
 
 
 def _fill(cfg, dm, layer, n):
-    """Seeded keys/values of one layer at positions < n, on the device and in a
-    one-layer oracle cache."""
-    K, V = W.synthetic_kv(cfg, n, seed=3, layer=layer)
-    kk, vv = dm.kv_layer(layer)
-    kk[:, :n] = torch.from_numpy(K).to(torch.bfloat16).cuda()
-    vv[:, :n] = torch.from_numpy(V).to(torch.bfloat16).cuda()
-    torch.cuda.synchronize()
-    cache = M.KVCache(dataclasses.replace(cfg, L=1), CTX + 320)
-    cache.K[0][:, :n] = K
-    cache.V[0][:, :n] = V
-    return cache
+    return fill_layer(cfg, dm, layer, n, CTX + 320)
 
 
 @pytest.mark.parametrize("layer", LAYERS)
@@ -69,21 +56,30 @@ def _fill(cfg, dm, layer, n):
 def test_full_size_sublayers(full, layer, R):
     cfg, dm = full
     n = CTX - 3  # ragged against the 320-position splits
-    model = _one_layer(cfg, layer)
-    cache = _fill(cfg, dm, layer, n)
-    dm.set_context(n, 0)
-    pos = np.arange(R) + n
-    x = W.synthetic_rows(R, cfg.d, seed=4, std=1.0, index=100 + R + layer)
-    for sub in (1, 2):  # attention, then MLP of the layer
-        i = 2 * layer + sub
-        out = torch.empty(R, cfg.d, device="cuda")
-        dm.sublayer_apply(i, torch.from_numpy(x).cuda(), pos, mode=0, out=out)
-        ref = M.sublayer(model, sub, x.astype(np.float64), pos, cache, mode="write")
-        got = out.cpu().numpy()
-        print(f"[full] layer {layer} sublayer {sub} R {R}: rel err {rel_err(got, ref):.2e}",
-              flush=True)
-        assert rel_err(got, ref) < TOL, (layer, sub, R, rel_err(got, ref))
-        x = got
+    check_sublayers(cfg, dm, _one_layer(cfg, layer), _fill(cfg, dm, layer, n), layer, n, R, TOL,
+                    "full")
+
+
+LONG = 131072
+
+
+@pytest.fixture(scope="module")
+def long_ctx(full):
+    """A 128K-position context over the same weights (the streaming decode
+    attention's launch configuration at that cache size)."""
+    cfg, dm = full
+    dl = dm.resized(LONG + 320)
+    yield cfg, dl
+    dl.close()
+
+
+@pytest.mark.parametrize("layer", LAYERS)
+@pytest.mark.parametrize("R", [1, 5])
+def test_full_size_long_context_sublayers(long_ctx, layer, R):
+    cfg, dl = long_ctx
+    n = LONG - 5  # ragged against the streaming splits
+    cache = fill_layer(cfg, dl, layer, n, LONG + 320)
+    check_sublayers(cfg, dl, one_layer_model(cfg, layer), cache, layer, n, R, TOL, "long")
 
 
 def test_full_size_head(full):
