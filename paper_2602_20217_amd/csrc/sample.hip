@@ -617,6 +617,15 @@ Chunking chunking(int V, int k) {
   return {nb, chunk};
 }
 
+// argmax of M rows: ~1024-logit chunks spread one row over ~128 CUs; from 16
+// rows on, 4096-logit chunks keep the workgroup count (and its per-workgroup
+// overhead) down while still filling the GPU
+Chunking argmax_chunking(int M, int V) {
+  if (M < 16) return chunking(V, 0);
+  const int chunk = SCAN_NT * SCAN_E;
+  return {(V + chunk - 1) / chunk, chunk};
+}
+
 }  // namespace
 
 bool vocab_fits(int V, int k) {
@@ -625,7 +634,7 @@ bool vocab_fits(int V, int k) {
 }
 
 size_t argmax_ws_bytes(int M, int V) {
-  return (size_t)M * chunking(V, 0).NB * sizeof(VStat);
+  return (size_t)M * std::max(chunking(V, 0).NB, argmax_chunking(M, V).NB) * sizeof(VStat);
 }
 
 size_t sample_ws_bytes(int R, int V, int k) {
@@ -640,7 +649,7 @@ size_t sample_ws_bytes_max(int R) {
 void argmax_rows(const float* logits, int M, int V, int ld, int32_t* am, float* top1, void* ws,
                  hipStream_t st) {
   if (M <= 0) return;
-  const Chunking ch = chunking(V, 0);
+  const Chunking ch = argmax_chunking(M, V);
   VStat* stat = (VStat*)ws;
   for (int m0 = 0; m0 < M; m0 += 65535) {
     const int mm = std::min(65535, M - m0);
