@@ -64,7 +64,12 @@ int dec_tiles(int n_max, int hkv) {
   const int tpw = (n_tiles + 4 * splits - 1) / (4 * splits);
   return 4 * std::max(2, tpw);
 }
-constexpr int BAT_TILES = 16;  // prefill/DP: 1024 positions per split
+#ifndef KS_BAT_TILES
+#define KS_BAT_TILES 16
+#endif
+// batched attention (prefill, DP): 64-position tiles per split; 16 (1024
+// positions) times the 8K selection as fast as 32 and 6% faster than 64
+constexpr int BAT_TILES = KS_BAT_TILES;
 
 size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
 
