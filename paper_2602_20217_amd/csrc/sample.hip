@@ -32,6 +32,7 @@ constexpr int ROW_NT = 512;    // threads of a row-selection workgroup
 constexpr int ROW_E = 16;      // candidates per thread (NB * k <= 8192)
 constexpr int CAND_MAX = ROW_NT * ROW_E;
 constexpr int NB_MAX = 128;
+static_assert(ROW_NT == 4 * KS_SAMPLE_KMAX, "the rank count splits each entry over 4 threads");
 
 struct VStat {
   float m;  // chunk max
@@ -39,6 +40,21 @@ struct VStat {
   int i;    // lowest id attaining m
   int pad;
 };
+
+// Cross-lane steps on DPP lane moves (no LDS round trip).  dpp(x, ctrl, rows):
+// the value of the lane the control names, 0 where the source lane lies
+// outside the row or the destination row is masked off.
+template <int CTRL, int ROWS = 0xF, bool BOUND = true>
+__device__ inline int dpp_i(int x) {
+  return __builtin_amdgcn_update_dpp(0, x, CTRL, ROWS, 0xF, BOUND);
+}
+template <int CTRL, int ROWS = 0xF, bool BOUND = true>
+__device__ inline float dpp_f(float x) {
+  return __int_as_float(dpp_i<CTRL, ROWS, BOUND>(__float_as_int(x)));
+}
+constexpr int ROW_SHR1 = 0x111, ROW_SHR2 = 0x112, ROW_SHR4 = 0x114, ROW_SHR8 = 0x118;
+constexpr int ROW_ROR1 = 0x121, ROW_ROR2 = 0x122, ROW_ROR4 = 0x124, ROW_ROR8 = 0x128;
+constexpr int ROW_BCAST15 = 0x142, ROW_BCAST31 = 0x143;
 
 __device__ inline uint32_t fkey(float f) {
   uint32_t u = __float_as_uint(f);
@@ -72,11 +88,9 @@ __device__ inline VStat st_merge(VStat a, VStat b) {
   return r;
 }
 template <int CTRL>
-__device__ inline VStat st_rot(VStat a) {
-  const int m = __builtin_amdgcn_update_dpp(0, __float_as_int(a.m), CTRL, 0xF, 0xF, false);
-  const int s = __builtin_amdgcn_update_dpp(0, __float_as_int(a.s), CTRL, 0xF, 0xF, false);
-  const int i = __builtin_amdgcn_update_dpp(0, a.i, CTRL, 0xF, 0xF, false);
-  return VStat{__int_as_float(m), __int_as_float(s), i, 0};
+__device__ inline VStat st_rot(VStat a) {  // row rotations: every source lane is valid
+  return VStat{dpp_f<CTRL, 0xF, false>(a.m), dpp_f<CTRL, 0xF, false>(a.s),
+               dpp_i<CTRL, 0xF, false>(a.i), 0};
 }
 __device__ inline VStat st_lane(VStat a, int l) {
   return VStat{__int_as_float(__builtin_amdgcn_readlane(__float_as_int(a.m), l)),
@@ -86,10 +100,10 @@ __device__ inline VStat st_lane(VStat a, int l) {
 // wave reduction (every lane gets the result): row rotations (DPP), then the
 // four row results (merge is commutative and associative up to rounding)
 __device__ inline VStat st_wave(VStat a) {
-  a = st_merge(a, st_rot<0x128>(a));
-  a = st_merge(a, st_rot<0x124>(a));
-  a = st_merge(a, st_rot<0x122>(a));
-  a = st_merge(a, st_rot<0x121>(a));
+  a = st_merge(a, st_rot<ROW_ROR8>(a));
+  a = st_merge(a, st_rot<ROW_ROR4>(a));
+  a = st_merge(a, st_rot<ROW_ROR2>(a));
+  a = st_merge(a, st_rot<ROW_ROR1>(a));
   return st_merge(st_merge(st_lane(a, 0), st_lane(a, 16)), st_merge(st_lane(a, 32), st_lane(a, 48)));
 }
 
@@ -111,21 +125,6 @@ __device__ inline float philox_uniform(uint32_t k0, uint32_t k1, uint32_t pos, u
   }
   return (float)(c0 >> 8) * (1.0f / 16777216.0f);
 }
-
-// Cross-lane steps on DPP lane moves (no LDS round trip).  dpp(x, ctrl, rows):
-// the value of the lane the control names, 0 where the source lane lies
-// outside the row or the destination row is masked off.
-template <int CTRL, int ROWS = 0xF, bool BOUND = true>
-__device__ inline int dpp_i(int x) {
-  return __builtin_amdgcn_update_dpp(0, x, CTRL, ROWS, 0xF, BOUND);
-}
-template <int CTRL, int ROWS = 0xF, bool BOUND = true>
-__device__ inline float dpp_f(float x) {
-  return __int_as_float(dpp_i<CTRL, ROWS, BOUND>(__float_as_int(x)));
-}
-constexpr int ROW_SHR1 = 0x111, ROW_SHR2 = 0x112, ROW_SHR4 = 0x114, ROW_SHR8 = 0x118;
-constexpr int ROW_ROR1 = 0x121, ROW_ROR2 = 0x122, ROW_ROR4 = 0x124, ROW_ROR8 = 0x128;
-constexpr int ROW_BCAST15 = 0x142, ROW_BCAST31 = 0x143;
 
 // inclusive prefix sum over the 64 lanes: scans of the four 16-lane rows, then
 // lane 15 added into row 1 and 3, lane 31 into rows 2 and 3
