@@ -129,6 +129,8 @@ def test_dp_terminal_states_match_backtracked_masks(tiny_hist):
         c = SEL.cos_matrix(dp.states[j], X[-1])
         assert c <= brute[j][0] + 1e-12
         n_opt += abs(c - brute[j][0]) < 1e-12
+    n_reach = int(np.sum(dp.reach))
+    print(f"[dp] optimal at {n_opt} of {n_reach} reachable budgets (brute force over 256 masks)")
     assert n_opt >= 1
 
 
