@@ -908,6 +908,7 @@ ks_status ks_sample_uniforms(uint64_t seed, const int32_t* pos, int n, int purpo
                              void* stream) {
   REQ(n >= 0 && purpose >= 0, "n and purpose must be >= 0");
   REQ(n == 0 || (pos && out), "null pointer");
+  if (n == 0) return KS_OK;
   uniforms(seed, pos, n, purpose, out, (hipStream_t)stream);
   HIPCHK(hipGetLastError());
   return KS_OK;

@@ -70,6 +70,40 @@ def test_null_and_range_errors_before_any_launch():
         K.ks_knapsack_batch(fake, fake, 1, 72, 64, -1, fake, fake, None)
 
 
+def test_sampling_calls_validate_before_any_launch():
+    fake = C.c_void_p(16)  # never dereferenced: validation fails first
+    ok = K.Sampling(0.7, 50, 0.95, 1)
+    ws = K.ks_sample_workspace_bytes(2, 128256, 50)
+    assert ws > 0 and K.ks_sample_workspace_bytes(2, 128256, 128) > 0
+    for rows, vocab, k in ((0, 1000, 5), (1, 0, 5), (1, 40, 50), (1, 1000, 0), (1, 1000, 129),
+                           (1, 600000, 128)):
+        assert K.ks_sample_workspace_bytes(rows, vocab, k) == 0, (rows, vocab, k)
+    for s in (K.Sampling(0.0, 50, 0.95, 1), K.Sampling(float("inf"), 50, 0.95, 1),
+              K.Sampling(0.7, 0, 0.95, 1), K.Sampling(0.7, 129, 0.95, 1),
+              K.Sampling(0.7, 50, 0.0, 1), K.Sampling(0.7, 50, 1.01, 1)):
+        with pytest.raises(K.KsError) as e:
+            K.ks_sample_filter(fake, 2, 128256, 128256, C.byref(s), 0, 2, fake, fake, fake, None,
+                               None, fake, ws, None)
+        assert e.value.status == K.KS_EINVAL
+    with pytest.raises(K.KsError) as e:  # workspace too small
+        K.ks_sample_filter(fake, 2, 128256, 128256, C.byref(ok), 0, 2, fake, fake, fake, None,
+                           None, fake, ws - 1, None)
+    assert e.value.status == K.KS_ENOMEM
+    with pytest.raises(K.KsError):  # row stride below the vocabulary
+        K.ks_sample_filter(fake, 2, 128256, 1000, C.byref(ok), 0, 2, fake, fake, fake, None,
+                           None, fake, ws, None)
+    with pytest.raises(K.KsError):
+        K.ks_sample_filter(None, 2, 128256, 128256, C.byref(ok), 0, 2, fake, fake, fake, None,
+                           None, fake, ws, None)
+    with pytest.raises(K.KsError):
+        K.ks_spec_accept(fake, fake, fake, fake, fake, fake, fake, 2000, 0, 0, fake, None)
+    with pytest.raises(K.KsError):
+        K.ks_spec_accept(fake, fake, fake, None, None, None, None, 3, 0, 0, fake, None)
+    with pytest.raises(K.KsError):
+        K.ks_sample_uniforms(0, fake, -1, 0, fake, None)
+    K.ks_sample_uniforms(0, None, 0, 0, None, None)  # nothing to do: no launch
+
+
 def test_knapsack_quantize_matches_oracle_bit_exact():
     inst = W.knapsack_instances(B=64, n_items=72, seed=2)
     w0, q0 = A.quantize_items(inst["t"], inst["s"], 4096)
