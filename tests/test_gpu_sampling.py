@@ -279,3 +279,34 @@ def test_sampling_with_dynamic_exit_matches_oracle(tiny):
             assert out.tolist() == ref, (tau, source, seed)
             assert st.n_drafted == sum(log.drafted) and st.n_accepted == sum(log.accepted)
     assert compared >= 3
+
+
+def test_sampling_edge_cases(tiny):
+    """One-token prompt, a single generated token (the prefill's draw), draft
+    length gamma_max, and a re-selection after every round: tokens equal the
+    oracle's where every decision clears the margin; the first token always
+    equals the prefill draw."""
+    from paper_2602_20217_amd.engine import select_params
+    cfg, dm, model = tiny
+    params = select_params(W.TINY_LATENCY, "bins", 64)
+    for prompt_len, n_new, gamma, every in ((1, 1, 4, 8), (1, 12, 4, 1), (40, 16, 4, 1),
+                                            (40, 1, 0, 8)):
+        prompt = W.prompt_ids(cfg.vocab, prompt_len, 7)
+        prm = S.SamplingParams(0.7, 50, 0.95, 21)
+        mg = []
+        if gamma == 0:
+            ref = S.ar_sample(model, prompt, n_new, 320, prm, mg)
+        else:
+            ref, _ = S.generate(model, prompt, n_new, gamma, every, W.TINY_LATENCY, prm,
+                                quant_mode="bins", bins=64, n_max=320, margins=mg)
+        dm.set_sampling(0.7, 50, 0.95, 21)
+        try:
+            out, st, _ = dm.generate(prompt, n_new, gamma=gamma, reselect_every=every,
+                                     params=params if gamma else None)
+        finally:
+            dm.set_sampling(0.0)
+        assert len(out) == n_new
+        print(f"[edge] prompt {prompt_len}, {n_new} tokens, gamma {gamma}: "
+              f"min margin {min(mg, default=1.0):.1e}", flush=True)
+        if min(mg, default=1.0) > MARGIN:
+            assert out.tolist() == ref, (prompt_len, n_new, gamma, every)
