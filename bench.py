@@ -417,14 +417,17 @@ def main():
             coeffs = tuple(float(x) for x in args.select_coeffs.split(","))
         params = select_params(coeffs, "paper_min", 0, tau=0.5, prune_half=True, D=10)
         dm.prefill(prompt)
+        log("prefill for the selections done")
         times = []
         for k in range(args.warmup + args.steps):
             torch.cuda.synchronize()
             t0 = time.perf_counter()
             sel = dm.select(params)
             torch.cuda.synchronize()
+            ms = (time.perf_counter() - t0) * 1e3
+            log(f"selection {k}: {ms:.1f} ms")
             if k >= args.warmup:
-                times.append(round((time.perf_counter() - t0) * 1e3, 2))
+                times.append(round(ms, 2))
         print(json.dumps({"mode": "profile-select", "C": sel.C, "w_attn": sel.w_attn,
                           "w_mlp": sel.w_mlp, "cells": sel.n_cells, "rows": sel.n_rows,
                           "j": sel.j_star, "select_ms": times}), flush=True)

@@ -46,7 +46,7 @@ namespace {
 
 constexpr int PB = 512;        // rows per batched attention / head pass
 // float32 split-K partials of the batched products (prefill chunks, selection)
-constexpr size_t GPART_BYTES = (size_t)64 << 20;
+constexpr size_t GPART_BYTES = (size_t)128 << 20;
 // decode/verify splits: 64-position tiles per split, by the model's cache size
 // and kv heads only (never by row count, so a verify row and the decode step
 // split alike).  Measured on MI355X (split kernel + merge, 1 and 5 rows): the

@@ -19,6 +19,9 @@
 // single bf16 activations.
 #include "ks_internal.h"
 
+#include <algorithm>
+#include <atomic>
+
 namespace ks {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -397,20 +400,59 @@ __global__ __launch_bounds__(256) void k_splitk_reduce(int M, int N, int SK,
   *(float4*)&out[(size_t)m * ldo + n] = s;
 }
 
+static int compute_units() {
+  static std::atomic<int> cached[16];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 16) return 256;
+  int n = cached[dev].load(std::memory_order_relaxed);
+  if (n <= 0) {
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        n <= 0)
+      n = 256;
+    cached[dev].store(n, std::memory_order_relaxed);
+  }
+  return n;
+}
+
+// Split-K factor (1..8) of a tiled product, by a cost model fitted on MI355X
+// to the 128 x 256 tile at the Llama-8B product shapes (400..1225 rows, every
+// factor 1..6 timed): one k step takes about 0.57 us while a workgroup has its
+// CU to itself and 0.97 us while two share it (the CU's matrix and LDS
+// throughput is then split, so the pair gains only ~15%); workgroups beyond
+// the resident set run in further rounds; SK > 1 adds a launch and SK + 2
+// float32 M x N planes of traffic (partials written and read, output) at
+// about 4.5 TB/s.  The model picks the measured best factor, or one within
+// 1 us of it, at every timed shape; split count 1 is kept when the partials
+// would not fit the caller's buffer.
+static int splitk_factor(const GemmArgs& g, int tiles, int KT, int lds_kib) {
+  constexpr double T_ALONE = 0.57, T_SHARED = 0.97, T_LAUNCH = 3.0, BYTES_PER_US = 4.5e6;
+  if (g.epi == EPI_SWIGLU || !g.part) return 1;
+  const int cus = compute_units();
+  const int resident = cus * std::max(1, 160 / lds_kib);
+  double best = 0.0;
+  int best_sk = 1;
+  for (int sk = 1; sk <= 8; ++sk) {
+    if (sk > 1 && ((size_t)sk * g.M * g.N * 4 > g.part_bytes || KT / sk < 8)) break;
+    const int steps = (KT + sk - 1) / sk;
+    double t = 0.0;
+    for (long left = (long)tiles * sk; left > 0; left -= resident)
+      t += steps * (std::min<long>(left, resident) > cus ? T_SHARED : T_ALONE);
+    if (sk > 1) t += T_LAUNCH + (sk + 2.0) * g.M * (double)g.N * 4.0 / BYTES_PER_US;
+    if (sk == 1 || t < best) {
+      best = t;
+      best_sk = sk;
+    }
+  }
+  return best_sk;
+}
+
 template <int ST, int WN, int NWM, int NWN>
 static void launch_tiled(const GemmArgs& g, hipStream_t st) {
   const int NT = g.N / 16;
   const int KT = g.K / 32;
   const int MB = (g.M + 64 * NWM - 1) / (64 * NWM);
   const int NB = (NT + NWN * WN - 1) / (NWN * WN);
-  // split K until about two workgroups per CU, keeping >= 16 k steps per split
-  // and the partials within the caller's buffer
-  int SK = 1;
-  if (g.epi != EPI_SWIGLU && g.part) {
-    while (SK < 8 && MB * NB * SK < 512 && KT / (2 * SK) >= 16 &&
-           (size_t)2 * SK * g.M * g.N * 4 <= g.part_bytes)
-      SK *= 2;
-  }
+  const int SK = splitk_factor(g, MB * NB, KT, ST * (4 * NWM + NWN * WN));
   dim3 grid(MB * NB * SK);
   const bf16_t* A = (const bf16_t*)g.A.hi;
   const bf16_t* W = (const bf16_t*)g.W;
