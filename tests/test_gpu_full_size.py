@@ -4,7 +4,10 @@ a 128K-position context (streaming attention splits, as in the context sweep).
 
 Sampled outputs the oracle computes one by one: single sublayers (first and last
 layer) on decode (1 row) and verify (5 rows) inputs over seeded caches of
-8189 and 131067 positions, the LM head on two rows (tolerance 2e-2 relative),
+8189 and 131067 positions, the last layer on 400, 800 and 1225 candidate rows
+of the selection (tiled MFMA products with 1 to 8 K splits, batched attention;
+sampled rows at tile edges and in the ragged tail), the LM head on two rows
+(tolerance 2e-2 relative),
 and the sampling filter of head logits against the oracle's filter of the same
 logits.  Properties that hold at any size: full-model drafts are accepted by
 the verify pass at the same positions, and speculative generation (with
@@ -58,6 +61,37 @@ def test_full_size_sublayers(full, layer, R):
     n = CTX - 3  # ragged against the 320-position splits
     check_sublayers(cfg, dm, _one_layer(cfg, layer), _fill(cfg, dm, layer, n), layer, n, R, TOL,
                     "full")
+
+
+# Row counts of the selection's candidate batches at 8K (up to 49 budgets x 25
+# history rows): the split-K factor of the tiled products follows the row
+# count, and these three take 1, 2, 3, 4, 5 and 8 splits among the QKV, O and
+# down products.
+@pytest.mark.parametrize("R", [400, 800, 1225])
+def test_full_size_batched_sublayers(full, R):
+    """Attention with each row's own key/value (the selection's candidate rows)
+    and then the MLP of the last layer on R rows.  Rows do not see each other in
+    this mode, so the oracle evaluates a sample of rows one by one: the first
+    and last rows of 128-row tiles and the ragged last tile."""
+    cfg, dm = full
+    layer = LAYERS[-1]
+    n = CTX - 3
+    cache = _fill(cfg, dm, layer, n)
+    model = _one_layer(cfg, layer)
+    pos = (n - R + np.arange(R)).astype(np.int32)
+    x = W.synthetic_rows(R, cfg.d, seed=4, std=1.0, index=700 + R)
+    sample = sorted({0, 127, 128, 255, R // 2, (R // 128) * 128, R - 1})
+    xin = torch.from_numpy(x).cuda()
+    for sub in (1, 2):
+        out = torch.empty(R, cfg.d, device="cuda")
+        dm.sublayer_apply(2 * layer + sub, xin, pos, mode=1, out=out)
+        got = out.cpu().numpy()
+        ref = M.sublayer(model, sub, x[sample].astype(np.float64), pos[sample], cache, mode="own")
+        e = rel_err(got[sample], ref)
+        print(f"[batched] layer {layer} sublayer {sub} R {R}: rel err {e:.2e} on rows {sample}",
+              flush=True)
+        assert e < TOL, (sub, R, e)
+        x, xin = got, out
 
 
 LONG = 131072
