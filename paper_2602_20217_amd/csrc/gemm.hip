@@ -65,6 +65,41 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_skinny(
   const int kg = lane >> 4;
   const bool rok = row < M;
 
+  static_assert(NB * 256 <= NW * 64, "one epilogue element per thread");
+  // epilogue element of this thread: tile et, MFMA lane el, accumulator
+  // register ev (row em, column en)
+  const int et = threadIdx.x >> 8, el = (threadIdx.x >> 2) & 63, ev = threadIdx.x & 3;
+  const int em = 4 * (el >> 4) + ev;
+  const int en = (nt0 + et) * 16 + (el & 15);
+  const bool eact = threadIdx.x < NB * 256 && em < M && nt0 + et < NT;
+
+  // Epilogue operands that do not depend on the product are requested before
+  // the weight stream, so that their memory latency overlaps it instead of
+  // trailing every workgroup: the RMSNorm tile sums of this wave's first NPRE
+  // rows (UPRE per lane), the residual and next-norm gain of the thread's
+  // element, the position of its row.
+  // (read unconditionally at clamped, valid indices; entries past M or nssq
+  // are dropped when the sums are formed)
+  constexpr int NPRE = AN ? (NW >= 16 ? 1 : 2) : 1;
+  constexpr int UPRE = 4;
+  float pre[NPRE][UPRE];
+  if (AN) {
+#pragma unroll
+    for (int q = 0; q < NPRE; ++q) {
+      const int m = min(wave + q * NW, M - 1);
+#pragma unroll
+      for (int u = 0; u < UPRE; ++u)
+        pre[q][u] = ssq_in[(size_t)m * nssq + min(lane + 64 * u, nssq - 1)];
+    }
+  }
+  float e_res = 0.f, e_gain = 0.f;
+  int e_pos = 0;
+  if (EPI == EPI_RESID && eact) {
+    e_res = res[(size_t)em * ldres + en];
+    if (next_gain) e_gain = next_gain[en];
+  }
+  if (EPI == EPI_QKV && eact) e_pos = qe.pos[em];
+
   f32x4 acc[NB];
 #pragma unroll
   for (int t = 0; t < NB; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -108,45 +143,59 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_skinny(
 #pragma unroll
   for (int t = 0; t < NB; ++t) red[wave][t][lane] = acc[t];
   if (AN) {
-    for (int m = wave; m < M; m += NW) {
-      float t = 0.f;
-      for (int j = lane; j < nssq; j += 64) t += ssq_in[(size_t)m * nssq + j];
+    // row sums in the order of a sequential sum over j = lane, lane + 64, ...,
+    // then a butterfly
+    auto finish = [&](int m, float t) {
 #pragma unroll
       for (int o = 32; o >= 1; o >>= 1) t += __shfl_xor(t, o);
       if (lane == 0) s_rs[m] = 1.0f / sqrtf(t / (float)K + eps);
+    };
+#pragma unroll
+    for (int q = 0; q < NPRE; ++q) {
+      const int m = wave + q * NW;
+      if (m < M) {
+        float t = 0.f;
+#pragma unroll
+        for (int u = 0; u < UPRE; ++u)
+          if (lane + 64 * u < nssq) t += pre[q][u];
+        for (int j = lane + 64 * UPRE; j < nssq; j += 64) t += ssq_in[(size_t)m * nssq + j];
+        finish(m, t);
+      }
+    }
+    for (int m = wave + NPRE * NW; m < M; m += NW) {
+      float t = 0.f;
+      for (int j = lane; j < nssq; j += 64) t += ssq_in[(size_t)m * nssq + j];
+      finish(m, t);
     }
   }
   __syncthreads();
 
   if (EPI == EPI_SWIGLU || EPI == EPI_QKV) {
     // tile rows 0..7 pair with rows 8..15 (gate/up, or rotary pairs)
-    for (int idx = threadIdx.x; idx < NB * 256; idx += NW * 64) {
-      const int t = idx >> 8, l = (idx >> 2) & 63, v = idx & 3;
-      const int m = 4 * (l >> 4) + v;
-      if (m >= M || nt0 + t >= NT || (l & 15) >= 8) continue;
+    if (eact && (el & 15) < 8) {
       float g = 0.f, u = 0.f;
       for (int w = 0; w < NW; ++w) {
-        g += red[w][t][l][v];
-        u += red[w][t][l + 8][v];
+        g += red[w][et][el][ev];
+        u += red[w][et][el + 8][ev];
       }
       if (AN) {
-        g *= s_rs[m];
-        u *= s_rs[m];
+        g *= s_rs[em];
+        u *= s_rs[em];
       }
       if (EPI == EPI_SWIGLU) {
-        const int c = (nt0 + t) * 8 + (l & 15);
-        store_split(ohi, olo, (size_t)m * ldact + c, silu_mul(g, u));
+        const int c = (nt0 + et) * 8 + (el & 15);
+        store_split(ohi, olo, (size_t)em * ldact + c, silu_mul(g, u));
       } else {
         const int tph = qe.hd >> 4, half = qe.hd >> 1;
-        const int hh = (nt0 + t) / tph;
-        const int f = 8 * ((nt0 + t) % tph) + (l & 15);
-        const int p = qe.pos[m];
+        const int hh = (nt0 + et) / tph;
+        const int f = 8 * ((nt0 + et) % tph) + (el & 15);
+        const int p = e_pos;
         if (hh < qe.hq + qe.hkv) {
           const float2 cs = *(const float2*)&qe.rope_cs[((size_t)p * half + f) * 2];
           const float y0 = g * cs.x - u * cs.y;
           const float y1 = u * cs.x + g * cs.y;
           if (hh < qe.hq) {
-            float* q = qe.q_out + ((size_t)m * qe.hq + hh) * qe.hd;
+            float* q = qe.q_out + ((size_t)em * qe.hq + hh) * qe.hd;
             q[f] = y0;
             q[f + half] = y1;
           } else {
@@ -162,31 +211,27 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_skinny(
       }
     }
   } else {
-    // thread idx < 256 owns (row 4 (l / 16) + v, column l % 16): in a wave the
+    // thread < 256 owns (row 4 (el / 16) + ev, column el % 16): in a wave the
     // 16 columns of a row sit on lane bits 2..5, so the tile's sum of squares
     // for the next norm is a 4-step butterfly
     static_assert(EPI != EPI_RESID || NB == 1, "next-norm sums assume one tile per block");
     const bool nn = EPI == EPI_RESID && next_gain != nullptr;
-    for (int idx = threadIdx.x; idx < NB * 256; idx += NW * 64) {
-      const int t = idx >> 8, l = (idx >> 2) & 63, v = idx & 3;
-      const int m = 4 * (l >> 4) + v;
-      const bool ok = m < M && nt0 + t < NT;
-      const int n = (nt0 + t) * 16 + (l & 15);
+    if (threadIdx.x < NB * 256) {
       float s = 0.f;
-      if (ok) {
-        for (int w = 0; w < NW; ++w) s += red[w][t][l][v];
-        if (AN) s *= s_rs[m];
-        if (EPI == EPI_RESID) s += res[(size_t)m * ldres + n];
-        out[(size_t)m * ldo + n] = s;
+      if (eact) {
+        for (int w = 0; w < NW; ++w) s += red[w][et][el][ev];
+        if (AN) s *= s_rs[em];
+        if (EPI == EPI_RESID) s += e_res;
+        out[(size_t)em * ldo + en] = s;
       }
       if (nn) {
         float sq = s * s;
-        if (ok) store_split(nhi, nlo, (size_t)m * ldn + n, s * next_gain[n]);
+        if (eact) store_split(nhi, nlo, (size_t)em * ldn + en, s * e_gain);
         sq += __shfl_xor(sq, 4);
         sq += __shfl_xor(sq, 8);
         sq += __shfl_xor(sq, 16);
         sq += __shfl_xor(sq, 32);
-        if (ok && (l & 15) == 0) next_ssq[(size_t)m * NT + nt0 + t] = sq;
+        if (eact && (el & 15) == 0) next_ssq[(size_t)em * NT + nt0 + et] = sq;
       }
     }
   }
