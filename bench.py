@@ -28,7 +28,7 @@ sys.path.insert(0, ROOT)
 # counter passes (FETCH_SIZE, WRITE_SIZE) scaled by a 256 MiB reference kernel
 # (profiles/decode_kernels_llama8b_ctx8k_counters.txt); valid only while the
 # product's source has the recorded digest
-GATE_UP_TRAFFIC = (235173360, "7cc6bfc3bff03a8d2ca0f65f9ab8924142c5c1e54dbac7663930561c1f2e70a2")
+GATE_UP_TRAFFIC = (235198445, "77e59681e9199fd513e4a871a9b9d58c3ff60c1f6566f57b80786136bf5c159a")
 
 
 def gate_up_traffic(cfg):
