@@ -224,6 +224,40 @@ def test_generate_ssd_equals_ar_and_oracle(setup):
             assert sg.j_star == sref.j_star and sg.gamma_star == sref.gamma_star
 
 
+def test_generation_fills_the_cache(setup):
+    """Speculative generation up to the last positions the cache holds
+    (prompt + n_new + gamma + 1 = n_max - 1; the last round's drafts and verify
+    rows reach position n_max - 3) equals AR and, teacher-forced, the oracle on
+    its last tokens; one more token is refused with KS_ECAPACITY before any
+    launch, and the context still generates afterwards."""
+    from paper_2602_20217_amd import _lib as K
+    from paper_2602_20217_amd.engine import select_params
+    name, cfg, dm, model = setup
+    c, mode, bins = LAT[name]
+    n_max, gamma = 320, 4
+    prompt = _prompt(cfg, 100, seed=5)
+    n_new = n_max - 1 - len(prompt) - gamma - 1
+    params = select_params(c, mode, bins)
+    ar, _, _ = dm.generate(prompt, n_new, gamma=0)
+    ssd, st, sels = dm.generate(prompt, n_new, gamma=gamma, reselect_every=16, params=params)
+    np.testing.assert_array_equal(ssd, ar)
+    assert st.n_selections == len(sels) >= n_new // 16
+    with pytest.raises(K.KsError) as e:
+        dm.generate(prompt, n_new + 1, gamma=gamma, reselect_every=16, params=params)
+    assert e.value.status == K.KS_ECAPACITY
+    again, _, _ = dm.generate(prompt, 8, gamma=gamma, reselect_every=16, params=params)
+    np.testing.assert_array_equal(again, ar[:8])
+    fw = M.forward(model, M.KVCache(cfg, n_max), list(prompt) + list(ar[:-1]), 0)
+    checked = 0
+    for k in range(n_new - 16, n_new):
+        lg = fw.logits[len(prompt) - 1 + k]
+        if margin(lg) > TOL[name] * np.max(np.abs(lg)):
+            assert ar[k] == int(np.argmax(lg)), k
+            checked += 1
+    print(f"[{name}] {n_new} tokens to the cache limit, {st.n_selections} selections, "
+          f"{checked}/16 final tokens pinned", flush=True)
+
+
 def test_first_selection_uses_gamma_rows(setup):
     """With a draft length below gamma_max, the first selection of a generation
     uses the last m (gamma + 1) prompt rows (here 15 of the 25 the prefill
