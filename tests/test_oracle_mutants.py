@@ -1,0 +1,307 @@
+"""Planted mistakes in the oracle, on the CPU: each mutant below is a plausible
+slip in one oracle function (a dropped term, a wrong sign, exponent or index,
+a transposed operand, a swapped role, an off-by-one).  With the mutant patched
+in, at least one of the pins listed for that function must fail; a mutant that
+every pin accepts would mean the pins do not fix that part of the oracle."""
+import math
+
+import numpy as np
+import pytest
+
+import workloads as W
+from oracle import additive as A
+from oracle import latency as LAT
+from oracle import model as M
+from oracle import sampling as S
+from oracle import select as SEL
+from tests import test_oracle_additive as TA
+from tests import test_oracle_model as TM
+from tests import test_oracle_primitives as TP
+from tests import test_oracle_sampling as TS
+from tests import test_oracle_select as TSEL
+
+_orig = {name: getattr(mod, name) for mod, name in [
+    (M, "attn_sublayer"), (M, "attn_qkv"), (S, "philox4x32_10"), (S, "filtered"),
+    (LAT, "fit_latency")]}
+
+
+# ------------------------------------------------------------------ mutants
+def rmsnorm_sum(x, g, eps):  # sum of squares instead of their mean
+    return x / np.sqrt(np.sum(x * x, axis=-1, keepdims=True) + eps) * g
+
+
+def rmsnorm_eps_outside(x, g, eps):  # eps added after the square root
+    return x / (np.sqrt(np.mean(x * x, axis=-1, keepdims=True)) + eps) * g
+
+
+def _rope(x, pos, theta, *, sign=1.0, fexp=2.0, interleaved=False, shift=0):
+    hd = x.shape[-1]
+    half = hd // 2
+    inv = theta ** (-fexp * np.arange(half, dtype=np.float64) / hd)
+    ang = (np.asarray(pos, dtype=np.float64) + shift)[..., None, None] * inv
+    c, s = np.cos(ang), np.sin(ang)
+    if interleaved:
+        a, b = x[..., 0::2], x[..., 1::2]
+        out = np.empty_like(x)
+        out[..., 0::2] = a * c - b * s
+        out[..., 1::2] = b * c + a * s
+        return out
+    a, b = x[..., :half], x[..., half:]
+    return np.concatenate([a * c - sign * b * s, b * c + sign * a * s], axis=-1)
+
+
+def attention_unscaled(q, K, V):
+    s = K @ q
+    p = np.exp(s - np.max(s))
+    return (p / p.sum()) @ V
+
+
+def attention_keys_as_values(q, K, V):
+    s = K @ q / np.sqrt(q.shape[-1])
+    p = np.exp(s - np.max(s))
+    return (p / p.sum()) @ K
+
+
+def silu_negated(x):
+    return x / (1.0 + np.exp(x))
+
+
+def bf16_truncate(x):
+    f = np.asarray(x, dtype=np.float64).astype(np.float32)
+    u = (f.view(np.uint32) >> 16) << 16
+    return u.astype(np.uint32).view(np.float32).astype(np.float64)
+
+
+def mlp_gate_up_swapped(model, layer, x):
+    c, Wl = model.cfg, model.layers[layer]
+    h = M.rmsnorm(x, Wl["mlp_norm"], c.eps)
+    return x + (M.silu(h @ Wl["w_up"].T) * (h @ Wl["w_gate"].T)) @ Wl["w_down"].T
+
+
+def mlp_without_norm(model, layer, x):
+    Wl = model.layers[layer]
+    return x + (M.silu(x @ Wl["w_gate"].T) * (x @ Wl["w_up"].T)) @ Wl["w_down"].T
+
+
+def qkv_values_unnormalised(model, layer, x, pos):
+    q, k, v = _orig["attn_qkv"](model, layer, x, pos)
+    c = model.cfg
+    return q, k, (x @ model.layers[layer]["wv"].T).reshape(-1, c.hkv, c.hd)
+
+
+def attn_wo_transposed(model, layer, x, pos, cache, mode):
+    Wl = model.layers[layer]
+    wo = Wl["wo"]
+    Wl["wo"] = wo.T.copy()
+    try:
+        return _orig["attn_sublayer"](model, layer, x, pos, cache, mode)
+    finally:
+        Wl["wo"] = wo
+
+
+def _attn(model, layer, x, pos, cache, mode, head_map, self_included=True):
+    c, Wl = model.cfg, model.layers[layer]
+    q, k, v = M.attn_qkv(model, layer, x, pos)
+    k, v = model.store(k), model.store(v)
+    for r in range(x.shape[0]):
+        cache.K[layer][:, pos[r]] = k[r]
+        cache.V[layer][:, pos[r]] = v[r]
+    o = np.zeros((x.shape[0], c.hq, c.hd))
+    for r in range(x.shape[0]):
+        end = int(pos[r]) + (1 if self_included else 0)
+        for h in range(c.hq):
+            kh = head_map(h, c)
+            o[r, h] = M.softmax_attention(q[r, h], cache.K[layer][kh, :end], cache.V[layer][kh, :end])
+    return x + o.reshape(x.shape[0], -1) @ Wl["wo"].T
+
+
+def attn_gqa_modulo(model, layer, x, pos, cache, mode):  # query head h -> kv head h % hkv
+    return _attn(model, layer, x, pos, cache, mode, lambda h, c: h % c.hkv)
+
+
+def attn_excludes_self(model, layer, x, pos, cache, mode):  # causal range one short
+    return _attn(model, layer, x, pos, cache, mode, lambda h, c: h // (c.hq // c.hkv), False)
+
+
+def head_without_final_norm(model, x):
+    logits = x @ model.lm_head.T
+    am = np.argmax(logits, axis=-1)
+    mx = logits[np.arange(len(am)), am]
+    return logits, am.astype(np.int64), 1.0 / np.sum(np.exp(logits - mx[:, None]), axis=-1)
+
+
+def expected_tokens_from_one(alpha, gamma):  # sum over i = 1..gamma
+    return sum(alpha ** i for i in range(1, gamma + 1))
+
+
+def tpt_skipped_weight(alpha, gamma, executed_weight, C):  # cost from the skipped weight
+    return SEL.expected_tokens(alpha, gamma) / (gamma * (C - executed_weight) + C)
+
+
+def cos_without_y_norm(X, Y):
+    X, Y = np.asarray(X, dtype=np.float64), np.asarray(Y, dtype=np.float64)
+    nx = np.sqrt(np.sum(X * X, axis=-1))
+    return np.where(nx > 0, np.sum(X * Y, axis=-1) / np.where(nx > 0, nx, 1.0), 0.0)
+
+
+def fit_latency_swapped(n_attn, t_attn, t_mlp):  # slope and intercept exchanged
+    c1, c2, c3 = _orig["fit_latency"](n_attn, t_attn, t_mlp)
+    return c1, c3, c2
+
+
+def round_floor(x):
+    return int(math.floor(x))
+
+
+def round_half_even(x):
+    return int(round(x))
+
+
+def dp_ties_to_skip(w, q, C, max_skip):
+    """knapsack_dp with <= in place of < (ties take the skip)."""
+    w = np.asarray(w, dtype=np.int64)
+    q = np.asarray(q, dtype=np.int64)
+    B, n = w.shape
+    best = np.full((B, C + 1), A.INF, dtype=np.int64)
+    best[:, 0] = 0
+    bits = np.zeros((B, n, C // 64 + 1), dtype=np.uint64)
+    jj = np.arange(C + 1)
+    for i in range(n):
+        src = jj[None, :] - w[:, i][:, None]
+        ok = src >= 0
+        prev = np.where(ok, best[np.arange(B)[:, None], np.clip(src, 0, C)], A.INF)
+        cand = np.where(prev < A.INF, prev + q[:, i][:, None], A.INF)
+        take = (cand <= best) & (cand < A.INF) & ok & (jj <= max_skip)[None, :]
+        best = np.where(take, cand, best)
+        for b in range(B):
+            for j in np.nonzero(take[b])[0]:
+                bits[b, i, j // 64] |= np.uint64(1) << np.uint64(j % 64)
+    return best.astype(np.int32), bits
+
+
+def philox_key_words_swapped(ctr, key):
+    return _orig["philox4x32_10"](ctr, np.asarray(key)[..., ::-1])
+
+
+def resample_from_target(p, q, x, u_acc, u_res, margins=None):
+    """Rejection draws from p itself instead of the residual max(0, p - q)."""
+    ratio = S.prob_of(*p, x) / S.prob_of(*q, x)
+    if u_acc < min(1.0, ratio):
+        return True, x
+    return False, S.draw(p[0], p[1], u_res)
+
+
+def accept_with_inverted_ratio(p, q, x, u_acc, u_res, margins=None):
+    """Acceptance test against q/p instead of p/q."""
+    ratio = S.prob_of(*q, x) / max(S.prob_of(*p, x), 1e-300)
+    if u_acc < min(1.0, ratio):
+        return True, x
+    pid, ppr = p
+    r = np.maximum(0.0, ppr - np.array([S.prob_of(*q, int(y)) for y in pid]))
+    if r.sum() <= 0.0:
+        return False, S.draw(pid, ppr, u_res)
+    return False, S.draw(pid, r / r.sum(), u_res)
+
+
+def top_p_one_short(logits, prm, margins=None):
+    ids, probs = _orig["filtered"](logits, prm, margins)
+    if len(ids) > 1 and prm.top_p < 1.0:
+        ids, probs = ids[:-1], probs[:-1] / probs[:-1].sum()
+    return ids, probs
+
+
+# ------------------------------------------------------------------ pins
+@pytest.fixture(scope="module")
+def tiny():
+    cfg = W.config("tiny")
+    return M.Model(cfg, W.generate_weights(cfg, seed=0))
+
+
+def _mutants(tiny):
+    rope_pins = [TP.test_rope_two_dims_is_plane_rotation,
+                 TP.test_rope_identity_norm_and_relative_position,
+                 TP.test_rope_pair_frequencies_worked_example]
+    attn_pins = [TP.test_attention_sublayer_first_position_worked_example,
+                 lambda: TM.test_gqa_mapping_matches_duplicated_heads(tiny),
+                 lambda: TM.test_prefill_rows_equal_incremental_decode(tiny)]
+    sampling_pins = [TS.test_acceptance_rule_preserves_target_exactly,
+                     TS.test_verify_chain_monte_carlo]
+    return [
+        ("rmsnorm: sum of squares", M, "rmsnorm", rmsnorm_sum, [TP.test_rmsnorm_closed_form]),
+        ("rmsnorm: eps after the root", M, "rmsnorm", rmsnorm_eps_outside,
+         [TP.test_rmsnorm_closed_form]),
+        ("rope: rotation sign", M, "rope", lambda x, p, t: _rope(x, p, t, sign=-1.0), rope_pins),
+        ("rope: theta^(-f/hd)", M, "rope", lambda x, p, t: _rope(x, p, t, fexp=1.0), rope_pins),
+        ("rope: interleaved pairs", M, "rope", lambda x, p, t: _rope(x, p, t, interleaved=True),
+         rope_pins),
+        ("rope: 1-based positions", M, "rope", lambda x, p, t: _rope(x, p, t, shift=1), rope_pins),
+        ("attention: no 1/sqrt(hd)", M, "softmax_attention", attention_unscaled,
+         [TP.test_attention_special_cases]),
+        ("attention: keys as values", M, "softmax_attention", attention_keys_as_values,
+         [TP.test_attention_special_cases]),
+        ("silu: sigmoid(-x)", M, "silu", silu_negated, [TP.test_silu]),
+        ("bf16: truncation", M, "to_bf16", bf16_truncate, [TP.test_bf16_rounding]),
+        ("mlp: gate and up swapped", M, "mlp_sublayer", mlp_gate_up_swapped,
+         [TP.test_swiglu_mlp_sublayer_worked_example]),
+        ("mlp: no RMSNorm", M, "mlp_sublayer", mlp_without_norm,
+         [TP.test_swiglu_mlp_sublayer_worked_example]),
+        ("attention sublayer: values from the unnormalised input", M, "attn_qkv",
+         qkv_values_unnormalised, attn_pins),
+        ("attention sublayer: Wo transposed", M, "attn_sublayer", attn_wo_transposed, attn_pins),
+        ("attention sublayer: head h -> kv head h % hkv", M, "attn_sublayer", attn_gqa_modulo,
+         attn_pins),
+        ("attention sublayer: own position excluded", M, "attn_sublayer", attn_excludes_self,
+         attn_pins),
+        ("head: no final RMSNorm", M, "head", head_without_final_norm, [TP.test_head_worked_example]),
+        ("expected tokens: sum from i = 1", SEL, "expected_tokens", expected_tokens_from_one,
+         [TP.test_expected_tokens_closed_form]),
+        ("cos: |y| dropped", SEL, "cos_rows", cos_without_y_norm, [TP.test_cos_closed_forms]),
+        ("TPT: cost from the skipped weight", SEL, "tpt", tpt_skipped_weight,
+         [TSEL.test_tpt_full_model_is_one_over_capacity,
+          TSEL.test_tpt_reduces_to_tpl_when_latencies_equal, TSEL.test_stage2_grid_toy]),
+        ("latency fit: slope and intercept exchanged", LAT, "fit_latency", fit_latency_swapped,
+         [TSEL.test_latency_fit_recovers_coefficients]),
+        ("weights: floor instead of rounding", LAT, "round_half_up", round_floor,
+         [TSEL.test_quantize_appendix_c_worked_example, TSEL.test_quantize_bins_tiny,
+          TSEL.test_quantize_rounds_halves_up]),
+        ("weights: halves to even", LAT, "round_half_up", round_half_even,
+         [TSEL.test_quantize_appendix_c_worked_example, TSEL.test_quantize_bins_tiny,
+          TSEL.test_quantize_rounds_halves_up]),
+        ("additive DP: ties take the skip", A, "knapsack_dp", dp_ties_to_skip,
+         [lambda: TA.test_dp_equals_brute_force_with_tie_break(1, 3),
+          lambda: TA.test_dp_equals_brute_force_with_tie_break(2, 0)]),
+        ("philox: key words exchanged", S, "philox4x32_10", philox_key_words_swapped,
+         [TS.test_philox_known_answers]),
+        ("sampling: rejection draws from p", S, "accept_or_resample", resample_from_target,
+         sampling_pins),
+        ("sampling: acceptance ratio q/p", S, "accept_or_resample", accept_with_inverted_ratio,
+         sampling_pins),
+        ("sampling: top-p cut one entry short", S, "filtered", top_p_one_short,
+         [TS.test_filter_top_p_keeps_shortest_sufficient_prefix]),
+    ]
+
+
+N_MUTANTS = 28
+
+
+def test_mutant_table_size(tiny):
+    assert len(_mutants(tiny)) == N_MUTANTS
+
+
+@pytest.mark.parametrize("idx", range(N_MUTANTS))
+def test_pins_reject_mutant(tiny, monkeypatch, idx):
+    name, mod, attr, mutant, pins = _mutants(tiny)[idx]
+    # the pins pass on the oracle as it is
+    for pin in pins:
+        pin()
+    monkeypatch.setattr(mod, attr, mutant)
+    rejected = []
+    for pin in pins:
+        try:
+            pin()
+        # an assertion, or arithmetic that breaks down (a mutant that raises
+        # anything else is itself broken, and the test errors)
+        except (AssertionError, ValueError, ZeroDivisionError, FloatingPointError) as e:
+            rejected.append((getattr(pin, "__name__", "pin"), type(e).__name__))
+    assert rejected, f"no pin rejects the mutant: {name}"
+    print(f"[mutant] {name}: rejected by {rejected}")

@@ -56,6 +56,77 @@ def test_rope_identity_norm_and_relative_position():
     assert np.count_nonzero(np.abs(r) > 1e-15) == 2 and abs(r[hd // 2]) > 0
 
 
+def test_rope_pair_frequencies_worked_example():
+    # theta = 64, hd = 6: pair f turns by p * 64^(-2f/6) = p / 4^f, so the unit
+    # vector on coordinate f goes to cos(p / 4^f) e_f + sin(p / 4^f) e_(f+3)
+    hd, p = 6, 3
+    for f in range(3):
+        e = np.zeros((1, 1, hd))
+        e[..., f] = 1.0
+        r = M.rope(e, np.array([p]), 64.0)[0, 0]
+        want = np.zeros(hd)
+        want[f], want[f + 3] = math.cos(p / 4 ** f), math.sin(p / 4 ** f)
+        np.testing.assert_allclose(r, want, atol=1e-14)
+
+
+def _one_layer(**dims):
+    """A one-layer oracle model of the given dimensions with zero weights
+    (tests set the matrices they use) and unit norm gains."""
+    import dataclasses
+    import workloads as W
+    cfg = dataclasses.replace(W.config("tiny"), L=1, eps=0.0, qk_norm=False, dtype="f32",
+                              **dims)
+    w = {("embed", -1): np.zeros((cfg.vocab, cfg.d)), ("lm_head", -1): np.zeros((cfg.vocab, cfg.d))}
+    shapes = {"wq": (cfg.hq * cfg.hd, cfg.d), "wk": (cfg.hkv * cfg.hd, cfg.d),
+              "wv": (cfg.hkv * cfg.hd, cfg.d), "wo": (cfg.d, cfg.hq * cfg.hd),
+              "w_gate": (cfg.ffn, cfg.d), "w_up": (cfg.ffn, cfg.d), "w_down": (cfg.d, cfg.ffn)}
+    for k, sh in shapes.items():
+        w[(k, 0)] = np.zeros(sh)
+    return M.Model(cfg, w)
+
+
+def test_swiglu_mlp_sublayer_worked_example():
+    # x = (3, 4), rms = sqrt(12.5); the gate row reads h0, the up row h1, the
+    # down column is (1, 2): out = x + (1, 2) * silu(h0) * h1 (hand-computed;
+    # gate and up exchanged would give 3.72585 in the first entry)
+    m = _one_layer(d=2, ffn=1, hq=1, hkv=1, hd=2, vocab=4)
+    W0 = m.layers[0]
+    W0["w_gate"][:] = [[1.0, 0.0]]
+    W0["w_up"][:] = [[0.0, 1.0]]
+    W0["w_down"][:] = [[1.0], [2.0]]
+    out = M.mlp_sublayer(m, 0, np.array([[3.0, 4.0]]))
+    np.testing.assert_allclose(out[0], [3.6722479628067237, 5.344495925613447], rtol=1e-13)
+
+
+def test_attention_sublayer_first_position_worked_example():
+    # one cached position: every head's softmax is 1, so the output is
+    # x + Wo (v, v) with v = Wv rmsnorm(x) (no rotation of values).  x = (1, 2, 3, 4),
+    # rms = sqrt(7.5); Wv picks h0 and h3; Wo is not symmetric (its transpose
+    # would give 4.92119 in the second entry)
+    m = _one_layer(d=4, hq=2, hkv=1, hd=2, ffn=2, vocab=4)
+    W0 = m.layers[0]
+    W0["wq"][:] = np.arange(16.0).reshape(4, 4) / 7.0
+    W0["wk"][:] = np.arange(8.0).reshape(2, 4) / 5.0
+    W0["wv"][:] = [[1.0, 0, 0, 0], [0, 0, 0, 1.0]]
+    W0["wo"][:] = [[1.0, 0, 0, 0], [0, 0, 1.0, 0], [0, 0, 0, 3.0], [0, 2.0, 0, 0]]
+    cache = M.KVCache(m.cfg, 4)
+    out = M.attn_sublayer(m, 0, np.array([[1.0, 2.0, 3.0, 4.0]]), np.array([0]), cache, "write")
+    np.testing.assert_allclose(out[0], [1.3651483716701107, 2.3651483716701107,
+                                        7.381780460041329, 6.921186973360886], rtol=1e-13)
+
+
+def test_head_worked_example():
+    # final RMSNorm then the head rows e0, e1, -e0: logits (3, 4, -3) / sqrt(12.5),
+    # argmax 1, top-1 probability 1 / sum exp(l - l_max) = 0.52862
+    m = _one_layer(d=2, ffn=1, hq=1, hkv=1, hd=2, vocab=3)
+    m.lm_head = np.array([[1.0, 0.0], [0.0, 1.0], [-1.0, 0.0]])
+    logits, am, top1 = M.head(m, np.array([[3.0, 4.0]]))
+    np.testing.assert_allclose(logits[0], [0.848528137423857, 1.131370849898476,
+                                           -0.848528137423857], rtol=1e-14)
+    assert am[0] == 1
+    assert top1[0] == pytest.approx(0.5286190379315163, rel=1e-13)
+
+
 def test_silu():
     x = np.linspace(-20, 20, 101)
     np.testing.assert_allclose(M.silu(x), x * scipy.special.expit(x), rtol=1e-13, atol=1e-300)

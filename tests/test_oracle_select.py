@@ -50,6 +50,20 @@ def test_quantize_bins_tiny():
         LAT.quantize((1.0, -1.0, 0.0), 10, 4, "paper_min")
 
 
+def test_quantize_rounds_halves_up():
+    # weights are floor(t / Delta + 1/2), at least 1 (exact binary fractions,
+    # so the halves are exact): t_A = 0.5, t_M = 1.25 -> Delta = 0.5, w_M = 2.5 -> 3
+    q = LAT.quantize((1.25, 0.0, 0.5), 1000, 4, "paper_min")
+    assert (q.delta, q.w_attn, q.w_mlp, q.C) == (0.5, 1, 3, 16)
+    # t_A = 1.75, t_M = 0.5 -> w_A = 3.5 -> 4
+    q = LAT.quantize((0.5, 0.0, 1.75), 1000, 2, "paper_min")
+    assert (q.w_attn, q.w_mlp, q.C) == (4, 1, 10)
+    # a sublayer far below Delta still weighs 1: one layer, 2 bins, Delta = 0.5625,
+    # t_A / Delta = 0.22 -> 1, t_M / Delta = 1.78 -> 2
+    q = LAT.quantize((1.0, 0.0, 0.125), 1000, 1, "bins", 2)
+    assert (q.delta, q.w_attn, q.w_mlp, q.C) == (0.5625, 1, 2, 3)
+
+
 def test_tpt_full_model_is_one_over_capacity():
     for C in (8, 64, 128):
         for g in range(1, 11):
