@@ -210,6 +210,67 @@ def top_p_one_short(logits, prm, margins=None):
     return ids, probs
 
 
+def _dp(model, cache, pos, X, w_attn, w_mlp, C, tau=0.5, prune_half=True, *,
+        ties_execute=True, strict_tau=True, reset_zero=True):
+    """Stage 1 with one rule changed by the flags."""
+    n_sub = model.n_sub
+    J = C // 2 if prune_half else C
+    reach = np.zeros(J + 1, dtype=bool)
+    reach[0] = True
+    g = [None] * (J + 1)
+    g[0] = X[0].copy()
+    bits = np.zeros((n_sub + 1, J + 1), dtype=np.uint8)
+    reach_rows = np.zeros((n_sub + 1, J + 1), dtype=bool)
+    reach_rows[0] = reach
+    sig_e = np.full((n_sub + 1, J + 1), np.nan)
+    sig_s = np.full((n_sub + 1, J + 1), np.nan)
+    valid = (lambda v: v > tau) if strict_tau else (lambda v: v >= tau)
+    for i in range(1, n_sub + 1):
+        w = SEL.item_weight(i, w_attn, w_mlp)
+        E = [None] * (J + 1)
+        for j in range(J + 1):
+            if reach[j]:
+                E[j] = M.sublayer(model, i, g[j], pos, cache, mode="own")
+                sig_e[i, j] = SEL.cos_matrix(E[j], X[i])
+            if j >= w and reach[j - w]:
+                sig_s[i, j] = SEL.cos_matrix(g[j - w], X[i])
+        ng, nr = [None] * (J + 1), np.zeros(J + 1, dtype=bool)
+        for j in range(J + 1):
+            e_ok = reach[j] and valid(sig_e[i, j])
+            s_ok = j >= w and reach[j - w] and valid(sig_s[i, j])
+            prefer_e = (sig_e[i, j] >= sig_s[i, j]) if ties_execute else (sig_e[i, j] > sig_s[i, j])
+            if e_ok and (not s_ok or prefer_e):
+                ng[j], nr[j] = E[j], True
+            elif s_ok:
+                ng[j], nr[j], bits[i, j] = g[j - w], True, 1
+        if reset_zero:
+            ng[0], nr[0], bits[i, 0] = X[i].copy(), True, 0
+        g, reach = ng, nr
+        reach_rows[i] = reach
+    return SEL.DPResult(J, reach, g, bits, reach_rows, sig_e, sig_s)
+
+
+def stage2_last_maximum(model, dp, X_last, w_attn, w_mlp, C, D=10):
+    """Stage 2 keeping the last of equal TPT values (>= in place of >)."""
+    _, y_ref, _ = M.head(model, X_last)
+    best = (0.0, None, 0, 0, 0.0)
+    alphas, nm = {}, {}
+    for j in range(dp.J + 1):
+        if not dp.reach[j]:
+            continue
+        ex = SEL.backtrack(dp.bits, j, w_attn, w_mlp)
+        _, y_j, _ = M.head(model, dp.states[j])
+        n_match = int(np.sum(y_j == y_ref))
+        a = n_match / X_last.shape[0]
+        alphas[j], nm[j] = a, n_match
+        for gam in range(1, D + 1):
+            v = SEL.tpt(a, gam, C - j, C)
+            if v >= best[0]:
+                best = (v, ex, j, gam, a)
+    v, ex, j, gam, a = best
+    return SEL.Selection(ex, j, gam, v, a, alphas, nm)
+
+
 # ------------------------------------------------------------------ pins
 @pytest.fixture(scope="module")
 def tiny():
@@ -217,7 +278,14 @@ def tiny():
     return M.Model(cfg, W.generate_weights(cfg, seed=0))
 
 
-def _mutants(tiny):
+@pytest.fixture(scope="module")
+def tiny_hist(tiny):
+    st = M.prefill(tiny, W.prompt_ids(tiny.cfg.vocab, 48, 1), 128, 10)
+    pos, X = M.history(st)
+    return tiny, st, pos, X
+
+
+def _mutants(tiny, tiny_hist):
     rope_pins = [TP.test_rope_two_dims_is_plane_rotation,
                  TP.test_rope_identity_norm_and_relative_position,
                  TP.test_rope_pair_frequencies_worked_example]
@@ -226,6 +294,10 @@ def _mutants(tiny):
                  lambda: TM.test_prefill_rows_equal_incremental_decode(tiny)]
     sampling_pins = [TS.test_acceptance_rule_preserves_target_exactly,
                      TS.test_verify_chain_monte_carlo]
+    dp_pins = [TSEL.test_dp_ties_go_to_execute_and_tau_is_strict,
+               lambda: TSEL.test_dp_reachable_cells_are_subset_sums(tiny_hist),
+               lambda: TSEL.test_dp_terminal_states_match_backtracked_masks(tiny_hist),
+               lambda: TSEL.test_stage2_fallback_and_alpha(tiny_hist)]
     return [
         ("rmsnorm: sum of squares", M, "rmsnorm", rmsnorm_sum, [TP.test_rmsnorm_closed_form]),
         ("rmsnorm: eps after the root", M, "rmsnorm", rmsnorm_eps_outside,
@@ -278,19 +350,27 @@ def _mutants(tiny):
          sampling_pins),
         ("sampling: top-p cut one entry short", S, "filtered", top_p_one_short,
          [TS.test_filter_top_p_keeps_shortest_sufficient_prefix]),
+        ("model-mode DP: ties take the skip", SEL, "dp_select",
+         lambda *a, **k: _dp(*a, ties_execute=False, **k), dp_pins),
+        ("model-mode DP: sigma >= tau", SEL, "dp_select",
+         lambda *a, **k: _dp(*a, strict_tau=False, **k), dp_pins),
+        ("model-mode DP: cell 0 not reset to X^(i)", SEL, "dp_select",
+         lambda *a, **k: _dp(*a, reset_zero=False, **k), dp_pins),
+        ("stage 2: last of equal TPT values", SEL, "stage2", stage2_last_maximum,
+         [lambda: TSEL.test_stage2_fallback_and_alpha(tiny_hist), TSEL.test_stage2_grid_toy]),
     ]
 
 
-N_MUTANTS = 28
+N_MUTANTS = 32
 
 
-def test_mutant_table_size(tiny):
-    assert len(_mutants(tiny)) == N_MUTANTS
+def test_mutant_table_size(tiny, tiny_hist):
+    assert len(_mutants(tiny, tiny_hist)) == N_MUTANTS
 
 
 @pytest.mark.parametrize("idx", range(N_MUTANTS))
-def test_pins_reject_mutant(tiny, monkeypatch, idx):
-    name, mod, attr, mutant, pins = _mutants(tiny)[idx]
+def test_pins_reject_mutant(tiny, tiny_hist, monkeypatch, idx):
+    name, mod, attr, mutant, pins = _mutants(tiny, tiny_hist)[idx]
     # the pins pass on the oracle as it is
     for pin in pins:
         pin()

@@ -148,6 +148,33 @@ def test_dp_terminal_states_match_backtracked_masks(tiny_hist):
     assert n_opt >= 1
 
 
+def test_dp_ties_go_to_execute_and_tau_is_strict():
+    """Every sublayer an identity (zero output projections): each budget's
+    execute and skip candidates are the same state, so every decision is a tie.
+    The >= of Eq. dp_main sends ties to execute, which with unit weights skips
+    the first j sublayers at budget j (ties sent to skip would skip the last j).
+    A candidate whose cosine equals tau exactly is not valid (sigma > tau)."""
+    import dataclasses
+    cfg = dataclasses.replace(W.config("tiny"), L=2)
+    w = W.generate_weights(cfg, seed=0)
+    for l in range(cfg.L):
+        w[("wo", l)] = np.zeros_like(w[("wo", l)])
+        w[("w_down", l)] = np.zeros_like(w[("w_down", l)])
+    model = M.Model(cfg, w)
+    X0 = np.random.default_rng(7).standard_normal((5, cfg.d))
+    X = [X0.copy() for _ in range(2 * cfg.L + 1)]
+    pos = np.arange(40, 45)
+    cache = M.KVCache(cfg, 64)
+    n = 2 * cfg.L
+    dp = SEL.dp_select(model, cache, pos, X, 1, 1, 8, tau=0.5, prune_half=False)
+    assert np.flatnonzero(dp.reach).tolist() == list(range(n + 1))
+    for j in range(n + 1):
+        np.testing.assert_array_equal(SEL.backtrack(dp.bits, j, 1, 1), np.arange(n) >= j)
+    c = SEL.cos_matrix(X0, X0)
+    dp = SEL.dp_select(model, cache, pos, X, 1, 1, 8, tau=c, prune_half=False)
+    assert np.flatnonzero(dp.reach).tolist() == [0]
+
+
 def test_stage2_fallback_and_alpha(tiny_hist):
     model, st, pos, X = tiny_hist
     dp = SEL.dp_select(model, st.cache, pos, X, 10, 6, 64, tau=0.5)
