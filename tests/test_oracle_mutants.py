@@ -10,6 +10,7 @@ import pytest
 
 import workloads as W
 from oracle import additive as A
+from oracle import generate as GENM
 from oracle import latency as LAT
 from oracle import model as M
 from oracle import sampling as S
@@ -271,6 +272,63 @@ def stage2_last_maximum(model, dp, X_last, w_attn, w_mlp, C, D=10):
     return SEL.Selection(ex, j, gam, v, a, alphas, nm)
 
 
+def _ssd_round(model, st, exec_mask, gamma, m_rounds=5, tau_conf=0.0, *, extra_accept=False,
+               keep_all_rows=False):
+    """One greedy round with one rule changed by the flags."""
+    drafts, tops = [], []
+    t = st.s
+    for k in range(gamma):
+        fw = M.forward(model, st.cache, [t], st.P + k, exec_mask)
+        t = int(fw.argmax[0])
+        drafts.append(t)
+        tops.append(float(fw.top1[0]))
+        if tau_conf > 0 and not tops[-1] >= tau_conf:
+            break
+    g = len(drafts)
+    fv = M.forward(model, st.cache, [st.s] + drafts, st.P)
+    y = fv.argmax
+    a = 0
+    while a < g and drafts[a] == y[a]:
+        a += 1
+    if extra_accept and a < g:
+        a += 1
+    emitted = drafts[:a] + [int(y[a])]
+    rows = g + 1 if keep_all_rows else a + 1
+    st.blocks.append((st.P + np.arange(rows), [sn[:rows] for sn in fv.snaps]))
+    st.blocks = st.blocks[-m_rounds:]
+    st.P += a + 1
+    st.s = int(y[a])
+    st.out.extend(emitted)
+    return M.Round(drafts, tops, y, a, emitted)
+
+
+def generate_reselect_on_multiples(model, prompt, n_new, gamma, T, lat, quant_mode="paper_min",
+                                   bins=0, tau=0.5, D=10, m_rounds=5, n_max=None, tau_conf=0.0,
+                                   gamma_source="fixed"):
+    """The generation loop re-selecting only when the produced count is a
+    multiple of T (instead of when a multiple has been passed)."""
+    from oracle import generate as GEN
+    n_max = n_max or (len(prompt) + n_new + gamma + 2)
+    st = M.prefill(model, prompt, n_max, m_rounds * (gamma + 1))
+    log = GEN.GenLog()
+
+    def choose():
+        wts = LAT.quantize(lat, st.P, model.cfg.L, quant_mode, bins)
+        sel, _ = SEL.select(model, st, wts.w_attn, wts.w_mlp, wts.C, tau, True, D)
+        log.selections.append((len(st.out), st.P, wts, sel))
+        return sel
+
+    sel = choose()
+    while len(st.out) < n_new:
+        rd = M.ssd_round(model, st, sel.exec_mask, gamma, m_rounds, tau_conf)
+        log.accepted.append(rd.n_accepted)
+        log.drafted.append(len(rd.drafts))
+        log.draft_top1.append(rd.draft_top1)
+        if len(st.out) < n_new and len(st.out) % T == 0:
+            sel = choose()
+    return st.out[:n_new], log
+
+
 # ------------------------------------------------------------------ pins
 @pytest.fixture(scope="module")
 def tiny():
@@ -294,6 +352,8 @@ def _mutants(tiny, tiny_hist):
                  lambda: TM.test_prefill_rows_equal_incremental_decode(tiny)]
     sampling_pins = [TS.test_acceptance_rule_preserves_target_exactly,
                      TS.test_verify_chain_monte_carlo]
+    round_pins = [lambda: TM.test_greedy_ssd_equals_greedy_ar(tiny, 0),
+                  lambda: TM.test_history_blocks_are_contiguous_recent_positions(tiny)]
     dp_pins = [TSEL.test_dp_ties_go_to_execute_and_tau_is_strict,
                lambda: TSEL.test_dp_reachable_cells_are_subset_sums(tiny_hist),
                lambda: TSEL.test_dp_terminal_states_match_backtracked_masks(tiny_hist),
@@ -358,10 +418,17 @@ def _mutants(tiny, tiny_hist):
          lambda *a, **k: _dp(*a, reset_zero=False, **k), dp_pins),
         ("stage 2: last of equal TPT values", SEL, "stage2", stage2_last_maximum,
          [lambda: TSEL.test_stage2_fallback_and_alpha(tiny_hist), TSEL.test_stage2_grid_toy]),
+        ("greedy round: one draft past the first mismatch accepted", M, "ssd_round",
+         lambda *a, **k: _ssd_round(*a, extra_accept=True, **k), round_pins),
+        ("greedy round: history keeps every verify row", M, "ssd_round",
+         lambda *a, **k: _ssd_round(*a, keep_all_rows=True, **k), round_pins),
+        ("generation: re-select only on multiples of T", GENM, "generate",
+         generate_reselect_on_multiples,
+         [TSEL.test_reselection_at_first_round_end_past_each_multiple]),
     ]
 
 
-N_MUTANTS = 32
+N_MUTANTS = 35
 
 
 def test_mutant_table_size(tiny, tiny_hist):

@@ -201,6 +201,27 @@ def test_generate_equals_ar_tiny():
     assert len(log.selections) >= 2
 
 
+def test_reselection_at_first_round_end_past_each_multiple():
+    """A new selection is made at the end of the first round after which the
+    number of produced tokens has passed a multiple of T, while tokens remain
+    (rounds emit a + 1 tokens; the token the prefill emits counts as produced);
+    the first selection precedes the first round."""
+    cfg = W.config("tiny")
+    model = M.Model(cfg, W.generate_weights(cfg, seed=0))
+    prompt = W.prompt_ids(cfg.vocab, 64, 3)
+    n_new, T = 40, 5
+    out, log = GEN.generate(model, prompt, n_new, gamma=4, T=T, lat=W.TINY_LATENCY,
+                            quant_mode="bins", bins=64)
+    produced, want = 1, [1]
+    for a in log.accepted:
+        before = produced
+        produced += a + 1
+        if produced < n_new and produced // T > before // T:
+            want.append(produced)
+    assert [sel[0] for sel in log.selections] == want
+    assert len(want) >= 4 and any(p % T for p in want[1:])
+
+
 def _tiny_gen(**kw):
     cfg = W.config("tiny")
     model = M.Model(cfg, W.generate_weights(cfg, seed=0))
