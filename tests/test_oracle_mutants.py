@@ -329,6 +329,27 @@ def generate_reselect_on_multiples(model, prompt, n_new, gamma, T, lat, quant_mo
     return st.out[:n_new], log
 
 
+def _additive_stage2(best_b, bits_b, w_b, s_b, D=10, *, alpha_executed=False,
+                     cost_skipped=False, keep_last=False):
+    """Stage 2 of the isolated knapsack with one rule changed by the flags."""
+    Wt = int(np.sum(w_b))
+    top = (0.0, -1, 0, None)
+    for j in range(len(best_b)):
+        if best_b[j] >= A.INF:
+            continue
+        skip = A.backtrack(bits_b, w_b, j)
+        a = 1.0
+        for i in range(len(w_b)):
+            if bool(skip[i]) != alpha_executed:
+                a *= float(s_b[i])
+        for g in range(1, D + 1):
+            e = sum(a ** t for t in range(g + 1))
+            v = e / float(g * (j if cost_skipped else Wt - j) + Wt)
+            if v > top[0] or (keep_last and v == top[0]):
+                top = (v, j, g, skip)
+    return top[1], top[2], top[0], top[3]
+
+
 # ------------------------------------------------------------------ pins
 @pytest.fixture(scope="module")
 def tiny():
@@ -352,6 +373,7 @@ def _mutants(tiny, tiny_hist):
                  lambda: TM.test_prefill_rows_equal_incremental_decode(tiny)]
     sampling_pins = [TS.test_acceptance_rule_preserves_target_exactly,
                      TS.test_verify_chain_monte_carlo]
+    additive_pins = [TA.test_stage2_no_skip_when_values_tiny, TA.test_stage2_prefers_free_skips]
     round_pins = [lambda: TM.test_greedy_ssd_equals_greedy_ar(tiny, 0),
                   lambda: TM.test_history_blocks_are_contiguous_recent_positions(tiny)]
     dp_pins = [TSEL.test_dp_ties_go_to_execute_and_tau_is_strict,
@@ -422,13 +444,19 @@ def _mutants(tiny, tiny_hist):
          lambda *a, **k: _ssd_round(*a, extra_accept=True, **k), round_pins),
         ("greedy round: history keeps every verify row", M, "ssd_round",
          lambda *a, **k: _ssd_round(*a, keep_all_rows=True, **k), round_pins),
+        ("knapsack stage 2: alpha over the executed items", A, "stage2",
+         lambda *a, **k: _additive_stage2(*a, alpha_executed=True, **k), additive_pins),
+        ("knapsack stage 2: cost from the skipped weight", A, "stage2",
+         lambda *a, **k: _additive_stage2(*a, cost_skipped=True, **k), additive_pins),
+        ("knapsack stage 2: last of equal TPT values", A, "stage2",
+         lambda *a, **k: _additive_stage2(*a, keep_last=True, **k), additive_pins),
         ("generation: re-select only on multiples of T", GENM, "generate",
          generate_reselect_on_multiples,
          [TSEL.test_reselection_at_first_round_end_past_each_multiple]),
     ]
 
 
-N_MUTANTS = 35
+N_MUTANTS = 38
 
 
 def test_mutant_table_size(tiny, tiny_hist):
