@@ -149,9 +149,21 @@ typedef struct ks_gen_stats {
 
 typedef struct ks_ctx ks_ctx;
 
+/*
+ * ks_last_error: the message of the last call on this thread that returned an
+ * error (thread-local, library-owned; valid until the next failing call on the
+ * same thread).
+ */
 const char* ks_last_error(void);
 
 /* ---- sizing ------------------------------------------------------------- */
+/*
+ * ks_kv_cache_bytes: bytes of the KV cache ks_create expects,
+ * L * 2 * hkv * n_max * hd elements of the model dtype.  ks_workspace_bytes:
+ * bytes of its workspace (activations, split-attention and split-K partials,
+ * logits, verify stage, history ring, DP states, sampling tables).  Both
+ * return 0 for a description or limits that ks_create would reject.
+ */
 size_t ks_kv_cache_bytes(const ks_model_desc* desc);
 size_t ks_workspace_bytes(const ks_model_desc* desc, const ks_limits* lim);
 
@@ -197,6 +209,15 @@ ks_status ks_pack_gate_up(const void* gate, const void* up, void* dst, int ffn, 
 ks_status ks_create(const ks_model_desc* desc, const ks_limits* lim, const ks_weights* w,
                     void* kv_cache, size_t kv_bytes, void* workspace, size_t ws_bytes,
                     void* stream, ks_ctx** out);
+/*
+ * ks_destroy: releases what the library allocated for the context (its pinned
+ * host staging buffer and timing events); the caller's weights, cache and
+ * workspace are untouched.  No work a context call leaves queued uses what it
+ * releases (calls that read results back synchronise the stream first;
+ * ks_create's rotary-table fill writes the caller's workspace), so it may be
+ * called between any two calls; the caller keeps its buffers alive until the
+ * stream has finished with them.
+ */
 ks_status ks_destroy(ks_ctx* ctx);
 
 /*
