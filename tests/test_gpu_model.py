@@ -148,6 +148,28 @@ def test_call_order_and_bounds_errors(setup):
     assert e.value.status == K.KS_ECAPACITY
     with pytest.raises(K.KsError):
         dm.prefill(np.array([cfg.vocab], dtype=np.int32))
+    # the refused calls left the four drafts pending: the generation loop refuses
+    # to start from that state
+    from paper_2602_20217_amd.engine import select_params
+    c, mode, bins = LAT[name]
+    params = select_params(c, mode, bins)
+    with pytest.raises(K.KsError) as e:
+        dm.decode(8, 0)
+    assert e.value.status == K.KS_ESTATE
+    # a context set by hand has no history: speculative decoding is refused,
+    # AR decoding runs; speculative decoding needs params; capacity is checked
+    dm.set_context(30, s)
+    with pytest.raises(K.KsError) as e:
+        dm.decode(8, 4, 8, params)
+    assert e.value.status == K.KS_ESTATE
+    with pytest.raises(K.KsError) as e:
+        dm.decode(8, 4, 8, None)
+    assert e.value.status == K.KS_EINVAL
+    with pytest.raises(K.KsError) as e:
+        dm.decode(320 - 30, 0)
+    assert e.value.status == K.KS_ECAPACITY
+    out, _, _ = dm.decode(8, 0)
+    assert len(out) == 8 and all(0 <= int(t) < cfg.vocab for t in out)
 
 
 def test_selection_matches_oracle(setup):
