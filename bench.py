@@ -28,7 +28,7 @@ sys.path.insert(0, ROOT)
 # counter passes (FETCH_SIZE, WRITE_SIZE) scaled by a 256 MiB reference kernel
 # (profiles/decode_kernels_llama8b_ctx8k_counters.txt); valid only while the
 # product's source has the recorded digest
-GATE_UP_TRAFFIC = (235198445, "77e59681e9199fd513e4a871a9b9d58c3ff60c1f6566f57b80786136bf5c159a")
+GATE_UP_TRAFFIC = (235197422, "d6bcfbb4a68d1ffea4ca112ee196be5e8bcaa32fb606eaaff73b89a75e270279")
 
 
 def gate_up_traffic(cfg):

@@ -335,7 +335,7 @@ __global__ __launch_bounds__(64 * S) void k_attn_dec(
       const int row = min(t0 + rr, n_max - 1);
       __builtin_amdgcn_global_load_lds(
           (const void*)(kb + (size_t)row * HD + ((slot ^ (rr & 15)) << 3)),
-          (__attribute__((address_space(3))) void*)&Ks[w][i * 64], 16, 0, 0);
+          (__attribute__((address_space(3))) void*)&Ks[w][i * 64], 16, 0, 2);
     }
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
@@ -343,7 +343,7 @@ __global__ __launch_bounds__(64 * S) void k_attn_dec(
       const int row = min(t0 + rr, n_max - 1);
       __builtin_amdgcn_global_load_lds(
           (const void*)(vb + (size_t)row * HD + ((slot ^ (rr & 15)) << 3)),
-          (__attribute__((address_space(3))) void*)&Vs[w][i * 64], 16, 0, 0);
+          (__attribute__((address_space(3))) void*)&Vs[w][i * 64], 16, 0, 2);
     }
   }
   int Lmax = 0;  // longest row of the workgroup

@@ -29,6 +29,9 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 __device__ inline bf16x8 ld_frag(const bf16_t* p) {
   return __builtin_bit_cast(bf16x8, *(const u32x4*)p);
 }
+__device__ inline bf16x8 ld_frag_nt(const bf16_t* p) {
+  return __builtin_bit_cast(bf16x8, __builtin_nontemporal_load((const u32x4*)p));
+}
 __device__ inline bf16x8 zero_frag() {
   u32x4 z = {0u, 0u, 0u, 0u};
   return __builtin_bit_cast(bf16x8, z);
@@ -120,7 +123,7 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_skinny(
     for (int u = 0; u < CH; ++u)
 #pragma unroll
       for (int t = 0; t < NB; ++t)
-        if (u < n) b[t][u] = ld_frag(wb[t] + (size_t)(kc + u) * 512);
+        if (u < n) b[t][u] = ld_frag_nt(wb[t] + (size_t)(kc + u) * 512);
 #pragma unroll
     for (int u = 0; u < CH; ++u) {
       if (u < n) {
