@@ -325,6 +325,8 @@ __global__ __launch_bounds__(64 * S) void k_attn_dec(
   }
   // piece i (1 KiB): rows 4 i .. + 3 of the tile; lane l writes chunk slot
   // l % 16 of row 4 i + l / 16
+  // (cache-policy operand 2 = nt: the cache is streamed once per step, so its
+  // lines are not kept in L2 ahead of the query, sums and partials)
   {
     const bf16_t* kb = kc + (size_t)kvh * n_max * HD;
     const bf16_t* vb = vc + (size_t)kvh * n_max * HD;
