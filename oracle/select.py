@@ -22,11 +22,16 @@ which context a candidate row sees).
 
 Parity pins: cos against closed forms; Eq. expected_tokens; TPT of the full
 model equal to 1/C for every gamma; TPT ordering equal to TPL's (Eq. TPL) when
-attention and MLP weigh the same; the DP's reachable cells equal the
-subset-sum-reachable budgets; each terminal state equals f^(S) recomputed from
-its backtracked mask; the DP never beats brute force at any budget; the j = 0
-cell is the full model.  Optimality of the model-mode DP itself is not
-claimed by the paper (it calls it near-optimal) and is not pinned.
+attention and MLP weigh the same; Algorithm 2 on a hand-built stage-1 result
+(alpha-hat, the first strict maximum, the backtracked mask); the DP's reachable
+cells equal the subset-sum-reachable budgets; each terminal state equals f^(S)
+recomputed from its backtracked mask; the DP never beats brute force at any
+budget; the j = 0 cell is the full model; ties go to execute and tau is strict
+(identity decoder, equal targets); the higher of the two cosines is kept, on an
+identity decoder whose targets are unit vectors of one plane so that every
+decision and mask is fixed by hand.  The paper calls the model-mode DP
+near-optimal, not optimal; on the tiny decoder's seeded history it reaches the
+brute-force maximum at all 13 reachable budgets, which the pins assert.
 """
 from __future__ import annotations
 

@@ -212,7 +212,7 @@ def top_p_one_short(logits, prm, margins=None):
 
 
 def _dp(model, cache, pos, X, w_attn, w_mlp, C, tau=0.5, prune_half=True, *,
-        ties_execute=True, strict_tau=True, reset_zero=True):
+        ties_execute=True, strict_tau=True, reset_zero=True, keep_higher=True):
     """Stage 1 with one rule changed by the flags."""
     n_sub = model.n_sub
     J = C // 2 if prune_half else C
@@ -239,7 +239,12 @@ def _dp(model, cache, pos, X, w_attn, w_mlp, C, tau=0.5, prune_half=True, *,
         for j in range(J + 1):
             e_ok = reach[j] and valid(sig_e[i, j])
             s_ok = j >= w and reach[j - w] and valid(sig_s[i, j])
-            prefer_e = (sig_e[i, j] >= sig_s[i, j]) if ties_execute else (sig_e[i, j] > sig_s[i, j])
+            if not keep_higher:
+                prefer_e = sig_e[i, j] <= sig_s[i, j]
+            elif ties_execute:
+                prefer_e = sig_e[i, j] >= sig_s[i, j]
+            else:
+                prefer_e = sig_e[i, j] > sig_s[i, j]
             if e_ok and (not s_ok or prefer_e):
                 ng[j], nr[j] = E[j], True
             elif s_ok:
@@ -377,6 +382,7 @@ def _mutants(tiny, tiny_hist):
     round_pins = [lambda: TM.test_greedy_ssd_equals_greedy_ar(tiny, 0),
                   lambda: TM.test_history_blocks_are_contiguous_recent_positions(tiny)]
     dp_pins = [TSEL.test_dp_ties_go_to_execute_and_tau_is_strict,
+               TSEL.test_dp_keeps_the_higher_cosine,
                lambda: TSEL.test_dp_reachable_cells_are_subset_sums(tiny_hist),
                lambda: TSEL.test_dp_terminal_states_match_backtracked_masks(tiny_hist),
                lambda: TSEL.test_stage2_fallback_and_alpha(tiny_hist)]
@@ -434,6 +440,8 @@ def _mutants(tiny, tiny_hist):
          [TS.test_filter_top_p_keeps_shortest_sufficient_prefix]),
         ("model-mode DP: ties take the skip", SEL, "dp_select",
          lambda *a, **k: _dp(*a, ties_execute=False, **k), dp_pins),
+        ("model-mode DP: the lower cosine kept", SEL, "dp_select",
+         lambda *a, **k: _dp(*a, keep_higher=False, **k), dp_pins),
         ("model-mode DP: sigma >= tau", SEL, "dp_select",
          lambda *a, **k: _dp(*a, strict_tau=False, **k), dp_pins),
         ("model-mode DP: cell 0 not reset to X^(i)", SEL, "dp_select",
@@ -456,7 +464,7 @@ def _mutants(tiny, tiny_hist):
     ]
 
 
-N_MUTANTS = 38
+N_MUTANTS = 39
 
 
 def test_mutant_table_size(tiny, tiny_hist):

@@ -86,21 +86,53 @@ def test_tpt_reduces_to_tpl_when_latencies_equal():
         assert v == pytest.approx(tpl / 2, rel=1e-12)
 
 
+def _identity_head_model(L, d):
+    """A decoder whose LM head is the identity on d = vocab: with unit norm gains
+    the head's argmax of a row is the index of the row's largest entry."""
+    import dataclasses
+    cfg = dataclasses.replace(W.config("tiny"), L=L, d=d, vocab=d, hq=2, hkv=1, hd=8,
+                              ffn=16)
+    w = W.generate_weights(cfg, seed=0)
+    w[("lm_head", -1)] = np.eye(d, dtype=np.float32)
+    return M.Model(cfg, w)
+
+
 def test_stage2_grid_toy():
-    """Three candidates enumerated by hand (C = 10, D = 3):
+    """Algorithm 2 on a hand-built stage-1 result.  Two layers, w_A = 4, w_M = 1,
+    C = 10, J = 5, D = 3; reachable budgets 0, 4 (attention 1 skipped) and 5
+    (attention 1 and MLP 1 skipped).  Ten history rows with head argmaxes
+    0..9; the j = 4 state agrees on 9 rows, the j = 5 state on 5.  By hand:
     j=0 alpha=1: TPT = 1/10 for all gamma.
     j=4 alpha=0.9, executed 6: gamma=1 1.9/16=.11875, gamma=2 2.71/22=.123181..,
         gamma=3 3.439/28=.122821..
     j=5 alpha=0.5, executed 5: gamma=1 1.5/15=.1, 2 1.75/20, 3 1.875/25.
-    The maximum is (j=4, gamma=2)."""
-    best = (0, None)
-    for j, a in ((0, 1.0), (4, 0.9), (5, 0.5)):
-        for g in (1, 2, 3):
-            v = SEL.tpt(a, g, 10 - j, 10)
-            if v > best[0]:
-                best = (v, (j, g))
-    assert best[1] == (4, 2)
-    assert best[0] == pytest.approx(2.71 / 22, rel=1e-14)
+    The maximum is (j=4, gamma=2), and the returned mask skips sublayer 1 only."""
+    d, r = 16, 10
+    model = _identity_head_model(2, d)
+    X_last = np.zeros((r, d))
+    X_last[np.arange(r), np.arange(r)] = 1.0
+    s4, s5 = X_last.copy(), X_last.copy()
+    s4[0] = np.eye(d)[12]                      # one row disagrees
+    for k in range(5):
+        s5[k] = np.eye(d)[10 + k]              # five rows disagree
+    J = 5
+    bits = np.zeros((5, J + 1), dtype=np.uint8)
+    bits[1, 4] = 1                             # budget 4: attention 1 skipped
+    bits[2, 5] = 1                             # budget 5: MLP 1 skipped, then budget 4
+    reach = np.array([True, False, False, False, True, True])
+    dp = SEL.DPResult(J, reach, [X_last, None, None, None, s4, s5], bits,
+                      np.zeros((5, J + 1), dtype=bool), np.zeros((5, J + 1)),
+                      np.zeros((5, J + 1)))
+    sel = SEL.stage2(model, dp, X_last, 4, 1, 10, D=3)
+    assert sel.alphas == {0: 1.0, 4: 0.9, 5: 0.5}
+    assert (sel.j_star, sel.gamma_star) == (4, 2)
+    assert sel.tpt_star == pytest.approx(2.71 / 22, rel=1e-14)
+    assert sel.alpha_hat == 0.9
+    np.testing.assert_array_equal(sel.exec_mask, [False, True, True, True])
+    # the same grid with D = 1 only offers gamma = 1: j = 4 still wins (1.9/16)
+    sel1 = SEL.stage2(model, dp, X_last, 4, 1, 10, D=1)
+    assert (sel1.j_star, sel1.gamma_star) == (4, 1)
+    assert sel1.tpt_star == pytest.approx(1.9 / 16, rel=1e-14)
 
 
 @pytest.fixture(scope="module")
@@ -145,7 +177,13 @@ def test_dp_terminal_states_match_backtracked_masks(tiny_hist):
         n_opt += abs(c - brute[j][0]) < 1e-12
     n_reach = int(np.sum(dp.reach))
     print(f"[dp] optimal at {n_opt} of {n_reach} reachable budgets (brute force over 256 masks)")
-    assert n_opt >= 1
+    # The paper calls the DP near-optimal, not optimal; on this seeded history it
+    # reaches the brute-force maximum at every reachable budget (a DP that keeps
+    # the lower of the two cosines reaches it at 2 of the 13).  A budget counts as
+    # reached when the cosine is within 1e-12 of the maximum, so masks that tie
+    # with the best one do not depend on summation order.
+    assert n_reach == 13
+    assert n_opt == n_reach
 
 
 def test_dp_ties_go_to_execute_and_tau_is_strict():
@@ -173,6 +211,55 @@ def test_dp_ties_go_to_execute_and_tau_is_strict():
     c = SEL.cos_matrix(X0, X0)
     dp = SEL.dp_select(model, cache, pos, X, 1, 1, 8, tau=c, prune_half=False)
     assert np.flatnonzero(dp.reach).tolist() == [0]
+
+
+def test_dp_keeps_the_higher_cosine():
+    """Eq. dp_main keeps, of the two candidates at a budget, the one whose cosine
+    with X^(i) is higher.  Every sublayer of this decoder is an identity (zero
+    output projections), so a candidate is the state it is built from, and every
+    state the DP can hold is one of the targets X^(k) (cell 0 is reset to X^(i)
+    after each sublayer).  The targets are unit vectors of one plane at angles
+    0, 10, 60, 20 and 50 degrees, so the cosine of two of them is the cosine of
+    their angle difference and each decision is fixed by hand (unit weights,
+    tau off, no prune, E = execute candidate g[i-1, j], S = skip candidate
+    g[i-1, j-1]):
+      i=1: g[1,1] = S = X0.
+      i=2 (target 60): j=1 E = X0 (60 apart), S = X1 (50) -> skip, X1;
+           j=2 S = X0 -> X0.
+      i=3 (target 20): j=1 E = X1 (10), S = X2 (40) -> execute, X1;
+           j=2 E = X0 (20), S = X1 (10) -> skip, X1; j=3 S = X0.
+      i=4 (target 50): j=1 E = X1 (40), S = X3 (30) -> skip, X3;
+           j=2 E = X1, S = X1 (a tie) -> execute, X1;
+           j=3 E = X0 (50), S = X1 (40) -> skip, X1; j=4 S = X0.
+    Backtracked exec masks: j=1 (1,1,1,0), j=2 (1,0,0,1), j=3 (1,0,0,0),
+    j=4 (0,0,0,0); terminal states X3, X1, X1, X0."""
+    import dataclasses
+    cfg = dataclasses.replace(W.config("tiny"), L=2)
+    w = W.generate_weights(cfg, seed=0)
+    for l in range(cfg.L):
+        w[("wo", l)] = np.zeros_like(w[("wo", l)])
+        w[("w_down", l)] = np.zeros_like(w[("w_down", l)])
+    model = M.Model(cfg, w)
+    ang = np.radians([0.0, 10.0, 60.0, 20.0, 50.0])
+    X = []
+    for a in ang:
+        v = np.zeros((3, cfg.d))
+        v[:, 0], v[:, 1] = np.cos(a), np.sin(a)
+        X.append(v)
+    pos = np.arange(20, 23)
+    cache = M.KVCache(cfg, 32)
+    dp = SEL.dp_select(model, cache, pos, X, 1, 1, 4, tau=-math.inf, prune_half=False)
+    assert dp.reach.all()
+    want_bits = {(2, 1): 1, (2, 2): 1, (3, 1): 0, (3, 2): 1, (3, 3): 1,
+                 (4, 1): 1, (4, 2): 0, (4, 3): 1, (4, 4): 1}
+    for (i, j), b in want_bits.items():
+        assert dp.bits[i, j] == b, (i, j)
+    masks = {1: [1, 1, 1, 0], 2: [1, 0, 0, 1], 3: [1, 0, 0, 0], 4: [0, 0, 0, 0]}
+    finals = {1: 3, 2: 1, 3: 1, 4: 0}
+    for j in range(1, 5):
+        np.testing.assert_array_equal(SEL.backtrack(dp.bits, j, 1, 1),
+                                      np.array(masks[j], dtype=bool))
+        np.testing.assert_array_equal(dp.states[j], X[finals[j]])
 
 
 def test_stage2_fallback_and_alpha(tiny_hist):
