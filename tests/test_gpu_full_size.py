@@ -21,7 +21,8 @@ import pytest
 
 import workloads as W
 from oracle import model as M
-from tests.gpu_helpers import rel_err, margin, one_layer_model, fill_layer, check_sublayers
+from tests.gpu_helpers import (rel_err, margin, one_layer_model, fill_layer, check_sublayers,
+                               check_rows, update_err)
 
 pytestmark = pytest.mark.gpu
 torch = pytest.importorskip("torch")
@@ -87,10 +88,10 @@ def test_full_size_batched_sublayers(full, R):
         dm.sublayer_apply(2 * layer + sub, xin, pos, mode=1, out=out)
         got = out.cpu().numpy()
         ref = M.sublayer(model, sub, x[sample].astype(np.float64), pos[sample], cache, mode="own")
-        e = rel_err(got[sample], ref)
-        print(f"[batched] layer {layer} sublayer {sub} R {R}: rel err {e:.2e} on rows {sample}",
-              flush=True)
-        assert e < TOL, (sub, R, e)
+        e, eu = rel_err(got[sample], ref), update_err(got[sample], x[sample], ref)
+        print(f"[batched] layer {layer} sublayer {sub} R {R}: rel err {e:.2e}, update {eu:.2e}"
+              f" on rows {sample}", flush=True)
+        check_rows(got[sample], x[sample], ref, TOL, (sub, R))
         x, xin = got, out
 
 

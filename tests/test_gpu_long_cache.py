@@ -11,7 +11,7 @@ import pytest
 
 import workloads as W
 from oracle import model as M
-from tests.gpu_helpers import build, rel_err
+from tests.gpu_helpers import build, rel_err, check_rows
 
 pytestmark = pytest.mark.gpu
 torch = pytest.importorskip("torch")
@@ -64,10 +64,11 @@ def test_long_cache_rows(setup, R, back):
     for i in range(1, 2 * cfg.L + 1):
         out = torch.empty_like(xd)
         dm.sublayer_apply(i, xd, pos, mode=0, out=out)
+        x_in = xd.cpu().numpy()
         xo = M.sublayer(model, i, xo, pos, cache, mode="write")
         got = out.cpu().numpy()
         assert np.all(np.isfinite(got)), i
-        assert rel_err(got, xo) < TOL, (i, rel_err(got, xo))
+        check_rows(got, x_in, xo, TOL, (n_max, back, R, i))
         xd = out
         xo = got.astype(np.float64)
     logits, am, top1 = dm.head_rows(xd)

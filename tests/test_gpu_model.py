@@ -1,6 +1,7 @@
 """GPU vs oracle parity of the decode step on oracle-sized models: the tiny fp32
 decoder (relative tolerance 1e-4) and small bf16 decoders with the 8B head
-geometry, one with Qwen3 q/k norms (relative tolerance 2e-2).  Every call goes
+geometry, one with Qwen3 q/k norms and one with eight layers (relative
+tolerance 2e-2).  Every call goes
 through the C ABI."""
 import numpy as np
 import pytest
@@ -9,16 +10,17 @@ import workloads as W
 from oracle import model as M
 from oracle import select as SEL
 from oracle import generate as GEN
-from tests.gpu_helpers import build, rel_err, margin
+from tests.gpu_helpers import build, rel_err, margin, check_rows
 
 pytestmark = pytest.mark.gpu
 torch = pytest.importorskip("torch")
 
-TOL = {"tiny": 1e-4, "small_bf16": 2e-2, "small_qwen_bf16": 2e-2}
+TOL = {"tiny": 1e-4, "small_bf16": 2e-2, "small_qwen_bf16": 2e-2, "deep_bf16": 2e-2}
 # latency models: tiny uses the explicit coefficients with 64 bins; the small
-# models use 32 bins
+# models use 32 bins, the eight-layer one 64
 LAT = {"tiny": (W.TINY_LATENCY, "bins", 64), "small_bf16": ((1.0, 0.004, 0.3), "bins", 32),
-       "small_qwen_bf16": ((1.0, 0.004, 0.3), "bins", 32)}
+       "small_qwen_bf16": ((1.0, 0.004, 0.3), "bins", 32),
+       "deep_bf16": ((1.0, 0.004, 0.3), "bins", 64)}
 NAMES = list(TOL)
 
 
@@ -71,9 +73,10 @@ def test_sublayers_and_head(setup, R, mode):
     for i in range(1, 2 * cfg.L + 1):
         out = torch.empty_like(xd)
         dm.sublayer_apply(i, xd, pos, mode=mode, out=out)
+        x_in = xd.cpu().numpy()
         xo = M.sublayer(model, i, xo, pos, st.cache, mode="write" if mode == 0 else "own")
         got = out.cpu().numpy()
-        assert rel_err(got, xo) < TOL[name], (i, rel_err(got, xo))
+        check_rows(got, x_in, xo, TOL[name], (name, R, mode, i))
         # continue from the GPU's rows so each sublayer is checked on its own
         xd = out
         xo = got.astype(np.float64)
@@ -98,7 +101,7 @@ def test_position_zero_own_row(setup):
     out = torch.empty(2, cfg.d, device="cuda")
     dm.sublayer_apply(1, torch.from_numpy(x).cuda(), pos, mode=1, out=out)
     ref = M.sublayer(model, 1, x.astype(np.float64), pos, st.cache, mode="own")
-    assert rel_err(out.cpu().numpy(), ref) < TOL[name]
+    check_rows(out.cpu().numpy(), x, ref, TOL[name], (name, "position 0"))
 
 
 def test_draft_verify_and_empty_mask(setup):
@@ -172,6 +175,58 @@ def test_call_order_and_bounds_errors(setup):
     assert len(out) == 8 and all(0 <= int(t) < cfg.vocab for t in out)
 
 
+def _dp_comparison(dp, dbg, J, w_attn, w_mlp, tol_sig):
+    """Cell by cell comparison of the device's stage 1 with the oracle's.
+
+    A decision is compared when both sides built its candidates from the same
+    states: none of the cells it reads was decided differently upstream.  A
+    decision whose cosines are within tol_sig of each other or of tau = 0.5 may
+    differ (floating-point order decides it); if it does, every cell that reads
+    it is left out.  Returns (decisions compared, decisions in total, decisions
+    not downstream of any near tie of the oracle)."""
+    n_sub = dp.bits.shape[0] - 1
+    taint = np.zeros((n_sub + 1, J + 1), dtype=bool)
+    quiet = np.zeros((n_sub + 1, J + 1), dtype=bool)
+    n_cmp = n_tot = n_floor = 0
+    for i in range(1, n_sub + 1):
+        w = w_attn if i % 2 == 1 else w_mlp
+        for j in range(J + 1):
+            e0, s0 = dp.sig_e[i, j], dp.sig_s[i, j]
+            e1, s1 = dbg["sig_e"][i, j], dbg["sig_s"][i, j]
+            has_e, has_s = not np.isnan(e0), not np.isnan(s0)
+            bad_in = (has_e and taint[i - 1, j]) or (has_s and taint[i - 1, j - w])
+            near_in = (has_e and quiet[i - 1, j]) or (has_s and quiet[i - 1, j - w])
+            near = (has_e and has_s and abs(e0 - s0) <= tol_sig) or \
+                   (has_e and abs(e0 - 0.5) <= tol_sig) or (has_s and abs(s0 - 0.5) <= tol_sig)
+            if j > 0 and (near or near_in):
+                quiet[i, j] = True
+            if bad_in:
+                taint[i, j] = j > 0
+            if not (has_e or has_s):
+                if not bad_in:
+                    assert np.isnan(e1) and np.isnan(s1), (i, j)
+                continue
+            n_tot += 1
+            n_floor += not (near or near_in)
+            if bad_in:
+                continue
+            # same candidate states on both sides
+            assert np.isnan(e1) == (not has_e) and np.isnan(s1) == (not has_s), (i, j)
+            if has_e:
+                assert abs(e0 - e1) < tol_sig, (i, j, e0, e1)
+            if has_s:
+                assert abs(s0 - s1) < tol_sig, (i, j, s0, s1)
+            same = dbg["bits"][i, j] == dp.bits[i, j] and \
+                bool(dbg["reach"][i, j]) == bool(dp.reach_rows[i, j])
+            if not near:
+                assert same, (i, j)
+            if same:
+                n_cmp += 1
+            elif j > 0:
+                taint[i, j] = True
+    return n_cmp, n_tot, n_floor, bool(taint[n_sub].any())
+
+
 def test_selection_matches_oracle(setup):
     name, cfg, dm, model = setup
     c, mode, bins = LAT[name]
@@ -186,27 +241,14 @@ def test_selection_matches_oracle(setup):
     assert (sel.w_attn, sel.w_mlp, sel.C) == (wts.w_attn, wts.w_mlp, wts.C)
     ref, dp = SEL.select(model, st, wts.w_attn, wts.w_mlp, wts.C)
     tol_sig = 1e-5 if cfg.dtype == "f32" else 2e-3
-    pinned = True
-    for i in range(1, 2 * cfg.L + 1):
-        for j in range(J + 1):
-            e0, s0 = dp.sig_e[i, j], dp.sig_s[i, j]
-            e1, s1 = dbg["sig_e"][i, j], dbg["sig_s"][i, j]
-            assert np.isnan(e0) == np.isnan(e1) and np.isnan(s0) == np.isnan(s1), (i, j)
-            if not np.isnan(e0):
-                assert abs(e0 - e1) < tol_sig, (i, j, e0, e1)
-            if not np.isnan(s0):
-                assert abs(s0 - s1) < tol_sig, (i, j, s0, s1)
-            near = (not np.isnan(e0) and not np.isnan(s0) and abs(e0 - s0) <= tol_sig) or \
-                   (not np.isnan(e0) and abs(e0 - 0.5) <= tol_sig) or \
-                   (not np.isnan(s0) and abs(s0 - 0.5) <= tol_sig)
-            if near:
-                pinned = False
-            elif pinned:
-                assert dbg["bits"][i, j] == dp.bits[i, j], (i, j)
-                assert bool(dbg["reach"][i, j]) == bool(dp.reach_rows[i, j]), (i, j)
-        if not pinned:
-            break
-    if pinned:
+    n_cmp, n_tot, n_floor, tainted = _dp_comparison(dp, dbg, J, wts.w_attn, wts.w_mlp, tol_sig)
+    print(f"[select {name}] C {wts.C}: {n_cmp} of {n_tot} decisions compared "
+          f"({n_floor} clear of every near tie of the oracle)", flush=True)
+    # decisions clear of every near tie are always compared
+    assert n_cmp >= n_floor
+    assert n_floor >= {"tiny": 68, "small_bf16": 12, "small_qwen_bf16": 10,
+                       "deep_bf16": 74}[name]
+    if not tainted:
         np.testing.assert_array_equal(np.array(sel.exec[:2 * cfg.L], dtype=bool), ref.exec_mask)
         assert sel.j_star == ref.j_star
         assert sel.n_cells == int(dp.reach.sum())

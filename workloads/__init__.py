@@ -79,6 +79,11 @@ CONFIGS = {
     "small_qwen_bf16": ModelConfig("small_qwen_bf16", L=2, d=1024, hq=8, hkv=2, hd=128,
                                    ffn=2048, vocab=4096, eps=1e-6, rope_theta=1e6,
                                    qk_norm=True, dtype="bf16"),
+    # The same geometry with eight layers (16 sublayers): enough DP stages and
+    # reachable budgets for the selection parity of the bf16 kernels.
+    "deep_bf16": ModelConfig("deep_bf16", L=8, d=1024, hq=8, hkv=2, hd=128, ffn=2816,
+                             vocab=4096, eps=1e-6, rope_theta=5e5, qk_norm=False,
+                             dtype="bf16"),
 }
 
 # Explicit latency coefficients (c1, c2, c3) for the tiny model: t_MLP = c1,
