@@ -1,17 +1,22 @@
 // libknapspec engine: context, workspace layout, the forward passes of the
 // self-speculative decode step, the knapsack selection and the C ABI.
 //
-//  decode / draft (1 row) and verify (gamma+1 rows): skinny MFMA products,
-//      128-position attention splits; identical per-row arithmetic, so greedy
-//      speculative output equals greedy AR output bit for bit.
-//  prefill (chunks) and selection DP (cells x history rows): tiled MFMA
-//      products, 1024-position attention splits.
-//  selection (Sections 3.3-3.5): the DP runs on the GPU one sublayer at a
-//      time over the reachable budgets only; per-cell cosines come back to the
-//      host, which applies Eq. dp_main with the tau / C/2 pruning, records the
-//      decision bits and launches one gather of the surviving states.  Stage 2
-//      (backtrack, alpha-hat, TPT grid) runs on the host from the bits and the
-//      GPU's argmax rows.
+//  decode / draft (1 row) and verify (gamma+1 rows): skinny MFMA products
+//      (norm carried in, RoPE + K/V stores, SwiGLU and residual epilogues) and
+//      decode attention over context splits whose size depends only on the
+//      cache size, so a verify row and the decode step at the same position
+//      compute the same bits and greedy speculative output equals greedy AR
+//      output.
+//  prefill (512-row chunks) and selection DP (budgets x history rows): tiled
+//      MFMA products with split-K, batched attention.
+//  selection (Sections 3.3-3.5): stage 1 runs on the device one sublayer at a
+//      time over the reachable budgets; per-row cosines (float64) of both
+//      candidates, the decisions of Eq. dp_main with the tau and C/2 pruning,
+//      the decision bits and the compacted list of reachable budgets are all
+//      produced by kernels, with no host round trip between stages.  Stage 2
+//      (argmax rows of the terminal states on the device; alpha-hat, the TPT
+//      grid and the backtrack from the decision bits on the host) follows one
+//      synchronisation.
 #include "ks_internal.h"
 
 #include <algorithm>

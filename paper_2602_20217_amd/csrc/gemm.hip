@@ -14,9 +14,12 @@
 // result does not depend on how many rows are in the batch: a verify row and
 // the decode step at the same position produce identical bits.
 //
-// Tiled path (batched rows of the selection DP and of prefill): 128 x 128
-// workgroup tiles staged through LDS, 64 x 64 wave tiles of 16x16x32 MFMAs over
-// single bf16 activations.
+// Tiled path (batched rows of the selection DP and of prefill): 128 x 256
+// workgroup tiles of eight 64 x 64 wave tiles of 16x16x32 MFMAs over single
+// bf16 activations, operands staged through a three-stage LDS ring by direct
+// global-to-LDS loads; K is split over workgroups when the row count leaves
+// CUs idle (factor from a cost model of resident rounds and partial traffic),
+// and the float32 partials are summed in split order.
 #include "ks_internal.h"
 
 #include <algorithm>
