@@ -484,7 +484,9 @@ ks_status ks_knapsack_quantize(const double* t, const double* s, int B, int n, i
  * best_{i-1}[j - w_i] + q_i < best_{i-1}[j] (strict; ties keep the item).
  * bits[b][i][j/64] bit j%64 records that decision (uint64 words, C/64 + 1 per
  * item).  Requires C <= 8191, n <= 4096, w and q >= 0 (negative entries are
- * read as 0) and total loss < 2^31.  Asynchronous.
+ * read as 0, by every ks_knapsack_* call) and total loss < 2^31.  Only the
+ * budgets 0..min(C, max_skip) are swept; the cells above them read INT32_MAX
+ * and their decision words 0.  Asynchronous.
  */
 ks_status ks_knapsack_batch(const int32_t* w, const int32_t* q, int B, int n, int C,
                             int max_skip, int32_t* best, uint64_t* bits, void* stream);
@@ -492,7 +494,8 @@ ks_status ks_knapsack_batch(const int32_t* w, const int32_t* q, int B, int n, in
  * ks_knapsack_backtrack: skip[b][i] (device uint8 [B][n]) of budget j[b]
  * (device int32 [B]) from the decision bits, following items n-1 down to 0.
  * Writes err[b] = 0, or 1 if the walk does not end at budget 0 or j[b] is out
- * of range (device int32 [B]).  Asynchronous.
+ * of range (device int32 [B]).  Negative weights are read as 0, as by
+ * ks_knapsack_batch.  Asynchronous.
  */
 ks_status ks_knapsack_backtrack(const uint64_t* bits, const int32_t* w, int B, int n, int C,
                                 const int32_t* j, uint8_t* skip, int32_t* err, void* stream);
@@ -502,7 +505,8 @@ ks_status ks_knapsack_backtrack(const uint64_t* bits, const int32_t* w, int B, i
  * every reachable budget j and gamma = 1..D, TPT = (sum_{k<=gamma} alpha^k) /
  * (gamma (W - j) + W) with W = sum_i w_i; j ascending, gamma ascending, first
  * strict maximum wins.  Outputs j_star, gamma_star (int32 [B]), tpt (double
- * [B]) and skip (uint8 [B][n]); s is device double [B][n].  Asynchronous.
+ * [B]) and skip (uint8 [B][n]); s is device double [B][n].  Negative weights
+ * are read as 0 (also in W), as by ks_knapsack_batch.  Asynchronous.
  */
 ks_status ks_knapsack_batch_select(const int32_t* best, const uint64_t* bits, const int32_t* w,
                                    const double* s, int B, int n, int C, int D,

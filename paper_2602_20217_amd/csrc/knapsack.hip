@@ -3,7 +3,8 @@
 //
 // One 256-thread workgroup per instance.  Thread t keeps budgets t + 256 e
 // (e < E) of the current row best_{i-1} in registers and mirrors them into
-// one of two LDS rows; for item i every budget j is updated in parallel from
+// one of two LDS rows; E covers only the budgets a skip set can reach
+// (0..min(C, max_skip)), the rest of the row stays INF without being swept; for item i every budget j is updated in parallel from
 // its own best_{i-1}[j] (keep) and best_{i-1}[j - w_i] + q_i (skip, strict),
 // the latter read from LDS, so a cell update costs one LDS read and one LDS
 // write.  A wave owns 64 consecutive budgets per slot e, so its 64 skip
@@ -60,6 +61,8 @@ __global__ __launch_bounds__(256) void k_knap_dp(const int32_t* __restrict__ w,
   int jv[E];
 #pragma unroll
   for (int e = 0; e < E; ++e) jv[e] = e * 256 + t <= jmax ? e * 256 + t : -1;
+  // decision words past the swept slots (budgets above min(C, max_skip)) are 0
+  const int swept_words = 4 * E < words ? 4 * E : words;
   auto item = [&](int i, const int32_t* src_row, int32_t* dst_row) {
     const int wi = max(wb[i], 0);                 // negative weights are read as 0
     const uint32_t qi = (uint32_t)max(qb[i], 0);  // so are negative losses
@@ -78,6 +81,7 @@ __global__ __launch_bounds__(256) void k_knap_dp(const int32_t* __restrict__ w,
     const int word = 4 * lane + wave;  // lane e stores word 4 e + wave
     if (lane < E && word < words)
       bits[((size_t)b * n + i) * words + word] = ((uint64_t)whi << 32) | wlo;
+    for (int k = swept_words + t; k < words; k += 256) bits[((size_t)b * n + i) * words + k] = 0;
     __syncthreads();
   };
   int i = 0;
@@ -92,6 +96,7 @@ __global__ __launch_bounds__(256) void k_knap_dp(const int32_t* __restrict__ w,
     const int j = e * 256 + t;
     if (j < cells) best[(size_t)b * cells + j] = v[e];
   }
+  for (int j = 256 * E + t; j < cells; j += 256) best[(size_t)b * cells + j] = KINF;
 }
 
 template <int E>
@@ -101,15 +106,30 @@ static void launch_knap_dp(const int32_t* w, const int32_t* q, int B, int n, int
   hipLaunchKernelGGL(k_knap_dp<E>, dim3(B), dim3(256), lds, st, w, q, n, C, max_skip, best, bits);
 }
 
+static int knapsack_dp_slots(int C, int max_skip) {
+  // slots per thread: 256 E budgets cover the reachable budgets 0..min(C, max_skip)
+  const int need = (max_skip < C ? max_skip : C) + 1;
+  for (int e : {1, 2, 3, 4, 5, 6, 8, 9, 12, 17, 24})
+    if (need <= 256 * e) return e;
+  return 32;  // C <= 8191
+}
+
 void knapsack_dp(const int32_t* w, const int32_t* q, int B, int n, int C, int max_skip,
                  int32_t* best, uint64_t* bits, hipStream_t st) {
-  // slots per thread: 256 E budgets cover the C / 64 + 1 decision words
-  const int need = (C / 64 + 1) * 64;
-  if (need <= 256 * 2) launch_knap_dp<2>(w, q, B, n, C, max_skip, best, bits, st);
-  else if (need <= 256 * 4) launch_knap_dp<4>(w, q, B, n, C, max_skip, best, bits, st);
-  else if (need <= 256 * 8) launch_knap_dp<8>(w, q, B, n, C, max_skip, best, bits, st);
-  else if (need <= 256 * 17) launch_knap_dp<17>(w, q, B, n, C, max_skip, best, bits, st);
-  else launch_knap_dp<32>(w, q, B, n, C, max_skip, best, bits, st);  // C <= 8191
+  switch (knapsack_dp_slots(C, max_skip)) {
+    case 1: launch_knap_dp<1>(w, q, B, n, C, max_skip, best, bits, st); break;
+    case 2: launch_knap_dp<2>(w, q, B, n, C, max_skip, best, bits, st); break;
+    case 3: launch_knap_dp<3>(w, q, B, n, C, max_skip, best, bits, st); break;
+    case 4: launch_knap_dp<4>(w, q, B, n, C, max_skip, best, bits, st); break;
+    case 5: launch_knap_dp<5>(w, q, B, n, C, max_skip, best, bits, st); break;
+    case 6: launch_knap_dp<6>(w, q, B, n, C, max_skip, best, bits, st); break;
+    case 8: launch_knap_dp<8>(w, q, B, n, C, max_skip, best, bits, st); break;
+    case 9: launch_knap_dp<9>(w, q, B, n, C, max_skip, best, bits, st); break;
+    case 12: launch_knap_dp<12>(w, q, B, n, C, max_skip, best, bits, st); break;
+    case 17: launch_knap_dp<17>(w, q, B, n, C, max_skip, best, bits, st); break;
+    case 24: launch_knap_dp<24>(w, q, B, n, C, max_skip, best, bits, st); break;
+    default: launch_knap_dp<32>(w, q, B, n, C, max_skip, best, bits, st); break;
+  }
 }
 
 __device__ inline int get_bit(const uint64_t* row, int j) { return (int)((row[j >> 6] >> (j & 63)) & 1ull); }
@@ -126,7 +146,7 @@ __global__ void k_knap_backtrack(const uint64_t* __restrict__ bits, const int32_
     uint8_t sk = 0;
     if (!bad && get_bit(bits + ((size_t)b * n + i) * words, j)) {
       sk = 1;
-      j -= w[(size_t)b * n + i];
+      j -= max(w[(size_t)b * n + i], 0);  // negative weights are read as 0, as in the DP
       if (j < 0) bad = 1;
     }
     skip[(size_t)b * n + i] = sk;
@@ -166,7 +186,7 @@ __global__ __launch_bounds__(256) void k_knap_select(
   if (BITS_IN_LDS)
     for (int k = tid; k < n * words; k += 256) lbits[k] = gb[k];
   for (int i = tid; i < n; i += 256) {
-    sw[i] = w[(size_t)b * n + i];
+    sw[i] = max(w[(size_t)b * n + i], 0);  // negative weights are read as 0, as in the DP
     ss[i] = s[(size_t)b * n + i];
   }
   __syncthreads();

@@ -91,3 +91,50 @@ def test_backtrack_flags_bad_budget(E):
     j = torch.tensor([2, 7], dtype=torch.int32, device="cuda")
     sk, err = E.knapsack_backtrack(bits, wd, 8, j)
     assert err.cpu().tolist() == [0, 1]
+
+
+@pytest.mark.parametrize("C,max_skip", [(4096, 2048), (4096, 4096), (4096, 0), (1000, 255),
+                                        (1000, 256), (300, 2000), (8191, 6000)])
+def test_dead_budgets_and_slot_sizes(E, C, max_skip):
+    """The DP sweeps only the budgets a skip set can reach (0..min(C, max_skip));
+    every other cell must still read INF and every decision word above them 0,
+    for slot counts from one to 32 per thread."""
+    rng = np.random.default_rng(C + max_skip)
+    B, n = 8, 40
+    w = rng.integers(1, max(2, C // 12), size=(B, n)).astype(np.int32)
+    q = rng.integers(0, 1 << 20, size=(B, n)).astype(np.int32)
+    _, best, bits = _run(E, w, q, C, max_skip)
+    best0, bits0 = A.knapsack_dp(w, q, C, max_skip)
+    np.testing.assert_array_equal(best.cpu().numpy(), best0)
+    np.testing.assert_array_equal(bits.cpu().numpy().view(np.uint64), bits0)
+
+
+def test_negative_weights_and_losses_read_as_zero(E):
+    """Every knapsack call reads a negative weight or loss as 0: the DP, the
+    backtrack and stage 2 agree with the oracle run on the clamped inputs."""
+    rng = np.random.default_rng(11)
+    B, n, C, max_skip = 16, 24, 600, 300
+    w = rng.integers(1, 40, size=(B, n)).astype(np.int32)
+    q = rng.integers(0, 1 << 20, size=(B, n)).astype(np.int32)
+    w[rng.random((B, n)) < 0.15] *= -1
+    q[rng.random((B, n)) < 0.15] *= -1
+    s = rng.uniform(0.9, 1.0, size=(B, n))
+    wc, qc = np.maximum(w, 0), np.maximum(q, 0)
+    wd, best, bits = _run(E, w, q, C, max_skip)
+    best0, bits0 = A.knapsack_dp(wc, qc, C, max_skip)
+    np.testing.assert_array_equal(best.cpu().numpy(), best0)
+    np.testing.assert_array_equal(bits.cpu().numpy().view(np.uint64), bits0)
+    sd = torch.from_numpy(s).cuda()
+    js, gs, tpt, skip = E.knapsack_batch_select(best, bits, wd, sd, C, D=10)
+    js, gs, tpt, skip = js.cpu().numpy(), gs.cpu().numpy(), tpt.cpu().numpy(), skip.cpu().numpy()
+    for b in range(B):
+        j0, g0, v0, sk0 = A.stage2(best0[b], bits0[b], wc[b], s[b], D=10)
+        assert (js[b], gs[b]) == (j0, g0) and v0 == tpt[b], b
+        np.testing.assert_array_equal(skip[b], sk0)
+        reach = np.flatnonzero(best0[b] < A.INF)
+        jj = torch.from_numpy(reach.astype(np.int32)).cuda()
+        sk, err = E.knapsack_backtrack(bits[b:b + 1].expand(len(reach), -1, -1).contiguous(),
+                                       wd[b:b + 1].expand(len(reach), -1).contiguous(), C, jj)
+        assert not err.cpu().numpy().any()
+        for k, j in enumerate(reach):
+            np.testing.assert_array_equal(sk.cpu().numpy()[k], A.backtrack(bits0[b], wc[b], int(j)))
