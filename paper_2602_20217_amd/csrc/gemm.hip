@@ -53,15 +53,15 @@ __device__ inline void store_split(bf16_t* hi, bf16_t* lo, size_t off, float a) 
 // products read those planes like any activation and scale row m by
 // 1/sqrt(sum/K + eps) at the end; the 256 tile sums of a row are added by one
 // wave in a fixed order, whatever the row count.
-template <int NB, int NW, int CH, int EPI, int AN>
-__global__ __launch_bounds__(NW * 64) void k_gemm_skinny(
+template <int NB, int NW, int CH, int MINB, int EPI, int AN>
+__global__ __launch_bounds__(NW * 64, MINB) void k_gemm_skinny(
     int M, int N, int K, const bf16_t* __restrict__ Ahi, const bf16_t* __restrict__ Alo,
     int lda, const bf16_t* __restrict__ Wp, float* out, int ldo, const float* res, int ldres,
     bf16_t* ohi, bf16_t* olo, int ldact, const float* __restrict__ ssq_in, int nssq, float eps,
     const float* __restrict__ next_gain, bf16_t* nhi, bf16_t* nlo, int ldn, float* next_ssq,
     QkvEpi qe) {
   const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int KT = K >> 5;
   const int NT = N >> 4;
   const int nt0 = blockIdx.x * NB;
@@ -109,6 +109,8 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_skinny(
   f32x4 acc[NB];
 #pragma unroll
   for (int t = 0; t < NB; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+  // Lanes of rows past M read row 0: their products land in result rows that
+  // are never stored (an MFMA result row depends only on its own A row).
   const bf16_t* ah = Ahi + (size_t)(rok ? row : 0) * lda + kg * 8;
   const bf16_t* al = Alo + (size_t)(rok ? row : 0) * lda + kg * 8;
   const bf16_t* wb[NB];
@@ -117,30 +119,59 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_skinny(
     int nt = nt0 + t < NT ? nt0 + t : NT - 1;
     wb[t] = Wp + (size_t)nt * KT * 512 + lane * 8;
   }
-  // chunks of CH k-steps: every weight fragment of a chunk is requested before
-  // the first matrix instruction of the chunk
-  for (int kc = kb; kc < ke; kc += CH) {
-    const int n = ke - kc < CH ? ke - kc : CH;
-    bf16x8 b[NB][CH];
-#pragma unroll
-    for (int u = 0; u < CH; ++u)
-#pragma unroll
-      for (int t = 0; t < NB; ++t)
-        if (u < n) b[t][u] = ld_frag_nt(wb[t] + (size_t)(kc + u) * 512);
+  // The wave's k steps [kb, ke) run in full chunks of CH through two register
+  // stages: the weight and activation fragments of chunk c + 1 are requested
+  // before the matrix instructions of chunk c, so every wave keeps a chunk in
+  // flight while it computes (branch-free chunk code, so the compiler counts
+  // the loads in flight exactly); the last (ke - kb) % CH steps follow one by
+  // one.  The order of the matrix instructions (k ascending, hi then lo) is
+  // that of a plain loop.
+  bf16x8 w0[NB][CH], x00[CH], x01[CH];
+  bf16x8 w1[NB][CH], x10[CH], x11[CH];
+  auto fetch = [&](int kc, bf16x8 (&w)[NB][CH], bf16x8 (&x0)[CH], bf16x8 (&x1)[CH]) {
 #pragma unroll
     for (int u = 0; u < CH; ++u) {
-      if (u < n) {
-        bf16x8 a0 = zero_frag(), a1 = zero_frag();
-        if (rok) {
-          a0 = ld_frag(ah + (kc + u) * 32);
-          a1 = ld_frag(al + (kc + u) * 32);
-        }
 #pragma unroll
-        for (int t = 0; t < NB; ++t) {
-          acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, b[t][u], acc[t], 0, 0, 0);
-          acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, b[t][u], acc[t], 0, 0, 0);
-        }
+      for (int t = 0; t < NB; ++t) w[t][u] = ld_frag_nt(wb[t] + (size_t)(kc + u) * 512);
+      x0[u] = ld_frag(ah + (kc + u) * 32);
+      x1[u] = ld_frag(al + (kc + u) * 32);
+    }
+  };
+  auto compute = [&](bf16x8 (&w)[NB][CH], bf16x8 (&x0)[CH], bf16x8 (&x1)[CH]) {
+#pragma unroll
+    for (int u = 0; u < CH; ++u) {
+#pragma unroll
+      for (int t = 0; t < NB; ++t) {
+        acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(x0[u], w[t][u], acc[t], 0, 0, 0);
+        acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(x1[u], w[t][u], acc[t], 0, 0, 0);
       }
+    }
+  };
+  const int nfull = (ke - kb) / CH;  // wave-uniform
+  if (nfull > 0) fetch(kb, w0, x00, x01);
+  int c = 0;
+  for (; c + 2 < nfull; c += 2) {  // chunk c is in stage 0 and in flight
+    fetch(kb + (c + 1) * CH, w1, x10, x11);
+    compute(w0, x00, x01);
+    fetch(kb + (c + 2) * CH, w0, x00, x01);
+    compute(w1, x10, x11);
+  }
+  if (c + 1 < nfull) {
+    fetch(kb + (c + 1) * CH, w1, x10, x11);
+    compute(w0, x00, x01);
+    compute(w1, x10, x11);
+  } else if (c < nfull) {
+    compute(w0, x00, x01);
+  }
+  for (int k = kb + nfull * CH; k < ke; ++k) {
+    bf16x8 b[NB];
+#pragma unroll
+    for (int t = 0; t < NB; ++t) b[t] = ld_frag_nt(wb[t] + (size_t)k * 512);
+    const bf16x8 a0 = ld_frag(ah + k * 32), a1 = ld_frag(al + k * 32);
+#pragma unroll
+    for (int t = 0; t < NB; ++t) {
+      acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, b[t], acc[t], 0, 0, 0);
+      acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, b[t], acc[t], 0, 0, 0);
     }
   }
 
@@ -243,7 +274,7 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_skinny(
   }
 }
 
-template <int NB, int NW, int CH, int AN>
+template <int NB, int NW, int CH, int MINB, int AN>
 static void launch_skinny_an(const GemmArgs& g, hipStream_t st) {
   const int NT = g.N / 16;
   const bf16_t* Ahi = (const bf16_t*)g.A.hi;
@@ -251,7 +282,7 @@ static void launch_skinny_an(const GemmArgs& g, hipStream_t st) {
   const bf16_t* W = (const bf16_t*)g.W;
   dim3 grid((NT + NB - 1) / NB), block(NW * 64);
 #define KS_SKINNY(E, OH, OL, OLD)                                                            \
-  hipLaunchKernelGGL((k_gemm_skinny<NB, NW, CH, E, AN>), grid, block, 0, st, g.M, g.N, g.K,  \
+  hipLaunchKernelGGL((k_gemm_skinny<NB, NW, CH, MINB, E, AN>), grid, block, 0, st, g.M, g.N, g.K,  \
                      Ahi, Alo, g.A.ld, W, g.out, g.ldo, g.res, g.ldres, OH, OL, OLD,         \
                      g.ssq_in, g.nssq, g.eps, g.next_gain, (bf16_t*)g.next_act.hi,           \
                      (bf16_t*)g.next_act.lo, g.next_act.ld, g.next_ssq, g.qe)
@@ -259,17 +290,18 @@ static void launch_skinny_an(const GemmArgs& g, hipStream_t st) {
     KS_SKINNY(EPI_SWIGLU, (bf16_t*)g.act_out.hi, (bf16_t*)g.act_out.lo, g.act_out.ld);
   else if (g.epi == EPI_QKV)
     KS_SKINNY(EPI_QKV, nullptr, nullptr, 0);
-  else if (g.epi == EPI_RESID)
-    KS_SKINNY(EPI_RESID, nullptr, nullptr, 0);
+  else if (g.epi == EPI_RESID) {
+    if constexpr (NB == 1) KS_SKINNY(EPI_RESID, nullptr, nullptr, 0);
+  }
   else
     KS_SKINNY(EPI_STORE, nullptr, nullptr, 0);
 #undef KS_SKINNY
 }
 
-template <int NB, int NW, int CH>
+template <int NB, int NW, int CH, int MINB>
 static void launch_skinny(const GemmArgs& g, hipStream_t st) {
-  if (g.ssq_in) launch_skinny_an<NB, NW, CH, 1>(g, st);
-  else launch_skinny_an<NB, NW, CH, 0>(g, st);
+  if (g.ssq_in) launch_skinny_an<NB, NW, CH, MINB, 1>(g, st);
+  else launch_skinny_an<NB, NW, CH, MINB, 0>(g, st);
 }
 
 // Launch shape by matrix shape only (never by row count), measured on MI355X
@@ -278,12 +310,29 @@ static void launch_skinny(const GemmArgs& g, hipStream_t st) {
 // 4 waves are all resident at once, 7 per CU, so no second round trails); the
 // vocabulary head 8 waves, 4-deep; the long-K down projection a 16-way K split;
 // the remaining square-ish products 16 (N <= 4096) or 8 waves, 8-deep.
+// (output tiles per workgroup, waves, k steps per chunk, workgroups per CU
+// the register budget must allow)
+#ifndef KS_SK_GU
+#define KS_SK_GU 1, 4, 2, 1
+#endif
+#ifndef KS_SK_DOWN
+#define KS_SK_DOWN 1, 16, 4, 1
+#endif
+#ifndef KS_SK_HEAD
+#define KS_SK_HEAD 1, 8, 4, 1
+#endif
+#ifndef KS_SK_SQ
+#define KS_SK_SQ 1, 16, 4, 1
+#endif
+#ifndef KS_SK_WIDE
+#define KS_SK_WIDE 1, 8, 4, 1
+#endif
 void gemm_bf16_skinny(const GemmArgs& g, hipStream_t st) {
-  if (g.epi == EPI_SWIGLU) launch_skinny<1, 4, 4>(g, st);
-  else if (g.K >= 8192) launch_skinny<1, 16, 8>(g, st);
-  else if (g.N >= 65536) launch_skinny<1, 8, 4>(g, st);
-  else if (g.N <= 4096) launch_skinny<1, 16, 8>(g, st);
-  else launch_skinny<1, 8, 8>(g, st);
+  if (g.epi == EPI_SWIGLU) launch_skinny<KS_SK_GU>(g, st);
+  else if (g.K >= 8192) launch_skinny<KS_SK_DOWN>(g, st);
+  else if (g.N >= 65536) launch_skinny<KS_SK_HEAD>(g, st);
+  else if (g.N <= 4096) launch_skinny<KS_SK_SQ>(g, st);
+  else launch_skinny<KS_SK_WIDE>(g, st);
 }
 
 // ------------------------------------------------------------------- tiled
