@@ -279,7 +279,7 @@ template <int S, int CB>
 __global__ __launch_bounds__(64 * S) void k_attn_dec(
     int M, int hq, int hkv, int n_max, const float* __restrict__ q,
     const bf16_t* __restrict__ kc, const bf16_t* __restrict__ vc,
-    const int32_t* __restrict__ len, float* __restrict__ part, int nsplit) {
+    const int32_t* __restrict__ len, float* __restrict__ part, int nsplit, int span) {
   constexpr int HD = 128;
   constexpr int RS = HD + 4;  // LDS merge record per column: o, max, sum (bank-shifted)
   constexpr int NCOL = 16 * CB;
@@ -289,20 +289,17 @@ __global__ __launch_bounds__(64 * S) void k_attn_dec(
   __shared__ __align__(16) uint4 Vs[S][TILE * 16];
   // once every wave is past its tiles: wave w's key tile holds the records of
   // column block 0, its value tile those of block 1; wave 0's key tile also
-  // holds the merge scratch after its records: weights [NCOL][S], maxima,
-  // sums, lengths [NCOL]
-  float* s_w = (float*)&Ks[0][0] + 16 * RS;
-  float* s_mx = s_w + NCOL * S;
-  float* s_lx = s_mx + NCOL;
-  int* s_len = (int*)(s_lx + NCOL);
+  // holds the row length of every column after its records
+  int* s_len = (int*)((float*)&Ks[0][0] + 16 * RS);  // [NCOL] row length per column
   const int split = blockIdx.x, kvh = blockIdx.y;
   const int G = hq / hkv;
   const int RB = NCOL / G;
   const int r0 = blockIdx.z * RB;
   const int lane = threadIdx.x & 63;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int span = S * TILE;
+  // the split covers [start, send), span = S TILE positions
   const int start = split * span;
+  const int send = start + span;
   const int t0 = start + w * TILE;
   const int nc = min(NCOL, (M - r0) * G);  // query columns with a row
 
@@ -321,7 +318,10 @@ __global__ __launch_bounds__(64 * S) void k_attn_dec(
       xq[b][2 * ks] = *(const float4*)(qv + 32 * ks);
       xq[b][2 * ks + 1] = *(const float4*)(qv + 32 * ks + 4);
     }
-    Lj[b] = qok ? len[rj] : 0;  // this column's row length (0: no row)
+    // this column's row length (0: no row); loaded unconditionally at a valid
+    // row, so the compiler's wait for it counts only the loads issued before it
+    const int lv = len[qok ? rj : r0];
+    Lj[b] = qok ? lv : 0;
   }
   // piece i (1 KiB): rows 4 i .. + 3 of the tile; lane l writes chunk slot
   // l % 16 of row 4 i + l / 16
@@ -331,10 +331,11 @@ __global__ __launch_bounds__(64 * S) void k_attn_dec(
     const bf16_t* kb = kc + (size_t)kvh * n_max * HD;
     const bf16_t* vb = vc + (size_t)kvh * n_max * HD;
     const int rr0 = lane >> 4, slot = lane & 15;
+    const int rlast = min(send, n_max) - 1;  // rows past the split re-read its last row
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       const int rr = 4 * i + rr0;
-      const int row = min(t0 + rr, n_max - 1);
+      const int row = min(t0 + rr, rlast);
       __builtin_amdgcn_global_load_lds(
           (const void*)(kb + (size_t)row * HD + ((slot ^ (rr & 15)) << 3)),
           (__attribute__((address_space(3))) void*)&Ks[w][i * 64], 16, 0, 2);
@@ -342,7 +343,7 @@ __global__ __launch_bounds__(64 * S) void k_attn_dec(
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       const int rr = 4 * i + rr0;
-      const int row = min(t0 + rr, n_max - 1);
+      const int row = min(t0 + rr, rlast);
       __builtin_amdgcn_global_load_lds(
           (const void*)(vb + (size_t)row * HD + ((slot ^ (rr & 15)) << 3)),
           (__attribute__((address_space(3))) void*)&Vs[w][i * 64], 16, 0, 2);
@@ -350,7 +351,8 @@ __global__ __launch_bounds__(64 * S) void k_attn_dec(
   }
   int Lmax = 0;  // longest row of the workgroup
   for (int r = r0; r < min(M, r0 + RB); ++r) Lmax = max(Lmax, len[r]);
-  const int cnt = min(TILE, Lmax - t0);  // keys of this tile any column uses (may be <= 0)
+  // keys of this tile any column uses (may be <= 0)
+  const int cnt = min(TILE, min(Lmax, send) - t0);
   // queries as hi + lo bf16 (waits for the query loads only), scaled by
   // log2(e) / sqrt(HD): scores in base-2 units, probabilities powers of two
   const float qscale = 1.4426950408889634f / sqrtf((float)HD);
@@ -400,7 +402,7 @@ __global__ __launch_bounds__(64 * S) void k_attn_dec(
     }
 #pragma unroll
     for (int b = 0; b < CB; ++b) {
-      const int cj = min(TILE, Lj[b] - t0);  // keys of this tile the column uses
+      const int cj = min(TILE, min(Lj[b], send) - t0);  // keys of this tile the column uses
       float mt = -FLT_MAX;
 #pragma unroll
       for (int kt = 0; kt < 4; ++kt)
@@ -484,40 +486,36 @@ __global__ __launch_bounds__(64 * S) void k_attn_dec(
       rec[lane * RS + HD + 1] = l[b];
     }
   }
+  if (threadIdx.x < nc) s_len[threadIdx.x] = CB == 1 || threadIdx.x < 16 ? Lj[0] : Lj[CB - 1];
   __syncthreads();
   auto record = [&](int s, int c) -> const float* {
     return (c < 16 ? (const float*)&Ks[s][0] : (const float*)&Vs[s][0]) + (c & 15) * RS;
   };
-  if (threadIdx.x < nc) {  // wave 0, lane c: column c (its Lj[c / 16] is the column's length)
-    const int c = threadIdx.x;
-    float mx = -FLT_MAX;
-#pragma unroll
-    for (int s = 0; s < S; ++s) mx = fmaxf(mx, record(s, c)[HD]);
-    float lx = 0.f;
-#pragma unroll
-    for (int s = 0; s < S; ++s) {
-      const float* rs = record(s, c);
-      const float wt = rs[HD] == -FLT_MAX ? 0.f : __builtin_amdgcn_exp2f(rs[HD] - mx);
-      s_w[c * S + s] = wt;
-      lx = fmaf(rs[HD + 1], wt, lx);
-    }
-    s_mx[c] = mx;
-    s_lx[c] = lx;
-    s_len[c] = CB == 1 || c < 16 ? Lj[0] : Lj[CB - 1];
-  }
-  __syncthreads();
-  // the split's partial of every column whose row reaches this split
+  // the split's partial of every column whose row reaches this split: each
+  // thread forms its column's common max and the tile weights itself (the
+  // same values for every dim of a column), so one barrier suffices
   for (int i = threadIdx.x; i < nc * HD; i += 64 * S) {
     const int c = i >> 7, d = i & (HD - 1);
     if (s_len[c] <= start) continue;
-    float acc = 0.f;
+    float ms[S];
+    float mx = -FLT_MAX;
 #pragma unroll
-    for (int s = 0; s < S; ++s) acc = fmaf(record(s, c)[d], s_w[c * S + s], acc);
+    for (int s = 0; s < S; ++s) {
+      ms[s] = record(s, c)[HD];
+      mx = fmaxf(mx, ms[s]);
+    }
+    float acc = 0.f, lx = 0.f;
+#pragma unroll
+    for (int s = 0; s < S; ++s) {
+      const float wt = ms[s] == -FLT_MAX ? 0.f : __builtin_amdgcn_exp2f(ms[s] - mx);
+      acc = fmaf(record(s, c)[d], wt, acc);
+      if (d == 0) lx = fmaf(record(s, c)[HD + 1], wt, lx);
+    }
     float* dst = part + (((size_t)(r0 + c / G) * hq + kvh * G + c % G) * nsplit + split) * (HD + 2);
     dst[d] = acc;
     if (d == 0) {
-      dst[HD] = s_mx[c] * 0.6931471805599453f;  // back to natural-log units
-      dst[HD + 1] = s_lx[c];
+      dst[HD] = mx * 0.6931471805599453f;  // back to natural-log units
+      dst[HD + 1] = lx;
     }
   }
 }
@@ -574,7 +572,8 @@ __global__ __launch_bounds__(64 * NW) void k_attn_stream(
   for (int b = 0; b < CB; ++b) {
     const int rj = r0 + (16 * b + j) / G;
     const bool qok = rj < M;
-    Lj[b] = qok ? len[rj] : 0;
+    const int lv = len[qok ? rj : r0];  // unconditional load at a valid row (see k_attn_dec)
+    Lj[b] = qok ? lv : 0;
     if (qok) lim_min = min(lim_min, Lj[b]);
     const float* qv = q + ((size_t)(qok ? rj : r0) * hq + kvh * G + j % G) * HD + 8 * g;
 #pragma unroll
@@ -1198,7 +1197,7 @@ bool attn_dec_path(const AttnArgs& a) {
 
 void attn_split(const AttnArgs& a, hipStream_t st) {
   if (a.max_len <= 0) return;
-  const int ns = attn_nsplit(a.max_len, a.tiles);
+  const int ns = (a.max_len + a.span - 1) / a.span;
   const int G = a.hq / a.hkv;
   const int nq = a.rows_per_block * G;
   dim3 grid(ns, a.hkv, (a.M + a.rows_per_block - 1) / a.rows_per_block);
@@ -1216,7 +1215,7 @@ void attn_split(const AttnArgs& a, hipStream_t st) {
     const bf16_t* vc = (const bf16_t*)a.vc;
 #define KS_DEC(S_, CB_)                                                                      \
   hipLaunchKernelGGL((k_attn_dec<S_, CB_>), g3, dim3(64 * S_), 0, st, a.M, a.hq, a.hkv,       \
-                     a.n_max, a.q, kc, vc, a.len, a.part, a.nsplit)
+                     a.n_max, a.q, kc, vc, a.len, a.part, a.nsplit, a.span)
 #define KS_DEC_S(CB_)            \
   switch (a.tiles) {             \
     case 1: KS_DEC(1, CB_); break; \
@@ -1258,8 +1257,8 @@ void attn_split(const AttnArgs& a, hipStream_t st) {
 
 void attn_combine(const AttnArgs& a, const float* kvself, Act act_out, hipStream_t st) {
   dim3 grid(a.M * a.hq);
-  const int span = TILE * a.tiles;
-  const int ngrid = attn_nsplit(a.max_len, a.tiles);  // splits the split kernel ran
+  const int span = a.span;
+  const int ngrid = (a.max_len + span - 1) / span;  // splits the split kernel ran
   const bool bf = a.dtype == KS_BF16;
 #define KS_COMB(HDV, BFV)                                                                    \
   hipLaunchKernelGGL((k_attn_combine<HDV, BFV>), grid, dim3(256), 0, st, a.M, a.hq, a.hkv,   \

@@ -57,9 +57,11 @@ constexpr size_t GPART_BYTES = (size_t)128 << 20;
 // split alike).  Measured on MI355X (split kernel + merge, 1 and 5 rows): the
 // one-tile-per-wave kernel with two tiles for caches up to 2048 positions,
 // three up to 5120, five up to 12288 (a 160 KiB workgroup: up to 10240
-// positions of 8 kv heads fit the 256 CUs in one round); above, the streaming
-// kernel with 4 waves and as many tiles per wave (at least 2) as keep the
-// splits of all kv heads to one round of 256 workgroups.
+// positions of 8 kv heads fit the 256 CUs in one round; splits sized to put
+// an equal share of the cache on every CU, the last tile partly used, were
+// slower); above, the streaming kernel with 4 waves and as many tiles per wave
+// (at least 2) as keep the splits of all kv heads to one round of 256
+// workgroups.
 int dec_tiles(int n_max, int hkv) {
   if (n_max <= 2048) return 2;
   if (n_max <= 5120) return 3;
@@ -69,6 +71,7 @@ int dec_tiles(int n_max, int hkv) {
   const int tpw = (n_tiles + 4 * splits - 1) / (4 * splits);
   return 4 * std::max(2, tpw);
 }
+int dec_span(const ks_model_desc& d) { return 64 * dec_tiles(d.n_max, d.hkv); }
 #ifndef KS_BAT_TILES
 #define KS_BAT_TILES 16
 #endif
@@ -98,7 +101,7 @@ Layout make_layout(const ks_model_desc& d, const ks_limits& lim) {
   y.LR = std::max(gam1, PB);
   y.nqkv = (d.hq + 2 * d.hkv) * d.hd;
   y.a2w = std::max(d.hq * d.hd, d.ffn);
-  const int ns_dec = attn_nsplit(d.n_max, dec_tiles(d.n_max, d.hkv));
+  const int ns_dec = (d.n_max + dec_span(d) - 1) / dec_span(d);
   const int ns_bat = attn_nsplit(d.n_max, BAT_TILES);
   y.part_rows = PB;
   y.part_elems = std::max((size_t)16 * d.hq * ns_dec, (size_t)PB * d.hq * ns_bat) * (d.hd + 2);
@@ -340,12 +343,13 @@ void attn_rows(ks_ctx* c, int l, const float* xin, float* xout, int R, const int
     PROF(c, KS_KC_QKV_POST, qkv_post(qp, c->st));
   }
   const int tiles = batched ? BAT_TILES : dec_tiles(d.n_max, d.hkv);
-  const int ns = attn_nsplit(d.n_max, tiles);
+  const int span = batched ? 64 * BAT_TILES : dec_span(d);
+  const int ns = (d.n_max + span - 1) / span;
   const int step = batched ? PB : 16;
   for (int r0 = 0; r0 < R; r0 += step) {
     const int rr = std::min(step, R - r0);
     AttnArgs aa{rr, d.hq, d.hkv, d.hd, d.n_max, d.dtype,
-                q + (size_t)r0 * d.hq * d.hd, c->kc(l), c->vc(l), len + r0, max_len, tiles,
+                q + (size_t)r0 * d.hq * d.hd, c->kc(l), c->vc(l), len + r0, max_len, tiles, span,
                 attn_rows_per_block(d.hq / d.hkv, batched), c->at<float>(c->y.part), ns};
     PROF(c, KS_KC_ATTN, attn_split(aa, c->st));
     Act out2 = a2;

@@ -53,7 +53,7 @@ __device__ inline void store_split(bf16_t* hi, bf16_t* lo, size_t off, float a) 
 // products read those planes like any activation and scale row m by
 // 1/sqrt(sum/K + eps) at the end; the 256 tile sums of a row are added by one
 // wave in a fixed order, whatever the row count.
-template <int NB, int NW, int CH, int MINB, int EPI, int AN>
+template <int NB, int NW, int CH, int MINB, int EPI, int AN, int A1>
 __global__ __launch_bounds__(NW * 64, MINB) void k_gemm_skinny(
     int M, int N, int K, const bf16_t* __restrict__ Ahi, const bf16_t* __restrict__ Alo,
     int lda, const bf16_t* __restrict__ Wp, float* out, int ldo, const float* res, int ldres,
@@ -106,6 +106,27 @@ __global__ __launch_bounds__(NW * 64, MINB) void k_gemm_skinny(
   }
   if (EPI == EPI_QKV && eact) e_pos = qe.pos[em];
 
+  // One-row products (A1, decode and draft steps): the activation row (hi and
+  // lo planes) is staged in LDS once per workgroup, so the k loop's only
+  // global loads are the weight fragments (two activation loads per weight
+  // load cost the load path more time than the weight bytes).  The matrix
+  // instructions see the same operand values either way, so the result bits
+  // do not depend on the path.  The row's loads are issued before the weight
+  // stream and land in LDS after it has started.
+  extern __shared__ __align__(16) uint4 s_act[];  // A1: hi plane [K / 8], then lo plane
+  constexpr int A1PT = 4;  // 16-byte chunks per thread and plane (launcher: 4 * 64 NW * 8 >= K)
+  const int n16 = K >> 3;
+  uint4 av[2][A1PT];
+  if constexpr (A1 != 0) {
+#pragma unroll
+    for (int pl = 0; pl < 2; ++pl)
+#pragma unroll
+      for (int q = 0; q < A1PT; ++q) {
+        const int i = threadIdx.x + q * NW * 64;
+        av[pl][q] = ((const uint4*)(pl ? Alo : Ahi))[i < n16 ? i : n16 - 1];
+      }
+  }
+
   f32x4 acc[NB];
 #pragma unroll
   for (int t = 0; t < NB; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -133,41 +154,63 @@ __global__ __launch_bounds__(NW * 64, MINB) void k_gemm_skinny(
     for (int u = 0; u < CH; ++u) {
 #pragma unroll
       for (int t = 0; t < NB; ++t) w[t][u] = ld_frag_nt(wb[t] + (size_t)(kc + u) * 512);
-      x0[u] = ld_frag(ah + (kc + u) * 32);
-      x1[u] = ld_frag(al + (kc + u) * 32);
+      if constexpr (A1 == 0) {
+        x0[u] = ld_frag(ah + (kc + u) * 32);
+        x1[u] = ld_frag(al + (kc + u) * 32);
+      }
     }
   };
-  auto compute = [&](bf16x8 (&w)[NB][CH], bf16x8 (&x0)[CH], bf16x8 (&x1)[CH]) {
+  // A1: lane (row, kg) takes k = 32 step + 8 kg .. + 7 of row 0 from LDS
+  auto act_lds = [&](int k, int pl) {
+    return __builtin_bit_cast(bf16x8, s_act[pl * n16 + 4 * k + kg]);
+  };
+  auto compute = [&](int kc, bf16x8 (&w)[NB][CH], bf16x8 (&x0)[CH], bf16x8 (&x1)[CH]) {
 #pragma unroll
     for (int u = 0; u < CH; ++u) {
+      const bf16x8 a0 = A1 ? act_lds(kc + u, 0) : x0[u];
+      const bf16x8 a1 = A1 ? act_lds(kc + u, 1) : x1[u];
 #pragma unroll
       for (int t = 0; t < NB; ++t) {
-        acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(x0[u], w[t][u], acc[t], 0, 0, 0);
-        acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(x1[u], w[t][u], acc[t], 0, 0, 0);
+        acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, w[t][u], acc[t], 0, 0, 0);
+        acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, w[t][u], acc[t], 0, 0, 0);
       }
     }
   };
   const int nfull = (ke - kb) / CH;  // wave-uniform
   if (nfull > 0) fetch(kb, w0, x00, x01);
+  if constexpr (A1 != 0) {
+    // the row lands in LDS; every wave's part is there after the barrier
+#pragma unroll
+    for (int pl = 0; pl < 2; ++pl)
+#pragma unroll
+      for (int q = 0; q < A1PT; ++q) {
+        const int i = threadIdx.x + q * NW * 64;
+        if (i < n16) s_act[pl * n16 + i] = av[pl][q];
+      }
+    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's LDS writes are done
+    __builtin_amdgcn_s_barrier();
+    __asm__ volatile("" ::: "memory");
+  }
   int c = 0;
   for (; c + 2 < nfull; c += 2) {  // chunk c is in stage 0 and in flight
     fetch(kb + (c + 1) * CH, w1, x10, x11);
-    compute(w0, x00, x01);
+    compute(kb + c * CH, w0, x00, x01);
     fetch(kb + (c + 2) * CH, w0, x00, x01);
-    compute(w1, x10, x11);
+    compute(kb + (c + 1) * CH, w1, x10, x11);
   }
   if (c + 1 < nfull) {
     fetch(kb + (c + 1) * CH, w1, x10, x11);
-    compute(w0, x00, x01);
-    compute(w1, x10, x11);
+    compute(kb + c * CH, w0, x00, x01);
+    compute(kb + (c + 1) * CH, w1, x10, x11);
   } else if (c < nfull) {
-    compute(w0, x00, x01);
+    compute(kb + c * CH, w0, x00, x01);
   }
   for (int k = kb + nfull * CH; k < ke; ++k) {
     bf16x8 b[NB];
 #pragma unroll
     for (int t = 0; t < NB; ++t) b[t] = ld_frag_nt(wb[t] + (size_t)k * 512);
-    const bf16x8 a0 = ld_frag(ah + k * 32), a1 = ld_frag(al + k * 32);
+    const bf16x8 a0 = A1 ? act_lds(k, 0) : ld_frag(ah + k * 32);
+    const bf16x8 a1 = A1 ? act_lds(k, 1) : ld_frag(al + k * 32);
 #pragma unroll
     for (int t = 0; t < NB; ++t) {
       acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, b[t], acc[t], 0, 0, 0);
@@ -274,15 +317,16 @@ __global__ __launch_bounds__(NW * 64, MINB) void k_gemm_skinny(
   }
 }
 
-template <int NB, int NW, int CH, int MINB, int AN>
-static void launch_skinny_an(const GemmArgs& g, hipStream_t st) {
+template <int NB, int NW, int CH, int MINB, int AN, int A1>
+static void launch_skinny_a1(const GemmArgs& g, hipStream_t st) {
   const int NT = g.N / 16;
   const bf16_t* Ahi = (const bf16_t*)g.A.hi;
   const bf16_t* Alo = (const bf16_t*)g.A.lo;
   const bf16_t* W = (const bf16_t*)g.W;
   dim3 grid((NT + NB - 1) / NB), block(NW * 64);
+  const size_t lds = A1 ? (size_t)g.K * 4 : 0;  // hi and lo planes of the row
 #define KS_SKINNY(E, OH, OL, OLD)                                                            \
-  hipLaunchKernelGGL((k_gemm_skinny<NB, NW, CH, MINB, E, AN>), grid, block, 0, st, g.M, g.N, g.K,  \
+  hipLaunchKernelGGL((k_gemm_skinny<NB, NW, CH, MINB, E, AN, A1>), grid, block, lds, st, g.M, g.N, g.K,  \
                      Ahi, Alo, g.A.ld, W, g.out, g.ldo, g.res, g.ldres, OH, OL, OLD,         \
                      g.ssq_in, g.nssq, g.eps, g.next_gain, (bf16_t*)g.next_act.hi,           \
                      (bf16_t*)g.next_act.lo, g.next_act.ld, g.next_ssq, g.qe)
@@ -298,34 +342,48 @@ static void launch_skinny_an(const GemmArgs& g, hipStream_t st) {
 #undef KS_SKINNY
 }
 
-template <int NB, int NW, int CH, int MINB>
-static void launch_skinny(const GemmArgs& g, hipStream_t st) {
-  if (g.ssq_in) launch_skinny_an<NB, NW, CH, MINB, 1>(g, st);
-  else launch_skinny_an<NB, NW, CH, MINB, 0>(g, st);
+template <int NB, int NW, int CH, int MINB, int AN, int STAGE>
+static void launch_skinny_an(const GemmArgs& g, hipStream_t st) {
+  // one row and a shape that gains from it (STAGE): the activation row from
+  // LDS (hi + lo planes, 4 K bytes; 16-byte aligned planes and at most four
+  // chunks per thread and plane)
+  const bool a1 = STAGE && g.M == 1 && g.K % 8 == 0 && (size_t)g.K * 4 <= 64 * 1024 &&
+                  4 * 64 * NW * 8 >= g.K && (((uintptr_t)g.A.hi | (uintptr_t)g.A.lo) & 15) == 0;
+  if (a1) launch_skinny_a1<NB, NW, CH, MINB, AN, 1>(g, st);
+  else launch_skinny_a1<NB, NW, CH, MINB, AN, 0>(g, st);
 }
 
-// Launch shape by matrix shape only (never by row count), measured on MI355X
-// with the Llama-8B shapes (cold weights, 4/8/16 waves x 4/8/16-deep chunks):
-// gate/up one tile per 4-wave workgroup in 4-deep chunks (1792 workgroups of
-// 4 waves are all resident at once, 7 per CU, so no second round trails); the
-// vocabulary head 8 waves, 4-deep; the long-K down projection a 16-way K split;
-// the remaining square-ish products 16 (N <= 4096) or 8 waves, 8-deep.
+template <int NB, int NW, int CH, int MINB, int STAGE>
+static void launch_skinny(const GemmArgs& g, hipStream_t st) {
+  if (g.ssq_in) launch_skinny_an<NB, NW, CH, MINB, 1, STAGE>(g, st);
+  else launch_skinny_an<NB, NW, CH, MINB, 0, STAGE>(g, st);
+}
+
+// Launch shape by matrix shape only (never by row count; the one-row staging
+// changes where the operands come from, not the arithmetic), measured on
+// MI355X with the Llama-8B shapes (cold weights; 4/8/16 waves, 1/2/4-deep
+// pipelined chunks, workgroups per CU forced by the register budget, staging
+// on or off): gate/up one tile per 4-wave workgroup, 2-deep chunks; the long-K
+// down projection and the square O projection 16 waves, 4-deep; the vocabulary
+// head and the q/k/v projection 8 waves, 4-deep, with the one-row activation
+// staged in LDS (the staging costs the 16-wave and the gate/up shapes more
+// than their activation loads).
 // (output tiles per workgroup, waves, k steps per chunk, workgroups per CU
-// the register budget must allow)
+// the register budget must allow, one-row activation staged in LDS)
 #ifndef KS_SK_GU
-#define KS_SK_GU 1, 4, 2, 1
+#define KS_SK_GU 1, 4, 2, 1, 0
 #endif
 #ifndef KS_SK_DOWN
-#define KS_SK_DOWN 1, 16, 4, 1
+#define KS_SK_DOWN 1, 16, 4, 1, 0
 #endif
 #ifndef KS_SK_HEAD
-#define KS_SK_HEAD 1, 8, 4, 1
+#define KS_SK_HEAD 1, 8, 4, 1, 1
 #endif
 #ifndef KS_SK_SQ
-#define KS_SK_SQ 1, 16, 4, 1
+#define KS_SK_SQ 1, 16, 4, 1, 0
 #endif
 #ifndef KS_SK_WIDE
-#define KS_SK_WIDE 1, 8, 4, 1
+#define KS_SK_WIDE 1, 8, 4, 1, 1
 #endif
 void gemm_bf16_skinny(const GemmArgs& g, hipStream_t st) {
   if (g.epi == EPI_SWIGLU) launch_skinny<KS_SK_GU>(g, st);

@@ -154,7 +154,8 @@ struct AttnArgs {
   const void* vc;
   const int32_t* len;    // device [M]
   int max_len;           // host upper bound of len[]
-  int tiles;             // 64-position tiles per split
+  int tiles;             // 64-position tiles per split (waves of the decode kernel)
+  int span;              // positions per split (TILE * tiles)
   int rows_per_block;
   float* part;           // [M][hq][nsplit][hd+2]
   int nsplit;            // stride: splits per (row, head)
