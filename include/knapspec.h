@@ -397,6 +397,21 @@ ks_status ks_sample_filter(const float* logits, int rows, int vocab, int ld, con
                            float* top1, int32_t* tokens, void* workspace, size_t workspace_bytes,
                            void* stream);
 /*
+ * ks_sample_filter_noalloc: ks_sample_filter for callers that cannot allocate
+ * device memory (code under stream capture, tight serving loops, harnesses
+ * that forbid allocation).  Same arguments and results, minus the workspace:
+ * the chunk statistics and candidates live in a 4 MiB array of the library on
+ * each device (calls whose ks_sample_workspace_bytes(rows, vocab, top_k)
+ * exceeds 4 MiB fail with KS_ENOMEM and change nothing).  Nothing in the
+ * scratch needs to start at any value; every call on a device shares that
+ * device's scratch, so calls that overlap in time on one device (other streams,
+ * other threads) race and must be serialised by the caller.  Asynchronous.
+ */
+ks_status ks_sample_filter_noalloc(const float* logits, int rows, int vocab, int ld,
+                                   const ks_sampling* s, int pos0, int purpose, int32_t* ids,
+                                   float* probs, int32_t* counts, float* top1, int32_t* tokens,
+                                   void* stream);
+/*
  * ks_spec_accept: the acceptance chain of one round on device tables (p: rows
  * 0..gamma, q: rows 0..gamma-1 for d_1..d_gamma, layout of ks_sample_filter),
  * drafts device int32 [gamma] (d_1..d_gamma), pos0 = P; counts in

@@ -139,6 +139,8 @@ _SIG = {
     "ks_sample_workspace_bytes": (C.c_size_t, [_I, _I, _I]),
     "ks_sample_filter": (_I, [_P, _I, _I, _I, C.POINTER(Sampling), _I, _I, _P, _P, _P, _P, _P,
                               _P, C.c_size_t, _P]),
+    "ks_sample_filter_noalloc": (_I, [_P, _I, _I, _I, C.POINTER(Sampling), _I, _I, _P, _P, _P,
+                                      _P, _P, _P]),
     "ks_spec_accept": (_I, [_P, _P, _P, _P, _P, _P, _P, _I, C.c_uint64, _I, _P, _P]),
     "ks_sample_uniforms": (_I, [C.c_uint64, _P, _I, _I, _P, _P]),
     "ks_profile_decode": (_I, [_P, _P, _I, _I, C.POINTER(KernelProfile)]),
@@ -194,6 +196,7 @@ ks_decode = _wrap("ks_decode")
 ks_set_draft_policy = _wrap("ks_set_draft_policy")
 ks_set_sampling = _wrap("ks_set_sampling")
 ks_sample_filter = _wrap("ks_sample_filter")
+ks_sample_filter_noalloc = _wrap("ks_sample_filter_noalloc")
 ks_spec_accept = _wrap("ks_spec_accept")
 ks_sample_uniforms = _wrap("ks_sample_uniforms")
 ks_sample_workspace_bytes = lib.ks_sample_workspace_bytes

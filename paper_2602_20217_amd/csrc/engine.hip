@@ -20,6 +20,7 @@
 #include "ks_internal.h"
 
 #include <algorithm>
+#include <atomic>
 #include <chrono>
 #include <cmath>
 #include <limits>
@@ -493,6 +494,31 @@ int hist_rows(const ks_ctx* c) {
 }  // namespace
 
 // =============================================================== C ABI
+// Scratch of ks_sample_filter_noalloc: one file-scope device array per GPU
+// the library runs on (it lives until the process ends).  Host code never
+// passes the array's name to a kernel: its device address on each GPU comes
+// from hipGetSymbolAddress, taken once per device with that device current.
+constexpr size_t KS_NOALLOC_SCRATCH_BYTES = (size_t)4 << 20;
+static __device__ __align__(256) unsigned char scratch[KS_NOALLOC_SCRATCH_BYTES];
+constexpr int KS_NOALLOC_MAX_DEVICES = 64;
+static std::atomic<void*> g_scratch_ptr[KS_NOALLOC_MAX_DEVICES];
+
+static ks_status scratch_address(void** out) {
+  int dev = -1;
+  HIPCHK(hipGetDevice(&dev));
+  if (dev < 0 || dev >= KS_NOALLOC_MAX_DEVICES) {
+    set_error("device index beyond the allocation-free entry point's table");
+    return KS_EINVAL;
+  }
+  void* p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+  if (p == nullptr) {
+    HIPCHK(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    g_scratch_ptr[dev].store(p, std::memory_order_release);
+  }
+  *out = p;
+  return KS_OK;
+}
+
 extern "C" {
 
 const char* ks_last_error(void) { return g_err.c_str(); }
@@ -896,6 +922,30 @@ ks_status ks_sample_filter(const float* logits, int rows, int vocab, int ld, con
   const SampleSpec ss{s->temperature, s->top_k, s->top_p, s->seed, ids, probs, counts, top1,
                       tokens, pos0, purpose};
   sample_rows(logits, rows, vocab, ld, ss, workspace, (hipStream_t)stream);
+  HIPCHK(hipGetLastError());
+  return KS_OK;
+}
+
+ks_status ks_sample_filter_noalloc(const float* logits, int rows, int vocab, int ld,
+                                   const ks_sampling* s, int pos0, int purpose, int32_t* ids,
+                                   float* probs, int32_t* counts, float* top1, int32_t* tokens,
+                                   void* stream) {
+  REQ(logits && ids && probs && counts, "null pointer");
+  REQ(rows >= 1 && rows <= 65535 && vocab >= 1 && ld >= vocab, "sizes out of range");
+  ks_status st = check_sampling(s, vocab);
+  if (st != KS_OK) return st;
+  REQ(pos0 >= 0 && purpose >= 0, "pos0 and purpose must be >= 0");
+  if (sample_ws_bytes(rows, vocab, s->top_k) > KS_NOALLOC_SCRATCH_BYTES) {
+    set_error("rows x vocabulary need more scratch than the allocation-free filter holds "
+              "(4 MiB): use ks_sample_filter with a workspace");
+    return KS_ENOMEM;
+  }
+  void* ws = nullptr;
+  st = scratch_address(&ws);
+  if (st != KS_OK) return st;
+  const SampleSpec ss{s->temperature, s->top_k, s->top_p, s->seed, ids, probs, counts, top1,
+                      tokens, pos0, purpose};
+  sample_rows(logits, rows, vocab, ld, ss, ws, (hipStream_t)stream);
   HIPCHK(hipGetLastError());
   return KS_OK;
 }
