@@ -344,6 +344,13 @@ def main():
     ap.add_argument("--no-knapsack", action="store_true",
                     help="skip the isolated knapsack batch leg")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-32k", action="store_true",
+                    help="skip the 32K leg (Qwen3-8B shape, 32768-token prompt, gamma 6)")
+    ap.add_argument("--include-head", action="store_true",
+                    help="add the measured LM head time to the TPT cost of the selection "
+                         "(the paper's cost leaves it out; off by default)")
+    ap.add_argument("--calibrate-stream", action="store_true",
+                    help="only the streaming-read reference at the decode launch sizes")
     ap.add_argument("--profile-kernels", action="store_true",
                     help="short run for hardware counters: prefill, 16 decode steps and a "
                          "256 MiB device copy (the reference for counter scaling)")
@@ -372,6 +379,14 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     cfg = W.config(args.model)
+    if args.calibrate_stream:
+        q, kv = cfg.hq * cfg.hd, cfg.hkv * cfg.hd
+        sizes = {"gemm_o": cfg.d * q * 2, "attn": args.ctx * kv * 2 * 2,
+                 "gemm_qkv": (q + 2 * kv) * cfg.d * 2, "gemm_down": cfg.d * cfg.ffn * 2,
+                 "gemm_gate_up": 2 * cfg.ffn * cfg.d * 2, "gemm_head": cfg.vocab * cfg.d * 2}
+        print(json.dumps({"mode": "calibrate-stream", "model": cfg.name, "ctx": args.ctx,
+                          "bytes": sizes, "GBps": stream_ceiling(sizes)}), flush=True)
+        return
     if args.sweep:
         return run_sweep(args, cfg)
     n_max = args.ctx + args.new + 64
@@ -437,64 +452,23 @@ def main():
                           "j": sel.j_star, "select_ms": times}), flush=True)
         dm.close()
         return
-    params = select_params(coeffs, "paper_min", 0, tau=0.5, prune_half=True, D=10)
-
-    def run(gamma):
-        dm.prefill(prompt)
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        out, st, sels = dm.decode(args.new, gamma, args.reselect, params if gamma else None)
-        torch.cuda.synchronize()
-        return (time.perf_counter() - t0) * 1e3, out, st, sels
-
-    ar_ms, ssd_ms, ssd_last, ar_out = [], [], None, None
-    for k in range(args.warmup + args.steps):
-        a_ms, ar_out, _, _ = run(0)
-        s_ms, out, st, sels = run(args.gamma)
-        if k >= args.warmup:
-            ar_ms.append(a_ms)
-            ssd_ms.append(s_ms)
-        ssd_last = (out, st, sels)
-        log(f"step {k}: AR {a_ms:.1f} ms, speculative {s_ms:.1f} ms "
-            f"(select {st.ms_select:.1f} ms, accepted {st.n_accepted}/{st.n_drafted})")
-    out, st, sels = ssd_last
-    # greedy: the speculative tokens equal the AR tokens; sampling draws differ
-    same = None if sampling else bool(np.array_equal(out, ar_out))
-
-    # roofline of the dominant kernel: the decode step's gate/up projection
-    prof = dm.profile_decode(None, 16, per_kernel=True)
-    ms_gu = prof["ms"]["gemm_gate_up"]
-    bytes_gu = 2 * cfg.ffn * cfg.d * 2 + cfg.d * 2 * 2 + cfg.ffn * 2 * 2
-    achieved = bytes_gu / (ms_gu * 1e-3) / 1e9
-    wbytes = {"gemm_qkv": (cfg.hq + 2 * cfg.hkv) * cfg.hd * cfg.d * 2,
-              "gemm_o": cfg.d * cfg.hq * cfg.hd * 2, "gemm_gate_up": bytes_gu,
-              "gemm_down": cfg.d * cfg.ffn * 2, "gemm_head": cfg.vocab * cfg.d * 2}
-    kern = {}
-    for name, ms in prof["ms"].items():
-        if prof["launches"][name] == 0:
-            continue
-        e = {"ms": round(ms, 5), "launches_per_token": prof["launches"][name]}
-        if name in wbytes and wbytes[name]:
-            e["GBps"] = round(wbytes[name] / (ms * 1e-3) / 1e9, 1)
-        kern[name] = e
-    P = args.ctx + args.new
-    kv_bytes = P * cfg.hkv * cfg.hd * 2 * 2  # per layer, K and V
-    if prof["ms"]["attn"] > 0:
-        kern["attn"]["GBps"] = round(kv_bytes / ((prof["ms"]["attn"] + prof["ms"]["combine"]) * 1e-3) / 1e9, 1)
-
-    mean_ssd = sum(ssd_ms) / len(ssd_ms)
-    mean_ar = sum(ar_ms) / len(ar_ms)
-    # decode(n) returns n tokens, the first of which the prefill produced before
-    # the timed region: the timed region generates n - 1
+    t_head = coeffs_head(sweep) if args.include_head else 0.0
+    params = select_params(coeffs, "paper_min", 0, tau=0.5, prune_half=True, D=10,
+                           t_head=t_head)
+    core = measure_decode(dm, cfg, prompt, args.ctx, args.new, args.gamma, args.reselect,
+                          args.steps, args.warmup, params, sampling is not None)
+    ceiling = stream_ceiling({n: b for n, b in core.pop("_launch_bytes").items()})
+    for name, e in core["kernels"].items():
+        if "GBps" in e:
+            e["frac_peak"] = round(e["GBps"] / HBM_PEAK_GBPS, 4)
+            if name in ceiling:
+                e["stream_ceiling_GBps"] = ceiling[name]
+                e["frac_ceiling"] = round(e["GBps"] / ceiling[name], 4)
     timed_tokens = args.new - 1
-    value = timed_tokens / (mean_ssd / 1e3)
-    ar_tps = timed_tokens / (mean_ar / 1e3)
-    token_bytes = (cfg.vocab * cfg.d * 2 + cfg.L * (((cfg.hq + 2 * cfg.hkv) * cfg.hd + cfg.hq * cfg.hd) * cfg.d * 2
-                   + 3 * cfg.ffn * cfg.d * 2) + cfg.L * kv_bytes)
     res = {
         "metric": "decode tok/s (bs=1) at 8K ctx, speedup vs AR; achieved HBM GB/s",
-        "value": round(value, 2), "unit": "tok/s", "n_gpus": 1, "steps": args.steps,
-        "warmup": args.warmup, "ms_per_step": round(mean_ssd, 2), "higher_is_better": True,
+        "value": core["value"], "unit": "tok/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": core["ms_per_step"], "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic (seeded random-init weights, random-id prompt)",
         "config": {"workload": f"{describe(cfg)}, bf16 weights and KV, "
@@ -505,30 +479,27 @@ def main():
                    "gamma": args.gamma, "reselect_every": args.reselect, "parallelism": "none",
                    "draft_policy": {"tau_conf": args.tau_conf,
                                     "gamma_source": args.gamma_source},
+                   "tpt_cost": ({"lm_head_ms": round(t_head, 5)} if t_head > 0
+                                else "paper (LM head excluded)"),
                    "decoding": ({"mode": "speculative sampling", **sampling} if sampling
                                 else {"mode": "greedy"})},
-        "speedup_vs_ar": round(value / ar_tps, 4), "ar_tok_s": round(ar_tps, 2),
-        "ar_ms_per_step": round(mean_ar, 2), "tokens_equal_ar": same,
-        "accepted": st.n_accepted, "drafted": st.n_drafted, "rounds": st.n_rounds,
-        "alpha": round(st.n_accepted / max(1, st.n_drafted), 4),
-        "tokens_per_round": round((st.n_accepted + st.n_rounds) / max(1, st.n_rounds), 3),
-        "select_ms": round(st.ms_select, 2), "selections": st.n_selections,
-        "select_overhead_pct": round(100.0 * st.ms_select / max(1e-9, ssd_ms[-1]), 2),
-        "masks": [{"j": s.j_star, "C": s.C, "w_attn": s.w_attn, "w_mlp": s.w_mlp,
-                   "skipped_attn": int(sum(1 for i in range(0, 2 * cfg.L, 2) if not s.exec[i])),
-                   "skipped_mlp": int(sum(1 for i in range(1, 2 * cfg.L, 2) if not s.exec[i])),
-                   "alpha_hat": round(s.alpha_hat, 3), "gamma_star": s.gamma_star} for s in sels],
-        "ar_step_GBps": round(token_bytes / (mean_ar / timed_tokens * 1e-3) / 1e9, 1),
-        "latency_model_ms": {"c1": coeffs[0], "c2": coeffs[1], "c3": coeffs[2], "sweep": sweep},
-        "kernels": kern,
-        "roofline": {"bound": "hbm", "kernel": "k_gemm_skinny, SwiGLU epilogue (gate/up product, 1 row)",
-                     "achieved": round(achieved, 1), "peak": 8000.0, "unit": "GB/s",
-                     "frac": round(achieved / 8000.0, 4), "traffic": gate_up_traffic(cfg),
-                     "bytes_per_launch": bytes_gu, "ms_per_launch": round(ms_gu, 5)},
     }
+    res.update({k: v for k, v in core.items() if k not in ("value", "ms_per_step")})
+    res["latency_model_ms"] = {"c1": coeffs[0], "c2": coeffs[1], "c3": coeffs[2], "sweep": sweep}
+    res["stream_ceiling_GBps"] = ceiling
+    gu = core["kernels"]["gemm_gate_up"]
+    res["roofline"] = {"bound": "hbm",
+                       "kernel": "k_gemm_skinny, SwiGLU epilogue (gate/up product, 1 row)",
+                       "achieved": gu["GBps"], "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                       "frac": gu["frac_peak"], "traffic": gate_up_traffic(cfg),
+                       "bytes_per_launch": gu["bytes_per_launch"], "ms_per_launch": gu["ms"],
+                       "stream_ceiling": ceiling.get("gemm_gate_up"),
+                       "frac_of_stream_ceiling": gu.get("frac_ceiling")}
     dm.close()
     del dm
     torch.cuda.empty_cache()
+    if not args.no_32k and args.model == "llama8b" and not sampling:
+        res["qwen32k"] = leg_32k(args)
     knap_in = None
     if not args.no_knapsack:
         res["knapsack_batch"], knap_in = knapsack_leg(max(args.steps, 5), max(args.warmup, 1))
@@ -541,6 +512,186 @@ def main():
             res["knapsack_batch"]["cpu_baseline"] = knapsack_cpu_baseline(*knap_in)
         log(f"cpu baseline {time.time() - t:.1f}s")
     print(json.dumps(res), flush=True)
+
+
+HBM_PEAK_GBPS = 8000.0
+
+
+def coeffs_head(sweep):
+    """LM head + embedding + argmax time of one decode step (the sweep's step
+    that runs no sublayer), averaged over the sweep's contexts (ms)."""
+    return float(sum(r["t_head_ms"] for r in sweep) / len(sweep))
+
+
+def stream_ceiling(sizes, pool_bytes=2 << 30, reps=40):
+    """Rate (GB/s) of ks_stream_read, a plain streaming read, over buffers of each
+    size, timed with HIP events around every launch like the decode kernels
+    (launch overhead included); the buffers rotate through a pool larger than
+    the 256 MiB last-level cache so no launch finds its bytes cached."""
+    import torch
+    from paper_2602_20217_amd import _lib as K
+    pool = torch.empty(pool_bytes, dtype=torch.uint8, device="cuda")
+    sink = torch.zeros(1, dtype=torch.float32, device="cuda")
+    st = torch.cuda.current_stream()
+    out = {}
+    for name, nb in sizes.items():
+        nb = (int(nb) + 15) // 16 * 16
+        if nb > pool_bytes:
+            continue
+        nrot = max(1, pool_bytes // nb)
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(reps)]
+        for k in range(3):
+            K.ks_stream_read(pool.data_ptr() + (k % nrot) * nb, nb, sink.data_ptr(), st.cuda_stream)
+        for k, (a, b) in enumerate(ev):
+            a.record(st)
+            K.ks_stream_read(pool.data_ptr() + ((k + 3) % nrot) * nb, nb, sink.data_ptr(),
+                             st.cuda_stream)
+            b.record(st)
+        torch.cuda.synchronize()
+        ms = sum(a.elapsed_time(b) for a, b in ev) / reps
+        out[name] = round(nb / (ms * 1e-3) / 1e9, 1)
+    del pool
+    return out
+
+
+def measure_decode(dm, cfg, prompt, ctx, new, gamma, reselect, steps, warmup, params, sampled):
+    """Timed AR and speculative generation of `new` tokens after a prefill of
+    the prompt (untimed), `warmup` + `steps` times; then per-kernel HIP-event
+    timings of 16 decode steps.  Returns the measured quantities."""
+    import numpy as np
+    import torch
+
+    def run(g):
+        dm.prefill(prompt)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        out, st, sels = dm.decode(new, g, reselect, params if g else None)
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t0) * 1e3, out, st, sels
+
+    ar_ms, ssd_ms, ssd_last, ar_out = [], [], None, None
+    for k in range(warmup + steps):
+        a_ms, ar_out, _, _ = run(0)
+        s_ms, out, st, sels = run(gamma)
+        if k >= warmup:
+            ar_ms.append(a_ms)
+            ssd_ms.append(s_ms)
+        ssd_last = (out, st, sels)
+        log(f"{cfg.name} step {k}: AR {a_ms:.1f} ms, speculative {s_ms:.1f} ms "
+            f"(select {st.ms_select:.1f} ms, accepted {st.n_accepted}/{st.n_drafted})")
+    out, st, sels = ssd_last
+    same = None if sampled else bool(np.array_equal(out, ar_out))
+
+    dm.set_context(ctx, int(prompt[-1]))
+    prof = dm.profile_decode(None, 16, per_kernel=True)
+    q, kv = cfg.hq * cfg.hd, cfg.hkv * cfg.hd
+    kv_bytes = ctx * kv * 2 * 2  # per layer, K and V, at the profiled context
+    launch_bytes = {
+        "gemm_qkv": (q + 2 * kv) * cfg.d * 2, "gemm_o": cfg.d * q * 2,
+        "gemm_gate_up": 2 * cfg.ffn * cfg.d * 2 + cfg.d * 2 * 2 + cfg.ffn * 2 * 2,
+        "gemm_down": cfg.d * cfg.ffn * 2, "gemm_head": cfg.vocab * cfg.d * 2, "attn": kv_bytes}
+    kern = {}
+    for name, ms in prof["ms"].items():
+        if prof["launches"][name] == 0:
+            continue
+        e = {"ms": round(ms, 5), "launches_per_token": prof["launches"][name]}
+        if name in launch_bytes:
+            e["bytes_per_launch"] = launch_bytes[name]
+            e["GBps"] = round(launch_bytes[name] / (ms * 1e-3) / 1e9, 1)
+        kern[name] = e
+    if "combine" in kern:
+        kern["attn"]["GBps_with_combine"] = round(
+            kv_bytes / ((prof["ms"]["attn"] + prof["ms"]["combine"]) * 1e-3) / 1e9, 1)
+
+    timed = new - 1  # decode(n) returns n tokens; the prefill produced the first
+    mean_ssd, mean_ar = sum(ssd_ms) / len(ssd_ms), sum(ar_ms) / len(ar_ms)
+    value, ar_tps = timed / (mean_ssd / 1e3), timed / (mean_ar / 1e3)
+    token_bytes = (cfg.vocab * cfg.d * 2 + cfg.L * ((q + 2 * kv + q) * cfg.d * 2
+                   + 3 * cfg.ffn * cfg.d * 2) + cfg.L * (ctx + new // 2) * kv * 2 * 2)
+    pvr = []
+    for s in sels:
+        e_tok = sum(s.alpha_hat ** i for i in range(gamma + 1))
+        hd = params.t_head / s.delta
+        cost = gamma * (s.C - s.j_star + hd) + (s.C + hd)  # units of Delta (ms / Delta)
+        pvr.append({"j": s.j_star, "alpha_hat": round(s.alpha_hat, 4),
+                    "predicted_tok_per_ms": round(e_tok / cost / s.delta, 4),
+                    "predicted_tok_per_ms_gamma_star": round(s.tpt_star / s.delta, 4),
+                    "realized_tok_per_ms": (round(s.iv_tokens / s.iv_ms, 4) if s.iv_ms > 0
+                                            else None),
+                    "realized_alpha": (round(s.iv_accepted / s.iv_drafted, 4) if s.iv_drafted
+                                       else None),
+                    "rounds": s.iv_rounds, "tokens": s.iv_tokens, "ms": round(s.iv_ms, 3)})
+    return {
+        "value": round(value, 2), "ms_per_step": round(mean_ssd, 2),
+        "speedup_vs_ar": round(value / ar_tps, 4), "ar_tok_s": round(ar_tps, 2),
+        "ar_ms_per_step": round(mean_ar, 2), "tokens_equal_ar": same,
+        "accepted": st.n_accepted, "drafted": st.n_drafted, "rounds": st.n_rounds,
+        "alpha": round(st.n_accepted / max(1, st.n_drafted), 4),
+        "tokens_per_round": round((st.n_accepted + st.n_rounds) / max(1, st.n_rounds), 3),
+        "select_ms": round(st.ms_select, 2), "selections": st.n_selections,
+        "select_overhead_pct": round(100.0 * st.ms_select / max(1e-9, ssd_ms[-1]), 2),
+        "masks": [{"j": s.j_star, "C": s.C, "w_attn": s.w_attn, "w_mlp": s.w_mlp,
+                   "skipped_attn": int(sum(1 for i in range(0, 2 * cfg.L, 2) if not s.exec[i])),
+                   "skipped_mlp": int(sum(1 for i in range(1, 2 * cfg.L, 2) if not s.exec[i])),
+                   "alpha_hat": round(s.alpha_hat, 3), "gamma_star": s.gamma_star} for s in sels],
+        "predicted_vs_realized": pvr,
+        "ar_step_GBps": round(token_bytes / (mean_ar / timed * 1e-3) / 1e9, 1),
+        "kernels": kern, "_launch_bytes": launch_bytes,
+    }
+
+
+def leg_32k(args):
+    """The 32K workload: Qwen3-8B-shaped decoder (36 layers, per-head q/k norms,
+    vocab 151936), bf16, 32768-token random prompt, 512 new tokens, gamma 6,
+    re-selection every 32; min(steps, 3) timed steps after one warm-up (the
+    leg's own count, to keep the run short).  Its attention runs the streaming
+    decode kernel; that kernel's roofline is reported."""
+    import torch
+    import workloads as W
+    from paper_2602_20217_amd.engine import DeviceModel, select_params
+    cfg = W.config("qwen8b")
+    ctx, new, gamma, reselect = 32768, 512, 6, 32
+    t = time.time()
+    dm = DeviceModel(cfg, n_max=ctx + new + 64, gamma_max=8, m_rounds=5, cap_max=256,
+                     prefill_chunk=512)
+    W.generate_weights(cfg, seed=0, consume=dm.upload)
+    dm.finalize()
+    log(f"qwen8b weights generated and packed in {time.time() - t:.1f}s")
+    prompt = W.prompt_ids(cfg.vocab, ctx, 1)
+    t = time.time()
+    first = dm.prefill(prompt)
+    torch.cuda.synchronize()
+    ms_prefill = (time.time() - t) * 1e3
+    coeffs, sweep = latency_sweep(dm, cfg, [4096, 8192, 16384, 32768], first)
+    params = select_params(coeffs, "paper_min", 0, tau=0.5, prune_half=True, D=10)
+    steps = max(1, min(args.steps, 3))
+    core = measure_decode(dm, cfg, prompt, ctx, new, gamma, reselect, steps, 1, params, False)
+    launch_bytes = core.pop("_launch_bytes")
+    ceiling = stream_ceiling({"attn": launch_bytes["attn"], "gemm_gate_up":
+                              launch_bytes["gemm_gate_up"]})
+    at = core["kernels"]["attn"]
+    at["frac_peak"] = round(at["GBps"] / HBM_PEAK_GBPS, 4)
+    at["stream_ceiling_GBps"] = ceiling["attn"]
+    at["frac_ceiling"] = round(at["GBps"] / ceiling["attn"], 4)
+    dm.close()
+    torch.cuda.empty_cache()
+    out = {"workload": f"{describe(cfg)}, bf16 weights and KV, {ctx}-token random prompt, "
+                       f"{new} new tokens, gamma {gamma}, mask re-selected every {reselect} "
+                       f"tokens", "steps": steps, "warmup": 1, "timed_tokens": new - 1,
+           "tok_s": core.pop("value"), "ms_per_step": core.pop("ms_per_step"),
+           "prefill_ms": round(ms_prefill, 1),
+           "latency_model_ms": {"c1": coeffs[0], "c2": coeffs[1], "c3": coeffs[2]}}
+    out.update(core)
+    out["roofline"] = {"bound": "hbm", "kernel": "k_attn_stream (decode attention, 1 row, "
+                       f"{ctx} cached positions x {cfg.hkv} kv heads)",
+                       "achieved": at["GBps"], "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                       "frac": at["frac_peak"], "traffic": None,
+                       "bytes_per_launch": launch_bytes["attn"], "ms_per_launch": at["ms"],
+                       "stream_ceiling": ceiling["attn"],
+                       "frac_of_stream_ceiling": at["frac_ceiling"]}
+    log(f"qwen8b 32K: {out['tok_s']} tok/s, AR {out['ar_tok_s']} tok/s")
+    return out
 
 
 if __name__ == "__main__":

@@ -110,6 +110,9 @@ typedef struct ks_select_params {
   float tau;          /* cosine pruning threshold (paper: 0.5); -inf disables */
   int prune_half;     /* 1: skipped weight <= C/2 (paper's second pruning rule) */
   int D;              /* largest draft length in the TPT grid (paper: 10) */
+  double t_head;      /* LM head latency in the unit of c1..c3, added to every draft
+                         step and to the verify pass in the TPT cost; 0 (the
+                         paper's cost, which leaves the head out) or > 0 */
 } ks_select_params;
 
 /* Result of one selection. */
@@ -124,6 +127,11 @@ typedef struct ks_selection {
   double tpt_star;   /* TPT of (S*, gamma*) in tokens per Delta */
   double alpha_hat;  /* estimated acceptance of S* (Eq. acceptance) */
   double delta;      /* latency unit Delta */
+  /* ks_generate / ks_decode: the speculative rounds run with this mask, until
+     the next selection or the end of the call (0 elsewhere) */
+  int iv_rounds, iv_drafted, iv_accepted;
+  int iv_tokens;     /* tokens those rounds emitted */
+  double iv_ms;      /* their wall time (selections excluded) */
 } ks_selection;
 
 /* Optional per-decision record of a selection (host arrays the caller sizes;
@@ -527,6 +535,16 @@ ks_status ks_knapsack_batch_select(const int32_t* best, const uint64_t* bits, co
                                    const double* s, int B, int n, int C, int D,
                                    int32_t* j_star, int32_t* gamma_star, double* tpt,
                                    uint8_t* skip, void* stream);
+
+/* ---- measurement reference ---------------------------------------------- */
+/*
+ * ks_stream_read: reads bytes (a multiple of 16; src device memory, 16-byte
+ * aligned) once with 16-byte streaming loads and keeps nothing (sink: device
+ * float32 [1], written only in a case no timing depends on).  The rate it
+ * reaches over a buffer of a decode launch's size is the achievable streaming
+ * rate that the HBM-bound kernels are compared against.  Asynchronous.
+ */
+ks_status ks_stream_read(const void* src, size_t bytes, float* sink, void* stream);
 
 #ifdef __cplusplus
 }

@@ -1,7 +1,8 @@
 """Oracle generation loop: greedy self-speculative decoding with periodic
 re-selection of the skip set (TEST INFRASTRUCTURE ONLY).
 
-The loop follows Section 3 and Appendix B.1: the skip set is chosen from the
+The loop follows Section 3 and Appendix B.1 (t_head, in the latency model's
+time unit, adds the LM head to the TPT cost; 0 keeps the paper's cost): the skip set is chosen from the
 hidden states of the most recent m = 5 speculation rounds (the last prompt rows
 before the first round) and re-chosen every T generated tokens, at the first
 round boundary after the count of generated tokens crosses a multiple of T.  The
@@ -35,7 +36,7 @@ class GenLog:
 def generate(model: M.Model, prompt, n_new: int, gamma: int, T: int, lat,
              quant_mode: str = "paper_min", bins: int = 0, tau: float = 0.5,
              D: int = 10, m_rounds: int = 5, n_max: int | None = None,
-             tau_conf: float = 0.0, gamma_source: str = "fixed"):
+             tau_conf: float = 0.0, gamma_source: str = "fixed", t_head: float = 0.0):
     assert gamma_source in ("fixed", "selected")
     L = model.cfg.L
     n_max = n_max or (len(prompt) + n_new + gamma + 2)
@@ -44,7 +45,8 @@ def generate(model: M.Model, prompt, n_new: int, gamma: int, T: int, lat,
 
     def choose():
         wts = LAT.quantize(lat, st.P, L, quant_mode, bins)
-        sel, _ = SEL.select(model, st, wts.w_attn, wts.w_mlp, wts.C, tau, True, D)
+        sel, _ = SEL.select(model, st, wts.w_attn, wts.w_mlp, wts.C, tau, True, D,
+                            t_head / wts.delta)
         log.selections.append((len(st.out), st.P, wts, sel))
         return sel
 

@@ -5,7 +5,10 @@
 * ``expected_tokens``: Eq. expected_tokens, sum_{i=0}^{gamma} alpha^i (the sum
   form, so alpha = 1 gives gamma + 1).
 * ``tpt``: Eq. TPT with the quantised latencies of Section 3.4, in units of Delta:
-  cost = gamma * (executed weight) + C.
+  cost = gamma * (executed weight) + C.  The paper's t_Draft and t_Target leave
+  out the LM head; ``head`` (in units of Delta, default 0 = the paper's cost)
+  adds it to every draft step and to the verify pass:
+  cost = gamma * (executed weight + head) + (C + head).
 * ``dp_select``: stage 1, Eq. h_candidates and Eq. dp_main with the pruning of
   Section 3.4 (cos threshold tau and skipped weight at most C/2), in the "pull"
   form: cell j of row i takes the execute candidate f^(i)(g[i-1, j]) or the skip
@@ -65,8 +68,8 @@ def expected_tokens(alpha: float, gamma: int) -> float:
     return e
 
 
-def tpt(alpha: float, gamma: int, executed_weight: int, C: int) -> float:
-    return expected_tokens(alpha, gamma) / (gamma * executed_weight + C)
+def tpt(alpha: float, gamma: int, executed_weight: int, C: int, head: float = 0.0) -> float:
+    return expected_tokens(alpha, gamma) / (gamma * (executed_weight + head) + (C + head))
 
 
 def item_weight(i: int, w_attn: int, w_mlp: int) -> int:
@@ -149,8 +152,9 @@ class Selection:
 
 
 def stage2(model: M.Model, dp: DPResult, X_last: np.ndarray, w_attn: int, w_mlp: int,
-           C: int, D: int = 10) -> Selection:
-    """Algorithm 2: backtrack, alpha-hat by argmax agreement, TPT grid."""
+           C: int, D: int = 10, head: float = 0.0) -> Selection:
+    """Algorithm 2: backtrack, alpha-hat by argmax agreement, TPT grid (head:
+    the LM head's latency in units of Delta, 0 for the paper's cost)."""
     _, y_ref, _ = M.head(model, X_last)
     r = X_last.shape[0]
     best = (0.0, None, 0, 0, 0.0)
@@ -164,7 +168,7 @@ def stage2(model: M.Model, dp: DPResult, X_last: np.ndarray, w_attn: int, w_mlp:
         a = n_match / r
         alphas[j], nm[j] = a, n_match
         for gam in range(1, D + 1):
-            v = tpt(a, gam, C - j, C)
+            v = tpt(a, gam, C - j, C, head)
             if v > best[0]:
                 best = (v, ex, j, gam, a)
     v, ex, j, gam, a = best
@@ -172,11 +176,11 @@ def stage2(model: M.Model, dp: DPResult, X_last: np.ndarray, w_attn: int, w_mlp:
 
 
 def select(model: M.Model, st: M.State, w_attn: int, w_mlp: int, C: int,
-           tau: float = 0.5, prune_half: bool = True, D: int = 10):
+           tau: float = 0.5, prune_half: bool = True, D: int = 10, head: float = 0.0):
     """Both stages on the session's history."""
     pos, X = M.history(st)
     dp = dp_select(model, st.cache, pos, X, w_attn, w_mlp, C, tau, prune_half)
-    return stage2(model, dp, X[-1], w_attn, w_mlp, C, D), dp
+    return stage2(model, dp, X[-1], w_attn, w_mlp, C, D, head), dp
 
 
 def brute_force_cos(model: M.Model, cache: M.KVCache, pos: np.ndarray, X: list,

@@ -44,14 +44,16 @@ class Weights(C.Structure):
 class SelectParams(C.Structure):
     _fields_ = [("c1", C.c_double), ("c2", C.c_double), ("c3", C.c_double),
                 ("quant_mode", C.c_int), ("bins", C.c_int), ("tau", C.c_float),
-                ("prune_half", C.c_int), ("D", C.c_int)]
+                ("prune_half", C.c_int), ("D", C.c_int), ("t_head", C.c_double)]
 
 
 class Selection(C.Structure):
     _fields_ = [("exec", C.c_uint8 * KS_MAX_SUBLAYERS), ("j_star", C.c_int),
                 ("gamma_star", C.c_int), ("C", C.c_int), ("w_attn", C.c_int), ("w_mlp", C.c_int),
                 ("n_rows", C.c_int), ("n_cells", C.c_int), ("tpt_star", C.c_double),
-                ("alpha_hat", C.c_double), ("delta", C.c_double)]
+                ("alpha_hat", C.c_double), ("delta", C.c_double), ("iv_rounds", C.c_int),
+                ("iv_drafted", C.c_int), ("iv_accepted", C.c_int), ("iv_tokens", C.c_int),
+                ("iv_ms", C.c_double)]
 
 
 class SelectionDebug(C.Structure):
@@ -150,6 +152,7 @@ _SIG = {
     "ks_knapsack_batch": (_I, [_P, _P, _I, _I, _I, _I, _P, _P, _P]),
     "ks_knapsack_backtrack": (_I, [_P, _P, _I, _I, _I, _P, _P, _P, _P]),
     "ks_knapsack_batch_select": (_I, [_P, _P, _P, _P, _I, _I, _I, _I, _P, _P, _P, _P, _P]),
+    "ks_stream_read": (_I, [_P, C.c_size_t, _P, _P]),
 }
 EXPORTS = tuple(_SIG)
 
@@ -207,5 +210,6 @@ ks_knapsack_quantize = _wrap("ks_knapsack_quantize")
 ks_knapsack_batch = _wrap("ks_knapsack_batch")
 ks_knapsack_backtrack = _wrap("ks_knapsack_backtrack")
 ks_knapsack_batch_select = _wrap("ks_knapsack_batch_select")
+ks_stream_read = _wrap("ks_stream_read")
 ks_kv_cache_bytes = lib.ks_kv_cache_bytes
 ks_workspace_bytes = lib.ks_workspace_bytes

@@ -13,7 +13,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libknapspec.so")
-SOURCES = ["gemm.hip", "attention.hip", "misc.hip", "knapsack.hip", "sample.hip", "engine.hip"]
+SOURCES = ["gemm.hip", "attention.hip", "misc.hip", "knapsack.hip", "sample.hip", "engine.hip",
+           "calibrate.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

@@ -1108,6 +1108,7 @@ static ks_status select_internal(ks_ctx* c, const ks_select_params* p, ks_select
   HIPCHK(hipMemcpyAsync(ham.data(), am, ham.size() * 4, hipMemcpyDeviceToHost, c->st));
   HIPCHK(hipStreamSynchronize(c->st));
   const int32_t* yref = ham.data() + (size_t)nc * r;
+  const double hd = p->t_head / delta;  // the head's cost in units of Delta (0: paper's cost)
   double best = 0.0;
   int bj = 0, bg = 1, bm = r;
   std::vector<uint8_t> bex(L2, 1);
@@ -1123,7 +1124,7 @@ static ks_status select_internal(ks_ctx* c, const ks_select_params* p, ks_select
         e += pw;
         pw *= a;
       }
-      const double v = e / (double)((long long)g * (C - j) + C);
+      const double v = e / ((double)g * ((double)(C - j) + hd) + ((double)C + hd));
       if (v > best) {
         best = v;
         bj = j;
@@ -1157,6 +1158,8 @@ static ks_status select_internal(ks_ctx* c, const ks_select_params* p, ks_select
   out->tpt_star = best;
   out->alpha_hat = (double)bm / r;
   out->delta = delta;
+  out->iv_rounds = out->iv_drafted = out->iv_accepted = out->iv_tokens = 0;
+  out->iv_ms = 0.0;
   return KS_OK;
 }
 
@@ -1170,6 +1173,7 @@ ks_status ks_knapsack_select(ks_ctx* c, const ks_select_params* p, ks_selection*
   REQ(p->D >= 1 && p->D <= 64, "D must be in [1, 64]");
   REQ(p->quant_mode == KS_QUANT_PAPER_MIN || p->quant_mode == KS_QUANT_BINS, "bad quant_mode");
   REQ(!std::isnan(p->tau), "tau is NaN");
+  REQ(std::isfinite(p->t_head) && p->t_head >= 0.0, "t_head must be finite and >= 0");
   if (dbg) REQ(dbg->bits && dbg->reach && dbg->sig_e && dbg->sig_s && dbg->n_match, "null debug array");
   return select_internal(c, p, out, dbg);
 }
@@ -1265,7 +1269,23 @@ static ks_status decode_internal(ks_ctx* c, int n_new, int gamma, int reselect_e
     }
   }
   ks_selection sel{};
+  // the rounds run with the current mask: recorded in its log entry when the
+  // next selection replaces it or the loop ends
+  ks_selection iv{};
+  auto iv_start = now();
+  auto close_interval = [&]() {
+    const int k = st.n_selections - 1;
+    if (sel_log && k >= 0 && k < max_sel_log) {
+      sel_log[k].iv_rounds = iv.iv_rounds;
+      sel_log[k].iv_drafted = iv.iv_drafted;
+      sel_log[k].iv_accepted = iv.iv_accepted;
+      sel_log[k].iv_tokens = iv.iv_tokens;
+      sel_log[k].iv_ms = ms(iv_start, now());
+    }
+    iv = ks_selection{};
+  };
   auto do_select = [&]() -> ks_status {
+    close_interval();
     const auto a = now();
     ks_status r = select_internal(c, p, &sel, nullptr);
     st.ms_select += ms(a, now());
@@ -1273,6 +1293,7 @@ static ks_status decode_internal(ks_ctx* c, int n_new, int gamma, int reselect_e
       if (sel_log && st.n_selections < max_sel_log) sel_log[st.n_selections] = sel;
       st.n_selections++;
     }
+    iv_start = now();
     return r;
   };
   ks_status s = do_select();
@@ -1306,6 +1327,10 @@ static ks_status decode_internal(ks_ctx* c, int n_new, int gamma, int reselect_e
     st.n_rounds++;
     st.n_drafted += g;
     st.n_accepted += a;
+    iv.iv_rounds++;
+    iv.iv_drafted += g;
+    iv.iv_accepted += a;
+    iv.iv_tokens += a + 1;
     const int before = produced;
     for (int t = 1; t <= a && produced < n_new; ++t) out_tokens[produced++] = toks[t];
     if (produced < n_new) out_tokens[produced++] = pred[a];
@@ -1315,6 +1340,7 @@ static ks_status decode_internal(ks_ctx* c, int n_new, int gamma, int reselect_e
     }
   }
   HIPCHK(hipStreamSynchronize(c->st));
+  close_interval();
   st.ms_total = ms(t0, now());
   if (stats) *stats = st;
   return KS_OK;
@@ -1330,6 +1356,7 @@ static ks_status check_decode_args(ks_ctx* c, int n_new, int gamma, int reselect
   if (p) {
     REQ(p->D >= 1 && p->D <= 64, "D must be in [1, 64]");
     REQ(p->quant_mode == KS_QUANT_PAPER_MIN || p->quant_mode == KS_QUANT_BINS, "bad quant_mode");
+    REQ(std::isfinite(p->t_head) && p->t_head >= 0.0, "t_head must be finite and >= 0");
   }
   return KS_OK;
 }

@@ -33,10 +33,11 @@ def _bf16_bits(a: np.ndarray) -> np.ndarray:
     return (u >> 16).astype(np.uint16)
 
 
-def select_params(c, quant_mode="paper_min", bins=0, tau=0.5, prune_half=True, D=10):
+def select_params(c, quant_mode="paper_min", bins=0, tau=0.5, prune_half=True, D=10,
+                  t_head=0.0):
     return K.SelectParams(float(c[0]), float(c[1]), float(c[2]),
                           K.KS_QUANT_BINS if quant_mode == "bins" else K.KS_QUANT_PAPER_MIN,
-                          int(bins), float(tau), 1 if prune_half else 0, int(D))
+                          int(bins), float(tau), 1 if prune_half else 0, int(D), float(t_head))
 
 
 class DeviceModel:

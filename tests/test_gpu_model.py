@@ -392,3 +392,31 @@ def test_draft_policy(setup, tau_mode, source):
         np.testing.assert_array_equal(np.array(sg.exec[:2 * cfg.L], dtype=bool),
                                       sref.exec_mask)
         assert sg.gamma_star == sref.gamma_star
+
+
+def test_head_cost_selections_and_intervals(setup):
+    """Selections with the LM head in the TPT cost (t_head > 0) equal the
+    oracle's on the fp32 decoder; on every model the per-selection interval
+    records add up to the generation's totals."""
+    name, cfg, dm, model = setup
+    c, mode, bins = LAT[name]
+    from paper_2602_20217_amd.engine import select_params
+    prompt = _prompt(cfg, 128, seed=3)
+    t_head = 8 * 0.1625 if name == "tiny" else 0.6  # tiny: 8 latency units (Delta = 0.1625)
+    ssd, st, sels = dm.generate(prompt, 32, gamma=4, reselect_every=8,
+                                params=select_params(c, mode, bins, t_head=t_head))
+    assert sum(s.iv_rounds for s in sels) == st.n_rounds
+    assert sum(s.iv_drafted for s in sels) == st.n_drafted
+    assert sum(s.iv_accepted for s in sels) == st.n_accepted
+    assert sum(s.iv_tokens for s in sels) >= 31  # the prefill's token is not a round's
+    assert all(s.iv_ms > 0 for s in sels if s.iv_rounds)
+    if cfg.dtype == "f32":
+        out, log = GEN.generate(model, prompt, 32, gamma=4, T=8, lat=c, quant_mode=mode,
+                                bins=bins, t_head=t_head)
+        assert list(ssd) == out
+        assert len(log.selections) == len(sels)
+        for (_, P, wts, sref), sg in zip(log.selections, sels):
+            np.testing.assert_array_equal(np.array(sg.exec[:2 * cfg.L], dtype=bool),
+                                          sref.exec_mask)
+            assert (sg.j_star, sg.gamma_star) == (sref.j_star, sref.gamma_star)
+            assert sg.tpt_star == pytest.approx(sref.tpt_star, rel=1e-12)

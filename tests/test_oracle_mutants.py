@@ -135,7 +135,11 @@ def expected_tokens_from_one(alpha, gamma):  # sum over i = 1..gamma
     return sum(alpha ** i for i in range(1, gamma + 1))
 
 
-def tpt_skipped_weight(alpha, gamma, executed_weight, C):  # cost from the skipped weight
+def tpt_head_once(alpha, gamma, executed_weight, C, head=0.0):  # head paid once per round
+    return SEL.expected_tokens(alpha, gamma) / (gamma * executed_weight + C + head)
+
+
+def tpt_skipped_weight(alpha, gamma, executed_weight, C, head=0.0):  # cost from the skipped weight
     return SEL.expected_tokens(alpha, gamma) / (gamma * (C - executed_weight) + C)
 
 
@@ -256,7 +260,7 @@ def _dp(model, cache, pos, X, w_attn, w_mlp, C, tau=0.5, prune_half=True, *,
     return SEL.DPResult(J, reach, g, bits, reach_rows, sig_e, sig_s)
 
 
-def stage2_last_maximum(model, dp, X_last, w_attn, w_mlp, C, D=10):
+def stage2_last_maximum(model, dp, X_last, w_attn, w_mlp, C, D=10, head=0.0):
     """Stage 2 keeping the last of equal TPT values (>= in place of >)."""
     _, y_ref, _ = M.head(model, X_last)
     best = (0.0, None, 0, 0, 0.0)
@@ -270,7 +274,7 @@ def stage2_last_maximum(model, dp, X_last, w_attn, w_mlp, C, D=10):
         a = n_match / X_last.shape[0]
         alphas[j], nm[j] = a, n_match
         for gam in range(1, D + 1):
-            v = SEL.tpt(a, gam, C - j, C)
+            v = SEL.tpt(a, gam, C - j, C, head)
             if v >= best[0]:
                 best = (v, ex, j, gam, a)
     v, ex, j, gam, a = best
@@ -419,6 +423,8 @@ def _mutants(tiny, tiny_hist):
         ("TPT: cost from the skipped weight", SEL, "tpt", tpt_skipped_weight,
          [TSEL.test_tpt_full_model_is_one_over_capacity,
           TSEL.test_tpt_reduces_to_tpl_when_latencies_equal, TSEL.test_stage2_grid_toy]),
+        ("TPT: head cost paid once per round", SEL, "tpt", tpt_head_once,
+         [TSEL.test_tpt_head_cost_closed_forms, TSEL.test_stage2_grid_toy]),
         ("latency fit: slope and intercept exchanged", LAT, "fit_latency", fit_latency_swapped,
          [TSEL.test_latency_fit_recovers_coefficients]),
         ("weights: floor instead of rounding", LAT, "round_half_up", round_floor,
@@ -464,7 +470,7 @@ def _mutants(tiny, tiny_hist):
     ]
 
 
-N_MUTANTS = 39
+N_MUTANTS = 40
 
 
 def test_mutant_table_size(tiny, tiny_hist):

@@ -70,6 +70,20 @@ def test_tpt_full_model_is_one_over_capacity():
             assert SEL.tpt(1.0, g, C, C) == pytest.approx(1.0 / C, rel=1e-15)
 
 
+def test_tpt_head_cost_closed_forms():
+    """With the LM head's cost h (units of Delta) in every draft step and in the
+    verify pass, the full model (alpha 1, executed weight C) still yields one
+    token per (C + h) for every gamma; h = 0 is the paper's cost; a hand value."""
+    for C in (8, 64, 128):
+        for h in (0.5, 3.0, 17.25):
+            for g in range(1, 11):
+                assert SEL.tpt(1.0, g, C, C, h) == pytest.approx(1.0 / (C + h), rel=1e-15)
+    for g in range(1, 11):
+        assert SEL.tpt(0.8, g, 6, 10, 0.0) == SEL.tpt(0.8, g, 6, 10)
+    # C = 10, executed 6, alpha 0.9, gamma 2, h = 2: 2.71 / (2 * 8 + 12)
+    assert SEL.tpt(0.9, 2, 6, 10, 2.0) == pytest.approx(2.71 / 28, rel=1e-14)
+
+
 def test_tpt_reduces_to_tpl_when_latencies_equal():
     """Eq. TPL: TPL(l, gamma) = (1 - a^(g+1))/(1 - a) / (gamma*l + L).  With equal
     sublayer latencies t an early exit at layer l costs 2*l sublayers, so
@@ -133,6 +147,13 @@ def test_stage2_grid_toy():
     sel1 = SEL.stage2(model, dp, X_last, 4, 1, 10, D=1)
     assert (sel1.j_star, sel1.gamma_star) == (4, 1)
     assert sel1.tpt_star == pytest.approx(1.9 / 16, rel=1e-14)
+    # a head costing h = 10 (units of Delta) per forward pass: j=0 gives 1/20 for
+    # every gamma; j=4 (executed 6): gamma 1 1.9/36 = .052777, 2 2.71/52 =
+    # .052115, 3 3.439/68 = .050573; j=5: 1.5/35 = .042857 at best.  The head
+    # makes every extra draft dearer, so gamma 1 wins.
+    selh = SEL.stage2(model, dp, X_last, 4, 1, 10, D=3, head=10.0)
+    assert (selh.j_star, selh.gamma_star) == (4, 1)
+    assert selh.tpt_star == pytest.approx(1.9 / 36, rel=1e-14)
 
 
 @pytest.fixture(scope="module")
