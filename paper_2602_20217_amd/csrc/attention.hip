@@ -491,29 +491,33 @@ __global__ __launch_bounds__(64 * S) void k_attn_dec(
   auto record = [&](int s, int c) -> const float* {
     return (c < 16 ? (const float*)&Ks[s][0] : (const float*)&Vs[s][0]) + (c & 15) * RS;
   };
-  // the split's partial of every column whose row reaches this split: each
-  // thread forms its column's common max and the tile weights itself (the
-  // same values for every dim of a column), so one barrier suffices
-  for (int i = threadIdx.x; i < nc * HD; i += 64 * S) {
-    const int c = i >> 7, d = i & (HD - 1);
-    if (s_len[c] <= start) continue;
-    float ms[S];
+  // the split's partial of every column whose row reaches this split: the
+  // threads are dealt out over the columns (tpc per column); each forms its
+  // column's common max and tile weights once, then its dims d = k, k + tpc, ..
+  // (one barrier; the arithmetic per dim is the same for any thread count)
+  const int tpc = (64 * S) / nc;
+  const int c = threadIdx.x / tpc, k = threadIdx.x - c * tpc;
+  if (c < nc && s_len[c] > start) {
+    float ms[S], wt[S];
     float mx = -FLT_MAX;
 #pragma unroll
     for (int s = 0; s < S; ++s) {
       ms[s] = record(s, c)[HD];
       mx = fmaxf(mx, ms[s]);
     }
-    float acc = 0.f, lx = 0.f;
 #pragma unroll
-    for (int s = 0; s < S; ++s) {
-      const float wt = ms[s] == -FLT_MAX ? 0.f : __builtin_amdgcn_exp2f(ms[s] - mx);
-      acc = fmaf(record(s, c)[d], wt, acc);
-      if (d == 0) lx = fmaf(record(s, c)[HD + 1], wt, lx);
-    }
+    for (int s = 0; s < S; ++s) wt[s] = ms[s] == -FLT_MAX ? 0.f : __builtin_amdgcn_exp2f(ms[s] - mx);
     float* dst = part + (((size_t)(r0 + c / G) * hq + kvh * G + c % G) * nsplit + split) * (HD + 2);
-    dst[d] = acc;
-    if (d == 0) {
+    for (int d = k; d < HD; d += tpc) {
+      float acc = 0.f;
+#pragma unroll
+      for (int s = 0; s < S; ++s) acc = fmaf(record(s, c)[d], wt[s], acc);
+      dst[d] = acc;
+    }
+    if (k == 0) {
+      float lx = 0.f;
+#pragma unroll
+      for (int s = 0; s < S; ++s) lx = fmaf(record(s, c)[HD + 1], wt[s], lx);
       dst[HD] = mx * 0.6931471805599453f;  // back to natural-log units
       dst[HD + 1] = lx;
     }
