@@ -619,8 +619,11 @@ def measure_decode(dm, cfg, prompt, ctx, new, gamma, reselect, steps, warmup, pa
                     "predicted_tok_per_ms_gamma_star": round(s.tpt_star / s.delta, 4),
                     "realized_tok_per_ms": (round(s.iv_tokens / s.iv_ms, 4) if s.iv_ms > 0
                                             else None),
-                    "realized_alpha": (round(s.iv_accepted / s.iv_drafted, 4) if s.iv_drafted
-                                       else None),
+                    "predicted_tokens_per_round": round(e_tok, 3),
+                    "realized_tokens_per_round": (round(s.iv_tokens / s.iv_rounds, 3)
+                                                  if s.iv_rounds else None),
+                    "realized_accept_rate": (round(s.iv_accepted / s.iv_drafted, 4)
+                                             if s.iv_drafted else None),
                     "rounds": s.iv_rounds, "tokens": s.iv_tokens, "ms": round(s.iv_ms, 3)})
     return {
         "value": round(value, 2), "ms_per_step": round(mean_ssd, 2),
