@@ -106,18 +106,22 @@ __global__ __launch_bounds__(NW * 64, MINB) void k_gemm_skinny(
   }
   if (EPI == EPI_QKV && eact) e_pos = qe.pos[em];
 
-  // One-row products (A1, decode and draft steps): the activation row (hi and
-  // lo planes) is staged in LDS once per workgroup, so the k loop's only
-  // global loads are the weight fragments (two activation loads per weight
-  // load cost the load path more time than the weight bytes).  The matrix
-  // instructions see the same operand values either way, so the result bits
-  // do not depend on the path.  The row's loads are issued before the weight
-  // stream and land in LDS after it has started.
+  // One-row products (A1 > 0, decode and draft steps): the activation row
+  // (hi and lo planes) is staged in LDS once per workgroup, so the k loop's
+  // only global loads are the weight fragments.  Loaded per k step, the
+  // activation fragments are two of every three load instructions (every
+  // lane of a row-0 fragment fetches 16 bytes, 16 lanes the same ones), and
+  // the address unit's time for them delays the weight stream's start.  The
+  // matrix instructions see the same operand values either way, so the result
+  // bits do not depend on the path.  A1 = 16-byte pieces per thread and plane
+  // (the launcher takes the least with 64 NW A1 >= K / 8).
   extern __shared__ __align__(16) uint4 s_act[];  // A1: hi plane [K / 8], then lo plane
-  constexpr int A1PT = 4;  // 16-byte chunks per thread and plane (launcher: 4 * 64 NW * 8 >= K)
+  constexpr int A1PT = A1 > 0 ? A1 : 1;
   const int n16 = K >> 3;
   uint4 av[2][A1PT];
   if constexpr (A1 != 0) {
+    // unconditional loads at clamped indices, so the wait before the LDS
+    // store counts only the weight loads issued after them
 #pragma unroll
     for (int pl = 0; pl < 2; ++pl)
 #pragma unroll
@@ -177,9 +181,14 @@ __global__ __launch_bounds__(NW * 64, MINB) void k_gemm_skinny(
     }
   };
   const int nfull = (ke - kb) / CH;  // wave-uniform
-  if (nfull > 0) fetch(kb, w0, x00, x01);
+  auto ck = [&](int c) { return kb + c * CH; };  // the wave's c-th full chunk
   if constexpr (A1 != 0) {
-    // the row lands in LDS; every wave's part is there after the barrier
+    // Two chunks in flight from the start (the launcher gives every wave at
+    // least two): both are requested before the wait for the row, so the
+    // stream does not pause while the row lands in LDS; then chunk c + 2 is
+    // requested after chunk c's matrix instructions.
+    fetch(ck(0), w0, x00, x01);
+    fetch(ck(1), w1, x10, x11);
 #pragma unroll
     for (int pl = 0; pl < 2; ++pl)
 #pragma unroll
@@ -190,20 +199,37 @@ __global__ __launch_bounds__(NW * 64, MINB) void k_gemm_skinny(
     __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's LDS writes are done
     __builtin_amdgcn_s_barrier();
     __asm__ volatile("" ::: "memory");
-  }
-  int c = 0;
-  for (; c + 2 < nfull; c += 2) {  // chunk c is in stage 0 and in flight
-    fetch(kb + (c + 1) * CH, w1, x10, x11);
-    compute(kb + c * CH, w0, x00, x01);
-    fetch(kb + (c + 2) * CH, w0, x00, x01);
-    compute(kb + (c + 1) * CH, w1, x10, x11);
-  }
-  if (c + 1 < nfull) {
-    fetch(kb + (c + 1) * CH, w1, x10, x11);
-    compute(kb + c * CH, w0, x00, x01);
-    compute(kb + (c + 1) * CH, w1, x10, x11);
-  } else if (c < nfull) {
-    compute(kb + c * CH, w0, x00, x01);
+    int c = 0;
+    for (; c + 3 < nfull; c += 2) {  // chunks c and c + 1 are in flight
+      compute(ck(c), w0, x00, x01);
+      fetch(ck(c + 2), w0, x00, x01);
+      compute(ck(c + 1), w1, x10, x11);
+      fetch(ck(c + 3), w1, x10, x11);
+    }
+    compute(ck(c), w0, x00, x01);
+    if (c + 2 < nfull) {
+      fetch(ck(c + 2), w0, x00, x01);
+      compute(ck(c + 1), w1, x10, x11);
+      compute(ck(c + 2), w0, x00, x01);
+    } else {
+      compute(ck(c + 1), w1, x10, x11);
+    }
+  } else {
+    if (nfull > 0) fetch(ck(0), w0, x00, x01);
+    int c = 0;
+    for (; c + 2 < nfull; c += 2) {  // chunk c is in stage 0 and in flight
+      fetch(ck(c + 1), w1, x10, x11);
+      compute(ck(c), w0, x00, x01);
+      fetch(ck(c + 2), w0, x00, x01);
+      compute(ck(c + 1), w1, x10, x11);
+    }
+    if (c + 1 < nfull) {
+      fetch(ck(c + 1), w1, x10, x11);
+      compute(ck(c), w0, x00, x01);
+      compute(ck(c + 1), w1, x10, x11);
+    } else if (c < nfull) {
+      compute(ck(c), w0, x00, x01);
+    }
   }
   for (int k = kb + nfull * CH; k < ke; ++k) {
     bf16x8 b[NB];
@@ -345,12 +371,16 @@ static void launch_skinny_a1(const GemmArgs& g, hipStream_t st) {
 template <int NB, int NW, int CH, int MINB, int AN, int STAGE>
 static void launch_skinny_an(const GemmArgs& g, hipStream_t st) {
   // one row and a shape that gains from it (STAGE): the activation row from
-  // LDS (hi + lo planes, 4 K bytes; 16-byte aligned planes and at most four
-  // chunks per thread and plane)
+  // LDS (hi + lo planes, 4 K bytes; 16-byte aligned planes, at most four
+  // pieces per thread and plane, every wave at least two full chunks)
+  const int pieces = g.K / 8, per = 64 * NW;
   const bool a1 = STAGE && g.M == 1 && g.K % 8 == 0 && (size_t)g.K * 4 <= 64 * 1024 &&
-                  4 * 64 * NW * 8 >= g.K && (((uintptr_t)g.A.hi | (uintptr_t)g.A.lo) & 15) == 0;
-  if (a1) launch_skinny_a1<NB, NW, CH, MINB, AN, 1>(g, st);
-  else launch_skinny_a1<NB, NW, CH, MINB, AN, 0>(g, st);
+                  4 * per >= pieces && (g.K / 32) / NW >= 2 * CH &&
+                  (((uintptr_t)g.A.hi | (uintptr_t)g.A.lo) & 15) == 0;
+  if (!a1) launch_skinny_a1<NB, NW, CH, MINB, AN, 0>(g, st);
+  else if (per >= pieces) launch_skinny_a1<NB, NW, CH, MINB, AN, 1>(g, st);
+  else if (2 * per >= pieces) launch_skinny_a1<NB, NW, CH, MINB, AN, 2>(g, st);
+  else launch_skinny_a1<NB, NW, CH, MINB, AN, 4>(g, st);
 }
 
 template <int NB, int NW, int CH, int MINB, int STAGE>
@@ -365,22 +395,22 @@ static void launch_skinny(const GemmArgs& g, hipStream_t st) {
 // pipelined chunks, workgroups per CU forced by the register budget, staging
 // on or off): gate/up one tile per 4-wave workgroup, 2-deep chunks; the long-K
 // down projection and the square O projection 16 waves, 4-deep; the vocabulary
-// head and the q/k/v projection 8 waves, 4-deep, with the one-row activation
-// staged in LDS (the staging costs the 16-wave and the gate/up shapes more
-// than their activation loads).
+// head and the q/k/v projection 8 waves, 4-deep; every shape with the one-row
+// activation staged in LDS and two chunks per wave in flight from the start
+// (8K decode step 3.22 -> 3.09 ms against per-step activation loads).
 // (output tiles per workgroup, waves, k steps per chunk, workgroups per CU
 // the register budget must allow, one-row activation staged in LDS)
 #ifndef KS_SK_GU
-#define KS_SK_GU 1, 4, 2, 1, 0
+#define KS_SK_GU 1, 4, 2, 1, 1
 #endif
 #ifndef KS_SK_DOWN
-#define KS_SK_DOWN 1, 16, 4, 1, 0
+#define KS_SK_DOWN 1, 16, 4, 1, 1
 #endif
 #ifndef KS_SK_HEAD
 #define KS_SK_HEAD 1, 8, 4, 1, 1
 #endif
 #ifndef KS_SK_SQ
-#define KS_SK_SQ 1, 16, 4, 1, 0
+#define KS_SK_SQ 1, 16, 4, 1, 1
 #endif
 #ifndef KS_SK_WIDE
 #define KS_SK_WIDE 1, 8, 4, 1, 1
