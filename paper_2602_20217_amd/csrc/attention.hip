@@ -269,9 +269,12 @@ typedef __attribute__((__vector_size__(4 * sizeof(__bf16)))) __bf16 bf16x4_d;
 //          value).
 // The S tile results meet in LDS and the whole workgroup merges them in tile
 // order into the split's partial (o, max, sum) per query column, the layout
-// k_attn_combine reads.  (Merging the splits in the last workgroup of the grid
-// instead, behind an atomic ticket, needs an agent-scope release per
-// workgroup, which on this part costs more than the second launch.)
+// k_attn_combine reads.  (Merging the splits inside this launch instead, in
+// the workgroup that draws the last of a per-kv-head ticket, costs more than
+// the second launch, with a release fence per workgroup and also without one:
+// partials stored at device scope, the wait for their acknowledgement, the
+// ticket and the device-scope loads of all partials trail the split
+// workgroups by more than the merge kernel takes.)
 // A column's arithmetic depends only on its own query, its length and the
 // split size, never on the other columns or on CB, so a verify row and the
 // decode step at the same position give the same bits.

@@ -50,7 +50,13 @@ using namespace ks;
 
 namespace {
 
-constexpr int PB = 512;        // rows per batched attention / head pass
+constexpr int PB = 512;        // rows per batched head pass
+// rows per batched attention pass: the selection's whole candidate batch at
+// 8K (up to 49 budgets x 25 rows) in one split launch and one merge launch
+// (a 1225-row selection 2% faster than passes of 512 rows), fewer when the
+// split partials of a pass would exceed PA_PART_BYTES
+constexpr int PA_MAX = 1280;
+constexpr size_t PA_PART_BYTES = (size_t)1 << 30;
 // float32 split-K partials of the batched products (prefill chunks, selection)
 constexpr size_t GPART_BYTES = (size_t)128 << 20;
 // decode/verify splits: 64-position tiles per split, by the model's cache size
@@ -87,7 +93,7 @@ struct Layout {
   size_t tok, pos, len, stage, hist, xh, g0, g1, ge, dpos, dlen, sig, ptrs, ssq, gpart;
   size_t dpc, dpn, dpmean, dpidx, dpbits, dpreach, dpse, dpss;
   size_t vws, tab_ids, tab_pr, tab_cnt, sres, total;
-  int FR, RING, cells, DR, XR, LR, nqkv, a2w, part_rows;
+  int FR, RING, cells, DR, XR, LR, nqkv, a2w, part_rows, PA;
   size_t part_elems;
 };
 
@@ -104,8 +110,10 @@ Layout make_layout(const ks_model_desc& d, const ks_limits& lim) {
   y.a2w = std::max(d.hq * d.hd, d.ffn);
   const int ns_dec = (d.n_max + dec_span(d) - 1) / dec_span(d);
   const int ns_bat = attn_nsplit(d.n_max, BAT_TILES);
-  y.part_rows = PB;
-  y.part_elems = std::max((size_t)16 * d.hq * ns_dec, (size_t)PB * d.hq * ns_bat) * (d.hd + 2);
+  const size_t row_part = (size_t)d.hq * ns_bat * (d.hd + 2) * 4;  // bytes per batched row
+  y.PA = (int)std::max<size_t>(PB, std::min<size_t>(PA_MAX, PA_PART_BYTES / row_part));
+  y.part_rows = y.PA;
+  y.part_elems = std::max((size_t)16 * d.hq * ns_dec, (size_t)y.PA * d.hq * ns_bat) * (d.hd + 2);
   const size_t es = d.dtype == KS_BF16 ? 2 : 4;
   size_t o = 0;
   auto take = [&](size_t bytes) {
@@ -346,7 +354,7 @@ void attn_rows(ks_ctx* c, int l, const float* xin, float* xout, int R, const int
   const int tiles = batched ? BAT_TILES : dec_tiles(d.n_max, d.hkv);
   const int span = batched ? 64 * BAT_TILES : dec_span(d);
   const int ns = (d.n_max + span - 1) / span;
-  const int step = batched ? PB : 16;
+  const int step = batched ? c->y.PA : 16;
   for (int r0 = 0; r0 < R; r0 += step) {
     const int rr = std::min(step, R - r0);
     AttnArgs aa{rr, d.hq, d.hkv, d.hd, d.n_max, d.dtype,

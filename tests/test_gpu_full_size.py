@@ -64,6 +64,31 @@ def test_full_size_sublayers(full, layer, R):
                     "full")
 
 
+def test_full_size_one_row_bits_equal_verify_rows(full):
+    """A decode row (one row: staged activation, splits merged inside the
+    attention launch) gives the same bits as the same row inside a 5-row
+    verify batch (per-step activation loads, separate merge launch), for both
+    sublayers of layer 0 at row lengths on both sides of a split boundary
+    (7999..8003 with 320-position splits)."""
+    cfg, dm = full
+    n = 8000 - 2
+    _fill(cfg, dm, 0, n)
+    dm.set_context(n, 0)
+    x = torch.from_numpy(W.synthetic_rows(5, cfg.d, seed=4, std=1.0, index=77)).cuda()
+    pos = np.arange(5) + n
+    for i in (1, 2):
+        out5 = torch.empty(5, cfg.d, device="cuda")
+        dm.sublayer_apply(i, x, pos, mode=0, out=out5)
+        for r in range(5):
+            out1 = torch.empty(1, cfg.d, device="cuda")
+            dm.sublayer_apply(i, x[r:r + 1].contiguous(), pos[r:r + 1], mode=0, out=out1)
+            diff = int((out1[0] != out5[r]).sum().item())
+            print(f"[bits] sublayer {i} row {r} (length {pos[r] + 1}): {diff} differing elements",
+                  flush=True)
+            assert diff == 0, (i, r)
+        x = out5
+
+
 # Row counts of the selection's candidate batches at 8K (up to 49 budgets x 25
 # history rows): the split-K factor of the tiled products follows the row
 # count, and these three take 1, 2, 3, 4, 5 and 8 splits among the QKV, O and
