@@ -424,9 +424,10 @@ void gemm_bf16_skinny(const GemmArgs& g, hipStream_t st) {
 }
 
 // ------------------------------------------------------------------- tiled
-// Batched rows (prefill chunks, selection DP).  Workgroup tile 64 NWM rows x
-// 16 NWN WN columns, NWM x NWN waves with 64 x 16 WN wave tiles (4 x WN MFMAs).
-// A 32-wide k step of the workgroup is 4 NWM + NWN WN operand tiles of 1 KiB, each
+// Batched rows (prefill chunks, selection DP).  Workgroup tile 16 WM NWM rows x
+// 16 NWN WN columns, NWM x NWN waves with 16 WM x 16 WN wave tiles (WM x WN
+// MFMAs per k step).
+// A 32-wide k step of the workgroup is WM NWM + NWN WN operand tiles of 1 KiB, each
 // laid out in LDS in MFMA register order (lane l at byte 16 l: row l % 16,
 // k 8 (l / 16)..), so every fragment read is one conflict-free 16-byte read.
 // The tiles travel with direct global-to-LDS loads (one 1 KiB load per tile:
@@ -438,21 +439,24 @@ void gemm_bf16_skinny(const GemmArgs& g, hipStream_t st) {
 // logical ids on the same XCD.  Split-K (SK > 1): workgroup (.., ks) adds up
 // k steps [ks KT / SK, (ks + 1) KT / SK) and stores float32 partials
 // part[ks][M][N]; gemm_splitk_reduce adds them in split order.
+#ifndef KS_TILED_WPE
+#define KS_TILED_WPE 1  // waves per SIMD the register budget must allow
+#endif
 __device__ constexpr int vmcnt_imm(int n) {
   // s_waitcnt immediate: vmcnt = n, expcnt and lgkmcnt not waited for
   return (n & 15) | (7 << 4) | (15 << 8) | ((n >> 4) << 14);
 }
 
-template <int EPI, int ST, int WN, int NWM, int NWN>
-__global__ __launch_bounds__(64 * NWM * NWN) void k_gemm_tiled(int M, int N, int K,
+template <int EPI, int ST, int WM, int WN, int NWM, int NWN>
+__global__ __launch_bounds__(64 * NWM * NWN) __attribute__((amdgpu_waves_per_eu(KS_TILED_WPE)))
+void k_gemm_tiled(int M, int N, int K,
                                                     const bf16_t* __restrict__ A, int lda,
                                                     const bf16_t* __restrict__ Wp, float* out,
                                                     int ldo, const float* res, int ldres,
                                                     bf16_t* ohi, bf16_t* olo, int ldact, int MB,
                                                     int NB, int SK, float* __restrict__ part) {
-  constexpr int WM = 4;           // 16-row fragments per wave (64 rows)
   constexpr int NWV = NWM * NWN;  // waves: NWM along M, NWN along N
-  constexpr int PA = NWM * WM;    // A pieces per step: 64 NWM rows
+  constexpr int PA = NWM * WM;    // A pieces per step: 16 WM NWM rows
   constexpr int PB = NWN * WN;   // W pieces per step: 16 NWN WN columns
   constexpr int PPW = (PA + PB) / NWV;
   static_assert((PA + PB) % NWV == 0, "pieces split evenly over the waves");
@@ -465,7 +469,7 @@ __global__ __launch_bounds__(64 * NWM * NWN) void k_gemm_tiled(int M, int N, int
   int lb = bid;
   if ((nblk & 7) == 0) lb = (bid & 7) * (nblk >> 3) + (bid >> 3);
   const int mb = lb % MB, nb = (lb / MB) % NB, ks = lb / (MB * NB);
-  const int m0 = mb * 64 * NWM, nt0 = nb * PB;
+  const int m0 = mb * 16 * WM * NWM, nt0 = nb * PB;
   const int kb = (ks * KT) / SK, nk = ((ks + 1) * KT) / SK - kb;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -531,7 +535,7 @@ __global__ __launch_bounds__(64 * NWM * NWN) void k_gemm_tiled(int M, int N, int
         acc[i][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[t], acc[i][t], 0, 0, 0);
   }
 
-  const int mw = m0 + wm * 64;
+  const int mw = m0 + wm * 16 * WM;
   const int nw = nt0 + wn * WN;
   float* pk = part + (size_t)ks * M * N;
 #pragma unroll
@@ -634,26 +638,26 @@ static int splitk_factor(const GemmArgs& g, int tiles, int KT, int lds_kib) {
   return best_sk;
 }
 
-template <int ST, int WN, int NWM, int NWN>
+template <int ST, int WM, int WN, int NWM, int NWN>
 static void launch_tiled(const GemmArgs& g, hipStream_t st) {
   const int NT = g.N / 16;
   const int KT = g.K / 32;
-  const int MB = (g.M + 64 * NWM - 1) / (64 * NWM);
+  const int MB = (g.M + 16 * WM * NWM - 1) / (16 * WM * NWM);
   const int NB = (NT + NWN * WN - 1) / (NWN * WN);
-  const int SK = splitk_factor(g, MB * NB, KT, ST * (4 * NWM + NWN * WN));
+  const int SK = splitk_factor(g, MB * NB, KT, ST * (WM * NWM + NWN * WN));
   dim3 grid(MB * NB * SK);
   const bf16_t* A = (const bf16_t*)g.A.hi;
   const bf16_t* W = (const bf16_t*)g.W;
   if (g.epi == EPI_SWIGLU)
-    hipLaunchKernelGGL((k_gemm_tiled<EPI_SWIGLU, ST, WN, NWM, NWN>), grid, dim3(64 * NWM * NWN), 0, st, g.M, g.N,
+    hipLaunchKernelGGL((k_gemm_tiled<EPI_SWIGLU, ST, WM, WN, NWM, NWN>), grid, dim3(64 * NWM * NWN), 0, st, g.M, g.N,
                        g.K, A, g.A.ld, W, g.out, g.ldo, g.res, g.ldres, (bf16_t*)g.act_out.hi,
                        (bf16_t*)g.act_out.lo, g.act_out.ld, MB, NB, 1, g.part);
   else if (g.epi == EPI_RESID)
-    hipLaunchKernelGGL((k_gemm_tiled<EPI_RESID, ST, WN, NWM, NWN>), grid, dim3(64 * NWM * NWN), 0, st, g.M, g.N, g.K,
+    hipLaunchKernelGGL((k_gemm_tiled<EPI_RESID, ST, WM, WN, NWM, NWN>), grid, dim3(64 * NWM * NWN), 0, st, g.M, g.N, g.K,
                        A, g.A.ld, W, g.out, g.ldo, g.res, g.ldres, nullptr, nullptr, 0, MB, NB,
                        SK, g.part);
   else
-    hipLaunchKernelGGL((k_gemm_tiled<EPI_STORE, ST, WN, NWM, NWN>), grid, dim3(64 * NWM * NWN), 0, st, g.M, g.N, g.K,
+    hipLaunchKernelGGL((k_gemm_tiled<EPI_STORE, ST, WM, WN, NWM, NWN>), grid, dim3(64 * NWM * NWN), 0, st, g.M, g.N, g.K,
                        A, g.A.ld, W, g.out, g.ldo, g.res, g.ldres, nullptr, nullptr, 0, MB, NB,
                        SK, g.part);
   if (SK > 1) {
@@ -673,6 +677,9 @@ static void launch_tiled(const GemmArgs& g, hipStream_t st) {
 // 128 x 128 / 4 waves (up to 1.3x slower: it moves 33% more operand bytes per
 // flop through the CU's load path), 256 x 128, 256 x 256, 64 x 128 wave tiles
 // and 2..5 stages.
+#ifndef KS_TILED_WM
+#define KS_TILED_WM 4
+#endif
 #ifndef KS_TILED_WN
 #define KS_TILED_WN 4
 #endif
@@ -686,7 +693,7 @@ static void launch_tiled(const GemmArgs& g, hipStream_t st) {
 #define KS_TILED_NWM 2
 #endif
 void gemm_bf16_tiled(const GemmArgs& g, hipStream_t st) {
-  launch_tiled<KS_TILED_ST, KS_TILED_WN, KS_TILED_NWM, KS_TILED_NWN>(g, st);
+  launch_tiled<KS_TILED_ST, KS_TILED_WM, KS_TILED_WN, KS_TILED_NWM, KS_TILED_NWN>(g, st);
 }
 
 // --------------------------------------------------------------------- f32
