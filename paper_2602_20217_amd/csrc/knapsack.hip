@@ -4,32 +4,66 @@
 // One 256-thread workgroup per instance.  Thread t keeps budgets t + 256 e
 // (e < E) of the current row best_{i-1} in registers and mirrors them into
 // one of two LDS rows; E covers only the budgets a skip set can reach
-// (0..min(C, max_skip)), the rest of the row stays INF without being swept; for item i every budget j is updated in parallel from
-// its own best_{i-1}[j] (keep) and best_{i-1}[j - w_i] + q_i (skip, strict),
-// the latter read from LDS, so a cell update costs one LDS read and one LDS
-// write.  A wave owns 64 consecutive budgets per slot e, so its 64 skip
-// decisions form one 64-bit ballot that a single lane stores: the decision
-// bitmap costs one word per 64 budgets per item.  Integer arithmetic only, so
-// results are exact.
+// (0..jmax = min(C, max_skip)), the rest of the row stays INF without being
+// swept.  For item i every budget j is updated in parallel from its own
+// best_{i-1}[j] (keep) and best_{i-1}[j - w_i] + q_i (skip, strict), the
+// latter read from LDS: each LDS row starts with jmax + 1 INF entries, so the
+// skip candidate of every budget is the entry at one per-item base address
+// plus a constant offset per slot (no clamp per cell; a weight above jmax,
+// which no budget can take, is read as jmax + 1).  A wave owns 64
+// consecutive budgets per slot e, so its 64 skip decisions are the compare's
+// own lane mask, written into lane e with one v_writelane per half: the
+// decision bitmap costs one word per 64 budgets per item.  Decision words
+// past the swept budgets are zeroed once, before the items.  Integer
+// arithmetic only, so results are exact.
 #include "ks_internal.h"
 
 namespace ks {
 
 constexpr int32_t KINF = 0x7FFFFFFF;
 
+// Lanes Q..Q+3 of wlo / whi receive the decision masks of slots Q..Q+3 (one
+// v_writelane per half).  The masks were just written to scalar registers by
+// vector compares, and v_writelane reads its scalar source early: without the
+// s_nop ahead of each block some words took the mask of the previous slot.
 template <int E, int Q>
+__device__ inline void knap_put(const uint64_t (&bal)[E], uint32_t& wlo, uint32_t& whi) {
+  if constexpr (Q < E) {
+    if constexpr (Q + 4 <= E) {
+      __asm__(
+          "s_nop 4\n\t"
+          "v_writelane_b32 %0, %2, %10\n\tv_writelane_b32 %1, %3, %10\n\t"
+          "v_writelane_b32 %0, %4, %11\n\tv_writelane_b32 %1, %5, %11\n\t"
+          "v_writelane_b32 %0, %6, %12\n\tv_writelane_b32 %1, %7, %12\n\t"
+          "v_writelane_b32 %0, %8, %13\n\tv_writelane_b32 %1, %9, %13"
+          : "+v"(wlo), "+v"(whi)
+          : "s"((uint32_t)bal[Q]), "s"((uint32_t)(bal[Q] >> 32)), "s"((uint32_t)bal[Q + 1]),
+            "s"((uint32_t)(bal[Q + 1] >> 32)), "s"((uint32_t)bal[Q + 2]),
+            "s"((uint32_t)(bal[Q + 2] >> 32)), "s"((uint32_t)bal[Q + 3]),
+            "s"((uint32_t)(bal[Q + 3] >> 32)), "i"(Q), "i"(Q + 1), "i"(Q + 2), "i"(Q + 3));
+      knap_put<E, Q + 4>(bal, wlo, whi);
+    } else {
+      __asm__("s_nop 4\n\tv_writelane_b32 %0, %2, %4\n\tv_writelane_b32 %1, %3, %4"
+              : "+v"(wlo), "+v"(whi)
+              : "s"((uint32_t)bal[Q]), "s"((uint32_t)(bal[Q] >> 32)), "i"(Q));
+      knap_put<E, Q + 1>(bal, wlo, whi);
+    }
+  }
+}
+
+// Skip decisions of every slot (strict: an equal candidate keeps), then the
+// masks into their lanes.
+template <int E>
 __device__ inline void knap_slots(const uint32_t (&cand)[E], int32_t (&v)[E], uint32_t& wlo,
                                   uint32_t& whi) {
-  if constexpr (Q < E) {
-    const bool take = cand[Q] < (uint32_t)v[Q];
-    v[Q] = take ? (int32_t)cand[Q] : v[Q];
-    const uint64_t ballot = __ballot(take);
-    if ((threadIdx.x & 63) == Q) {
-      wlo = (uint32_t)ballot;
-      whi = (uint32_t)(ballot >> 32);
-    }
-    knap_slots<E, Q + 1>(cand, v, wlo, whi);
+  uint64_t bal[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const bool take = cand[e] < (uint32_t)v[e];
+    v[e] = take ? (int32_t)cand[e] : v[e];
+    bal[e] = __ballot(take);
   }
+  knap_put<E, 0>(bal, wlo, whi);
 }
 
 template <int E>
@@ -37,10 +71,12 @@ __global__ __launch_bounds__(256) void k_knap_dp(const int32_t* __restrict__ w,
                                                  const int32_t* __restrict__ q, int n, int C,
                                                  int max_skip, int32_t* __restrict__ best,
                                                  uint64_t* __restrict__ bits) {
-  // two LDS rows of 256 E + 1 entries: slot e of thread t is budget 256 e + t,
-  // entry 256 E a sentinel that stays INF (budgets past C stay INF too)
+  // two LDS rows of GU + 256 E entries: GU = jmax + 1 INF entries, then slot
+  // e of thread t (budget 256 e + t) at GU + 256 e + t
   extern __shared__ int32_t buf[];
-  constexpr int ROW = 256 * E + 1;
+  const int jmax = min(C, max_skip);
+  const int GU = jmax + 1;
+  const int ROW = GU + 256 * E;
   const int b = blockIdx.x, t = threadIdx.x;
   const int lane = t & 63, wave = t >> 6;
   const int words = C / 64 + 1;
@@ -50,38 +86,40 @@ __global__ __launch_bounds__(256) void k_knap_dp(const int32_t* __restrict__ w,
 #pragma unroll
   for (int e = 0; e < E; ++e) {
     v[e] = e * 256 + t == 0 ? 0 : KINF;
-    row0[e * 256 + t] = v[e];
+    row0[GU + e * 256 + t] = v[e];
   }
-  if (t == 0) row0[256 * E] = row1[256 * E] = KINF;
-  __syncthreads();
+  for (int k = t; k < GU; k += 256) row0[k] = row1[k] = KINF;
   const int32_t* wb = w + (size_t)b * n;
   const int32_t* qb = q + (size_t)b * n;
-  // jv[e]: budget of slot e, or -1 where no skip can land (beyond C or max_skip)
-  const int jmax = min(C, max_skip);
-  int jv[E];
-#pragma unroll
-  for (int e = 0; e < E; ++e) jv[e] = e * 256 + t <= jmax ? e * 256 + t : -1;
-  // decision words past the swept slots (budgets above min(C, max_skip)) are 0
+  // decision words past the swept slots (budgets above jmax) are 0 for every item
   const int swept_words = 4 * E < words ? 4 * E : words;
+  const int rest = words - swept_words;
+  if (rest > 0)
+    for (int k = t; k < n * rest; k += 256)
+      bits[((size_t)b * n + k / rest) * words + swept_words + k % rest] = 0;
+  __syncthreads();
   auto item = [&](int i, const int32_t* src_row, int32_t* dst_row) {
-    const int wi = max(wb[i], 0);                 // negative weights are read as 0
+    const int wi = min(max(wb[i], 0), GU);        // negative weights are read as 0
     const uint32_t qi = (uint32_t)max(qb[i], 0);  // so are negative losses
-    // all reads first (one wait), then the updates, then all writes.  Skip
-    // candidate of slot e: row entry jv[e] - w_i, or the sentinel (entry 256 E)
-    // when that is negative (unsigned min).  An INF candidate never wins:
-    // INF + q_i >= INF >= best, all below 2^32.
+    // all reads first (one wait), then the updates, then all writes.  An INF
+    // candidate never wins: INF + q_i >= INF >= best, all below 2^32.
+    const int32_t* cb = src_row + GU + t - wi;  // >= src_row: wi <= GU
     uint32_t cand[E];
 #pragma unroll
-    for (int e = 0; e < E; ++e)
-      cand[e] = (uint32_t)src_row[min((uint32_t)(jv[e] - wi), (uint32_t)(256 * E))] + qi;
+    for (int e = 0; e < E; ++e) {
+      cand[e] = (uint32_t)cb[e * 256] + qi;
+      // budgets past jmax never take a skip (unreachable); up to 9 slots the
+      // launcher sizes E to the reachable budgets, so only the last slot can
+      // reach past jmax
+      if (e == E - 1 || E > 9) cand[e] |= e * 256 + t > jmax ? 0xFFFFFFFFu : 0u;
+    }
     uint32_t wlo = 0, whi = 0;  // lane e: the 64 decisions of slot e of this wave
-    knap_slots<E, 0>(cand, v, wlo, whi);
+    knap_slots<E>(cand, v, wlo, whi);
 #pragma unroll
-    for (int e = 0; e < E; ++e) dst_row[e * 256 + t] = v[e];
+    for (int e = 0; e < E; ++e) dst_row[GU + e * 256 + t] = v[e];
     const int word = 4 * lane + wave;  // lane e stores word 4 e + wave
     if (lane < E && word < words)
       bits[((size_t)b * n + i) * words + word] = ((uint64_t)whi << 32) | wlo;
-    for (int k = swept_words + t; k < words; k += 256) bits[((size_t)b * n + i) * words + k] = 0;
     __syncthreads();
   };
   int i = 0;
@@ -102,14 +140,16 @@ __global__ __launch_bounds__(256) void k_knap_dp(const int32_t* __restrict__ w,
 template <int E>
 static void launch_knap_dp(const int32_t* w, const int32_t* q, int B, int n, int C, int max_skip,
                            int32_t* best, uint64_t* bits, hipStream_t st) {
-  const size_t lds = 2 * (size_t)(256 * E + 1) * sizeof(int32_t);
+  const int jmax = max_skip < C ? max_skip : C;
+  const size_t lds = 2 * (size_t)(jmax + 1 + 256 * E) * sizeof(int32_t);
   hipLaunchKernelGGL(k_knap_dp<E>, dim3(B), dim3(256), lds, st, w, q, n, C, max_skip, best, bits);
 }
 
 static int knapsack_dp_slots(int C, int max_skip) {
-  // slots per thread: 256 E budgets cover the reachable budgets 0..min(C, max_skip)
+  // slots per thread: 256 E budgets cover the reachable budgets 0..min(C,
+  // max_skip), with no slot wholly past them up to E = 9
   const int need = (max_skip < C ? max_skip : C) + 1;
-  for (int e : {1, 2, 3, 4, 5, 6, 8, 9, 12, 17, 24})
+  for (int e : {1, 2, 3, 4, 5, 6, 7, 8, 9, 12, 17, 24})
     if (need <= 256 * e) return e;
   return 32;  // C <= 8191
 }
@@ -123,6 +163,7 @@ void knapsack_dp(const int32_t* w, const int32_t* q, int B, int n, int C, int ma
     case 4: launch_knap_dp<4>(w, q, B, n, C, max_skip, best, bits, st); break;
     case 5: launch_knap_dp<5>(w, q, B, n, C, max_skip, best, bits, st); break;
     case 6: launch_knap_dp<6>(w, q, B, n, C, max_skip, best, bits, st); break;
+    case 7: launch_knap_dp<7>(w, q, B, n, C, max_skip, best, bits, st); break;
     case 8: launch_knap_dp<8>(w, q, B, n, C, max_skip, best, bits, st); break;
     case 9: launch_knap_dp<9>(w, q, B, n, C, max_skip, best, bits, st); break;
     case 12: launch_knap_dp<12>(w, q, B, n, C, max_skip, best, bits, st); break;
@@ -161,88 +202,135 @@ void knapsack_backtrack(const uint64_t* bits, const int32_t* w, int B, int n, in
 }
 
 // Stage 2 with the surrogate acceptance alpha_j = prod_{i skipped} s_i.
-// One workgroup per instance, threads over budgets; each thread keeps the
-// first strict maximum over gamma for its budget, then a tree keeps the
+// One workgroup per instance, thread t owning budgets t + 256 e.  Instead of a
+// backtrack per budget, one sweep over the items in ascending order carries
+// for every budget the product of the path that ends there: P_i[j] =
+// P_{i-1}[j - w_i] * s_i where item i's decision bit at budget j is set, else
+// P_{i-1}[j], from P_{-1}[0] = 1 (NaN marks a budget no consistent path
+// reaches).  Following the decisions back from (n - 1, j) retraces exactly
+// the path whose skipped items this product takes, in ascending order, so
+// each alpha_j has the bits of the backtrack-then-multiply definition.  The
+// sweep keeps the row in LDS (reads of row i - 1, a barrier, then the writes
+// of row i) and stops at the largest reachable budget.  Then each thread keeps
+// the first strict maximum over gamma for its budgets, and a tree keeps the
 // largest value and, on equal values, the smallest budget: the same winner as
 // a sequential scan over (j ascending, gamma ascending) with strict ">".
-// The instance's decision words (and w, s) are staged in LDS when they fit;
-// a thread walks four of its budgets' backtracks side by side so their
-// dependent reads overlap.  Items are limited to 128 so a backtracked mask
-// fits two 64-bit words.
-template <bool BITS_IN_LDS>
+// Items are limited to 128 (the per-item weights and scores live in LDS).
+// The sweep and the TPT grid over the first EL slots (EL covers the largest
+// reachable budget): branch-free per slot, so each phase's LDS reads are in
+// flight together.
+template <int EL>
+__device__ __forceinline__ void knap_select_sweep(int n, int C, int D, int tid, int lane,
+                                                  int wave, int words,
+                                                  const uint64_t* __restrict__ bb, double* row,
+                                                  const int32_t* sw, const double* ss,
+                                                  uint32_t live, long long W, double& bv, int& bj,
+                                                  int& bg) {
+#pragma clang fp contract(off)
+  const double NaN = __builtin_nan("");
+  double pv[EL];
+#pragma unroll
+  for (int e = 0; e < EL; ++e) pv[e] = 256 * e + tid == 0 ? 1.0 : NaN;
+  for (int i = 0; i < n; ++i) {
+    const int wi = sw[i];
+    const double si = ss[i];
+    double cand[EL];
+    uint64_t word[EL];
+#pragma unroll
+    for (int e = 0; e < EL; ++e) {
+      const int j = 256 * e + tid;
+      const double c = row[j >= wi ? j - wi : 0];
+      cand[e] = j >= wi ? c : NaN;
+      const int wd = 4 * e + wave;  // word of budgets 256 e + 64 wave + lane
+      word[e] = bb[(size_t)i * words + (wd < words ? wd : 0)];
+      if (wd >= words) word[e] = 0ull;
+    }
+    __syncthreads();  // row i - 1 read by every thread before it is overwritten
+#pragma unroll
+    for (int e = 0; e < EL; ++e) {
+      const double m = cand[e] * si;
+      pv[e] = ((word[e] >> lane) & 1ull) ? m : pv[e];
+      row[256 * e + tid] = pv[e];
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int e = 0; e < EL; ++e) {  // ascending budgets
+    const double a = pv[e];
+    if (!((live >> e) & 1u) || a != a) continue;  // unreached, or inconsistent decisions
+    const int j0 = 256 * e + tid;
+    // e_g = 1 + a + ... + a^g, summed in ascending powers; one running sum
+    // over g gives the same additions in the same order as summing anew
+    double eg = 1.0, p = a;
+    for (int g = 1; g <= D; ++g) {
+      eg = eg + p;
+      p = p * a;
+      const double cost = (double)((long long)g * (W - j0) + W);
+      const double v = eg / cost;
+      if (v > bv) {
+        bv = v;
+        bj = j0;
+        bg = g;
+      }
+    }
+  }
+}
+
+template <int E>
 __global__ __launch_bounds__(256) void k_knap_select(
     const int32_t* __restrict__ best, const uint64_t* __restrict__ bits,
     const int32_t* __restrict__ w, const double* __restrict__ s, int n, int C, int D,
     int32_t* j_star, int32_t* g_star, double* tpt, uint8_t* skip) {
-#pragma clang fp contract(off)
-  extern __shared__ uint64_t lbits[];
+  extern __shared__ double row[];  // 256 E: budget 256 e + tid at 256 e + tid
   __shared__ double sv[256];
   __shared__ int sj[256], sg[256];
   __shared__ int32_t sw[128];
   __shared__ double ss[128];
+  __shared__ int s_jl;
   const int b = blockIdx.x, tid = threadIdx.x;
+  const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int words = C / 64 + 1;
-  const uint64_t* gb = bits + (size_t)b * n * words;
-  if (BITS_IN_LDS)
-    for (int k = tid; k < n * words; k += 256) lbits[k] = gb[k];
+  // the instance's decision words: one word per wave and slot, read with
+  // scalar loads (the address is the same for every lane of the wave)
+  const uint64_t* bb = bits + (size_t)b * n * words;
   for (int i = tid; i < n; i += 256) {
     sw[i] = max(w[(size_t)b * n + i], 0);  // negative weights are read as 0, as in the DP
     ss[i] = s[(size_t)b * n + i];
   }
+  if (tid == 0) s_jl = 0;
+  uint32_t live = 0;  // bit e: budget 256 e + tid is reachable
+  int jl = 0;
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const int j = 256 * e + tid;
+    if (j <= C && best[(size_t)b * (C + 1) + j] != KINF) {
+      live |= 1u << e;
+      jl = j;
+    }
+    row[j] = j == 0 ? 1.0 : __builtin_nan("");
+  }
   __syncthreads();
-  const uint64_t* bb = BITS_IN_LDS ? lbits : gb;
+  atomicMax(&s_jl, jl);
+  __syncthreads();
+  const int EL = s_jl / 256 + 1;  // slots up to the largest reachable budget
   long long W = 0;
   for (int i = 0; i < n; ++i) W += sw[i];
   double bv = 0.0;
   int bj = 0x7FFFFFFF, bg = 0;
-  constexpr int G = 4;
-  for (int k0 = 0; k0 * 256 <= C; k0 += G) {
-    int jj[G], j0[G];
-    uint64_t m0[G], m1[G];
-    bool live[G];
-#pragma unroll
-    for (int u = 0; u < G; ++u) {
-      j0[u] = (k0 + u) * 256 + tid;
-      live[u] = j0[u] <= C && best[(size_t)b * (C + 1) + j0[u]] != KINF;
-      jj[u] = j0[u];
-      m0[u] = m1[u] = 0;
-    }
-    if (!(live[0] || live[1] || live[2] || live[3])) continue;
-    for (int i = n - 1; i >= 0; --i) {
-      const int wi = sw[i];
-#pragma unroll
-      for (int u = 0; u < G; ++u) {
-        if (live[u] && jj[u] >= 0 && jj[u] <= C &&
-            ((bb[i * words + (jj[u] >> 6)] >> (jj[u] & 63)) & 1ull)) {
-          if (i < 64) m0[u] |= 1ull << i; else m1[u] |= 1ull << (i - 64);
-          jj[u] -= wi;
-        }
-      }
-    }
-#pragma unroll
-    for (int u = 0; u < G; ++u) {  // ascending budgets
-      if (!live[u] || jj[u] != 0) continue;  // inconsistent decisions: not a candidate
-      double a = 1.0;
-      for (int i = 0; i < n; ++i) {
-        const bool sk = i < 64 ? ((m0[u] >> i) & 1ull) : ((m1[u] >> (i - 64)) & 1ull);
-        if (sk) a = a * ss[i];
-      }
-      // e_g = 1 + a + ... + a^g, summed in ascending powers; one running sum
-      // over g gives the same additions in the same order as summing anew
-      double e = 1.0, p = a;
-      for (int g = 1; g <= D; ++g) {
-        e = e + p;
-        p = p * a;
-        const double cost = (double)((long long)g * (W - j0[u]) + W);
-        const double v = e / cost;
-        if (v > bv) {
-          bv = v;
-          bj = j0[u];
-          bg = g;
-        }
-      }
-    }
-  }
+#define KS_SWEEP(L_)                                                                          \
+  knap_select_sweep<(L_ < E ? L_ : E)>(n, C, D, tid, lane, wave, words, bb, row, sw, ss, live, \
+                                       W, bv, bj, bg)
+  if (EL <= 1) KS_SWEEP(1);
+  else if (EL <= 2) KS_SWEEP(2);
+  else if (EL <= 3) KS_SWEEP(3);
+  else if (EL <= 4) KS_SWEEP(4);
+  else if (EL <= 6) KS_SWEEP(6);
+  else if (EL <= 9) KS_SWEEP(9);
+  else if (EL <= 12) KS_SWEEP(12);
+  else if (EL <= 17) KS_SWEEP(17);
+  else if (EL <= 24) KS_SWEEP(24);
+  else KS_SWEEP(32);
+#undef KS_SWEEP
   sv[tid] = bv;
   sj[tid] = bj;
   sg[tid] = bg;
@@ -276,16 +364,36 @@ __global__ __launch_bounds__(256) void k_knap_select(
   }
 }
 
+template <int E>
+static void launch_knap_select(const int32_t* best, const uint64_t* bits, const int32_t* w,
+                               const double* s, int B, int n, int C, int D, int32_t* j_star,
+                               int32_t* g_star, double* tpt, uint8_t* skip, hipStream_t st) {
+  const size_t rowb = (size_t)256 * E * sizeof(double);
+  hipLaunchKernelGGL(k_knap_select<E>, dim3(B), dim3(256), rowb, st, best, bits, w, s, n, C, D,
+                     j_star, g_star, tpt, skip);
+}
+
 void knapsack_select(const int32_t* best, const uint64_t* bits, const int32_t* w,
                      const double* s, int B, int n, int C, int D, int32_t* j_star,
                      int32_t* g_star, double* tpt, uint8_t* skip, hipStream_t st) {
-  const size_t lds = (size_t)n * (C / 64 + 1) * 8;
-  if (lds <= 48 * 1024)
-    hipLaunchKernelGGL(k_knap_select<true>, dim3(B), dim3(256), lds, st, best, bits, w, s, n, C, D,
-                       j_star, g_star, tpt, skip);
-  else
-    hipLaunchKernelGGL(k_knap_select<false>, dim3(B), dim3(256), 0, st, best, bits, w, s, n, C, D,
-                       j_star, g_star, tpt, skip);
+#define KS_SEL(E_)                                                                           \
+  launch_knap_select<E_>(best, bits, w, s, B, n, C, D, j_star, g_star, tpt, skip, st); break
+  switch (knapsack_dp_slots(C, C)) {  // slots covering every budget 0..C
+    case 1: KS_SEL(1);
+    case 2: KS_SEL(2);
+    case 3: KS_SEL(3);
+    case 4: KS_SEL(4);
+    case 5: KS_SEL(5);
+    case 6: KS_SEL(6);
+    case 7: KS_SEL(7);
+    case 8: KS_SEL(8);
+    case 9: KS_SEL(9);
+    case 12: KS_SEL(12);
+    case 17: KS_SEL(17);
+    case 24: KS_SEL(24);
+    default: KS_SEL(32);
+  }
+#undef KS_SEL
 }
 
 // ------------------------------------------------------- model-mode step
