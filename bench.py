@@ -343,6 +343,8 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=20.0)
     ap.add_argument("--no-knapsack", action="store_true",
                     help="skip the isolated knapsack batch leg")
+    ap.add_argument("--knapsack-only", action="store_true",
+                    help="only the isolated knapsack batch leg (for traces of its kernels)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-32k", action="store_true",
                     help="skip the 32K leg (Qwen3-8B shape, 32768-token prompt, gamma 6)")
@@ -379,6 +381,10 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     cfg = W.config(args.model)
+    if args.knapsack_only:
+        leg, _ = knapsack_leg(args.steps, args.warmup)
+        print(json.dumps({"mode": "knapsack-only", **leg}), flush=True)
+        return
     if args.calibrate_stream:
         q, kv = cfg.hq * cfg.hd, cfg.hkv * cfg.hd
         sizes = {"gemm_o": cfg.d * q * 2, "attn": args.ctx * kv * 2 * 2,
