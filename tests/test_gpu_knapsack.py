@@ -98,15 +98,25 @@ def test_backtrack_flags_bad_budget(E):
 def test_dead_budgets_and_slot_sizes(E, C, max_skip):
     """The DP sweeps only the budgets a skip set can reach (0..min(C, max_skip));
     every other cell must still read INF and every decision word above them 0,
-    for slot counts from one to 32 per thread."""
+    for slot counts from one to 32 per thread.  Stage 2 sweeps up to the largest
+    reachable budget (one to 24 slots here): its selection, TPT and mask must
+    equal the oracle's on the same instances."""
     rng = np.random.default_rng(C + max_skip)
     B, n = 8, 40
     w = rng.integers(1, max(2, C // 12), size=(B, n)).astype(np.int32)
     q = rng.integers(0, 1 << 20, size=(B, n)).astype(np.int32)
-    _, best, bits = _run(E, w, q, C, max_skip)
+    wd, best, bits = _run(E, w, q, C, max_skip)
     best0, bits0 = A.knapsack_dp(w, q, C, max_skip)
     np.testing.assert_array_equal(best.cpu().numpy(), best0)
     np.testing.assert_array_equal(bits.cpu().numpy().view(np.uint64), bits0)
+    s = rng.uniform(0.9, 1.0, size=(B, n))
+    js, gs, tpt, skip = E.knapsack_batch_select(best, bits, wd, torch.from_numpy(s).cuda(), C,
+                                                D=10)
+    js, gs, tpt, skip = js.cpu().numpy(), gs.cpu().numpy(), tpt.cpu().numpy(), skip.cpu().numpy()
+    for b in (0, B - 1):
+        j0, g0, v0, sk0 = A.stage2(best0[b], bits0[b], w[b], s[b], D=10)
+        assert (js[b], gs[b]) == (j0, g0) and v0 == tpt[b], b
+        np.testing.assert_array_equal(skip[b], sk0)
 
 
 def test_negative_weights_and_losses_read_as_zero(E):
