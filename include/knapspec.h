@@ -529,7 +529,8 @@ ks_status ks_knapsack_backtrack(const uint64_t* bits, const int32_t* w, int B, i
  * (gamma (W - j) + W) with W = sum_i w_i; j ascending, gamma ascending, first
  * strict maximum wins.  Outputs j_star, gamma_star (int32 [B]), tpt (double
  * [B]) and skip (uint8 [B][n]); s is device double [B][n].  Negative weights
- * are read as 0 (also in W), as by ks_knapsack_batch.  Asynchronous.
+ * are read as 0 (also in W), as by ks_knapsack_batch.  Requires 1 <= n <= 128,
+ * 0 <= C <= 8191 and 1 <= D <= 64 (KS_EINVAL otherwise).  Asynchronous.
  */
 ks_status ks_knapsack_batch_select(const int32_t* best, const uint64_t* bits, const int32_t* w,
                                    const double* s, int B, int n, int C, int D,
