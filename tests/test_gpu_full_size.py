@@ -4,8 +4,9 @@ a 128K-position context (streaming attention splits, as in the context sweep).
 
 Sampled outputs the oracle computes one by one: single sublayers (first and last
 layer) on decode (1 row) and verify (5 rows) inputs over seeded caches of
-8189 and 131067 positions, the last layer on 400, 800 and 1225 candidate rows
-of the selection (tiled MFMA products with 1 to 8 K splits, batched attention;
+8189 and 131067 positions, the last layer on 400, 600, 800 and 1225 candidate
+rows of the selection (tiled MFMA products with 1 to 8 K splits, batched
+attention;
 sampled rows at tile edges and in the ragged tail), the LM head on two rows
 (tolerance 2e-2 relative),
 and the sampling filter of head logits against the oracle's filter of the same
@@ -91,9 +92,9 @@ def test_full_size_one_row_bits_equal_verify_rows(full):
 
 # Row counts of the selection's candidate batches at 8K (up to 49 budgets x 25
 # history rows): the split-K factor of the tiled products follows the row
-# count, and these three take 1, 2, 3, 4, 5 and 8 splits among the QKV, O and
-# down products.
-@pytest.mark.parametrize("R", [400, 800, 1225])
+# count, and these take 1, 2, 3, 4, 5 and 8 splits among the QKV, O and down
+# products (600 rows: a fifth 128-row tile with 88 rows).
+@pytest.mark.parametrize("R", [400, 600, 800, 1225])
 def test_full_size_batched_sublayers(full, R):
     """Attention with each row's own key/value (the selection's candidate rows)
     and then the MLP of the last layer on R rows.  Rows do not see each other in
