@@ -363,12 +363,23 @@ def test_draft_policy(setup, tau_mode, source):
     else:
         _, log0 = GEN.generate(model, prompt, 24, gamma=4, T=8, lat=c, quant_mode=mode,
                                bins=bins)
-        # the midpoint of the widest gap between observed confidences in their
-        # middle half: a threshold that splits them with a margin
+        # midpoints of the gaps between observed confidences in their middle
+        # half, widest first: a threshold that splits them with a margin.  On
+        # the fp32 model (compared with the oracle round by round) the first
+        # one whose own run keeps every draft confidence clear of it by 1e-3
+        # (relative) is taken, since the exit changes which drafts are made.
         tops = np.sort([p for r in log0.draft_top1 for p in r])
         lo, hi = len(tops) // 4, max(len(tops) // 4 + 1, 3 * len(tops) // 4)
-        i = lo + int(np.argmax(np.diff(tops[lo:hi + 1])))
-        tau = float(0.5 * (tops[i] + tops[i + 1]))
+        gaps = np.diff(tops[lo:hi + 1])
+        cands = [float(0.5 * (tops[lo + i] + tops[lo + i + 1])) for i in np.argsort(-gaps)]
+        tau = cands[0]
+        if cfg.dtype == "f32":
+            for t in cands:
+                _, lg = GEN.generate(model, prompt, 24, gamma=4, T=8, lat=c, quant_mode=mode,
+                                     bins=bins, tau_conf=t, gamma_source=source)
+                if min(abs(p - t) for r in lg.draft_top1 for p in r) >= 1e-3 * t:
+                    tau = t
+                    break
     try:
         dm.set_draft_policy(tau, source)
         sd, st, sels = dm.generate(prompt, 24, gamma=4, reselect_every=8, params=params)
