@@ -47,6 +47,33 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
+def launch_timer(n):
+    """n pairs of timing-enabled HIP events, each recorded once so its handle
+    exists, and a call that times what `fn` launches with one pair: the
+    library's kernels carry the pair in their own dispatches (ks_time_launches),
+    so the elapsed time is the kernels' execution, as a kernel trace reports it."""
+    import torch
+    from paper_2602_20217_amd import _lib as K
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(n)]
+    for a, b in ev:
+        a.record()
+        b.record()
+
+    def timed(k, fn):
+        K.ks_time_launches(ev[k][0].cuda_event, ev[k][1].cuda_event)
+        try:
+            fn()
+        finally:
+            K.ks_time_launches(None, None)
+
+    def median_ms():
+        torch.cuda.synchronize()
+        return sorted(a.elapsed_time(b) for a, b in ev)[n // 2]
+
+    return timed, median_ms
+
+
 def fit_line(n, t):
     """least-squares t = a n + b"""
     import numpy as np
@@ -126,8 +153,8 @@ KNAP_OPS_PER_CELL = 3  # one add, one compare, one select per cell update
 def knapsack_leg(steps, warmup):
     """The isolated knapsack batch (1024 instances x 72 items x 4097 budgets,
     Llama-8B-shaped latencies, 4096 bins, skipped weight <= 2048): DP with
-    decision bits, then stage 2 (backtrack + TPT grid, D = 10), timed with HIP
-    events on the launch stream."""
+    decision bits, then stage 2 (backtrack + TPT grid, D = 10); the median
+    launch of each, timed by HIP events carried in the launches."""
     import torch
     import workloads as W
     from paper_2602_20217_amd.engine import (knapsack_quantize, knapsack_batch,
@@ -141,20 +168,18 @@ def knapsack_leg(steps, warmup):
         best, bits = knapsack_batch(wd, qd, C, max_skip)
         knapsack_batch_select(best, bits, wd, sd, C, 10)
     torch.cuda.synchronize()
-    # back-to-back launches between the events, so host submission gaps are
-    # hidden behind the queued work
-    e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
-    reps = 10
-    e[0].record()
-    for _ in range(reps * steps):
-        best, bits = knapsack_batch(wd, qd, C, max_skip)
-    e[1].record()
-    for _ in range(reps * steps):
-        knapsack_batch_select(best, bits, wd, sd, C, 10)
-    e[2].record()
-    e[2].synchronize()
-    ms_dp = e[0].elapsed_time(e[1]) / (reps * steps)
-    ms_sel = e[1].elapsed_time(e[2]) / (reps * steps)
+    # median launch of each kernel, timed by events its dispatches carry
+    reps = 10 * steps
+    out = {}
+    timed, median_ms = launch_timer(reps)
+    for k in range(reps):
+        timed(k, lambda: out.update(r=knapsack_batch(wd, qd, C, max_skip)))
+    ms_dp = median_ms()
+    best, bits = out["r"]
+    timed, median_ms = launch_timer(reps)
+    for k in range(reps):
+        timed(k, lambda: knapsack_batch_select(best, bits, wd, sd, C, 10))
+    ms_sel = median_ms()
     # algorithmic work: the budgets a skip set can reach (0..min(C, max_skip));
     # the cells above max_skip are INF by definition and not swept
     live = min(C, max_skip) + 1
@@ -531,10 +556,9 @@ def coeffs_head(sweep):
 
 def stream_ceiling(sizes, pool_bytes=2 << 30, reps=40):
     """Rate (GB/s) of ks_stream_read, a plain streaming read, over buffers of each
-    size, timed with HIP events around every launch like the decode kernels
-    (launch overhead included; median launch); the buffers rotate through a
-    pool larger than the 256 MiB last-level cache so no launch finds its bytes
-    cached."""
+    size, timed like the decode kernels by HIP events carried in each launch
+    (median launch); the buffers rotate through a pool larger than the 256 MiB
+    last-level cache so no launch finds its bytes cached."""
     import torch
     from paper_2602_20217_amd import _lib as K
     pool = torch.empty(pool_bytes, dtype=torch.uint8, device="cuda")
@@ -552,18 +576,14 @@ def stream_ceiling(sizes, pool_bytes=2 << 30, reps=40):
             continue
         if nb not in by_size:
             nrot = max(1, pool_bytes // nb)
-            ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-                  for _ in range(reps)]
+            timed, median_ms = launch_timer(reps)
             for k in range(5):
                 K.ks_stream_read(pool.data_ptr() + (k % nrot) * nb, nb, sink.data_ptr(),
                                  st.cuda_stream)
-            for k, (a, b) in enumerate(ev):
-                a.record(st)
-                K.ks_stream_read(pool.data_ptr() + ((k + 5) % nrot) * nb, nb, sink.data_ptr(),
-                                 st.cuda_stream)
-                b.record(st)
-            torch.cuda.synchronize()
-            ms = sorted(a.elapsed_time(b) for a, b in ev)[reps // 2]
+            for k in range(reps):
+                src = pool.data_ptr() + ((k + 5) % nrot) * nb
+                timed(k, lambda: K.ks_stream_read(src, nb, sink.data_ptr(), st.cuda_stream))
+            ms = median_ms()
             by_size[nb] = round(nb / (ms * 1e-3) / 1e9, 1)
         out[name] = by_size[nb]
     del pool

@@ -459,13 +459,26 @@ typedef struct ks_kernel_profile {
 /*
  * ks_profile_decode: runs `steps` single-row decode steps with mask exec (NULL =
  * every sublayer) at the committed position P and times them with HIP events
- * on the context stream; with per_kernel = 1 an event pair also brackets every
- * kernel launch (ms[] and launches[] are filled; otherwise they are 0).  Each
+ * on the context stream; with per_kernel = 1 every kernel launch also carries
+ * an event pair in its own dispatch, as under ks_time_launches (ms[] and
+ * launches[] are filled; otherwise they are 0).  Each
  * step writes the keys/values of position P (as a draft step would) and
  * commits nothing.
  */
 ks_status ks_profile_decode(ks_ctx* ctx, const uint8_t* exec, int steps, int per_kernel,
                             ks_kernel_profile* out);
+/*
+ * ks_time_launches: opens a kernel timing bracket on the calling thread
+ * (start_event and stop_event: hipEvent_t handles created by the caller with
+ * timing enabled), or closes it (both NULL).  While it is open, every kernel the
+ * library launches from this thread carries the events in its own dispatch:
+ * the first launch records start_event when that kernel begins, every launch
+ * records stop_event when it ends, so the elapsed time between them covers the
+ * kernels' execution only (no event packets between launches).  A bracket
+ * closed without launches records neither event.  Opening a bracket replaces
+ * an open one.  Both handles must be set or both NULL (KS_EINVAL otherwise).
+ */
+ks_status ks_time_launches(void* start_event, void* stop_event);
 
 /* ---- lower-level calls (per-sublayer parity and latency profiling) ------- */
 /*

@@ -146,6 +146,7 @@ _SIG = {
     "ks_spec_accept": (_I, [_P, _P, _P, _P, _P, _P, _P, _I, C.c_uint64, _I, _P, _P]),
     "ks_sample_uniforms": (_I, [C.c_uint64, _P, _I, _I, _P, _P]),
     "ks_profile_decode": (_I, [_P, _P, _I, _I, C.POINTER(KernelProfile)]),
+    "ks_time_launches": (_I, [_P, _P]),
     "ks_sublayer_apply": (_I, [_P, _I, _P, _P, _P, _I, _I]),
     "ks_head_rows": (_I, [_P, _P, _I, _P, _P, _P]),
     "ks_knapsack_quantize": (_I, [_P, _P, _I, _I, _I, _P, _P]),
@@ -204,6 +205,7 @@ ks_spec_accept = _wrap("ks_spec_accept")
 ks_sample_uniforms = _wrap("ks_sample_uniforms")
 ks_sample_workspace_bytes = lib.ks_sample_workspace_bytes
 ks_profile_decode = _wrap("ks_profile_decode")
+ks_time_launches = _wrap("ks_time_launches")
 ks_sublayer_apply = _wrap("ks_sublayer_apply")
 ks_head_rows = _wrap("ks_head_rows")
 ks_knapsack_quantize = _wrap("ks_knapsack_quantize")

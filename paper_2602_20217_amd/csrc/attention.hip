@@ -1209,7 +1209,7 @@ void attn_split(const AttnArgs& a, hipStream_t st) {
   const int nq = a.rows_per_block * G;
   dim3 grid(ns, a.hkv, (a.M + a.rows_per_block - 1) / a.rows_per_block);
 #define KS_ATTN(HDV, BFV, QM)                                                                \
-  hipLaunchKernelGGL((k_attn_split<HDV, BFV, QM>), grid, dim3(256), 0, st, a.M, a.hq, a.hkv, \
+  KS_LAUNCH((k_attn_split<HDV, BFV, QM>), grid, dim3(256), 0, st, a.M, a.hq, a.hkv, \
                      a.n_max, a.q, a.kc, a.vc, a.len, a.tiles, a.rows_per_block, a.part,     \
                      a.nsplit)
   if (attn_dec_path(a)) {
@@ -1221,7 +1221,7 @@ void attn_split(const AttnArgs& a, hipStream_t st) {
     const bf16_t* kc = (const bf16_t*)a.kc;
     const bf16_t* vc = (const bf16_t*)a.vc;
 #define KS_DEC(S_, CB_)                                                                      \
-  hipLaunchKernelGGL((k_attn_dec<S_, CB_>), g3, dim3(64 * S_), 0, st, a.M, a.hq, a.hkv,       \
+  KS_LAUNCH((k_attn_dec<S_, CB_>), g3, dim3(64 * S_), 0, st, a.M, a.hq, a.hkv,       \
                      a.n_max, a.q, kc, vc, a.len, a.part, a.nsplit, a.span)
 #define KS_DEC_S(CB_)            \
   switch (a.tiles) {             \
@@ -1234,10 +1234,10 @@ void attn_split(const AttnArgs& a, hipStream_t st) {
     if (a.tiles > 5) {
       const int tpw = a.tiles / STREAM_NW;
       if (CB == 1)
-        hipLaunchKernelGGL((k_attn_stream<STREAM_NW, 1>), g3, dim3(64 * STREAM_NW), 0, st, a.M,
+        KS_LAUNCH((k_attn_stream<STREAM_NW, 1>), g3, dim3(64 * STREAM_NW), 0, st, a.M,
                            a.hq, a.hkv, a.n_max, a.q, kc, vc, a.len, a.part, a.nsplit, tpw);
       else
-        hipLaunchKernelGGL((k_attn_stream<STREAM_NW, 2>), g3, dim3(64 * STREAM_NW), 0, st, a.M,
+        KS_LAUNCH((k_attn_stream<STREAM_NW, 2>), g3, dim3(64 * STREAM_NW), 0, st, a.M,
                            a.hq, a.hkv, a.n_max, a.q, kc, vc, a.len, a.part, a.nsplit, tpw);
     } else if (CB == 1) {
       KS_DEC_S(1);
@@ -1251,7 +1251,7 @@ void attn_split(const AttnArgs& a, hipStream_t st) {
     const int span = TILE * a.tiles;
     constexpr int QWG = 16 * KS_BAT_NW * KS_BAT_CB;  // query vectors per workgroup
     dim3 g2((a.max_len + span - 1) / span, a.hkv, (a.M * G + QWG - 1) / QWG);
-    hipLaunchKernelGGL((k_attn_bat<KS_BAT_NW, KS_BAT_ST, KS_BAT_CB>), g2, dim3(64 * KS_BAT_NW), 0,
+    KS_LAUNCH((k_attn_bat<KS_BAT_NW, KS_BAT_ST, KS_BAT_CB>), g2, dim3(64 * KS_BAT_NW), 0,
                        st, a.M, a.hq, a.hkv, a.n_max, a.q, (const bf16_t*)a.kc,
                        (const bf16_t*)a.vc, a.len, a.max_len, span, a.part, a.nsplit);
   } else if (a.hd == 128) {
@@ -1268,7 +1268,7 @@ void attn_combine(const AttnArgs& a, const float* kvself, Act act_out, hipStream
   const int ngrid = (a.max_len + span - 1) / span;  // splits the split kernel ran
   const bool bf = a.dtype == KS_BF16;
 #define KS_COMB(HDV, BFV)                                                                    \
-  hipLaunchKernelGGL((k_attn_combine<HDV, BFV>), grid, dim3(256), 0, st, a.M, a.hq, a.hkv,   \
+  KS_LAUNCH((k_attn_combine<HDV, BFV>), grid, dim3(256), 0, st, a.M, a.hq, a.hkv,   \
                      span, ngrid, a.q, a.part, a.nsplit, a.len, kvself,                      \
                      bf ? (bf16_t*)act_out.hi : nullptr, bf ? (bf16_t*)act_out.lo : nullptr, \
                      bf ? nullptr : (float*)act_out.hi, act_out.ld)

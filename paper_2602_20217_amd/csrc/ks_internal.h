@@ -3,6 +3,7 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <hip/hip_ext.h>
 
 #include <cstddef>
 #include <cstdint>
@@ -18,6 +19,30 @@ namespace ks {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint16_t bf16_t;  // raw bf16 storage
+
+// ------------------------------------------------------------ kernel timing
+// While a timing bracket is open on a thread (stop != nullptr), every kernel
+// the library launches from that thread carries the bracket's events in its
+// own dispatch: the first launch takes `start` when it begins, each launch
+// takes `stop` when it ends.  Elapsed time then covers the kernels' execution
+// only, without the separate event packets that would sit between launches.
+struct LaunchTiming {
+  hipEvent_t start = nullptr, stop = nullptr;
+  int launches = 0;
+};
+extern thread_local LaunchTiming g_timing;
+
+#define KS_LAUNCH(kern, grid, block, lds, st, ...)                                  \
+  do {                                                                             \
+    if (::ks::g_timing.stop) {                                                     \
+      hipExtLaunchKernelGGL(kern, grid, block, lds, st, ::ks::g_timing.start,      \
+                            ::ks::g_timing.stop, 0, __VA_ARGS__);                  \
+      ::ks::g_timing.start = nullptr;                                              \
+      ++::ks::g_timing.launches;                                                   \
+    } else {                                                                       \
+      hipLaunchKernelGGL(kern, grid, block, lds, st, __VA_ARGS__);                 \
+    }                                                                              \
+  } while (0)
 
 // ---------------------------------------------------------------- bf16 helpers
 __host__ __device__ inline float bf2f(bf16_t b) {

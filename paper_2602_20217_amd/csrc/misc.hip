@@ -44,7 +44,7 @@ __global__ __launch_bounds__(256) void k_embed(const void* __restrict__ E, int b
 void embed_rows(const void* E, int dtype, const int32_t* tok, int M, int d, float* x, int ldx,
                 hipStream_t st) {
   if (M <= 0) return;
-  hipLaunchKernelGGL(k_embed, dim3(M), dim3(256), 0, st, E, dtype == KS_BF16 ? 1 : 0, tok, d, x,
+  KS_LAUNCH(k_embed, dim3(M), dim3(256), 0, st, E, dtype == KS_BF16 ? 1 : 0, tok, d, x,
                      ldx);
 }
 
@@ -97,7 +97,7 @@ __global__ __launch_bounds__(256) void k_act_prep(const float* __restrict__ xin,
 void act_prep(const float* xin, int ldx, const void* E, int dtype, const int32_t* tok, int M,
               int d, float* xout, const float* gain, Act act, float* ssq, hipStream_t st) {
   if (M <= 0) return;
-  hipLaunchKernelGGL(k_act_prep, dim3(M), dim3(256), 0, st, xin, ldx, E,
+  KS_LAUNCH(k_act_prep, dim3(M), dim3(256), 0, st, xin, ldx, E,
                      dtype == KS_BF16 ? 1 : 0, tok, d, xout, gain, (bf16_t*)act.hi,
                      (bf16_t*)act.lo, act.ld, ssq);
 }
@@ -168,7 +168,7 @@ __global__ __launch_bounds__(256) void k_norm_act(const float* __restrict__ x, i
 void norm_act(const float* x, int ldx, const float* g, float eps, int M, int d, int dtype,
               Act act, hipStream_t st) {
   if (M <= 0) return;
-  hipLaunchKernelGGL(k_norm_act, dim3(M), dim3(256), 0, st, x, ldx, g, eps, d,
+  KS_LAUNCH(k_norm_act, dim3(M), dim3(256), 0, st, x, ldx, g, eps, d,
                      dtype == KS_BF16 ? 1 : 0, act.hi, act.lo, act.ld);
 }
 
@@ -245,7 +245,7 @@ __global__ __launch_bounds__(256) void k_qkv_post(QkvPostArgs a) {
 void qkv_post(const QkvPostArgs& a, hipStream_t st) {
   if (a.M <= 0) return;
   const int nh = a.hq + 2 * a.hkv;
-  hipLaunchKernelGGL(k_qkv_post, dim3((nh + 3) / 4, a.M), dim3(256), 0, st, a);
+  KS_LAUNCH(k_qkv_post, dim3((nh + 3) / 4, a.M), dim3(256), 0, st, a);
 }
 
 // ------------------------------------------------------------------ argmax
@@ -320,14 +320,14 @@ __global__ __launch_bounds__(1024) void k_cos_groups(const float* __restrict__ X
 void cos_groups(const float* X, const float* Y, int groups, int r, int d, float* out,
                 hipStream_t st) {
   if (groups <= 0) return;
-  hipLaunchKernelGGL(k_cos_groups<float>, dim3(groups), dim3(1024), r * sizeof(double), st, X,
+  KS_LAUNCH(k_cos_groups<float>, dim3(groups), dim3(1024), r * sizeof(double), st, X,
                      Y, r, d, out);
 }
 
 void cos_groups_f64(const float* X, const float* Y, int groups, int r, int d, double* out,
                     hipStream_t st) {
   if (groups <= 0) return;
-  hipLaunchKernelGGL(k_cos_groups<double>, dim3(groups), dim3(1024), r * sizeof(double), st, X,
+  KS_LAUNCH(k_cos_groups<double>, dim3(groups), dim3(1024), r * sizeof(double), st, X,
                      Y, r, d, out);
 }
 
@@ -344,7 +344,7 @@ __global__ __launch_bounds__(256) void k_cos_rows(const float* __restrict__ X,
 void cos_rows(const float* X, const float* Y, int rows, int ry, int d, double* out,
               hipStream_t st) {
   if (rows <= 0) return;
-  hipLaunchKernelGGL(k_cos_rows, dim3((rows + 3) / 4), dim3(256), 0, st, X, Y, rows, ry, d, out);
+  KS_LAUNCH(k_cos_rows, dim3((rows + 3) / 4), dim3(256), 0, st, X, Y, rows, ry, d, out);
 }
 
 // Both candidate sets of a DP stage in one launch: rows t < rows of X1 into
@@ -365,7 +365,7 @@ __global__ __launch_bounds__(256) void k_cos_rows2(const float* __restrict__ X1,
 void cos_rows2(const float* X1, const float* X2, const float* Y, int rows, int ry, int d,
                double* out1, double* out2, hipStream_t st) {
   if (rows <= 0) return;
-  hipLaunchKernelGGL(k_cos_rows2, dim3((2 * rows + 3) / 4), dim3(256), 0, st, X1, X2, Y, rows,
+  KS_LAUNCH(k_cos_rows2, dim3((2 * rows + 3) / 4), dim3(256), 0, st, X1, X2, Y, rows,
                      ry, d, out1, out2);
 }
 
@@ -385,7 +385,7 @@ __global__ void k_copy_blocks(const float* const* src, float* const* dst, size_t
 void copy_rows(const float* const* src, float* const* dst, int cnt, int n, hipStream_t st) {
   if (cnt <= 0 || n <= 0) return;
   const int bx = (n + 255) / 256 < 64 ? (n + 255) / 256 : 64;
-  hipLaunchKernelGGL(k_copy_blocks, dim3(bx, cnt), dim3(256), 0, st, src, dst, (size_t)n);
+  KS_LAUNCH(k_copy_blocks, dim3(bx, cnt), dim3(256), 0, st, src, dst, (size_t)n);
 }
 
 // History ring copies, one launch for every plane: row t < n of plane i,
@@ -405,7 +405,7 @@ __global__ __launch_bounds__(256) void k_ring_copy(const float* __restrict__ src
 void ring_copy(const float* src, float* dst, size_t plane_stride, int planes, int n, int RING,
                int p0, int d, bool to_ring, hipStream_t st) {
   if (n <= 0 || planes <= 0) return;
-  hipLaunchKernelGGL(k_ring_copy, dim3(n, planes), dim3(256), 0, st, src, dst, plane_stride,
+  KS_LAUNCH(k_ring_copy, dim3(n, planes), dim3(256), 0, st, src, dst, plane_stride,
                      RING, p0, d, to_ring ? 1 : 0);
 }
 
@@ -423,7 +423,7 @@ __global__ void k_rope_table(float* cs, int n_max, int hd, double theta) {
 
 void rope_table(float* cs, int n_max, int hd, double theta, hipStream_t st) {
   const size_t n = (size_t)n_max * (hd / 2);
-  hipLaunchKernelGGL(k_rope_table, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, cs,
+  KS_LAUNCH(k_rope_table, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, cs,
                      n_max, hd, theta);
 }
 
@@ -440,14 +440,14 @@ __global__ void k_fill_pos(int32_t* pos, int32_t* len, int base, int r, int tota
 void fill_pos(int32_t* pos, int32_t* len, int base, int r, int total, int len_add,
               hipStream_t st) {
   if (total <= 0) return;
-  hipLaunchKernelGGL(k_fill_pos, dim3((total + 255) / 256), dim3(256), 0, st, pos, len, base, r,
+  KS_LAUNCH(k_fill_pos, dim3((total + 255) / 256), dim3(256), 0, st, pos, len, base, r,
                      total, len_add);
 }
 
 __global__ void k_set_i32(int32_t* p, int v) { *p = v; }
 
 void set_i32(int32_t* p, int v, hipStream_t st) {
-  hipLaunchKernelGGL(k_set_i32, dim3(1), dim3(1), 0, st, p, v);
+  KS_LAUNCH(k_set_i32, dim3(1), dim3(1), 0, st, p, v);
 }
 
 }  // namespace ks

@@ -68,6 +68,10 @@ def test_null_and_range_errors_before_any_launch():
                                    None)
     with pytest.raises(K.KsError):
         K.ks_knapsack_batch(fake, fake, 1, 72, 64, -1, fake, fake, None)
+    with pytest.raises(K.KsError) as e:  # a timing bracket needs both events
+        K.ks_time_launches(fake, None)
+    assert e.value.status == K.KS_EINVAL
+    K.ks_time_launches(None, None)  # closing with nothing open: no HIP call
 
 
 def test_sampling_calls_validate_before_any_launch():
