@@ -1209,9 +1209,9 @@ void attn_split(const AttnArgs& a, hipStream_t st) {
   const int nq = a.rows_per_block * G;
   dim3 grid(ns, a.hkv, (a.M + a.rows_per_block - 1) / a.rows_per_block);
 #define KS_ATTN(HDV, BFV, QM)                                                                \
-  KS_LAUNCH((k_attn_split<HDV, BFV, QM>), grid, dim3(256), 0, st, a.M, a.hq, a.hkv, \
-                     a.n_max, a.q, a.kc, a.vc, a.len, a.tiles, a.rows_per_block, a.part,     \
-                     a.nsplit)
+  KS_LAUNCH((k_attn_split<HDV, BFV, QM>), grid, dim3(256), 0, st, a.M, a.hq, a.hkv,          \
+            a.n_max, a.q, a.kc, a.vc, a.len, a.tiles, a.rows_per_block, a.part,              \
+            a.nsplit)
   if (attn_dec_path(a)) {
     // decode / verify rows: 16 query columns per workgroup when one block holds
     // all rows, else 32 (16 CB / G rows per workgroup)
@@ -1221,8 +1221,8 @@ void attn_split(const AttnArgs& a, hipStream_t st) {
     const bf16_t* kc = (const bf16_t*)a.kc;
     const bf16_t* vc = (const bf16_t*)a.vc;
 #define KS_DEC(S_, CB_)                                                                      \
-  KS_LAUNCH((k_attn_dec<S_, CB_>), g3, dim3(64 * S_), 0, st, a.M, a.hq, a.hkv,       \
-                     a.n_max, a.q, kc, vc, a.len, a.part, a.nsplit, a.span)
+  KS_LAUNCH((k_attn_dec<S_, CB_>), g3, dim3(64 * S_), 0, st, a.M, a.hq, a.hkv,               \
+            a.n_max, a.q, kc, vc, a.len, a.part, a.nsplit, a.span)
 #define KS_DEC_S(CB_)            \
   switch (a.tiles) {             \
     case 1: KS_DEC(1, CB_); break; \
@@ -1235,10 +1235,10 @@ void attn_split(const AttnArgs& a, hipStream_t st) {
       const int tpw = a.tiles / STREAM_NW;
       if (CB == 1)
         KS_LAUNCH((k_attn_stream<STREAM_NW, 1>), g3, dim3(64 * STREAM_NW), 0, st, a.M,
-                           a.hq, a.hkv, a.n_max, a.q, kc, vc, a.len, a.part, a.nsplit, tpw);
+                  a.hq, a.hkv, a.n_max, a.q, kc, vc, a.len, a.part, a.nsplit, tpw);
       else
         KS_LAUNCH((k_attn_stream<STREAM_NW, 2>), g3, dim3(64 * STREAM_NW), 0, st, a.M,
-                           a.hq, a.hkv, a.n_max, a.q, kc, vc, a.len, a.part, a.nsplit, tpw);
+                  a.hq, a.hkv, a.n_max, a.q, kc, vc, a.len, a.part, a.nsplit, tpw);
     } else if (CB == 1) {
       KS_DEC_S(1);
     } else {
@@ -1252,8 +1252,8 @@ void attn_split(const AttnArgs& a, hipStream_t st) {
     constexpr int QWG = 16 * KS_BAT_NW * KS_BAT_CB;  // query vectors per workgroup
     dim3 g2((a.max_len + span - 1) / span, a.hkv, (a.M * G + QWG - 1) / QWG);
     KS_LAUNCH((k_attn_bat<KS_BAT_NW, KS_BAT_ST, KS_BAT_CB>), g2, dim3(64 * KS_BAT_NW), 0,
-                       st, a.M, a.hq, a.hkv, a.n_max, a.q, (const bf16_t*)a.kc,
-                       (const bf16_t*)a.vc, a.len, a.max_len, span, a.part, a.nsplit);
+              st, a.M, a.hq, a.hkv, a.n_max, a.q, (const bf16_t*)a.kc,
+              (const bf16_t*)a.vc, a.len, a.max_len, span, a.part, a.nsplit);
   } else if (a.hd == 128) {
     if (nq <= 4) KS_ATTN(128, true, 1); else KS_ATTN(128, true, 8);
   } else {
@@ -1268,10 +1268,10 @@ void attn_combine(const AttnArgs& a, const float* kvself, Act act_out, hipStream
   const int ngrid = (a.max_len + span - 1) / span;  // splits the split kernel ran
   const bool bf = a.dtype == KS_BF16;
 #define KS_COMB(HDV, BFV)                                                                    \
-  KS_LAUNCH((k_attn_combine<HDV, BFV>), grid, dim3(256), 0, st, a.M, a.hq, a.hkv,   \
-                     span, ngrid, a.q, a.part, a.nsplit, a.len, kvself,                      \
-                     bf ? (bf16_t*)act_out.hi : nullptr, bf ? (bf16_t*)act_out.lo : nullptr, \
-                     bf ? nullptr : (float*)act_out.hi, act_out.ld)
+  KS_LAUNCH((k_attn_combine<HDV, BFV>), grid, dim3(256), 0, st, a.M, a.hq, a.hkv,            \
+            span, ngrid, a.q, a.part, a.nsplit, a.len, kvself,                               \
+            bf ? (bf16_t*)act_out.hi : nullptr, bf ? (bf16_t*)act_out.lo : nullptr,          \
+            bf ? nullptr : (float*)act_out.hi, act_out.ld)
   if (a.hd == 128) KS_COMB(128, true);
   else KS_COMB(64, false);
 #undef KS_COMB

@@ -51,10 +51,10 @@ extern "C" ks_status ks_stream_read(const void* src, size_t bytes, float* sink, 
   if (bytes <= ((size_t)128 << 20)) {
     const size_t nwg = std::max<size_t>(1, std::min<size_t>(2048, n16 / 256));
     KS_LAUNCH(k_stream_read<256>, dim3((unsigned)nwg), dim3(256), 0, st,
-                       (const u32x4c*)src, n16, n16 / nwg, sink);
+              (const u32x4c*)src, n16, n16 / nwg, sink);
   } else {
     KS_LAUNCH(k_stream_read<1024>, dim3(256), dim3(1024), 0, st, (const u32x4c*)src,
-                       n16, n16 / 256, sink);
+              n16, n16 / 256, sink);
   }
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) {

@@ -351,11 +351,11 @@ static void launch_skinny_a1(const GemmArgs& g, hipStream_t st) {
   const bf16_t* W = (const bf16_t*)g.W;
   dim3 grid((NT + NB - 1) / NB), block(NW * 64);
   const size_t lds = A1 ? (size_t)g.K * 4 : 0;  // hi and lo planes of the row
-#define KS_SKINNY(E, OH, OL, OLD)                                                            \
+#define KS_SKINNY(E, OH, OL, OLD)                                                               \
   KS_LAUNCH((k_gemm_skinny<NB, NW, CH, MINB, E, AN, A1>), grid, block, lds, st, g.M, g.N, g.K,  \
-                     Ahi, Alo, g.A.ld, W, g.out, g.ldo, g.res, g.ldres, OH, OL, OLD,         \
-                     g.ssq_in, g.nssq, g.eps, g.next_gain, (bf16_t*)g.next_act.hi,           \
-                     (bf16_t*)g.next_act.lo, g.next_act.ld, g.next_ssq, g.qe)
+            Ahi, Alo, g.A.ld, W, g.out, g.ldo, g.res, g.ldres, OH, OL, OLD,                     \
+            g.ssq_in, g.nssq, g.eps, g.next_gain, (bf16_t*)g.next_act.hi,                       \
+            (bf16_t*)g.next_act.lo, g.next_act.ld, g.next_ssq, g.qe)
   if (g.epi == EPI_SWIGLU)
     KS_SKINNY(EPI_SWIGLU, (bf16_t*)g.act_out.hi, (bf16_t*)g.act_out.lo, g.act_out.ld);
   else if (g.epi == EPI_QKV)
@@ -650,25 +650,25 @@ static void launch_tiled(const GemmArgs& g, hipStream_t st) {
   const bf16_t* W = (const bf16_t*)g.W;
   if (g.epi == EPI_SWIGLU)
     KS_LAUNCH((k_gemm_tiled<EPI_SWIGLU, ST, WM, WN, NWM, NWN>), grid, dim3(64 * NWM * NWN), 0, st, g.M, g.N,
-                       g.K, A, g.A.ld, W, g.out, g.ldo, g.res, g.ldres, (bf16_t*)g.act_out.hi,
-                       (bf16_t*)g.act_out.lo, g.act_out.ld, MB, NB, 1, g.part);
+              g.K, A, g.A.ld, W, g.out, g.ldo, g.res, g.ldres, (bf16_t*)g.act_out.hi,
+              (bf16_t*)g.act_out.lo, g.act_out.ld, MB, NB, 1, g.part);
   else if (g.epi == EPI_RESID)
     KS_LAUNCH((k_gemm_tiled<EPI_RESID, ST, WM, WN, NWM, NWN>), grid, dim3(64 * NWM * NWN), 0, st, g.M, g.N, g.K,
-                       A, g.A.ld, W, g.out, g.ldo, g.res, g.ldres, nullptr, nullptr, 0, MB, NB,
-                       SK, g.part);
+              A, g.A.ld, W, g.out, g.ldo, g.res, g.ldres, nullptr, nullptr, 0, MB, NB,
+              SK, g.part);
   else
     KS_LAUNCH((k_gemm_tiled<EPI_STORE, ST, WM, WN, NWM, NWN>), grid, dim3(64 * NWM * NWN), 0, st, g.M, g.N, g.K,
-                       A, g.A.ld, W, g.out, g.ldo, g.res, g.ldres, nullptr, nullptr, 0, MB, NB,
-                       SK, g.part);
+              A, g.A.ld, W, g.out, g.ldo, g.res, g.ldres, nullptr, nullptr, 0, MB, NB,
+              SK, g.part);
   if (SK > 1) {
     const size_t n4 = (size_t)g.M * (g.N / 4);
     dim3 rg((unsigned)((n4 + 255) / 256));
     if (g.epi == EPI_RESID)
       KS_LAUNCH(k_splitk_reduce<EPI_RESID>, rg, dim3(256), 0, st, g.M, g.N, SK, g.part,
-                         g.out, g.ldo, g.res, g.ldres);
+                g.out, g.ldo, g.res, g.ldres);
     else
       KS_LAUNCH(k_splitk_reduce<EPI_STORE>, rg, dim3(256), 0, st, g.M, g.N, SK, g.part,
-                         g.out, g.ldo, g.res, g.ldres);
+                g.out, g.ldo, g.res, g.ldres);
   }
 }
 
@@ -739,14 +739,14 @@ void gemm_f32(const GemmArgs& g, hipStream_t st) {
   const float* W = (const float*)g.W;
   if (g.epi == EPI_SWIGLU)
     KS_LAUNCH(k_gemm_f32<EPI_SWIGLU>, grid, dim3(256), 0, st, g.M, Nout, g.K, A,
-                       g.A.ld, W, g.out, g.ldo, g.res, g.ldres, (float*)g.act_out.hi,
-                       g.act_out.ld);
+              g.A.ld, W, g.out, g.ldo, g.res, g.ldres, (float*)g.act_out.hi,
+              g.act_out.ld);
   else if (g.epi == EPI_RESID)
     KS_LAUNCH(k_gemm_f32<EPI_RESID>, grid, dim3(256), 0, st, g.M, Nout, g.K, A, g.A.ld,
-                       W, g.out, g.ldo, g.res, g.ldres, nullptr, 0);
+              W, g.out, g.ldo, g.res, g.ldres, nullptr, 0);
   else
     KS_LAUNCH(k_gemm_f32<EPI_STORE>, grid, dim3(256), 0, st, g.M, Nout, g.K, A, g.A.ld,
-                       W, g.out, g.ldo, g.res, g.ldres, nullptr, 0);
+              W, g.out, g.ldo, g.res, g.ldres, nullptr, 0);
 }
 
 // ----------------------------------------------------------------- packing
@@ -779,20 +779,20 @@ __global__ void k_pack(const bf16_t* __restrict__ src0, const bf16_t* __restrict
 void pack_matrix_bf16(const bf16_t* src, bf16_t* dst, int N, int K, hipStream_t st) {
   const size_t nfrag = (size_t)N * K / 8;
   KS_LAUNCH(k_pack, dim3((unsigned)((nfrag + 255) / 256)), dim3(256), 0, st, src,
-                     nullptr, dst, N, K, 0, 0);
+            nullptr, dst, N, K, 0, 0);
 }
 
 void pack_qkv_bf16(const bf16_t* src, bf16_t* dst, int heads, int hd, int d, hipStream_t st) {
   const size_t nfrag = (size_t)heads * hd * d / 8;
   KS_LAUNCH(k_pack, dim3((unsigned)((nfrag + 255) / 256)), dim3(256), 0, st, src,
-                     nullptr, dst, heads * hd, d, 2, hd);
+            nullptr, dst, heads * hd, d, 2, hd);
 }
 
 void pack_gate_up_bf16(const bf16_t* gate, const bf16_t* up, bf16_t* dst, int ffn, int d,
                        hipStream_t st) {
   const size_t nfrag = (size_t)2 * ffn * d / 8;
   KS_LAUNCH(k_pack, dim3((unsigned)((nfrag + 255) / 256)), dim3(256), 0, st, gate, up,
-                     dst, 2 * ffn, d, 1, 0);
+            dst, 2 * ffn, d, 1, 0);
 }
 
 }  // namespace ks

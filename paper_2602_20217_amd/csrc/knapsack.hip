@@ -198,7 +198,7 @@ __global__ void k_knap_backtrack(const uint64_t* __restrict__ bits, const int32_
 void knapsack_backtrack(const uint64_t* bits, const int32_t* w, int B, int n, int C,
                         const int32_t* j, uint8_t* skip, int32_t* err, hipStream_t st) {
   KS_LAUNCH(k_knap_backtrack, dim3((B + 255) / 256), dim3(256), 0, st, bits, w, B, n, C,
-                     j, skip, err);
+            j, skip, err);
 }
 
 // Stage 2 with the surrogate acceptance alpha_j = prod_{i skipped} s_i.
@@ -370,7 +370,7 @@ static void launch_knap_select(const int32_t* best, const uint64_t* bits, const 
                                int32_t* g_star, double* tpt, uint8_t* skip, hipStream_t st) {
   const size_t rowb = (size_t)256 * E * sizeof(double);
   KS_LAUNCH(k_knap_select<E>, dim3(B), dim3(256), rowb, st, best, bits, w, s, n, C, D,
-                     j_star, g_star, tpt, skip);
+            j_star, g_star, tpt, skip);
 }
 
 void knapsack_select(const int32_t* best, const uint64_t* bits, const int32_t* w,
@@ -477,9 +477,9 @@ __global__ __launch_bounds__(256) void k_dp_step(
 
 void dp_step(const DpStepArgs& a, hipStream_t st) {
   KS_LAUNCH(k_dp_step, dim3(1), dim3(256), 0, st, a.i, a.J, a.w, a.tau, a.r, a.M,
-                     a.stride, a.sig, a.cells_in, a.cnt_in, a.cells_out, a.cnt_out, a.mean, a.idx,
-                     a.bits, a.reach, a.sig_e, a.sig_s, a.E, a.gprev, a.gnext, a.Xi, a.cell,
-                     a.ptr_src, a.ptr_dst, a.bound_out);
+            a.stride, a.sig, a.cells_in, a.cnt_in, a.cells_out, a.cnt_out, a.mean, a.idx,
+            a.bits, a.reach, a.sig_e, a.sig_s, a.E, a.gprev, a.gnext, a.Xi, a.cell,
+            a.ptr_src, a.ptr_dst, a.bound_out);
 }
 
 }  // namespace ks

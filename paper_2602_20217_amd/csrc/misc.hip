@@ -45,7 +45,7 @@ void embed_rows(const void* E, int dtype, const int32_t* tok, int M, int d, floa
                 hipStream_t st) {
   if (M <= 0) return;
   KS_LAUNCH(k_embed, dim3(M), dim3(256), 0, st, E, dtype == KS_BF16 ? 1 : 0, tok, d, x,
-                     ldx);
+            ldx);
 }
 
 // Normed-product input (bf16 models): one block per row; thread c4 owns
@@ -98,8 +98,8 @@ void act_prep(const float* xin, int ldx, const void* E, int dtype, const int32_t
               int d, float* xout, const float* gain, Act act, float* ssq, hipStream_t st) {
   if (M <= 0) return;
   KS_LAUNCH(k_act_prep, dim3(M), dim3(256), 0, st, xin, ldx, E,
-                     dtype == KS_BF16 ? 1 : 0, tok, d, xout, gain, (bf16_t*)act.hi,
-                     (bf16_t*)act.lo, act.ld, ssq);
+            dtype == KS_BF16 ? 1 : 0, tok, d, xout, gain, (bf16_t*)act.hi,
+            (bf16_t*)act.lo, act.ld, ssq);
 }
 
 // ---------------------------------------------------------------- RMSNorm
@@ -169,7 +169,7 @@ void norm_act(const float* x, int ldx, const float* g, float eps, int M, int d, 
               Act act, hipStream_t st) {
   if (M <= 0) return;
   KS_LAUNCH(k_norm_act, dim3(M), dim3(256), 0, st, x, ldx, g, eps, d,
-                     dtype == KS_BF16 ? 1 : 0, act.hi, act.lo, act.ld);
+            dtype == KS_BF16 ? 1 : 0, act.hi, act.lo, act.ld);
 }
 
 // ------------------------------------------------------- q/k norm, RoPE, KV
@@ -321,14 +321,14 @@ void cos_groups(const float* X, const float* Y, int groups, int r, int d, float*
                 hipStream_t st) {
   if (groups <= 0) return;
   KS_LAUNCH(k_cos_groups<float>, dim3(groups), dim3(1024), r * sizeof(double), st, X,
-                     Y, r, d, out);
+            Y, r, d, out);
 }
 
 void cos_groups_f64(const float* X, const float* Y, int groups, int r, int d, double* out,
                     hipStream_t st) {
   if (groups <= 0) return;
   KS_LAUNCH(k_cos_groups<double>, dim3(groups), dim3(1024), r * sizeof(double), st, X,
-                     Y, r, d, out);
+            Y, r, d, out);
 }
 
 __global__ __launch_bounds__(256) void k_cos_rows(const float* __restrict__ X,
@@ -366,7 +366,7 @@ void cos_rows2(const float* X1, const float* X2, const float* Y, int rows, int r
                double* out1, double* out2, hipStream_t st) {
   if (rows <= 0) return;
   KS_LAUNCH(k_cos_rows2, dim3((2 * rows + 3) / 4), dim3(256), 0, st, X1, X2, Y, rows,
-                     ry, d, out1, out2);
+            ry, d, out1, out2);
 }
 
 // ------------------------------------------------------------------- copies
@@ -406,7 +406,7 @@ void ring_copy(const float* src, float* dst, size_t plane_stride, int planes, in
                int p0, int d, bool to_ring, hipStream_t st) {
   if (n <= 0 || planes <= 0) return;
   KS_LAUNCH(k_ring_copy, dim3(n, planes), dim3(256), 0, st, src, dst, plane_stride,
-                     RING, p0, d, to_ring ? 1 : 0);
+            RING, p0, d, to_ring ? 1 : 0);
 }
 
 // ------------------------------------------------------------ rotary table
@@ -424,7 +424,7 @@ __global__ void k_rope_table(float* cs, int n_max, int hd, double theta) {
 void rope_table(float* cs, int n_max, int hd, double theta, hipStream_t st) {
   const size_t n = (size_t)n_max * (hd / 2);
   KS_LAUNCH(k_rope_table, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, cs,
-                     n_max, hd, theta);
+            n_max, hd, theta);
 }
 
 // --------------------------------------------------------- small fillers
@@ -441,7 +441,7 @@ void fill_pos(int32_t* pos, int32_t* len, int base, int r, int total, int len_ad
               hipStream_t st) {
   if (total <= 0) return;
   KS_LAUNCH(k_fill_pos, dim3((total + 255) / 256), dim3(256), 0, st, pos, len, base, r,
-                     total, len_add);
+            total, len_add);
 }
 
 __global__ void k_set_i32(int32_t* p, int v) { *p = v; }

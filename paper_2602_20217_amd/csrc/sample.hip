@@ -653,8 +653,8 @@ void argmax_rows(const float* logits, int M, int V, int ld, int32_t* am, float* 
   for (int m0 = 0; m0 < M; m0 += 65535) {
     const int mm = std::min(65535, M - m0);
     KS_LAUNCH(k_vocab_scan, dim3(ch.NB, mm), dim3(SCAN_NT), 0, st,
-                       logits + (size_t)m0 * ld, ld, V, ch.chunk, 0, stat + (size_t)m0 * ch.NB,
-                       nullptr);
+              logits + (size_t)m0 * ld, ld, V, ch.chunk, 0, stat + (size_t)m0 * ch.NB,
+              nullptr);
   }
   KS_LAUNCH(k_argmax_merge, dim3(M), dim3(128), 0, st, stat, ch.NB, am, top1);
 }
@@ -667,7 +667,7 @@ void sample_rows(const float* logits, int R, int V, int ld, const SampleSpec& s,
   VStat* stat = (VStat*)ws;
   uint2* cand = (uint2*)((char*)ws + (size_t)R * ch.NB * sizeof(VStat));  // 16-byte aligned
   KS_LAUNCH(k_vocab_scan, dim3(ch.NB, R), dim3(SCAN_NT), 0, st, logits, ld, V, ch.chunk,
-                     k, stat, cand);
+            k, stat, cand);
   RowArgs A{stat, ch.NB, cand, k, s.temperature, s.top_p, (uint32_t)s.seed,
             (uint32_t)(s.seed >> 32), s.ids, s.probs, s.count, s.top1, s.tok, s.pos0, s.purpose};
   KS_LAUNCH(k_sample_row, dim3(R), dim3(ROW_NT), 0, st, A);
@@ -677,13 +677,13 @@ void spec_accept(const int32_t* pid, const float* ppr, const int32_t* pcnt, cons
                  const float* qpr, const int32_t* qcnt, const int32_t* drafts, int g,
                  uint64_t seed, int pos0, int32_t* out, hipStream_t st) {
   KS_LAUNCH(k_spec_accept, dim3(1), dim3(64), 0, st, pid, ppr, pcnt, qid, qpr, qcnt,
-                     drafts, g, (uint32_t)seed, (uint32_t)(seed >> 32), pos0, out);
+            drafts, g, (uint32_t)seed, (uint32_t)(seed >> 32), pos0, out);
 }
 
 void uniforms(uint64_t seed, const int32_t* pos, int n, int purpose, float* out, hipStream_t st) {
   if (n <= 0) return;
   KS_LAUNCH(k_uniforms, dim3((n + 255) / 256), dim3(256), 0, st, (uint32_t)seed,
-                     (uint32_t)(seed >> 32), pos, n, purpose, out);
+            (uint32_t)(seed >> 32), pos, n, purpose, out);
 }
 
 }  // namespace ks
