@@ -6,13 +6,15 @@
 // load therefore reads one contiguous KiB of HBM.
 //
 // Skinny path (M <= 16 rows: decode, draft, verify): the batch-1 decode step
-// is HBM-bound, so every weight byte is read once.  Rows are padded to the 16
-// of the matrix instruction; activations enter as two bf16 planes hi + lo
-// (two MFMAs per weight fragment, free in the HBM-bound regime) so the product
-// keeps ~16 mantissa bits of the float32 activations.  K is split over the
-// 16 waves of a workgroup and reduced in LDS in a fixed order, so a row's
-// result does not depend on how many rows are in the batch: a verify row and
-// the decode step at the same position produce identical bits.
+// is HBM-bound, so every weight byte is read once.  Activations enter as two
+// bf16 planes hi + lo so the product keeps ~16 mantissa bits of the float32
+// activations; the 16 rows of the matrix instruction hold the hi planes of
+// up to 8 activation rows in rows 0..7 and their lo planes in rows 8..15, so
+// one instruction per weight fragment serves 8 rows (two for 9..16 rows, one
+// per group of 8), and the two planes' sums are added in the epilogue.  K is
+// split over the waves of a workgroup and reduced in LDS in a fixed order, so
+// a row's result does not depend on how many rows are in the batch: a verify
+// row and the decode step at the same position produce identical bits.
 //
 // Tiled path (batched rows of the selection DP and of prefill): 128 x 256
 // workgroup tiles of eight 64 x 64 wave tiles of 16x16x32 MFMAs over single
@@ -53,7 +55,7 @@ __device__ inline void store_split(bf16_t* hi, bf16_t* lo, size_t off, float a) 
 // products read those planes like any activation and scale row m by
 // 1/sqrt(sum/K + eps) at the end; the 256 tile sums of a row are added by one
 // wave in a fixed order, whatever the row count.
-template <int NB, int NW, int CH, int MINB, int EPI, int AN, int A1>
+template <int NB, int NW, int CH, int MINB, int EPI, int AN, int A1, int MH>
 __global__ __launch_bounds__(NW * 64, MINB) void k_gemm_skinny(
     int M, int N, int K, const bf16_t* __restrict__ Ahi, const bf16_t* __restrict__ Alo,
     int lda, const bf16_t* __restrict__ Wp, float* out, int ldo, const float* res, int ldres,
@@ -67,17 +69,21 @@ __global__ __launch_bounds__(NW * 64, MINB) void k_gemm_skinny(
   const int nt0 = blockIdx.x * NB;
   const int kb = (wave * KT) / NW;
   const int ke = ((wave + 1) * KT) / NW;
-  const int row = lane & 15;
+  // matrix row of this lane: plane (0 hi, 1 lo) of activation row 8 h + (slot & 7)
+  const int slot = lane & 15;
+  const int plane = slot >> 3;
   const int kg = lane >> 4;
-  const bool rok = row < M;
 
   static_assert(NB * 256 <= NW * 64, "one epilogue element per thread");
-  // epilogue element of this thread: tile et, MFMA lane el, accumulator
-  // register ev (row em, column en)
-  const int et = threadIdx.x >> 8, el = (threadIdx.x >> 2) & 63, ev = threadIdx.x & 3;
-  const int em = 4 * (el >> 4) + ev;
+  static_assert(MH == 1 || (MH == 2 && A1 == 0), "one-row staging serves one group of 8 rows");
+  // epilogue element of this thread: tile et, row group eh, hi-plane MFMA lane
+  // el (its lo-plane partner is el + 32), accumulator register ev (row em,
+  // column en)
+  const int et = threadIdx.x >> 8, eh = (threadIdx.x >> 7) & 1, ev = threadIdx.x & 3;
+  const int el = (threadIdx.x >> 2) & 31;
+  const int em = 8 * eh + 4 * (el >> 4) + ev;
   const int en = (nt0 + et) * 16 + (el & 15);
-  const bool eact = threadIdx.x < NB * 256 && em < M && nt0 + et < NT;
+  const bool eact = threadIdx.x < NB * 256 && eh < MH && em < M && nt0 + et < NT;
 
   // Epilogue operands that do not depend on the product are requested before
   // the weight stream, so that their memory latency overlaps it instead of
@@ -131,13 +137,19 @@ __global__ __launch_bounds__(NW * 64, MINB) void k_gemm_skinny(
       }
   }
 
-  f32x4 acc[NB];
+  f32x4 acc[MH][NB];
 #pragma unroll
-  for (int t = 0; t < NB; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int h = 0; h < MH; ++h)
+#pragma unroll
+    for (int t = 0; t < NB; ++t) acc[h][t] = f32x4{0.f, 0.f, 0.f, 0.f};
   // Lanes of rows past M read row 0: their products land in result rows that
   // are never stored (an MFMA result row depends only on its own A row).
-  const bf16_t* ah = Ahi + (size_t)(rok ? row : 0) * lda + kg * 8;
-  const bf16_t* al = Alo + (size_t)(rok ? row : 0) * lda + kg * 8;
+  const bf16_t* ap[MH];
+#pragma unroll
+  for (int h = 0; h < MH; ++h) {
+    const int r = 8 * h + (slot & 7);
+    ap[h] = (plane ? Alo : Ahi) + (size_t)(r < M ? r : 0) * lda + kg * 8;
+  }
   const bf16_t* wb[NB];
 #pragma unroll
   for (int t = 0; t < NB; ++t) {
@@ -151,32 +163,33 @@ __global__ __launch_bounds__(NW * 64, MINB) void k_gemm_skinny(
   // the loads in flight exactly); the last (ke - kb) % CH steps follow one by
   // one.  The order of the matrix instructions (k ascending, hi then lo) is
   // that of a plain loop.
-  bf16x8 w0[NB][CH], x00[CH], x01[CH];
-  bf16x8 w1[NB][CH], x10[CH], x11[CH];
-  auto fetch = [&](int kc, bf16x8 (&w)[NB][CH], bf16x8 (&x0)[CH], bf16x8 (&x1)[CH]) {
+  bf16x8 w0[NB][CH], x0[MH][CH];
+  bf16x8 w1[NB][CH], x1[MH][CH];
+  auto fetch = [&](int kc, bf16x8 (&w)[NB][CH], bf16x8 (&x)[MH][CH]) {
 #pragma unroll
     for (int u = 0; u < CH; ++u) {
 #pragma unroll
       for (int t = 0; t < NB; ++t) w[t][u] = ld_frag_nt(wb[t] + (size_t)(kc + u) * 512);
       if constexpr (A1 == 0) {
-        x0[u] = ld_frag(ah + (kc + u) * 32);
-        x1[u] = ld_frag(al + (kc + u) * 32);
+#pragma unroll
+        for (int h = 0; h < MH; ++h) x[h][u] = ld_frag(ap[h] + (kc + u) * 32);
       }
     }
   };
-  // A1: lane (row, kg) takes k = 32 step + 8 kg .. + 7 of row 0 from LDS
-  auto act_lds = [&](int k, int pl) {
-    return __builtin_bit_cast(bf16x8, s_act[pl * n16 + 4 * k + kg]);
+  // A1: lane (slot, kg) takes k = 32 step + 8 kg .. + 7 of its plane of row 0
+  // from LDS
+  auto act_lds = [&](int k) {
+    return __builtin_bit_cast(bf16x8, s_act[plane * n16 + 4 * k + kg]);
   };
-  auto compute = [&](int kc, bf16x8 (&w)[NB][CH], bf16x8 (&x0)[CH], bf16x8 (&x1)[CH]) {
+  auto compute = [&](int kc, bf16x8 (&w)[NB][CH], bf16x8 (&x)[MH][CH]) {
 #pragma unroll
     for (int u = 0; u < CH; ++u) {
-      const bf16x8 a0 = A1 ? act_lds(kc + u, 0) : x0[u];
-      const bf16x8 a1 = A1 ? act_lds(kc + u, 1) : x1[u];
 #pragma unroll
-      for (int t = 0; t < NB; ++t) {
-        acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, w[t][u], acc[t], 0, 0, 0);
-        acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, w[t][u], acc[t], 0, 0, 0);
+      for (int h = 0; h < MH; ++h) {
+        const bf16x8 a = A1 ? act_lds(kc + u) : x[h][u];
+#pragma unroll
+        for (int t = 0; t < NB; ++t)
+          acc[h][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, w[t][u], acc[h][t], 0, 0, 0);
       }
     }
   };
@@ -187,8 +200,8 @@ __global__ __launch_bounds__(NW * 64, MINB) void k_gemm_skinny(
     // least two): both are requested before the wait for the row, so the
     // stream does not pause while the row lands in LDS; then chunk c + 2 is
     // requested after chunk c's matrix instructions.
-    fetch(ck(0), w0, x00, x01);
-    fetch(ck(1), w1, x10, x11);
+    fetch(ck(0), w0, x0);
+    fetch(ck(1), w1, x1);
 #pragma unroll
     for (int pl = 0; pl < 2; ++pl)
 #pragma unroll
@@ -201,53 +214,66 @@ __global__ __launch_bounds__(NW * 64, MINB) void k_gemm_skinny(
     __asm__ volatile("" ::: "memory");
     int c = 0;
     for (; c + 3 < nfull; c += 2) {  // chunks c and c + 1 are in flight
-      compute(ck(c), w0, x00, x01);
-      fetch(ck(c + 2), w0, x00, x01);
-      compute(ck(c + 1), w1, x10, x11);
-      fetch(ck(c + 3), w1, x10, x11);
+      compute(ck(c), w0, x0);
+      fetch(ck(c + 2), w0, x0);
+      compute(ck(c + 1), w1, x1);
+      fetch(ck(c + 3), w1, x1);
     }
-    compute(ck(c), w0, x00, x01);
+    compute(ck(c), w0, x0);
     if (c + 2 < nfull) {
-      fetch(ck(c + 2), w0, x00, x01);
-      compute(ck(c + 1), w1, x10, x11);
-      compute(ck(c + 2), w0, x00, x01);
+      fetch(ck(c + 2), w0, x0);
+      compute(ck(c + 1), w1, x1);
+      compute(ck(c + 2), w0, x0);
     } else {
-      compute(ck(c + 1), w1, x10, x11);
+      compute(ck(c + 1), w1, x1);
     }
   } else {
-    if (nfull > 0) fetch(ck(0), w0, x00, x01);
+    if (nfull > 0) fetch(ck(0), w0, x0);
     int c = 0;
     for (; c + 2 < nfull; c += 2) {  // chunk c is in stage 0 and in flight
-      fetch(ck(c + 1), w1, x10, x11);
-      compute(ck(c), w0, x00, x01);
-      fetch(ck(c + 2), w0, x00, x01);
-      compute(ck(c + 1), w1, x10, x11);
+      fetch(ck(c + 1), w1, x1);
+      compute(ck(c), w0, x0);
+      fetch(ck(c + 2), w0, x0);
+      compute(ck(c + 1), w1, x1);
     }
     if (c + 1 < nfull) {
-      fetch(ck(c + 1), w1, x10, x11);
-      compute(ck(c), w0, x00, x01);
-      compute(ck(c + 1), w1, x10, x11);
+      fetch(ck(c + 1), w1, x1);
+      compute(ck(c), w0, x0);
+      compute(ck(c + 1), w1, x1);
     } else if (c < nfull) {
-      compute(ck(c), w0, x00, x01);
+      compute(ck(c), w0, x0);
     }
   }
   for (int k = kb + nfull * CH; k < ke; ++k) {
     bf16x8 b[NB];
 #pragma unroll
     for (int t = 0; t < NB; ++t) b[t] = ld_frag_nt(wb[t] + (size_t)k * 512);
-    const bf16x8 a0 = A1 ? act_lds(k, 0) : ld_frag(ah + k * 32);
-    const bf16x8 a1 = A1 ? act_lds(k, 1) : ld_frag(al + k * 32);
 #pragma unroll
-    for (int t = 0; t < NB; ++t) {
-      acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, b[t], acc[t], 0, 0, 0);
-      acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, b[t], acc[t], 0, 0, 0);
+    for (int h = 0; h < MH; ++h) {
+      const bf16x8 a = A1 ? act_lds(k) : ld_frag(ap[h] + k * 32);
+#pragma unroll
+      for (int t = 0; t < NB; ++t)
+        acc[h][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b[t], acc[h][t], 0, 0, 0);
     }
   }
 
-  __shared__ f32x4 red[NW][NB][64];
+  __shared__ f32x4 red[NW][NB][MH][64];
   __shared__ float s_rs[AN ? 16 : 1];
 #pragma unroll
-  for (int t = 0; t < NB; ++t) red[wave][t][lane] = acc[t];
+  for (int h = 0; h < MH; ++h)
+#pragma unroll
+    for (int t = 0; t < NB; ++t) red[wave][t][h][lane] = acc[h][t];
+  // the product at (tile t, row group h, hi-plane lane l, register v): the
+  // waves' hi-plane partials in wave order, plus their lo-plane partials in
+  // wave order
+  auto rsum = [&](int t, int h, int l, int v) {
+    float a = 0.f, b = 0.f;
+    for (int w = 0; w < NW; ++w) {
+      a += red[w][t][h][l][v];
+      b += red[w][t][h][l + 32][v];
+    }
+    return a + b;
+  };
   if (AN) {
     // row sums in the order of a sequential sum over j = lane, lane + 64, ...,
     // then a butterfly
@@ -279,11 +305,7 @@ __global__ __launch_bounds__(NW * 64, MINB) void k_gemm_skinny(
   if (EPI == EPI_SWIGLU || EPI == EPI_QKV) {
     // tile rows 0..7 pair with rows 8..15 (gate/up, or rotary pairs)
     if (eact && (el & 15) < 8) {
-      float g = 0.f, u = 0.f;
-      for (int w = 0; w < NW; ++w) {
-        g += red[w][et][el][ev];
-        u += red[w][et][el + 8][ev];
-      }
+      float g = rsum(et, eh, el, ev), u = rsum(et, eh, el + 8, ev);
       if (AN) {
         g *= s_rs[em];
         u *= s_rs[em];
@@ -317,15 +339,15 @@ __global__ __launch_bounds__(NW * 64, MINB) void k_gemm_skinny(
       }
     }
   } else {
-    // thread < 256 owns (row 4 (el / 16) + ev, column el % 16): in a wave the
-    // 16 columns of a row sit on lane bits 2..5, so the tile's sum of squares
-    // for the next norm is a 4-step butterfly
+    // thread < 256 owns (row em, column el % 16): in a wave the 16 columns of
+    // a row sit on lane bits 2..5, so the tile's sum of squares for the next
+    // norm is a 4-step butterfly
     static_assert(EPI != EPI_RESID || NB == 1, "next-norm sums assume one tile per block");
     const bool nn = EPI == EPI_RESID && next_gain != nullptr;
     if (threadIdx.x < NB * 256) {
       float s = 0.f;
       if (eact) {
-        for (int w = 0; w < NW; ++w) s += red[w][et][el][ev];
+        s = rsum(et, eh, el, ev);
         if (AN) s *= s_rs[em];
         if (EPI == EPI_RESID) s += e_res;
         out[(size_t)em * ldo + en] = s;
@@ -343,7 +365,7 @@ __global__ __launch_bounds__(NW * 64, MINB) void k_gemm_skinny(
   }
 }
 
-template <int NB, int NW, int CH, int MINB, int AN, int A1>
+template <int NB, int NW, int CH, int MINB, int AN, int A1, int MH>
 static void launch_skinny_a1(const GemmArgs& g, hipStream_t st) {
   const int NT = g.N / 16;
   const bf16_t* Ahi = (const bf16_t*)g.A.hi;
@@ -352,8 +374,8 @@ static void launch_skinny_a1(const GemmArgs& g, hipStream_t st) {
   dim3 grid((NT + NB - 1) / NB), block(NW * 64);
   const size_t lds = A1 ? (size_t)g.K * 4 : 0;  // hi and lo planes of the row
 #define KS_SKINNY(E, OH, OL, OLD)                                                               \
-  KS_LAUNCH((k_gemm_skinny<NB, NW, CH, MINB, E, AN, A1>), grid, block, lds, st, g.M, g.N, g.K,  \
-            Ahi, Alo, g.A.ld, W, g.out, g.ldo, g.res, g.ldres, OH, OL, OLD,                     \
+  KS_LAUNCH((k_gemm_skinny<NB, NW, CH, MINB, E, AN, A1, MH>), grid, block, lds, st, g.M, g.N,   \
+            g.K, Ahi, Alo, g.A.ld, W, g.out, g.ldo, g.res, g.ldres, OH, OL, OLD,                \
             g.ssq_in, g.nssq, g.eps, g.next_gain, (bf16_t*)g.next_act.hi,                       \
             (bf16_t*)g.next_act.lo, g.next_act.ld, g.next_ssq, g.qe)
   if (g.epi == EPI_SWIGLU)
@@ -377,10 +399,11 @@ static void launch_skinny_an(const GemmArgs& g, hipStream_t st) {
   const bool a1 = STAGE && g.M == 1 && g.K % 8 == 0 && (size_t)g.K * 4 <= 64 * 1024 &&
                   4 * per >= pieces && (g.K / 32) / NW >= 2 * CH &&
                   (((uintptr_t)g.A.hi | (uintptr_t)g.A.lo) & 15) == 0;
-  if (!a1) launch_skinny_a1<NB, NW, CH, MINB, AN, 0>(g, st);
-  else if (per >= pieces) launch_skinny_a1<NB, NW, CH, MINB, AN, 1>(g, st);
-  else if (2 * per >= pieces) launch_skinny_a1<NB, NW, CH, MINB, AN, 2>(g, st);
-  else launch_skinny_a1<NB, NW, CH, MINB, AN, 4>(g, st);
+  if (!a1 && g.M > 8) launch_skinny_a1<NB, NW, CH, MINB, AN, 0, 2>(g, st);
+  else if (!a1) launch_skinny_a1<NB, NW, CH, MINB, AN, 0, 1>(g, st);
+  else if (per >= pieces) launch_skinny_a1<NB, NW, CH, MINB, AN, 1, 1>(g, st);
+  else if (2 * per >= pieces) launch_skinny_a1<NB, NW, CH, MINB, AN, 2, 1>(g, st);
+  else launch_skinny_a1<NB, NW, CH, MINB, AN, 4, 1>(g, st);
 }
 
 template <int NB, int NW, int CH, int MINB, int STAGE>
