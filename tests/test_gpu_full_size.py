@@ -57,7 +57,7 @@ def _fill(cfg, dm, layer, n):
 
 
 @pytest.mark.parametrize("layer", LAYERS)
-@pytest.mark.parametrize("R", [1, 5])
+@pytest.mark.parametrize("R", [1, 5, 12])
 def test_full_size_sublayers(full, layer, R):
     cfg, dm = full
     n = CTX - 3  # ragged against the 320-position splits
@@ -65,22 +65,23 @@ def test_full_size_sublayers(full, layer, R):
                     "full")
 
 
-def test_full_size_one_row_bits_equal_verify_rows(full):
-    """A decode row (one row: staged activation, splits merged inside the
-    attention launch) gives the same bits as the same row inside a 5-row
-    verify batch (per-step activation loads, separate merge launch), for both
-    sublayers of layer 0 at row lengths on both sides of a split boundary
-    (7999..8003 with 320-position splits)."""
+@pytest.mark.parametrize("R", [5, 12])
+def test_full_size_one_row_bits_equal_verify_rows(full, R):
+    """A decode row (one row: activation staged in LDS) gives the same bits as
+    the same row inside an R-row verify batch (per-step activation loads; at
+    12 rows two groups of 8 rows per matrix instruction and two 16-column
+    attention blocks), for both sublayers of layer 0 at row lengths on both
+    sides of a split boundary (7999..8003 with 320-position splits)."""
     cfg, dm = full
     n = 8000 - 2
     _fill(cfg, dm, 0, n)
     dm.set_context(n, 0)
-    x = torch.from_numpy(W.synthetic_rows(5, cfg.d, seed=4, std=1.0, index=77)).cuda()
-    pos = np.arange(5) + n
+    x = torch.from_numpy(W.synthetic_rows(R, cfg.d, seed=4, std=1.0, index=77)).cuda()
+    pos = np.arange(R) + n
     for i in (1, 2):
-        out5 = torch.empty(5, cfg.d, device="cuda")
+        out5 = torch.empty(R, cfg.d, device="cuda")
         dm.sublayer_apply(i, x, pos, mode=0, out=out5)
-        for r in range(5):
+        for r in range(R):
             out1 = torch.empty(1, cfg.d, device="cuda")
             dm.sublayer_apply(i, x[r:r + 1].contiguous(), pos[r:r + 1], mode=0, out=out1)
             diff = int((out1[0] != out5[r]).sum().item())

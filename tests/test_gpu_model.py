@@ -57,7 +57,9 @@ def test_prefill_cache_and_first_token(setup):
         assert first == st.s
 
 
-@pytest.mark.parametrize("R", [1, 5, 37])
+# 1 and 5 rows: one group of 8 rows per matrix instruction in the bf16
+# products; 12: two groups; 37: the batched (tiled) path
+@pytest.mark.parametrize("R", [1, 5, 12, 37])
 @pytest.mark.parametrize("mode", [1, 0])
 def test_sublayers_and_head(setup, R, mode):
     name, cfg, dm, model = setup
