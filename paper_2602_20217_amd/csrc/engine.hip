@@ -460,12 +460,14 @@ void decode_row(ks_ctx* c, const int32_t* tok_dev, int p, const uint8_t* exec, i
     while (j <= L2 && exec && !exec[j - 1]) ++j;
     return j;
   };
-  PROF(c, KS_KC_OTHER, fill_pos(pos, len, p, 1, 1, 1, c->st));
   if (c->bf()) {
+    // the embedding launch also writes the row's position and length
     PROF(c, KS_KC_EMBED,
          act_prep(nullptr, d.d, c->embed, d.dtype, tok_dev, 1, d.d, x,
-                  gain_of(c, next_exec(0)), c->act1(), c->at<float>(c->y.ssq), c->st));
+                  gain_of(c, next_exec(0)), c->act1(), c->at<float>(c->y.ssq), c->st,
+                  PosFill{pos, len, p, 1, 1}));
   } else {
+    PROF(c, KS_KC_OTHER, fill_pos(pos, len, p, 1, 1, 1, c->st));
     PROF(c, KS_KC_EMBED, embed_rows(c->embed, d.dtype, tok_dev, 1, d.d, x, d.d, c->st));
   }
   for (int i = 1; i <= L2; ++i)
@@ -480,11 +482,11 @@ void verify_rows(ks_ctx* c, const int32_t* tok_dev, int R, int32_t* am_out,
   const ks_model_desc& d = c->md;
   int32_t* pos = c->at<int32_t>(c->y.pos);
   int32_t* len = c->at<int32_t>(c->y.len);
-  fill_pos(pos, len, c->P, R, R, 1, c->st);
   if (skinny(c, R, false)) {
     act_prep(nullptr, d.d, c->embed, d.dtype, tok_dev, R, d.d, c->stage_row(0, 0), gain_of(c, 1),
-             c->act1(), c->at<float>(c->y.ssq), c->st);
+             c->act1(), c->at<float>(c->y.ssq), c->st, PosFill{pos, len, c->P, R, 1});
   } else {
+    fill_pos(pos, len, c->P, R, R, 1, c->st);
     embed_rows(c->embed, d.dtype, tok_dev, R, d.d, c->stage_row(0, 0), d.d, c->st);
   }
   for (int i = 1; i <= 2 * d.L; ++i)

@@ -141,11 +141,20 @@ __host__ __device__ inline int qkv_perm(int i, int hd) {
 // x[m][:] = embed[tok[m]][:]
 void embed_rows(const void* E, int dtype, const int32_t* tok, int M, int d, float* x,
                 int ldx, hipStream_t st);
+// Positions of R rows starting at base (row m: base + m % r) and their
+// lengths (position + len_add), written by the launch that prepares the rows.
+struct PosFill {
+  int32_t* pos = nullptr;
+  int32_t* len = nullptr;
+  int base = 0, r = 1, len_add = 0;
+};
 // RMSNorm input of a skinny product: for row m, x = (E ? embedding row tok[m] :
 // xin row m) is written to xout (when not null and not xin), act = bf16 split of
-// x * gain and ssq[m][j] = sum of x^2 over columns 16 j..16 j + 15 (ld d/16).
+// x * gain and ssq[m][j] = sum of x^2 over columns 16 j..16 j + 15 (ld d/16);
+// with pf.pos also pos[m] and len[m] (as fill_pos).
 void act_prep(const float* xin, int ldx, const void* E, int dtype, const int32_t* tok, int M,
-              int d, float* xout, const float* gain, Act act, float* ssq, hipStream_t st);
+              int d, float* xout, const float* gain, Act act, float* ssq, hipStream_t st,
+              PosFill pf = PosFill{});
 // act = bf16 split (or f32 copy) of rmsnorm(x) * g ; g == nullptr means no norm (plain
 // conversion).
 void norm_act(const float* x, int ldx, const float* g, float eps, int M, int d, int dtype,

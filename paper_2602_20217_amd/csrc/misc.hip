@@ -55,8 +55,14 @@ __global__ __launch_bounds__(256) void k_act_prep(const float* __restrict__ xin,
                                                   const void* __restrict__ E, int bf,
                                                   const int32_t* __restrict__ tok, int d,
                                                   float* xout, const float* __restrict__ gain,
-                                                  bf16_t* hi, bf16_t* lo, int lda, float* ssq) {
+                                                  bf16_t* hi, bf16_t* lo, int lda, float* ssq,
+                                                  PosFill pf) {
   const int m = blockIdx.x;
+  if (pf.pos && threadIdx.x == 0) {
+    const int p = pf.base + m % pf.r;
+    pf.pos[m] = p;
+    pf.len[m] = p + pf.len_add;
+  }
   const size_t eb = E ? (size_t)tok[m] * d : 0;
   for (int c4 = threadIdx.x; c4 < (d >> 2); c4 += 256) {
     const int c = 4 * c4;
@@ -95,11 +101,12 @@ __global__ __launch_bounds__(256) void k_act_prep(const float* __restrict__ xin,
 }
 
 void act_prep(const float* xin, int ldx, const void* E, int dtype, const int32_t* tok, int M,
-              int d, float* xout, const float* gain, Act act, float* ssq, hipStream_t st) {
+              int d, float* xout, const float* gain, Act act, float* ssq, hipStream_t st,
+              PosFill pf) {
   if (M <= 0) return;
   KS_LAUNCH(k_act_prep, dim3(M), dim3(256), 0, st, xin, ldx, E,
             dtype == KS_BF16 ? 1 : 0, tok, d, xout, gain, (bf16_t*)act.hi,
-            (bf16_t*)act.lo, act.ld, ssq);
+            (bf16_t*)act.lo, act.ld, ssq, pf);
 }
 
 // ---------------------------------------------------------------- RMSNorm
