@@ -476,7 +476,9 @@ ks_status ks_profile_decode(ks_ctx* ctx, const uint8_t* exec, int steps, int per
  * records stop_event when it ends, so the elapsed time between them covers the
  * kernels' execution only (no event packets between launches).  A bracket
  * closed without launches records neither event.  Opening a bracket replaces
- * an open one.  Both handles must be set or both NULL (KS_EINVAL otherwise).
+ * an open one, and ks_profile_decode with per_kernel = 1 uses the same
+ * mechanism and leaves no bracket open.  Both handles must be set or both NULL
+ * (KS_EINVAL otherwise).
  */
 ks_status ks_time_launches(void* start_event, void* stop_event);
 
