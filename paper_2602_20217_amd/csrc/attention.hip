@@ -21,6 +21,20 @@
 namespace ks {
 
 constexpr int TILE = 64;  // positions per LDS tile of the split kernel
+
+// Workgroups are dealt to the 8 XCDs round-robin by linear id (id mod 8), and
+// each XCD has its own L2.  With 8 kv heads, k_attn_dec runs on a
+// one-dimensional grid of 8 ns workgroups that keeps every split of kv head h
+// on XCD h, and the merge launch places the query heads of kv head h there
+// too, so the split partials it reads were written through its own L2.
+// (Decode step at 8K: 3.07 -> 3.03 ms against the two-dimensional grid.)
+struct SplitId {
+  int split, kvh;
+};
+__device__ inline SplitId split_id(int xmap) {
+  if (xmap) return SplitId{(int)(blockIdx.x >> 3), (int)(blockIdx.x & 7)};
+  return SplitId{(int)blockIdx.x, (int)blockIdx.y};
+}
 #ifndef KS_BAT_NW
 #define KS_BAT_NW 8  // waves (16 query vectors each) per batched workgroup
 #endif
@@ -282,7 +296,7 @@ template <int S, int CB>
 __global__ __launch_bounds__(64 * S) void k_attn_dec(
     int M, int hq, int hkv, int n_max, const float* __restrict__ q,
     const bf16_t* __restrict__ kc, const bf16_t* __restrict__ vc,
-    const int32_t* __restrict__ len, float* __restrict__ part, int nsplit, int span) {
+    const int32_t* __restrict__ len, float* __restrict__ part, int nsplit, int span, int xmap) {
   constexpr int HD = 128;
   constexpr int RS = HD + 4;  // LDS merge record per column: o, max, sum (bank-shifted)
   constexpr int NCOL = 16 * CB;
@@ -294,7 +308,8 @@ __global__ __launch_bounds__(64 * S) void k_attn_dec(
   // column block 0, its value tile those of block 1; wave 0's key tile also
   // holds the row length of every column after its records
   int* s_len = (int*)((float*)&Ks[0][0] + 16 * RS);  // [NCOL] row length per column
-  const int split = blockIdx.x, kvh = blockIdx.y;
+  const SplitId sid = split_id(xmap);
+  const int split = sid.split, kvh = sid.kvh;
   const int G = hq / hkv;
   const int RB = NCOL / G;
   const int r0 = blockIdx.z * RB;
@@ -549,7 +564,7 @@ template <int NW, int CB>
 __global__ __launch_bounds__(64 * NW) void k_attn_stream(
     int M, int hq, int hkv, int n_max, const float* __restrict__ q,
     const bf16_t* __restrict__ kc, const bf16_t* __restrict__ vc,
-    const int32_t* __restrict__ len, float* __restrict__ part, int nsplit, int tpw) {
+    const int32_t* __restrict__ len, float* __restrict__ part, int nsplit, int tpw, int xmap) {
   constexpr int HD = 128;
   constexpr int RS = HD + 4;  // LDS merge record per column: o, max, sum (bank-shifted)
   constexpr int NCOL = 16 * CB;
@@ -559,7 +574,8 @@ __global__ __launch_bounds__(64 * NW) void k_attn_stream(
   // loads into one stage never alias reads of the other
   __shared__ __align__(16) uint4 Vr0[NW][TILE * 16];
   __shared__ __align__(16) uint4 Vr1[NW][TILE * 16];
-  const int split = blockIdx.x, kvh = blockIdx.y;
+  const SplitId sid = split_id(xmap);
+  const int split = sid.split, kvh = sid.kvh;
   const int G = hq / hkv;
   const int RB = NCOL / G;
   const int r0 = blockIdx.z * RB;
@@ -1075,15 +1091,18 @@ __global__ __launch_bounds__(256) void k_attn_combine(int M, int hq, int hkv, in
                                                       const int32_t* __restrict__ len,
                                                       const float* __restrict__ kvself,
                                                       bf16_t* ohi, bf16_t* olo, float* of,
-                                                      int ldact) {
+                                                      int ldact, int xmap) {
   constexpr int DPL = HD / 64;
   constexpr int CB = 8;
   __shared__ float s_m[4], s_l[4];
   __shared__ float s_acc[4][DPL * 64];
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
-  const int r = blockIdx.x / hq, h = blockIdx.x % hq;
   const int G = hq / hkv;
+  // xmap: query head h of kv head h / G on XCD h / G (see split_id)
+  const int rest = blockIdx.x >> 3;
+  const int r = xmap ? rest / G : blockIdx.x / hq;
+  const int h = xmap ? (blockIdx.x & 7) * G + rest % G : blockIdx.x % hq;
   const int kvh = h / G;
   const float* pr = part + ((size_t)r * hq + h) * nsplit * (HD + 2);
   const int d0 = BF ? 2 * lane : lane;
@@ -1217,12 +1236,15 @@ void attn_split(const AttnArgs& a, hipStream_t st) {
     // all rows, else 32 (16 CB / G rows per workgroup)
     const int CB = a.M * G <= 16 ? 1 : 2;
     const int RB = 16 * CB / G;
-    dim3 g3(ns, a.hkv, (a.M + RB - 1) / RB);
+    // the XCD placement pays for the one-round split kernel (k_attn_dec), not
+    // for the streaming one (32K: 27.9 -> 28.3 us and the merge 4.2 -> 4.4 us)
+    const int xmap = a.hkv == 8 && a.tiles <= 5;
+    const dim3 g3 = xmap ? dim3(8 * ns, 1, (a.M + RB - 1) / RB) : dim3(ns, a.hkv, (a.M + RB - 1) / RB);
     const bf16_t* kc = (const bf16_t*)a.kc;
     const bf16_t* vc = (const bf16_t*)a.vc;
 #define KS_DEC(S_, CB_)                                                                      \
   KS_LAUNCH((k_attn_dec<S_, CB_>), g3, dim3(64 * S_), 0, st, a.M, a.hq, a.hkv,               \
-            a.n_max, a.q, kc, vc, a.len, a.part, a.nsplit, a.span)
+            a.n_max, a.q, kc, vc, a.len, a.part, a.nsplit, a.span, xmap)
 #define KS_DEC_S(CB_)            \
   switch (a.tiles) {             \
     case 1: KS_DEC(1, CB_); break; \
@@ -1235,10 +1257,10 @@ void attn_split(const AttnArgs& a, hipStream_t st) {
       const int tpw = a.tiles / STREAM_NW;
       if (CB == 1)
         KS_LAUNCH((k_attn_stream<STREAM_NW, 1>), g3, dim3(64 * STREAM_NW), 0, st, a.M,
-                  a.hq, a.hkv, a.n_max, a.q, kc, vc, a.len, a.part, a.nsplit, tpw);
+                  a.hq, a.hkv, a.n_max, a.q, kc, vc, a.len, a.part, a.nsplit, tpw, xmap);
       else
         KS_LAUNCH((k_attn_stream<STREAM_NW, 2>), g3, dim3(64 * STREAM_NW), 0, st, a.M,
-                  a.hq, a.hkv, a.n_max, a.q, kc, vc, a.len, a.part, a.nsplit, tpw);
+                  a.hq, a.hkv, a.n_max, a.q, kc, vc, a.len, a.part, a.nsplit, tpw, xmap);
     } else if (CB == 1) {
       KS_DEC_S(1);
     } else {
@@ -1264,6 +1286,7 @@ void attn_split(const AttnArgs& a, hipStream_t st) {
 
 void attn_combine(const AttnArgs& a, const float* kvself, Act act_out, hipStream_t st) {
   dim3 grid(a.M * a.hq);
+  const int xmap = attn_dec_path(a) && a.hkv == 8 && a.tiles <= 5;  // placed like the split kernel
   const int span = a.span;
   const int ngrid = (a.max_len + span - 1) / span;  // splits the split kernel ran
   const bool bf = a.dtype == KS_BF16;
@@ -1271,7 +1294,7 @@ void attn_combine(const AttnArgs& a, const float* kvself, Act act_out, hipStream
   KS_LAUNCH((k_attn_combine<HDV, BFV>), grid, dim3(256), 0, st, a.M, a.hq, a.hkv,            \
             span, ngrid, a.q, a.part, a.nsplit, a.len, kvself,                               \
             bf ? (bf16_t*)act_out.hi : nullptr, bf ? (bf16_t*)act_out.lo : nullptr,          \
-            bf ? nullptr : (float*)act_out.hi, act_out.ld)
+            bf ? nullptr : (float*)act_out.hi, act_out.ld, xmap)
   if (a.hd == 128) KS_COMB(128, true);
   else KS_COMB(64, false);
 #undef KS_COMB
