@@ -231,28 +231,85 @@ __device__ __forceinline__ void knap_select_sweep(int n, int C, int D, int tid, 
   double pv[EL];
 #pragma unroll
   for (int e = 0; e < EL; ++e) pv[e] = 256 * e + tid == 0 ? 1.0 : NaN;
-  for (int i = 0; i < n; ++i) {
-    const int wi = sw[i];
-    const double si = ss[i];
-    double cand[EL];
-    uint64_t word[EL];
+  // The decision words of item i are requested PF items ahead, as vector loads
+  // (a zero the compiler cannot see through keeps them off the scalar path,
+  // whose waits would also wait for every LDS access), so their memory latency
+  // overlaps the sweep of the items before; the ring index of each unrolled
+  // copy is a constant.  The barriers wait for this wave's LDS accesses only
+  // (a full __syncthreads would also wait for the words in flight).
+  // (above 9 slots per thread the ring would cost the occupancy that keeps
+  // 1024 instances in one round: those sweeps load each item's words in turn)
+  constexpr int PF = EL <= 4 ? 4 : (EL <= 9 ? 3 : 0);
+  int vz;
+  __asm__ volatile("v_mov_b32 %0, 0" : "=v"(vz));
+  uint64_t wr[PF > 0 ? PF : 1][EL];
+  auto fetch = [&](int i, uint64_t (&wd_)[EL]) {
+    const int ic = i < n ? i : n - 1;
 #pragma unroll
     for (int e = 0; e < EL; ++e) {
-      const int j = 256 * e + tid;
-      const double c = row[j >= wi ? j - wi : 0];
-      cand[e] = j >= wi ? c : NaN;
       const int wd = 4 * e + wave;  // word of budgets 256 e + 64 wave + lane
-      word[e] = bb[(size_t)i * words + (wd < words ? wd : 0)];
-      if (wd >= words) word[e] = 0ull;
+      wd_[e] = bb[(size_t)ic * words + (wd < words ? wd : 0) + vz];
     }
-    __syncthreads();  // row i - 1 read by every thread before it is overwritten
+  };
+  auto lds_barrier = [] {
+    __asm__ volatile("" ::: "memory");
+    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's LDS accesses are done
+    __builtin_amdgcn_s_barrier();
+    __asm__ volatile("" ::: "memory");
+  };
+  if constexpr (PF == 0) {
+    for (int i = 0; i < n; ++i) {
+      const int wi = sw[i];
+      const double si = ss[i];
+      double cand[EL];
+      uint64_t word[EL];
 #pragma unroll
-    for (int e = 0; e < EL; ++e) {
-      const double m = cand[e] * si;
-      pv[e] = ((word[e] >> lane) & 1ull) ? m : pv[e];
-      row[256 * e + tid] = pv[e];
+      for (int e = 0; e < EL; ++e) {
+        const int j = 256 * e + tid;
+        const double c = row[j >= wi ? j - wi : 0];
+        cand[e] = j >= wi ? c : NaN;
+        const int wd = 4 * e + wave;
+        word[e] = wd < words ? bb[(size_t)i * words + wd] : 0ull;
+      }
+      __syncthreads();  // row i - 1 read by every thread before it is overwritten
+#pragma unroll
+      for (int e = 0; e < EL; ++e) {
+        const double m = cand[e] * si;
+        pv[e] = ((word[e] >> lane) & 1ull) ? m : pv[e];
+        row[256 * e + tid] = pv[e];
+      }
+      __syncthreads();
     }
-    __syncthreads();
+  } else {
+#pragma unroll
+    for (int k = 0; k < PF; ++k) fetch(k, wr[k]);
+    for (int i0 = 0; i0 < n; i0 += PF) {
+#pragma unroll
+      for (int k = 0; k < PF; ++k) {
+        const int i = i0 + k;
+        if (i < n) {
+          const int wi = sw[i];
+          const double si = ss[i];
+          double cand[EL];
+#pragma unroll
+          for (int e = 0; e < EL; ++e) {
+            const int j = 256 * e + tid;
+            const double c = row[j >= wi ? j - wi : 0];
+            cand[e] = j >= wi ? c : NaN;
+          }
+          lds_barrier();  // row i - 1 read by every thread before it is overwritten
+#pragma unroll
+          for (int e = 0; e < EL; ++e) {
+            const uint64_t word = 4 * e + wave < words ? wr[k][e] : 0ull;
+            const double m = cand[e] * si;
+            pv[e] = ((word >> lane) & 1ull) ? m : pv[e];
+            row[256 * e + tid] = pv[e];
+          }
+          fetch(i + PF, wr[k]);
+          lds_barrier();
+        }
+      }
+    }
   }
 #pragma unroll
   for (int e = 0; e < EL; ++e) {  // ascending budgets
