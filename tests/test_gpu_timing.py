@@ -66,3 +66,32 @@ def test_launches_after_a_closed_bracket_leave_its_events(K):
         K.ks_stream_read(buf.data_ptr(), nb, sink.data_ptr(), st)
     torch.cuda.synchronize()
     assert a.elapsed_time(b) == t
+
+
+def test_decode_profile_launch_counts_and_times(K):
+    """The decode-step profile (its launches carry their class's events): every
+    class of a bf16 decode step has the launch count the step's structure fixes,
+    positive times, and the classes add up to at most the step's own time."""
+    import numpy as np
+    import workloads as W
+    from gpu_helpers import build
+    cfg, dm, _ = build("small_bf16", n_max=160, gamma_max=4)
+    try:
+        dm.prefill(np.arange(40, dtype=np.int32) % cfg.vocab)
+        pr = dm.profile_decode(None, 4, per_kernel=True)
+        L = cfg.L
+        want = {"embed": 1, "gemm_qkv": L, "attn": L, "combine": L, "gemm_o": L,
+                "gemm_gate_up": L, "gemm_down": L, "gemm_head": 1, "argmax": 1}
+        for name, n in want.items():
+            assert pr["launches"][name] == n, (name, pr["launches"][name])
+            assert pr["ms"][name] > 0, name
+        total = sum(pr["ms"][k] * pr["launches"][k] for k in pr["ms"])
+        assert 0 < total <= pr["ms_step"] * 1.02, (total, pr["ms_step"])
+        # a mask that skips every attention sublayer drops their launches
+        exec_mask = np.ones(2 * L, dtype=bool)
+        exec_mask[0::2] = False
+        pm = dm.profile_decode(exec_mask, 2, per_kernel=True)
+        assert pm["launches"]["attn"] == 0 and pm["launches"]["gemm_qkv"] == 0
+        assert pm["launches"]["gemm_gate_up"] == L
+    finally:
+        dm.close()
