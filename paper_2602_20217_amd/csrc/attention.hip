@@ -1,15 +1,24 @@
-// GQA decode attention over a contiguous KV cache, split over the context.
+// GQA attention of the decoder's attention sublayers (Section 2, the
+// attention sublayer of each block) over a contiguous KV cache
+// [layer][K | V][kv head][position][dim], split over the context.  Each split
+// kernel writes a partial (o, max, sum) per (row, query head, split) and
+// k_attn_combine merges the splits of a row in ascending order.
 //
-// Grid: (split, kv head, row group).  A workgroup owns `tiles` consecutive
-// 64-position tiles of one kv head.  Every thread issues its share of a
-// tile's K and V loads at once (16-byte chunks, all in flight together) and
-// stores them to LDS after one wait.  K rows are padded by four 32-bit words
-// so that 16-byte LDS reads of 64 different rows cover all banks.  Each wave
-// owns a fixed set of query vectors (the G = hq/hkv query heads of a row share
-// the tile); a lane scores one key, softmax statistics use wave shuffles, and
-// the output accumulation broadcasts each probability with a lane read.  The
-// partial (o, max, sum) of each (row, query head, split) goes to memory and a
-// second kernel merges the splits in ascending order.
+//  k_attn_dec      decode and verify rows, bf16 caches of up to 12288
+//                  positions: splits of 2, 3 or 5 tiles of 64 keys (by cache
+//                  size), one tile per wave, scores and P V on matrix
+//                  instructions.
+//  k_attn_stream   decode and verify rows, bf16 caches above 12288 positions:
+//                  each wave walks several tiles of its split with the next
+//                  tile's loads in flight.
+//  k_attn_bat      batched rows (prefill chunks, the selection's candidate
+//                  rows), bf16 caches: query blocks of several rows against a
+//                  ring of key/value tiles.
+//  k_attn_split    every other case, on the vector ALU: the float32 caches
+//                  (head dim 64) of the float32 models and head shapes the
+//                  matrix kernels do not take.
+//  k_attn_combine  the split merge (plus, for selection rows, the row's own
+//                  key and value).
 //
 // A row's arithmetic depends only on its own query, its length and the split
 // size, never on the other rows of the launch, so the decode step and a verify
@@ -68,6 +77,13 @@ int attn_nsplit(int n_positions, int tiles) {
   return (n_positions + span - 1) / span;
 }
 
+// Vector-ALU split kernel.  Grid: (split, kv head, row group); a workgroup
+// owns `tiles` consecutive 64-position tiles of one kv head.  K rows are
+// padded by four 32-bit words in LDS so that 16-byte reads of 64 different
+// rows cover all banks.  Each wave owns a fixed set of query vectors (the G =
+// hq / hkv query heads of a row share the tile); a lane scores one key,
+// softmax statistics use wave shuffles, and the output accumulation
+// broadcasts each probability with a lane read.
 // HD: head dim (128 for bf16 caches, 64 for float32 caches).  QMAX: query
 // vectors per wave (rows_per_block * G <= 4 QMAX).
 //
