@@ -1,8 +1,10 @@
-// Row-wise kernels of the decode step: embedding gather, RMSNorm into matrix
-// activations, q/k normalisation + rotary embedding + KV store, greedy argmax
-// with top-1 probability, cosine similarity (Section 2 of the paper), row
-// copies and the rotary table.  All reductions use a fixed order so results
-// are reproducible run to run and independent of how many rows a launch holds.
+// Row-wise kernels of the decode step: embedding gather, RMSNorm into the
+// products' bf16 hi/lo activation planes, the per-head q/k normalisation +
+// rotary embedding + KV store of q/k-normed models, cosine similarity
+// (Section 2 of the paper), copies into the history ring, block copies, the
+// rotary table and small fills.  (The greedy argmax lives with the other
+// vocabulary reductions.)  All reductions use a fixed order so results are
+// reproducible run to run and independent of how many rows a launch holds.
 #include "ks_internal.h"
 
 #include <cfloat>
