@@ -217,13 +217,16 @@ void knapsack_backtrack(const uint64_t* bits, const int32_t* w, int B, int n, in
 // a sequential scan over (j ascending, gamma ascending) with strict ">".
 // Items are limited to 128 (the per-item weights and scores live in LDS).
 // The sweep and the TPT grid over the first EL slots (EL covers the largest
-// reachable budget): branch-free per slot, so each phase's LDS reads are in
-// flight together.
+// reachable budget): branch-free per slot, and a budget below the item's
+// weight reads a NaN cell instead of selecting NaN after its load, so no
+// lane mask has to live across a load and the item's LDS reads are in flight
+// together.
 template <int EL>
 __device__ __forceinline__ void knap_select_sweep(int n, int C, int D, int tid, int lane,
                                                   int wave, int words,
                                                   const uint64_t* __restrict__ bb, double* row,
-                                                  const int32_t* sw, const double* ss,
+                                                  const double* nanp, const int32_t* sw,
+                                                  const double* ss,
                                                   uint32_t live, long long W, double& bv, int& bj,
                                                   int& bg) {
 #pragma clang fp contract(off)
@@ -266,8 +269,7 @@ __device__ __forceinline__ void knap_select_sweep(int n, int C, int D, int tid, 
 #pragma unroll
       for (int e = 0; e < EL; ++e) {
         const int j = 256 * e + tid;
-        const double c = row[j >= wi ? j - wi : 0];
-        cand[e] = j >= wi ? c : NaN;
+        cand[e] = *(j >= wi ? &row[j - wi] : nanp);
         const int wd = 4 * e + wave;
         word[e] = wd < words ? bb[(size_t)i * words + wd] : 0ull;
       }
@@ -288,22 +290,29 @@ __device__ __forceinline__ void knap_select_sweep(int n, int C, int D, int tid, 
       for (int k = 0; k < PF; ++k) {
         const int i = i0 + k;
         if (i < n) {
-          const int wi = sw[i];
+          const int wi = __builtin_amdgcn_readfirstlane(sw[i]);
           const double si = ss[i];
+          // rows alternate between the two halves: item i reads row i - 1
+          // from one and writes row i to the other, so one barrier per item
+          // (after the writes) orders both the reads and the reuse
+          const double* src = row + (i & 1) * 256 * EL;
+          double* dst = row + ((i & 1) ^ 1) * 256 * EL;
+          const double* cb = src + tid - wi;  // skip candidate of budget 256 e + tid at cb[256 e]
           double cand[EL];
 #pragma unroll
           for (int e = 0; e < EL; ++e) {
-            const int j = 256 * e + tid;
-            const double c = row[j >= wi ? j - wi : 0];
-            cand[e] = j >= wi ? c : NaN;
+            if (256 * e >= wi) cand[e] = cb[256 * e];  // every budget of the slot covers w_i
+            else cand[e] = *(256 * e + tid >= wi ? &cb[256 * e] : nanp);
           }
-          lds_barrier();  // row i - 1 read by every thread before it is overwritten
 #pragma unroll
           for (int e = 0; e < EL; ++e) {
-            const uint64_t word = 4 * e + wave < words ? wr[k][e] : 0ull;
+            // a word past the instance's last (4 e + wave >= words) holds the
+            // bits of other budgets: the budgets of such a slot lie above C,
+            // are never live and are never read by a live budget
+            const uint64_t word = wr[k][e];
             const double m = cand[e] * si;
             pv[e] = ((word >> lane) & 1ull) ? m : pv[e];
-            row[256 * e + tid] = pv[e];
+            dst[256 * e + tid] = pv[e];
           }
           fetch(i + PF, wr[k]);
           lds_barrier();
@@ -334,15 +343,20 @@ __device__ __forceinline__ void knap_select_sweep(int n, int C, int D, int tid, 
 }
 
 template <int E>
-__global__ __launch_bounds__(256) void k_knap_select(
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void k_knap_select(
     const int32_t* __restrict__ best, const uint64_t* __restrict__ bits,
     const int32_t* __restrict__ w, const double* __restrict__ s, int n, int C, int D,
     int32_t* j_star, int32_t* g_star, double* tpt, uint8_t* skip) {
-  extern __shared__ double row[];  // 256 E: budget 256 e + tid at 256 e + tid
-  __shared__ double sv[256];
-  __shared__ int sj[256], sg[256];
+  // 256 E doubles, budget 256 e + tid at 256 e + tid (sweeps of up to 9 slots
+  // use two rows of 256 EL); after the sweep the same space holds the
+  // reduction's values, budgets and draft lengths
+  extern __shared__ double row[];
+  double* sv = row;
+  int* sj = (int*)(row + 256);
+  int* sg = sj + 256;
   __shared__ int32_t sw[128];
   __shared__ double ss[128];
+  __shared__ double s_nan;
   __shared__ int s_jl;
   const int b = blockIdx.x, tid = threadIdx.x;
   const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -354,7 +368,10 @@ __global__ __launch_bounds__(256) void k_knap_select(
     sw[i] = max(w[(size_t)b * n + i], 0);  // negative weights are read as 0, as in the DP
     ss[i] = s[(size_t)b * n + i];
   }
-  if (tid == 0) s_jl = 0;
+  if (tid == 0) {
+    s_jl = 0;
+    s_nan = __builtin_nan("");
+  }
   uint32_t live = 0;  // bit e: budget 256 e + tid is reachable
   int jl = 0;
 #pragma unroll
@@ -375,8 +392,8 @@ __global__ __launch_bounds__(256) void k_knap_select(
   double bv = 0.0;
   int bj = 0x7FFFFFFF, bg = 0;
 #define KS_SWEEP(L_)                                                                          \
-  knap_select_sweep<(L_ < E ? L_ : E)>(n, C, D, tid, lane, wave, words, bb, row, sw, ss, live, \
-                                       W, bv, bj, bg)
+  knap_select_sweep<(L_ < E ? L_ : E)>(n, C, D, tid, lane, wave, words, bb, row, &s_nan, sw, ss, \
+                                       live, W, bv, bj, bg)
   if (EL <= 1) KS_SWEEP(1);
   else if (EL <= 2) KS_SWEEP(2);
   else if (EL <= 3) KS_SWEEP(3);
@@ -425,7 +442,10 @@ template <int E>
 static void launch_knap_select(const int32_t* best, const uint64_t* bits, const int32_t* w,
                                const double* s, int B, int n, int C, int D, int32_t* j_star,
                                int32_t* g_star, double* tpt, uint8_t* skip, hipStream_t st) {
-  const size_t rowb = (size_t)256 * E * sizeof(double);
+  // one row of every budget, or two rows of up to 9 slots; at least the
+  // reduction's 512 doubles
+  const int two = 2 * (E < 9 ? E : 9);
+  const size_t rowb = (size_t)256 * (E > two ? E : (two > 2 ? two : 2)) * sizeof(double);
   KS_LAUNCH(k_knap_select<E>, dim3(B), dim3(256), rowb, st, best, bits, w, s, n, C, D,
             j_star, g_star, tpt, skip);
 }
